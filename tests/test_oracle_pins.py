@@ -1,0 +1,268 @@
+"""Pins for the CPU oracle: checks against facts the paper and the mathematics
+fix, none of which re-types the oracle's own index formula.
+
+  * brute force: K assembled with numpy's kron from the Kronecker structure of
+    Definition 2.1 (sum over (i, j) of e_i e_i^T (x) K_ij (x) e_j e_j^T), then a
+    dense fp64 matmul;
+  * support invariant: exactly a*b*c*d nonzeros, exactly on
+    kron(kron(I_a, 1_{b x c}), I_d), density 1/(a*d) (Section 2, after Def 2.1);
+  * special cases: a = d = 1 is a dense GEMM (Appendix B.1, Table 5 "Dense"
+    row); b = c = 1 is a diagonal scaling; identity blocks give Y = X;
+  * Figure 4 index sets (tests/golden/fig4_index_sets.json);
+  * two independent formulations written from Appendix A.1 (the batched-GEMM
+    reshape / bmm / reshape steps and the 4-D tensor contraction);
+  * chains equal the product of the dense factors (Appendix B.1, Table 5), and
+    the dyadic butterfly chain with all blocks [[1,1],[1,-1]] is the
+    Sylvester-Hadamard matrix (scipy.linalg.hadamard), the real analogue of the
+    FFT factorisation of Section 1 / Figure 1;
+  * the adjoint identity <X K^T, Z> = <X, Z K> with K^T a KS factor of pattern
+    (a, c, b, d);
+  * layout: the BSL result is the transpose of the BSF result.
+"""
+import itertools
+import json
+import os
+
+import numpy as np
+import pytest
+import scipy.linalg
+
+import oracle
+from paper_2405_15013_amd import inputs
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+def kron_dense(pattern, kv):
+    """Dense K from Definition 2.1's Kronecker structure, assembled with kron."""
+    a, b, c, d = pattern
+    kv = np.asarray(kv, dtype=np.float64).reshape(a * d, b, c)
+    K = np.zeros((a * b * d, a * c * d))
+    for i in range(a):
+        Ea = np.zeros((a, a))
+        Ea[i, i] = 1.0
+        for j in range(d):
+            Ed = np.zeros((d, d))
+            Ed[j, j] = 1.0
+            K += np.kron(np.kron(Ea, kv[i * d + j]), Ed)
+    return K
+
+
+def rand_case(pattern, batch, seed, dist_k="normal"):
+    rng = np.random.default_rng(seed)
+    a, b, c, d = pattern
+    kv = rng.standard_normal((a * d, b, c)) if dist_k == "normal" else rng.uniform(0.5, 1.5, (a * d, b, c))
+    x = rng.standard_normal((batch, a * c * d))
+    return kv, x
+
+
+SMALL_PATTERNS = [p for p in itertools.product([1, 2, 3], [1, 2, 3], [1, 2, 4], [1, 2, 3])][::3] + [
+    (2, 4, 4, 2), (1, 5, 3, 1), (3, 1, 4, 2), (2, 3, 2, 3), (4, 2, 2, 1), (1, 2, 2, 4)]
+
+
+@pytest.mark.parametrize("pattern", SMALL_PATTERNS)
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_bruteforce_dense(pattern, layout):
+    batch = 5
+    kv, x = rand_case(pattern, batch, seed=hash(pattern) % 1000)
+    K = kron_dense(pattern, kv)
+    y_ref = x @ K.T
+    y = oracle.matmul(pattern, kv, inputs.to_layout(x, layout), batch, layout)
+    np.testing.assert_allclose(inputs.from_layout(y, layout), y_ref, rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("pattern", SMALL_PATTERNS)
+def test_dense_materialisation_and_support(pattern):
+    a, b, c, d = pattern
+    kv, _ = rand_case(pattern, 1, seed=7, dist_k="positive")
+    K = oracle.dense(pattern, kv)
+    np.testing.assert_array_equal(K, kron_dense(pattern, kv))
+    mask = np.kron(np.kron(np.eye(a), np.ones((b, c))), np.eye(d)) != 0
+    assert K.shape == (a * b * d, a * c * d)
+    assert np.array_equal(K != 0, mask)
+    assert int(np.count_nonzero(K)) == a * b * c * d
+    assert np.isclose(np.count_nonzero(K) / K.size, 1.0 / (a * d))
+
+
+def test_tiny_config_support_count():
+    # (2,4,4,2): K is 16 x 16 with a*b*c*d = 64 nonzeros (density 1/(a*d) = 1/4).
+    kv = inputs.to_f64(inputs.make_kv(0, (2, 4, 4, 2), 32, "f32", dist="normal"), "f32")
+    K = oracle.dense((2, 4, 4, 2), kv)
+    assert K.shape == (16, 16)
+    assert np.count_nonzero(K) == 64
+
+
+@pytest.mark.parametrize("bc", [(3, 5), (8, 8), (16, 4)])
+def test_dense_gemm_special_case(bc):
+    b, c = bc
+    kv, x = rand_case((1, b, c, 1), 7, seed=3)
+    y = oracle.matmul((1, b, c, 1), kv, x, 7, "bsf")
+    np.testing.assert_allclose(y, x @ kv[0].T, rtol=1e-13, atol=1e-13)
+
+
+@pytest.mark.parametrize("ad", [(1, 6), (3, 2), (4, 1)])
+def test_diagonal_special_case(ad):
+    a, d = ad
+    kv, x = rand_case((a, 1, 1, d), 4, seed=11)
+    y = oracle.matmul((a, 1, 1, d), kv, x, 4, "bsf")
+    np.testing.assert_allclose(y, x * kv.reshape(-1)[None, :], rtol=0, atol=0)
+
+
+@pytest.mark.parametrize("pattern", [(2, 3, 3, 2), (1, 4, 4, 5), (3, 2, 2, 1)])
+def test_identity_blocks(pattern):
+    a, b, c, d = pattern
+    kv = np.broadcast_to(np.eye(b), (a * d, b, c)).copy()
+    _, x = rand_case(pattern, 6, seed=5)
+    y = oracle.matmul(pattern, kv, x, 6, "bsf")
+    np.testing.assert_array_equal(y, x)
+
+
+def test_figure4_index_sets():
+    with open(os.path.join(HERE, "golden", "fig4_index_sets.json")) as f:
+        g = json.load(f)
+    a, b, c, d = g["pattern"]
+    for blk in g["blocks"]:
+        kv = np.zeros((a * d, b, c))
+        kv[blk["i"] * d + blk["j"]] = 1.0
+        K = oracle.dense((a, b, c, d), kv)
+        rows = sorted(np.nonzero(K.any(axis=1))[0].tolist())
+        cols = sorted(np.nonzero(K.any(axis=0))[0].tolist())
+        assert rows == blk["rows"]
+        assert cols == blk["cols"]
+    # the row sets and the column sets of all (i, j) partition [M] and [N]
+    seen_r, seen_c = [], []
+    for ij in range(a * d):
+        kv = np.zeros((a * d, b, c))
+        kv[ij] = 1.0
+        K = oracle.dense((a, b, c, d), kv)
+        seen_r += np.nonzero(K.any(axis=1))[0].tolist()
+        seen_c += np.nonzero(K.any(axis=0))[0].tolist()
+    assert sorted(seen_r) == list(range(a * b * d))
+    assert sorted(seen_c) == list(range(a * c * d))
+
+
+def bmm_formulation(pattern, kv, x):
+    """Appendix A.1 batched-GEMM route: permute X, batched matmul with the
+    (ad, b, c) blocks, permute back (written from the described steps)."""
+    a, b, c, d = pattern
+    B = x.shape[0]
+    xp = x.reshape(B, a, c, d).transpose(0, 1, 3, 2).reshape(B, a * d, c).transpose(1, 0, 2)  # (ad, B, c)
+    yp = np.matmul(xp, np.transpose(kv, (0, 2, 1)))  # (ad, B, b)
+    return yp.transpose(1, 0, 2).reshape(B, a, d, b).transpose(0, 1, 3, 2).reshape(B, a * b * d)
+
+
+def contraction_formulation(pattern, kv, x):
+    """Appendix A.1 tensor-contraction route with K held as an (a, b, c, d) tensor."""
+    a, b, c, d = pattern
+    B = x.shape[0]
+    k4 = kv.reshape(a, d, b, c).transpose(0, 2, 3, 1)  # (a, b, c, d)
+    y4 = np.einsum("zicj,ikcj->zikj", x.reshape(B, a, c, d), k4)
+    return y4.reshape(B, a * b * d)
+
+
+@pytest.mark.parametrize("pattern", [(2, 3, 2, 3), (1, 4, 8, 2), (3, 5, 2, 1), (2, 2, 2, 4), (1, 6, 6, 1)])
+def test_independent_formulations(pattern):
+    kv, x = rand_case(pattern, 9, seed=13)
+    y = oracle.matmul(pattern, kv, x, 9, "bsf")
+    np.testing.assert_allclose(y, bmm_formulation(pattern, kv, x), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(y, contraction_formulation(pattern, kv, x), rtol=1e-12, atol=1e-12)
+
+
+@pytest.mark.parametrize("patterns", [
+    [(1, 4, 4, 4), (4, 4, 4, 1)],                    # Monarch-shaped pair, N = 16
+    [(1, 2, 2, 4), (2, 2, 2, 2), (4, 2, 2, 1)],      # dyadic butterfly, N = 8
+    [(2, 3, 4, 1), (1, 8, 6, 1), (3, 2, 2, 1)],      # deformable: a c d of one = a b d of next
+    [(1, 5, 2, 1), (1, 2, 7, 1)],                    # low rank
+])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_chain_is_product_of_dense_factors(patterns, layout):
+    rng = np.random.default_rng(17)
+    kvs = [rng.standard_normal((p[0] * p[3], p[1], p[2])) for p in patterns]
+    W = np.eye(kron_dense(patterns[0], kvs[0]).shape[0])
+    for p, kv in zip(patterns, kvs):
+        W = W @ kron_dense(p, kv)
+    last = patterns[-1]
+    x = rng.standard_normal((6, last[0] * last[2] * last[3]))
+    y = oracle.chain(patterns, kvs, inputs.to_layout(x, layout), 6, layout)
+    np.testing.assert_allclose(inputs.from_layout(y, layout), x @ W.T, rtol=1e-11, atol=1e-11)
+
+
+def butterfly_patterns(L):
+    return [(2 ** (l - 1), 2, 2, 2 ** (L - l)) for l in range(1, L + 1)]
+
+
+@pytest.mark.parametrize("L", [1, 3, 6, 10])
+def test_butterfly_chain_is_hadamard(L):
+    n = 2 ** L
+    pats = butterfly_patterns(L)
+    h2 = np.array([[1.0, 1.0], [1.0, -1.0]])
+    kvs = [np.broadcast_to(h2, (p[0] * p[3], 2, 2)).copy() for p in pats]
+    rng = np.random.default_rng(L)
+    x = rng.integers(-1, 2, size=(3, n)).astype(np.float64)
+    y = oracle.chain(pats, kvs, x, 3, "bsf")
+    H = scipy.linalg.hadamard(n).astype(np.float64)
+    np.testing.assert_array_equal(y, x @ H.T)
+    # H H^T = n I
+    eye = oracle.chain(pats, kvs, H, n, "bsf")
+    np.testing.assert_array_equal(eye, n * np.eye(n))
+
+
+def test_chain_rejects_incompatible_dims():
+    with pytest.raises(ValueError):
+        oracle.chain([(1, 4, 4, 1), (1, 3, 3, 1)], [np.ones((1, 4, 4)), np.ones((1, 3, 3))], np.ones((2, 3)), 2, "bsf")
+
+
+@pytest.mark.parametrize("pattern", [(2, 3, 5, 2), (1, 4, 2, 3), (3, 1, 2, 2)])
+def test_adjoint_identity(pattern):
+    a, b, c, d = pattern
+    rng = np.random.default_rng(23)
+    kv = rng.standard_normal((a * d, b, c))
+    x = rng.standard_normal((4, a * c * d))
+    z = rng.standard_normal((4, a * b * d))
+    y = oracle.matmul(pattern, kv, x, 4, "bsf")                                  # X K^T
+    zk = oracle.matmul((a, c, b, d), np.transpose(kv, (0, 2, 1)), z, 4, "bsf")  # Z (K^T)^T = Z K
+    assert np.isclose(np.sum(y * z), np.sum(x * zk), rtol=1e-12)
+
+
+@pytest.mark.parametrize("pattern", [(2, 4, 4, 2), (1, 3, 5, 4), (3, 2, 6, 1)])
+def test_layouts_are_transposes(pattern):
+    kv, x = rand_case(pattern, 7, seed=29)
+    y_bsf = oracle.matmul(pattern, kv, x, 7, "bsf")
+    y_bsl = oracle.matmul(pattern, kv, np.ascontiguousarray(x.T), 7, "bsl")
+    np.testing.assert_array_equal(y_bsl, y_bsf.T)
+
+
+def test_batch_permutation_permutes_rows():
+    pattern = (2, 3, 4, 2)
+    kv, x = rand_case(pattern, 8, seed=31)
+    perm = np.random.default_rng(1).permutation(8)
+    y = oracle.matmul(pattern, kv, x, 8, "bsf")
+    yp = oracle.matmul(pattern, kv, x[perm], 8, "bsf")
+    np.testing.assert_array_equal(yp, y[perm])
+
+
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_entries_match_full(layout):
+    pattern = (3, 4, 5, 2)
+    kv, x = rand_case(pattern, 11, seed=37)
+    y = inputs.from_layout(oracle.matmul(pattern, kv, inputs.to_layout(x, layout), 11, layout), layout)
+    rng = np.random.default_rng(2)
+    bi = rng.integers(0, 11, 50)
+    mi = rng.integers(0, 3 * 4 * 2, 50)
+    e = oracle.entries(pattern, kv, inputs.to_layout(x, layout), 11, layout, bi, mi)
+    np.testing.assert_array_equal(e, y[bi, mi])
+
+
+def test_empty_batch():
+    y = oracle.matmul((2, 3, 3, 2), np.ones((4, 3, 3)), np.ones((0, 12)), 0, "bsf")
+    assert y.shape == (0, 12)
+
+
+def test_inputs_rounding_is_rne():
+    # bfloat16 RNE: 1 + 2^-8 is a tie between 1 and 1 + 2^-7 -> rounds to even (1.0);
+    # 1 + 3*2^-8 is a tie between 1 + 2^-7 and 1 + 2^-6 -> rounds to even (1 + 2^-6).
+    v = np.array([1 + 2.0 ** -8, 1 + 3 * 2.0 ** -8, -2.5, 0.0])
+    bits = inputs.round_to(v, "bf16")
+    back = inputs.to_f64(bits, "bf16")
+    np.testing.assert_array_equal(back, [1.0, 1 + 2.0 ** -6, -2.5, 0.0])
+    np.testing.assert_array_equal(inputs.to_f64(inputs.round_to(v, "f16"), "f16"), np.float16(v).astype(np.float64))
