@@ -1,0 +1,241 @@
+"""MI355X (gfx950) Kronecker-sparse matrix multiplication.
+
+Python binding of libks.so.  The functions named like the C ABI
+(``ks_matmul``, ``ks_chain``, ...) only marshal arguments; every step of the
+computation runs in the library's HIP kernels.  PyTorch is used for device
+buffers and streams only.  If libks.so is missing the first call raises
+``RuntimeError``; there is no CPU fallback.
+
+Semantics (paper Section 1, Definition 2.1, Section 2.2 layouts): for a KS
+factor K of pattern (a, b, c, d) with packed values ``K_values`` of shape
+(a*d, b, c), ``ks_matmul`` computes Y = X K^T for a batch in batch-size-first
+(X: (batch, a*c*d)) or batch-size-last (X: (a*c*d, batch)) layout.
+"""
+import ctypes
+import os
+
+__all__ = [
+    "BSF", "BSL", "F32", "BF16", "F16", "KsError",
+    "ks_matmul", "ks_chain", "ks_chain_workspace_bytes", "ks_status_string",
+    "ks_last_hip_error", "ks_plan_describe", "ks_force_variant",
+    "matmul", "chain", "library_path", "load_library", "EXPORTED_SYMBOLS",
+]
+
+BSF, BSL = 0, 1
+F32, BF16, F16 = 0, 1, 2
+
+KS_OK = 0
+STATUS_NAMES = {
+    0: "KS_OK", 1: "KS_ERR_INVALID_PATTERN", 2: "KS_ERR_INVALID_ARG", 3: "KS_ERR_DIM_MISMATCH",
+    4: "KS_ERR_ALIAS", 5: "KS_ERR_UNSUPPORTED", 6: "KS_ERR_WORKSPACE", 7: "KS_ERR_HIP",
+}
+
+# Every function declared in include/ks.h.
+EXPORTED_SYMBOLS = (
+    "ks_matmul", "ks_chain_workspace_bytes", "ks_chain", "ks_status_string",
+    "ks_last_hip_error", "ks_plan_describe", "ks_force_variant",
+)
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_LIB_PATH = os.path.join(_HERE, "libks.so")
+_lib = None
+
+
+class KsError(RuntimeError):
+    """A libks call returned a status other than KS_OK."""
+
+    def __init__(self, status, where):
+        self.status = int(status)
+        self.name = STATUS_NAMES.get(self.status, str(status))
+        msg = "%s failed: %s" % (where, ks_status_string(self.status))
+        if self.status == 7:
+            msg += " (hipError_t %d)" % ks_last_hip_error()
+        super().__init__(msg)
+
+
+class _Factor(ctypes.Structure):
+    _fields_ = [("a", ctypes.c_int64), ("b", ctypes.c_int64), ("c", ctypes.c_int64),
+                ("d", ctypes.c_int64), ("K_values", ctypes.c_void_p)]
+
+
+def library_path():
+    return _LIB_PATH
+
+
+def load_library():
+    """Load libks.so (raises RuntimeError if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(_LIB_PATH):
+        raise RuntimeError("libks.so is not built (expected at %s); run "
+                           "`python -m paper_2405_15013_amd.build`" % _LIB_PATH)
+    lib = ctypes.CDLL(_LIB_PATH)
+    i64, vp, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
+    lib.ks_matmul.argtypes = [i64, i64, i64, i64, vp, vp, vp, i64, ci, ci, vp]
+    lib.ks_matmul.restype = ci
+    lib.ks_chain_workspace_bytes.argtypes = [ctypes.POINTER(_Factor), ci, i64, ci]
+    lib.ks_chain_workspace_bytes.restype = ctypes.c_size_t
+    lib.ks_chain.argtypes = [ctypes.POINTER(_Factor), ci, vp, vp, i64, ci, ci, vp, ctypes.c_size_t, vp]
+    lib.ks_chain.restype = ci
+    lib.ks_status_string.argtypes = [ci]
+    lib.ks_status_string.restype = ctypes.c_char_p
+    lib.ks_last_hip_error.argtypes = []
+    lib.ks_last_hip_error.restype = ci
+    lib.ks_plan_describe.argtypes = [i64, i64, i64, i64, i64, ci, ci, ctypes.c_char_p, ctypes.c_size_t]
+    lib.ks_plan_describe.restype = ci
+    lib.ks_force_variant.argtypes = [ci]
+    lib.ks_force_variant.restype = None
+    _lib = lib
+    return lib
+
+
+def _code(v, table, what):
+    if isinstance(v, str):
+        key = v.lower()
+        if key not in table:
+            raise ValueError("unknown %s %r" % (what, v))
+        return table[key]
+    return int(v)
+
+
+_LAYOUTS = {"bsf": BSF, "bsl": BSL}
+_DTYPES = {"f32": F32, "fp32": F32, "float32": F32, "bf16": BF16, "bfloat16": BF16, "f16": F16, "fp16": F16,
+           "float16": F16}
+
+
+def _ptr(t):
+    """Device pointer of a tensor (or an int / None passed through)."""
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def ks_status_string(status):
+    return load_library().ks_status_string(int(status)).decode()
+
+
+def ks_last_hip_error():
+    return int(load_library().ks_last_hip_error())
+
+
+def ks_force_variant(variant):
+    load_library().ks_force_variant(-1 if variant is None else int(variant))
+
+
+def ks_plan_describe(a, b, c, d, batch, layout, dtype):
+    buf = ctypes.create_string_buffer(512)
+    st = load_library().ks_plan_describe(a, b, c, d, batch, _code(layout, _LAYOUTS, "layout"),
+                                         _code(dtype, _DTYPES, "dtype"), buf, 512)
+    if st != KS_OK:
+        raise KsError(st, "ks_plan_describe")
+    return buf.value.decode()
+
+
+def ks_matmul(a, b, c, d, K_values, X, Y, batch, layout, dtype, stream=None, check=True):
+    """C-ABI ks_matmul: tensors (or raw device pointers) are passed as pointers."""
+    st = load_library().ks_matmul(a, b, c, d, _ptr(K_values), _ptr(X), _ptr(Y), batch,
+                                  _code(layout, _LAYOUTS, "layout"), _code(dtype, _DTYPES, "dtype"),
+                                  _stream(stream))
+    if check and st != KS_OK:
+        raise KsError(st, "ks_matmul")
+    return st
+
+
+def _factor_array(factors):
+    arr = (_Factor * len(factors))()
+    for q, f in enumerate(factors):
+        (a, b, c, d), kv = f
+        arr[q] = _Factor(a, b, c, d, _ptr(kv))
+    return arr
+
+
+def ks_chain_workspace_bytes(factors, batch, dtype):
+    """factors: sequence of ((a, b, c, d), K_values) in product order."""
+    arr = _factor_array(factors)
+    return int(load_library().ks_chain_workspace_bytes(arr, len(factors), batch, _code(dtype, _DTYPES, "dtype")))
+
+
+def ks_chain(factors, X, Y, batch, layout, dtype, workspace, workspace_bytes, stream=None, check=True):
+    """C-ABI ks_chain: Y = X (K_1 ... K_L)^T, factors in product order."""
+    arr = _factor_array(factors)
+    st = load_library().ks_chain(arr, len(factors), _ptr(X), _ptr(Y), batch, _code(layout, _LAYOUTS, "layout"),
+                                 _code(dtype, _DTYPES, "dtype"), _ptr(workspace), int(workspace_bytes),
+                                 _stream(stream))
+    if check and st != KS_OK:
+        raise KsError(st, "ks_chain")
+    return st
+
+
+_TORCH_DTYPE_CODES = None
+
+
+def _dtype_of(t):
+    global _TORCH_DTYPE_CODES
+    import torch
+    if _TORCH_DTYPE_CODES is None:
+        _TORCH_DTYPE_CODES = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
+    if t.dtype not in _TORCH_DTYPE_CODES:
+        raise TypeError("unsupported dtype %s" % t.dtype)
+    return _TORCH_DTYPE_CODES[t.dtype]
+
+
+def _check_tensor(t, name):
+    if not t.is_cuda:
+        raise ValueError("%s must be a device tensor" % name)
+    if not t.is_contiguous():
+        raise ValueError("%s must be contiguous" % name)
+
+
+def matmul(X, K_values, pattern, layout="bsl", out=None):
+    """Allocate Y and run ks_matmul.  X is (batch, a*c*d) for BSF or (a*c*d, batch)
+    for BSL; K_values is (a*d, b, c) or flat; all three share one dtype."""
+    import torch
+    a, b, c, d = (int(v) for v in pattern)
+    lay = _code(layout, _LAYOUTS, "layout")
+    _check_tensor(X, "X")
+    _check_tensor(K_values, "K_values")
+    if X.dtype != K_values.dtype:
+        raise TypeError("X and K_values must share a dtype")
+    N, M = a * c * d, a * b * d
+    if X.numel() % N:
+        raise ValueError("X has %d elements, not a multiple of N = %d" % (X.numel(), N))
+    batch = X.numel() // N
+    if X.dim() == 2 and X.shape != ((batch, N) if lay == BSF else (N, batch)):
+        raise ValueError("X has shape %s, expected %s" % (tuple(X.shape), (batch, N) if lay == BSF else (N, batch)))
+    shape = (batch, M) if lay == BSF else (M, batch)
+    if out is None:
+        out = torch.empty(shape, dtype=X.dtype, device=X.device)
+    ks_matmul(a, b, c, d, K_values, X, out, batch, lay, _dtype_of(X))
+    return out
+
+
+def chain(X, factors, layout="bsl", out=None, workspace=None):
+    """Y = X (K_1 ... K_L)^T; factors = [((a,b,c,d), K_values), ...] in product order."""
+    import torch
+    lay = _code(layout, _LAYOUTS, "layout")
+    _check_tensor(X, "X")
+    (a1, b1, c1, d1), _ = factors[0]
+    (aL, bL, cL, dL), _ = factors[-1]
+    N, M = aL * cL * dL, a1 * b1 * d1
+    batch = X.numel() // N
+    dt = _dtype_of(X)
+    ws_bytes = ks_chain_workspace_bytes(factors, batch, dt)
+    if workspace is None and ws_bytes > 0:
+        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=X.device)
+    if out is None:
+        out = torch.empty((batch, M) if lay == BSF else (M, batch), dtype=X.dtype, device=X.device)
+    ws_avail = workspace.numel() * workspace.element_size() if workspace is not None else 0
+    ks_chain(factors, X, out, batch, lay, dt, workspace, ws_avail)
+    return out

@@ -1,0 +1,374 @@
+// Host side of libks: argument validation, the tiling planner and plan cache,
+// the C ABI entry points and the chain driver.
+//
+// Every check runs on the host before anything is enqueued, so each error path
+// can be exercised without a GPU.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <unordered_map>
+
+#include "../../include/ks.h"
+#include "ks_internal.h"
+
+namespace ks {
+namespace {
+
+thread_local int g_last_hip_error = 0;
+thread_local int g_forced_variant = -1;
+
+constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
+
+int elem_size(int dtype) { return dtype == F32 ? 4 : 2; }
+
+bool mul_ok(int64_t x, int64_t y, int64_t* out) { return !__builtin_mul_overflow(x, y, out); }
+
+// Pattern sizes with overflow checks.
+struct Dims {
+  int64_t N = 0, M = 0, nnz = 0;
+};
+
+ks_status_t check_pattern(int64_t a, int64_t b, int64_t c, int64_t d, Dims* dims) {
+  if (a < 1 || b < 1 || c < 1 || d < 1) return KS_ERR_INVALID_PATTERN;
+  int64_t ad, N, M, nnz;
+  if (!mul_ok(a, d, &ad) || !mul_ok(ad, c, &N) || !mul_ok(ad, b, &M) || !mul_ok(M, c, &nnz))
+    return KS_ERR_INVALID_PATTERN;
+  dims->N = N;
+  dims->M = M;
+  dims->nnz = nnz;
+  return KS_OK;
+}
+
+bool overlaps(const void* p, int64_t pbytes, const void* q, int64_t qbytes) {
+  if (pbytes <= 0 || qbytes <= 0) return false;
+  const uintptr_t a0 = reinterpret_cast<uintptr_t>(p), a1 = a0 + (uintptr_t)pbytes;
+  const uintptr_t b0 = reinterpret_cast<uintptr_t>(q), b1 = b0 + (uintptr_t)qbytes;
+  return a0 < b1 && b0 < a1;
+}
+
+bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// ---------------------------------------------------------------------------
+// Planner.  Each variant planner fills `pl` and returns true when the variant
+// can run the problem.
+// ---------------------------------------------------------------------------
+
+bool plan_generic(const Problem& p, Plan* pl) {
+  pl->variant = V_GENERIC;
+  const int64_t total = (int64_t)p.batch * p.M;
+  const int64_t blocks = (total + 255) / 256;
+  pl->block = 256;
+  pl->grid = (unsigned)std::max<int64_t>(1, std::min<int64_t>(blocks, 256 * 64));
+  return true;
+}
+
+// Batch-size-last VALU streaming: b, c <= 16; 16-byte vectors along the batch
+// when the batch is a multiple of the vector width and the buffers are
+// 16-byte aligned, single elements otherwise.
+bool plan_valu_bsl(const Problem& p, bool al16, Plan* pl) {
+  if (p.layout != BSL || p.b > kValuMaxBC || p.c > kValuMaxBC) return false;
+  if ((int64_t)p.a * p.d > 65535) return false;
+  const int vec16 = 16 / elem_size(p.dtype);
+  const int vec = (al16 && p.batch % vec16 == 0) ? vec16 : 1;
+  const int u = valu_bsl_unroll(p.b, p.c);
+  const int nvec = p.batch / vec;
+  pl->variant = V_VALU_BSL;
+  pl->vec = vec;
+  pl->unroll = u;
+  pl->block = 256;
+  pl->grid = (unsigned)((nvec + 256 * u - 1) / (256 * u));
+  return true;
+}
+
+// Batch-size-first VALU: b, c <= 16; a thread owns V consecutive j, V the
+// largest power of two dividing d that fits a 16-byte vector (given alignment).
+bool plan_valu_bsf(const Problem& p, bool al16, Plan* pl) {
+  if (p.layout != BSF || p.b > kValuMaxBC || p.c > kValuMaxBC) return false;
+  const int vec16 = 16 / elem_size(p.dtype);
+  int v = 1;
+  if (al16)
+    while (v * 2 <= vec16 && p.d % (v * 2) == 0) v *= 2;
+  const int64_t total = (int64_t)p.batch * p.a * (p.d / v);
+  const int64_t blocks = (total + 255) / 256;
+  if (blocks > 0x7fffffff) return false;
+  pl->variant = V_VALU_BSF;
+  pl->vec = v;
+  pl->block = 256;
+  pl->grid = (unsigned)blocks;
+  return true;
+}
+
+bool plan_mfma(const Problem& p, bool al16, Plan* pl);
+
+bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
+  switch (v) {
+    case V_GENERIC: return plan_generic(p, pl);
+    case V_VALU_BSL: return plan_valu_bsl(p, al16, pl);
+    case V_VALU_BSF: return plan_valu_bsf(p, al16, pl);
+    case V_MFMA: return plan_mfma(p, al16, pl);
+    default: return false;
+  }
+}
+
+// Automatic choice: MFMA block GEMM when b and c make each (i, j) block a real
+// dense contraction; VALU kernels for small blocks; the generic kernel for
+// whatever is left.
+bool plan_auto(const Problem& p, bool al16, Plan* pl) {
+  if (plan_mfma(p, al16, pl)) return true;
+  if (p.layout == BSL && plan_valu_bsl(p, al16, pl)) return true;
+  if (p.layout == BSF && plan_valu_bsf(p, al16, pl)) return true;
+  return plan_generic(p, pl);
+}
+
+struct PlanKey {
+  int64_t a, b, c, d, batch;
+  int layout, dtype, al16, forced;
+  bool operator==(const PlanKey& o) const {
+    return a == o.a && b == o.b && c == o.c && d == o.d && batch == o.batch && layout == o.layout &&
+           dtype == o.dtype && al16 == o.al16 && forced == o.forced;
+  }
+};
+struct PlanKeyHash {
+  size_t operator()(const PlanKey& k) const {
+    uint64_t h = 1469598103934665603ull;
+    const int64_t v[9] = {k.a, k.b, k.c, k.d, k.batch, k.layout, k.dtype, k.al16, k.forced};
+    for (int64_t x : v) { h ^= (uint64_t)x; h *= 1099511628211ull; }
+    return (size_t)h;
+  }
+};
+
+std::mutex g_plan_mu;
+std::unordered_map<PlanKey, Plan, PlanKeyHash>* g_plans = nullptr;
+
+// Returns false when a forced variant cannot run the problem.
+bool get_plan(const Problem& p, bool al16, Plan* out) {
+  const int forced = g_forced_variant;
+  PlanKey key{p.a, p.b, p.c, p.d, p.batch, p.layout, p.dtype, al16 ? 1 : 0, forced};
+  {
+    std::lock_guard<std::mutex> lk(g_plan_mu);
+    if (!g_plans) g_plans = new std::unordered_map<PlanKey, Plan, PlanKeyHash>();
+    auto it = g_plans->find(key);
+    if (it != g_plans->end()) { *out = it->second; return true; }
+  }
+  Plan pl;
+  bool ok = forced >= 0 ? plan_variant(forced, p, al16, &pl) : plan_auto(p, al16, &pl);
+  if (!ok) return false;
+  std::lock_guard<std::mutex> lk(g_plan_mu);
+  (*g_plans)[key] = pl;
+  *out = pl;
+  return true;
+}
+
+hipError_t launch(const Problem& p, const Plan& pl, hipStream_t s) {
+  switch (pl.variant) {
+    case V_GENERIC: return launch_generic(p, pl, s);
+    case V_VALU_BSL: return launch_valu_bsl(p, pl, s);
+    case V_VALU_BSF: return launch_valu_bsf(p, pl, s);
+    case V_MFMA: return launch_mfma(p, pl, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// Full validation of a single-factor call; fills `p` on success.
+ks_status_t validate(int64_t a, int64_t b, int64_t c, int64_t d, const void* kv, const void* x, void* y,
+                     int64_t batch, int layout, int dtype, Problem* p, bool* empty) {
+  Dims dm;
+  ks_status_t st = check_pattern(a, b, c, d, &dm);
+  if (st != KS_OK) return st;
+  if (layout != KS_LAYOUT_BSF && layout != KS_LAYOUT_BSL) return KS_ERR_UNSUPPORTED;
+  if (dtype != KS_F32 && dtype != KS_BF16 && dtype != KS_F16) return KS_ERR_UNSUPPORTED;
+  if (batch < 0) return KS_ERR_INVALID_ARG;
+  if (kv == nullptr) return KS_ERR_INVALID_ARG;
+  *empty = (batch == 0);
+  if (*empty) return KS_OK;
+  if (x == nullptr || y == nullptr) return KS_ERR_INVALID_ARG;
+  int64_t xe, ye;
+  if (!mul_ok(batch, dm.N, &xe) || !mul_ok(batch, dm.M, &ye)) return KS_ERR_UNSUPPORTED;
+  if (xe > kMaxElems || ye > kMaxElems || dm.nnz > kMaxElems || batch > kMaxElems) return KS_ERR_UNSUPPORTED;
+  const int s = elem_size(dtype);
+  if (overlaps(x, xe * s, y, ye * s)) return KS_ERR_ALIAS;
+  if (overlaps(kv, dm.nnz * s, y, ye * s)) return KS_ERR_ALIAS;
+  p->a = (int)a; p->b = (int)b; p->c = (int)c; p->d = (int)d;
+  p->batch = (int)batch;
+  p->N = (int)dm.N; p->M = (int)dm.M;
+  p->layout = layout; p->dtype = dtype;
+  p->kv = kv; p->x = x; p->y = y;
+  return KS_OK;
+}
+
+bool all_aligned(const Problem& p) { return aligned16(p.kv) && aligned16(p.x) && aligned16(p.y); }
+
+ks_status_t run_one(const Problem& p, hipStream_t s) {
+  Plan pl;
+  if (!get_plan(p, all_aligned(p), &pl)) return KS_ERR_UNSUPPORTED;
+  hipError_t e = launch(p, pl, s);
+  if (e != hipSuccess) {
+    g_last_hip_error = (int)e;
+    return KS_ERR_HIP;
+  }
+  return KS_OK;
+}
+
+std::string describe(const Plan& pl) {
+  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "mfma"};
+  char buf[320];
+  snprintf(buf, sizeof buf,
+           "variant=%d name=%s vec=%d bt=%d jg=%d unroll=%d waves_m=%d waves_n=%d lds=%d grid=%u block=%u xcd=%d",
+           pl.variant, (pl.variant >= 0 && pl.variant < V_COUNT) ? names[pl.variant] : "?", pl.vec, pl.bt, pl.jg,
+           pl.unroll, pl.waves_m, pl.waves_n, pl.lds_bytes, pl.grid, pl.block, pl.xcd_remap);
+  return buf;
+}
+
+constexpr size_t kWsAlign = 256;
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Bytes of one intermediate buffer of the chain (largest intermediate width),
+// or 0 if the arguments are invalid.
+ks_status_t chain_check(const ks_factor_t* f, int n, int64_t batch, int dtype, size_t* per_buf) {
+  if (f == nullptr || n < 1) return KS_ERR_INVALID_ARG;
+  if (dtype != KS_F32 && dtype != KS_BF16 && dtype != KS_F16) return KS_ERR_UNSUPPORTED;
+  if (batch < 0) return KS_ERR_INVALID_ARG;
+  int64_t widest = 0;
+  for (int q = 0; q < n; ++q) {
+    Dims dm;
+    ks_status_t st = check_pattern(f[q].a, f[q].b, f[q].c, f[q].d, &dm);
+    if (st != KS_OK) return st;
+    if (q + 1 < n) {
+      Dims nx;
+      st = check_pattern(f[q + 1].a, f[q + 1].b, f[q + 1].c, f[q + 1].d, &nx);
+      if (st != KS_OK) return st;
+      if (dm.N != nx.M) return KS_ERR_DIM_MISMATCH;
+      widest = std::max(widest, dm.N);  // output of factor q+1 = input of factor q
+    }
+  }
+  int64_t elems;
+  if (!mul_ok(widest, batch, &elems) || elems > kMaxElems) return KS_ERR_UNSUPPORTED;
+  *per_buf = round_up((size_t)elems * (size_t)elem_size(dtype), kWsAlign);
+  return KS_OK;
+}
+
+}  // namespace
+}  // namespace ks
+
+using namespace ks;
+
+extern "C" {
+
+ks_status_t ks_matmul(int64_t a, int64_t b, int64_t c, int64_t d, const void* K_values, const void* X, void* Y,
+                      int64_t batch, int layout, int dtype, void* stream) {
+  Problem p;
+  bool empty = false;
+  ks_status_t st = validate(a, b, c, d, K_values, X, Y, batch, layout, dtype, &p, &empty);
+  if (st != KS_OK || empty) return st;
+  return run_one(p, static_cast<hipStream_t>(stream));
+}
+
+size_t ks_chain_workspace_bytes(const ks_factor_t* factors, int nfactors, int64_t batch, int dtype) {
+  size_t per = 0;
+  if (chain_check(factors, nfactors, batch, dtype, &per) != KS_OK) return 0;
+  if (nfactors <= 1) return 0;
+  return nfactors == 2 ? per : 2 * per;
+}
+
+ks_status_t ks_chain(const ks_factor_t* factors, int nfactors, const void* X, void* Y, int64_t batch, int layout,
+                     int dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  size_t per = 0;
+  ks_status_t st = chain_check(factors, nfactors, batch, dtype, &per);
+  if (st != KS_OK) return st;
+  if (layout != KS_LAYOUT_BSF && layout != KS_LAYOUT_BSL) return KS_ERR_UNSUPPORTED;
+  for (int q = 0; q < nfactors; ++q)
+    if (factors[q].K_values == nullptr) return KS_ERR_INVALID_ARG;
+  if (batch == 0) return KS_OK;
+  if (X == nullptr || Y == nullptr) return KS_ERR_INVALID_ARG;
+  const size_t need = nfactors <= 1 ? 0 : (nfactors == 2 ? per : 2 * per);
+  if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return KS_ERR_WORKSPACE;
+  const int s = elem_size(dtype);
+  Dims first, last;
+  check_pattern(factors[0].a, factors[0].b, factors[0].c, factors[0].d, &first);
+  check_pattern(factors[nfactors - 1].a, factors[nfactors - 1].b, factors[nfactors - 1].c,
+                factors[nfactors - 1].d, &last);
+  int64_t xe, ye;
+  if (!mul_ok(batch, last.N, &xe) || !mul_ok(batch, first.M, &ye) || xe > kMaxElems || ye > kMaxElems)
+    return KS_ERR_UNSUPPORTED;
+  if (overlaps(X, xe * s, Y, ye * s)) return KS_ERR_ALIAS;
+  if (need > 0 && (overlaps(workspace, (int64_t)need, X, xe * s) || overlaps(workspace, (int64_t)need, Y, ye * s)))
+    return KS_ERR_ALIAS;
+  // Validate every step before enqueueing anything.
+  char* ws = static_cast<char*>(workspace);
+  void* bufs[2] = {ws, ws + per};
+  Problem steps[64];
+  Problem* pv = nfactors <= 64 ? steps : new Problem[nfactors];
+  const void* in = X;
+  int which = 0;
+  for (int q = nfactors - 1; q >= 0; --q) {
+    void* out = (q == 0) ? Y : bufs[which];
+    bool empty = false;
+    st = validate(factors[q].a, factors[q].b, factors[q].c, factors[q].d, factors[q].K_values, in, out, batch, layout,
+                  dtype, &pv[q], &empty);
+    if (st != KS_OK) break;
+    in = out;
+    which ^= 1;
+  }
+  if (st == KS_OK) {
+    for (int q = nfactors - 1; q >= 0 && st == KS_OK; --q) st = run_one(pv[q], static_cast<hipStream_t>(stream));
+  }
+  if (pv != steps) delete[] pv;
+  return st;
+}
+
+const char* ks_status_string(int status) {
+  switch (status) {
+    case KS_OK: return "KS_OK";
+    case KS_ERR_INVALID_PATTERN: return "KS_ERR_INVALID_PATTERN: a, b, c and d must be >= 1 and their products fit int64";
+    case KS_ERR_INVALID_ARG: return "KS_ERR_INVALID_ARG: null pointer, negative batch or bad factor count";
+    case KS_ERR_DIM_MISMATCH: return "KS_ERR_DIM_MISMATCH: chain factors do not compose (a*c*d of one != a*b*d of next)";
+    case KS_ERR_ALIAS: return "KS_ERR_ALIAS: output overlaps an input or the workspace";
+    case KS_ERR_UNSUPPORTED: return "KS_ERR_UNSUPPORTED: unsupported dtype/layout/size, or forced variant cannot run";
+    case KS_ERR_WORKSPACE: return "KS_ERR_WORKSPACE: chain workspace missing or too small";
+    case KS_ERR_HIP: return "KS_ERR_HIP: the HIP runtime reported an error";
+    default: return "unknown ks_status_t";
+  }
+}
+
+int ks_last_hip_error(void) { return g_last_hip_error; }
+
+ks_status_t ks_plan_describe(int64_t a, int64_t b, int64_t c, int64_t d, int64_t batch, int layout, int dtype,
+                             char* buf, size_t len) {
+  if (buf == nullptr || len == 0) return KS_ERR_INVALID_ARG;
+  buf[0] = 0;
+  // Validate with stand-in, 256-byte-aligned, non-overlapping addresses: the plan
+  // depends on pointer alignment only, and aligned buffers are the common case.
+  Dims dm;
+  ks_status_t st = check_pattern(a, b, c, d, &dm);
+  if (st != KS_OK) return st;
+  const uintptr_t base = uintptr_t(1) << 44;
+  const uintptr_t span = uintptr_t(1) << 40;
+  Problem p;
+  bool empty = false;
+  st = validate(a, b, c, d, reinterpret_cast<const void*>(base), reinterpret_cast<const void*>(base + span),
+                reinterpret_cast<void*>(base + 2 * span), batch, layout, dtype, &p, &empty);
+  if (st != KS_OK) return st;
+  if (empty) {
+    snprintf(buf, len, "empty");
+    return KS_OK;
+  }
+  Plan pl;
+  if (!get_plan(p, true, &pl)) return KS_ERR_UNSUPPORTED;
+  snprintf(buf, len, "%s", describe(pl).c_str());
+  return KS_OK;
+}
+
+void ks_force_variant(int variant) { g_forced_variant = variant < 0 ? -1 : variant; }
+
+}  // extern "C"
+
+namespace ks {
+bool plan_mfma_impl(const Problem& p, bool al16, Plan* pl);
+namespace {
+bool plan_mfma(const Problem& p, bool al16, Plan* pl) { return plan_mfma_impl(p, al16, pl); }
+}  // namespace
+}  // namespace ks

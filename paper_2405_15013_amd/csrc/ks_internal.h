@@ -1,0 +1,68 @@
+// Internal interface between the host planner (ks_host.cpp) and the HIP
+// kernels (ks_kernels.hip).  Not part of the public ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+namespace ks {
+
+enum Layout : int { BSF = 0, BSL = 1 };
+enum Dtype : int { F32 = 0, BF16 = 1, F16 = 2 };
+
+// Kernel variants (the numbering is the "variant=" field of ks_plan_describe
+// and the argument of ks_force_variant).
+enum Variant : int {
+  V_GENERIC = 0,   // one thread per output element, any pattern
+  V_VALU_BSL = 1,  // VALU streaming, batch-size-last, small b and c
+  V_VALU_BSF = 2,  // VALU, batch-size-first, small b and c
+  V_MFMA = 3,      // MFMA block GEMM, both layouts, b and c multiples of 16
+  V_COUNT = 4
+};
+
+// Problem description shared by all kernels.  Sizes fit in int32 (checked by
+// the host: every tensor has < 2^31 elements).
+struct Problem {
+  int a, b, c, d;
+  int batch;
+  int N, M;      // a*c*d, a*b*d
+  int layout;
+  int dtype;
+  const void* kv;
+  const void* x;
+  void* y;
+};
+
+// Launch description produced by the planner.
+struct Plan {
+  int variant = V_GENERIC;
+  // variant-specific tile parameters
+  int vec = 1;      // elements per memory vector along the contiguous dimension
+  int bt = 0;       // batch rows (BSF) / batch columns (BSL) per workgroup tile
+  int jg = 1;       // j values per workgroup (BSF MFMA / VALU)
+  int unroll = 1;   // vectors per thread (VALU)
+  int waves_m = 1;  // MFMA: waves along the output-channel (k) dimension
+  int waves_n = 1;  // MFMA: waves along the batch dimension
+  int lds_bytes = 0;
+  unsigned grid = 1;
+  unsigned block = 256;
+  int xcd_remap = 0;  // remap blockIdx so neighbouring tiles share an XCD
+};
+
+// Each launcher enqueues one kernel and returns the hipError_t of the launch.
+hipError_t launch_generic(const Problem& p, const Plan& pl, hipStream_t s);
+hipError_t launch_valu_bsl(const Problem& p, const Plan& pl, hipStream_t s);
+hipError_t launch_valu_bsf(const Problem& p, const Plan& pl, hipStream_t s);
+hipError_t launch_mfma(const Problem& p, const Plan& pl, hipStream_t s);
+
+}  // namespace ks
+
+namespace ks {
+// Vectors per thread of the batch-size-last VALU kernel for a given block
+// shape (shared by the planner, which sizes the grid, and the launcher, which
+// picks the kernel instance).
+inline int valu_bsl_unroll(int b, int c) {
+  const int m = b > c ? b : c;
+  return m <= 2 ? 4 : (m <= 4 ? 2 : 1);
+}
+constexpr int kValuMaxBC = 16;
+}  // namespace ks

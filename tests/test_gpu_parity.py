@@ -1,0 +1,169 @@
+"""GPU parity: the HIP path (through the C ABI) against the fp64 CPU oracle on
+the same seeded inputs, for every workload family of the benchmark and the
+edge cases of the method.  Outputs are pre-filled with NaN so that an element
+a kernel fails to write shows up as an infinite error."""
+import numpy as np
+import pytest
+
+import oracle
+import paper_2405_15013_amd as ks
+from paper_2405_15013_amd import inputs
+from parity_util import TOL, case, from_device, nan_tensor, oracle_y, rel_err, to_device
+
+pytestmark = pytest.mark.gpu
+
+VARIANTS = {"generic": 0, "valu_bsl": 1, "valu_bsf": 2, "mfma": 3}
+
+
+def run_gpu(pattern, x_logical, kv, batch, dtype, layout, variant=None, x_offset=0, y_offset=0):
+    """Lay out X, run ks_matmul on the device, return Y in logical (batch, M) order.
+    x_offset / y_offset shift the buffers by that many elements (alignment tests)."""
+    import torch
+    a, b, c, d = pattern
+    M = a * b * d
+    xd_full = to_device(np.concatenate([np.zeros(x_offset, dtype=x_logical.dtype),
+                                        inputs.to_layout(x_logical, layout).reshape(-1)]), dtype)
+    xd = xd_full[x_offset:]
+    kd = to_device(kv, dtype)
+    yd_full = nan_tensor((y_offset + batch * M,), dtype)
+    yd = yd_full[y_offset:]
+    ks.ks_force_variant(variant)
+    try:
+        ks.ks_matmul(a, b, c, d, kd, xd, yd, batch, layout, dtype)
+    finally:
+        ks.ks_force_variant(None)
+    torch.cuda.synchronize()
+    y = from_device(yd, dtype)
+    y = y.reshape((batch, M) if layout == "bsf" else (M, batch))
+    return inputs.from_layout(y, layout)
+
+
+def check(pattern, batch, dtype, layout, cfg=0, variant=None, xdist="normal", kdist="uniform_c", tol=None, **kw):
+    x, kv, _, _ = case(cfg, pattern, batch, dtype, xdist, kdist)
+    y = run_gpu(pattern, x, kv, batch, dtype, layout, variant=variant, **kw)
+    y64 = oracle_y(cfg, pattern, batch, dtype, xdist, kdist)
+    err = rel_err(y, y64)
+    assert err <= (TOL[dtype] if tol is None else tol), "pattern %s batch %d %s %s variant %s: rel err %.3e" % (
+        pattern, batch, dtype, layout, variant, err)
+    return err
+
+
+# --- tiny: (2,4,4,2), B = 32, K is 16 x 16 with 64 nonzeros ------------------
+
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("variant", [None, "generic", "valu"])
+def test_tiny(layout, dtype, variant):
+    v = None if variant is None else (0 if variant == "generic" else (1 if layout == "bsl" else 2))
+    check((2, 4, 4, 2), 32, dtype, layout, cfg=1, variant=v, kdist="normal")
+
+
+# --- butterfly factors for N = 1024, B = 4096 --------------------------------
+
+BUTTERFLY = [(2 ** (l - 1), 2, 2, 2 ** (10 - l)) for l in range(1, 11)]
+
+
+@pytest.mark.parametrize("pattern", BUTTERFLY)
+@pytest.mark.parametrize("layout", ["bsl", "bsf"])
+def test_butterfly_single(pattern, layout):
+    check(pattern, 4096, "f32", layout, cfg=2, kdist="normal")
+
+
+@pytest.mark.parametrize("layout", ["bsl", "bsf"])
+def test_butterfly_chain(layout):
+    import torch
+    batch = 4096
+    pats = BUTTERFLY
+    x = inputs.make_x(2, pats[-1], batch, "f32")
+    kvs = [inputs.make_kv(2, p, batch, "f32", dist="normal", factor=f) for f, p in enumerate(pats)]
+    kds = [to_device(k, "f32") for k in kvs]
+    xd = to_device(inputs.to_layout(x, layout), "f32")
+    y = ks.chain(xd, [(p, k) for p, k in zip(pats, kds)], layout=layout)
+    torch.cuda.synchronize()
+    y = inputs.from_layout(from_device(y, "f32"), layout)
+    y64 = oracle.chain(pats, [inputs.to_f64(k, "f32") for k in kvs], x.astype(np.float64), batch, "bsf")
+    assert rel_err(y, y64) <= TOL["f32"]
+
+
+@pytest.mark.parametrize("layout", ["bsl", "bsf"])
+def test_butterfly_chain_hadamard_bit_exact(layout):
+    """All blocks [[1,1],[1,-1]] and inputs in {-1,0,1}: every intermediate is a
+    small integer, exact in fp32, so the result must equal X H exactly."""
+    import scipy.linalg
+    import torch
+    batch = 4096
+    pats = BUTTERFLY
+    x = inputs.make_x(2, pats[-1], batch, "f32", dist="sign")
+    h2 = np.array([[1, 1], [1, -1]], dtype=np.float32)
+    kds = [to_device(np.broadcast_to(h2, (p[0] * p[3], 2, 2)).copy(), "f32") for p in pats]
+    xd = to_device(inputs.to_layout(x, layout), "f32")
+    y = ks.chain(xd, list(zip(pats, kds)), layout=layout)
+    torch.cuda.synchronize()
+    y = inputs.from_layout(from_device(y, "f32"), layout)
+    H = scipy.linalg.hadamard(1024).astype(np.float64)
+    np.testing.assert_array_equal(y, x.astype(np.float64) @ H)
+
+
+# --- Monarch factors for N = 1024, B = 16384 ---------------------------------
+
+MONARCH = [(1, 32, 32, 32), (32, 32, 32, 1)]
+
+
+@pytest.mark.parametrize("pattern", MONARCH)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_monarch_single(pattern, dtype, layout):
+    check(pattern, 16384, dtype, layout, cfg=3, kdist="normal_c")
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_monarch_chain(dtype, layout):
+    import torch
+    batch = 16384
+    x = inputs.make_x(3, MONARCH[-1], batch, dtype)
+    kvs = [inputs.make_kv(3, p, batch, dtype, dist="normal_c", factor=f) for f, p in enumerate(MONARCH)]
+    xd = to_device(inputs.to_layout(x, layout), dtype)
+    y = ks.chain(xd, [(p, to_device(k, dtype)) for p, k in zip(MONARCH, kvs)], layout=layout)
+    torch.cuda.synchronize()
+    y = inputs.from_layout(from_device(y, dtype).reshape(y.shape), layout)
+    y64 = oracle.chain(MONARCH, [inputs.to_f64(k, dtype) for k in kvs], inputs.to_f64(x, dtype), batch, "bsf")
+    assert rel_err(y, y64) <= TOL[dtype]
+
+
+# --- Transformer-MLP-shaped layers, B = 25088 --------------------------------
+
+MLP = [(6, 64, 16, 8), (6, 16, 64, 8)]
+
+
+@pytest.mark.parametrize("pattern", MLP)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_mlp(pattern, dtype, layout):
+    check(pattern, 25088, dtype, layout, cfg=4)
+
+
+# --- edge cases ---------------------------------------------------------------
+
+@pytest.mark.parametrize("pattern", [(3, 5, 7, 2), (1, 17, 33, 3), (2, 1, 1, 5), (5, 3, 2, 1), (1, 20, 12, 1),
+                                     (2, 16, 16, 3), (1, 48, 32, 5), (4, 32, 16, 1)])
+@pytest.mark.parametrize("batch", [1, 37, 130])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_odd_shapes(pattern, batch, layout):
+    check(pattern, batch, "f32", layout, cfg=5)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+@pytest.mark.parametrize("pattern", [(2, 4, 4, 2), (1, 32, 32, 4), (2, 2, 2, 8)])
+def test_unaligned_buffers(dtype, layout, pattern):
+    check(pattern, 64, dtype, layout, cfg=6, x_offset=1, y_offset=3)
+
+
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_empty_batch(layout):
+    import torch
+    kd = to_device(np.ones((4, 3, 3), dtype=np.float32), "f32")
+    x = torch.empty(0, device="cuda")
+    y = torch.empty(0, device="cuda")
+    assert ks.ks_matmul(2, 3, 3, 2, kd, x, y, 0, layout, "f32") == 0
