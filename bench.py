@@ -1,0 +1,365 @@
+#!/usr/bin/env python3
+"""Benchmark of the MI355X Kronecker-sparse matmul (Y = X K^T, K with support
+I_a (x) 1_{b x c} (x) I_d) against the MI355X roofline.
+
+Workload (the metric is the median over it): the pattern sweep
+a in {1,2,4,8}, b, c in {16,32,48,64,96,128}, d in {1,2,4,8,16} with
+a*b*d <= 8192 and a*c*d <= 8192 (700 patterns), batch B in {4096, 25088},
+fp32 and bf16 (fp32 accumulate), batch-size-first and batch-size-last:
+5600 points.  X and K are i.i.d. N(0, 1), synthetic.
+
+Per point the fused method's minimum traffic (X read once, K read once, Y
+written once; paper Section 4.3) and work are
+    bytes = (B*N + B*M + a*b*c*d) * s,    flops = 2 * B * a*b*c*d,
+the roof time is max(bytes / 8.0 TB/s, flops / peak) with peak = 157.3 TFLOP/s
+(fp32) or 2516.6 TFLOP/s (bf16 MFMA), and the point's fraction of roofline is
+roof time / measured time.
+
+Timing: every point gets a launch graph of L ks_matmul calls, each on its own
+buffer set taken from a rotating pool so that >= 768 MB (three times the
+256 MB Infinity Cache) pass between two uses of the same buffers (L capped at
+256 for the smallest points).  After --warmup untimed replays, --steps replays
+are bracketed by HIP events on the replay stream; the point's time is the
+elapsed time / (steps * L).  A "step" is one pass over the whole sweep, so
+ms_per_step is the sum of the per-point times.
+
+Also reported: the same measurements for the other workload families (tiny,
+butterfly factors and 10-chain, Monarch factors and 2-chain, Transformer-MLP
+layers) as context, the dominant kernel's roofline and the fp64 CPU oracle
+timed on a bounded sample on the host cores (cpu_baseline).
+
+Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--sample S]
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "KS matmul achieved GB/s & TFLOP/s, fraction of roofline (median over patterns)"
+HBM_BW = 8.0e12
+PEAK = {"f32": 157.3e12, "bf16": 2516.6e12, "f16": 2516.6e12}
+ESIZE = {"f32": 4, "bf16": 2, "f16": 2}
+POOL_BYTES = 3 << 30
+ROTATE_BYTES = 768 << 20
+MAX_LAUNCHES = 256
+
+
+def sweep_patterns():
+    pats = []
+    for a in (1, 2, 4, 8):
+        for b in (16, 32, 48, 64, 96, 128):
+            for c in (16, 32, 48, 64, 96, 128):
+                for d in (1, 2, 4, 8, 16):
+                    if a * b * d <= 8192 and a * c * d <= 8192:
+                        pats.append((a, b, c, d))
+    return pats
+
+
+def roof(pattern, batch, dtype):
+    a, b, c, d = pattern
+    nnz = a * b * c * d
+    nbytes = (batch * a * c * d + batch * a * b * d + nnz) * ESIZE[dtype]
+    flops = 2.0 * batch * nnz
+    t_hbm = nbytes / HBM_BW
+    t_flop = flops / PEAK[dtype]
+    return nbytes, flops, max(t_hbm, t_flop), ("hbm" if t_hbm >= t_flop else "mfma")
+
+
+def kernel_key(desc, dtype, layout):
+    f = dict(kv.split("=", 1) for kv in desc.split())
+    name = f["name"]
+    if name == "mfma":
+        return "ks_mfma_kernel<%s,%s,NT=%s,MT=%s>" % (dtype, layout, f["waves_n"], f["waves_m"])
+    return "ks_%s_kernel<%s>" % (name, dtype)
+
+
+class Runner:
+    def __init__(self, steps, warmup):
+        import torch
+        import paper_2405_15013_amd as ks
+        if not os.path.exists(ks.library_path()):
+            from paper_2405_15013_amd import build
+            build.build()
+        self.torch = torch
+        self.ks = ks
+        self.lib = ks.load_library()
+        self.steps = steps
+        self.warmup = warmup
+        self.dev = torch.device("cuda:0")
+        self.pool_x = torch.empty(POOL_BYTES, dtype=torch.uint8, device=self.dev)
+        self.pool_y = torch.empty(POOL_BYTES, dtype=torch.uint8, device=self.dev)
+        self.stream = torch.cuda.Stream(device=self.dev)
+        self.filled = None
+
+    def fill(self, dtype):
+        """Fill the input pool with N(0,1) values of the storage dtype."""
+        torch = self.torch
+        if self.filled == dtype:
+            return
+        tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
+        view = self.pool_x.view(tdt)
+        g = torch.Generator(device=self.dev)
+        g.manual_seed(20240523)
+        chunk = 1 << 26
+        for s in range(0, view.numel(), chunk):
+            view[s:s + chunk].normal_(generator=g)
+        torch.cuda.synchronize()
+        self.filled = dtype
+
+    def time_calls(self, calls, set_bytes, launch):
+        """Capture a graph of L launches over rotating buffer sets, replay it.
+        `launch(r, stream_handle)` issues one call on buffer set r."""
+        torch = self.torch
+        nsets = max(1, POOL_BYTES // max(1, set_bytes))
+        L = max(8, min(MAX_LAUNCHES, math.ceil(ROTATE_BYTES / max(1, set_bytes * calls))))
+        L = min(L, nsets)
+        with torch.cuda.stream(self.stream):
+            h = self.stream.cuda_stream
+            launch(0, h)  # eager call: plan creation outside the capture
+            torch.cuda.synchronize()
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g, stream=self.stream):
+                hc = torch.cuda.current_stream().cuda_stream
+                for r in range(L):
+                    launch(r % nsets, hc)
+            for _ in range(self.warmup):
+                g.replay()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            self.stream.synchronize()
+            e0.record(self.stream)
+            for _ in range(self.steps):
+                g.replay()
+            e1.record(self.stream)
+            e1.synchronize()
+        ms = e0.elapsed_time(e1)
+        del g
+        return ms * 1e-3 / (self.steps * L), L
+
+    def point(self, pattern, batch, dtype, layout):
+        torch = self.torch
+        a, b, c, d = pattern
+        s = ESIZE[dtype]
+        N, M = a * c * d, a * b * d
+        xb = (batch * N * s + 255) // 256 * 256
+        yb = (batch * M * s + 255) // 256 * 256
+        tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
+        kv = torch.randn(a * d * b * c, device=self.dev).to(tdt)
+        px, py = self.pool_x.data_ptr(), self.pool_y.data_ptr()
+        lay = 0 if layout == "bsf" else 1
+        dt = {"f32": 0, "bf16": 1, "f16": 2}[dtype]
+        kp = kv.data_ptr()
+        nsets = max(1, POOL_BYTES // max(xb, yb))
+        lib = self.lib
+
+        def launch(r, h):
+            st = lib.ks_matmul(a, b, c, d, kp, px + (r % nsets) * xb, py + (r % nsets) * yb, batch, lay, dt, h)
+            if st != 0:
+                raise RuntimeError("ks_matmul failed: %s" % self.ks.ks_status_string(st))
+
+        t, L = self.time_calls(1, xb + yb, launch)
+        nbytes, flops, t_roof, bound = roof(pattern, batch, dtype)
+        desc = self.ks.ks_plan_describe(a, b, c, d, batch, layout, dtype)
+        return {"pattern": list(pattern), "batch": batch, "dtype": dtype, "layout": layout, "us": t * 1e6,
+                "gbps": nbytes / t / 1e9, "tflops": flops / t / 1e12, "frac": t_roof / t, "bound": bound,
+                "roof_us": t_roof * 1e6, "bytes": nbytes, "flops": flops, "launches": L,
+                "kernel": kernel_key(desc, dtype, layout), "plan": desc}
+
+    def chain(self, patterns, batch, dtype, layout):
+        torch = self.torch
+        ks = self.ks
+        s = ESIZE[dtype]
+        tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
+        kvs = [torch.randn(p[0] * p[1] * p[2] * p[3], device=self.dev).to(tdt) for p in patterns]
+        factors = [(p, k) for p, k in zip(patterns, kvs)]
+        aL, bL, cL, dL = patterns[-1]
+        a1, b1, c1, d1 = patterns[0]
+        N, M = aL * cL * dL, a1 * b1 * d1
+        xb = (batch * N * s + 255) // 256 * 256
+        yb = (batch * M * s + 255) // 256 * 256
+        wsb = ks.ks_chain_workspace_bytes(factors, batch, dtype)
+        ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=self.dev)
+        px, py = self.pool_x.data_ptr(), self.pool_y.data_ptr()
+        nsets = max(1, POOL_BYTES // max(xb, yb))
+
+        def launch(r, h):
+            ks.ks_chain(factors, px + (r % nsets) * xb, py + (r % nsets) * yb, batch, layout, dtype, ws, wsb,
+                        stream=h)
+
+        t, L = self.time_calls(len(patterns), xb + yb, launch)
+        unfused = sum(roof(p, batch, dtype)[0] for p in patterns)
+        fused = (batch * (N + M) + sum(p[0] * p[1] * p[2] * p[3] for p in patterns)) * s
+        flops = sum(roof(p, batch, dtype)[1] for p in patterns)
+        t_roof = max(unfused / HBM_BW, flops / PEAK[dtype])
+        return {"chain": [list(p) for p in patterns], "batch": batch, "dtype": dtype, "layout": layout,
+                "us": t * 1e6, "gbps_unfused": unfused / t / 1e9, "frac_unfused": t_roof / t,
+                "fused_lower_bound_us": max(fused / HBM_BW, flops / PEAK[dtype]) * 1e6}
+
+
+def cpu_baseline(sample_every=50, batch=1024):
+    """fp64 oracle on a bounded sample of the sweep (every `sample_every`-th
+    pattern, fp32 inputs, batch `batch`, batch-size-first)."""
+    import numpy as np
+    import oracle
+    from paper_2405_15013_amd import inputs
+    pats = sweep_patterns()[::sample_every]
+    fracs, gbps = [], []
+    total = 0.0
+    for p in pats:
+        x = inputs.to_f64(inputs.make_x(9, p, batch, "f32"), "f32")
+        kv = inputs.to_f64(inputs.make_kv(9, p, batch, "f32", dist="normal"), "f32")
+        t0 = time.perf_counter()
+        oracle.matmul(p, kv, x, batch, "bsf")
+        t = time.perf_counter() - t0
+        total += t
+        nbytes, flops, t_roof, _ = roof(p, batch, "f32")
+        fracs.append(t_roof / t)
+        gbps.append(nbytes / t / 1e9)
+    return {"value": float(np.median(fracs)), "unit": "fraction of MI355X roofline (median over sampled patterns)",
+            "gbps_median": float(np.median(gbps)), "cores": oracle.threads(), "kind": "oracle",
+            "seconds": total,
+            "sample": "%d of the 700 sweep patterns (every %dth), batch %d, fp32 values, BSF, fp64 arithmetic"
+                      % (len(pats), sample_every, batch)}
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=5)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--sample", type=int, default=1, help="time every S-th sweep point (1 = all 5600)")
+    ap.add_argument("--points-out", default=os.path.join(ROOT, "gpurun_out", "bench_points.jsonl"))
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-families", action="store_true")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU only: the KS matmul path shards over the batch with no "
+              "communication, so there is no multi-GPU step to time (got --gpus %d)" % args.gpus, file=sys.stderr)
+        sys.exit(2)
+    import numpy as np
+    import torch
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    t_start = time.time()
+    run = Runner(args.steps, args.warmup)
+    os.makedirs(os.path.dirname(args.points_out) or ".", exist_ok=True)
+    pats = sweep_patterns()
+    points = []
+    idx = 0
+    with open(args.points_out, "w") as fout:
+        for dtype in ("f32", "bf16"):
+            run.fill(dtype)
+            for batch in (4096, 25088):
+                for layout in ("bsf", "bsl"):
+                    for p in pats:
+                        idx += 1
+                        if (idx - 1) % args.sample:
+                            continue
+                        r = run.point(p, batch, dtype, layout)
+                        points.append(r)
+                        fout.write(json.dumps(r) + "\n")
+                print("[bench] %s done: %d points, %.0f s" % (dtype, len(points), time.time() - t_start),
+                      file=sys.stderr, flush=True)
+        families = {}
+        if not args.no_families:
+            run.fill("f32")
+            fam = []
+            for layout in ("bsf", "bsl"):
+                fam.append(run.point((2, 4, 4, 2), 32, "f32", layout))
+            for l in range(1, 11):
+                fam.append(run.point((2 ** (l - 1), 2, 2, 2 ** (10 - l)), 4096, "f32", "bsl"))
+            for dtype in ("f32", "bf16"):
+                run.fill(dtype)
+                for layout in ("bsf", "bsl"):
+                    for p in ((1, 32, 32, 32), (32, 32, 32, 1)):
+                        fam.append(run.point(p, 16384, dtype, layout))
+                    for p in ((6, 64, 16, 8), (6, 16, 64, 8)):
+                        fam.append(run.point(p, 25088, dtype, layout))
+            for r in fam:
+                fout.write(json.dumps(r) + "\n")
+            run.fill("f32")
+            ch = [run.chain([(2 ** (l - 1), 2, 2, 2 ** (10 - l)) for l in range(1, 11)], 4096, "f32", "bsl")]
+            for dtype in ("f32", "bf16"):
+                run.fill(dtype)
+                for layout in ("bsf", "bsl"):
+                    ch.append(run.chain([(1, 32, 32, 32), (32, 32, 32, 1)], 16384, dtype, layout))
+            for r in ch:
+                fout.write(json.dumps(r) + "\n")
+
+            def fam_summary(sel):
+                return {"median_frac": float(np.median([r["frac"] for r in sel])),
+                        "median_gbps": float(np.median([r["gbps"] for r in sel]))}
+            families = {
+                "tiny_(2,4,4,2)_B32_f32": fam_summary(fam[0:2]),
+                "butterfly_N1024_B4096_f32_bsl": fam_summary(fam[2:12]),
+                "monarch_B16384": fam_summary([r for r in fam[12:] if r["batch"] == 16384]),
+                "mlp_768_3072_B25088": fam_summary([r for r in fam[12:] if r["batch"] == 25088]),
+                "butterfly_10chain_B4096_f32_bsl_us": ch[0]["us"],
+                "monarch_2chain_B16384_us": {"%s_%s" % (r["dtype"], r["layout"]): r["us"] for r in ch[1:]},
+            }
+    fr = np.array([r["frac"] for r in points])
+    # dominant kernel: largest share of the sweep's time
+    per_k = {}
+    for r in points:
+        k = per_k.setdefault(r["kernel"], {"t": 0.0, "bytes": 0.0, "flops": 0.0, "n": 0, "t_hbm": 0.0, "t_flop": 0.0})
+        k["t"] += r["us"] * 1e-6
+        k["bytes"] += r["bytes"]
+        k["flops"] += r["flops"]
+        k["n"] += 1
+        k["t_hbm"] += r["bytes"] / HBM_BW
+        k["t_flop"] += r["flops"] / PEAK[r["dtype"]]
+    dom_name, dom = max(per_k.items(), key=lambda kv: kv[1]["t"])
+    dtype_dom = "f32" if "<f32" in dom_name else "bf16"
+    if dom["t_hbm"] >= dom["t_flop"]:
+        achieved = dom["bytes"] / dom["t"] / 1e9
+        roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_BW / 1e9, "unit": "GB/s",
+                    "frac": achieved / (HBM_BW / 1e9), "traffic": None}
+    else:
+        achieved = dom["flops"] / dom["t"] / 1e12
+        roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK[dtype_dom] / 1e12, "unit": "TFLOP/s",
+                    "frac": achieved / (PEAK[dtype_dom] / 1e12), "traffic": None}
+    roofline["kernel"] = dom_name
+    roofline["points"] = dom["n"]
+    roofline["avg_launch_us"] = dom["t"] / dom["n"] * 1e6
+    roofline["share_of_sweep_time"] = dom["t"] / sum(v["t"] for v in per_k.values())
+    ms_per_step = float(sum(r["us"] for r in points) * 1e-3)
+    out = {
+        "metric": METRIC,
+        "value": float(np.median(fr)),
+        "unit": "fraction of roofline (median over sweep points)",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32+bf16 (fp32 accumulate)",
+        "data": "synthetic: X, K i.i.d. N(0,1), seeded",
+        "config": {"workload": "KS pattern sweep a{1,2,4,8} x b,c{16..128} x d{1..16}, abd,acd<=8192 "
+                               "(700 patterns) x B{4096,25088} x {fp32,bf16} x {BSF,BSL}",
+                   "points": len(points), "sample_every": args.sample, "parallelism": "single GPU"},
+        "median_gbps": float(np.median([r["gbps"] for r in points])),
+        "median_tflops": float(np.median([r["tflops"] for r in points])),
+        "frac_quantiles_10_25_50_75_90": [float(np.quantile(fr, q)) for q in (0.1, 0.25, 0.5, 0.75, 0.9)],
+        "median_frac_by": {
+            "%s_%s_B%d" % (dt, lay, B): float(np.median([r["frac"] for r in points
+                                                        if r["dtype"] == dt and r["layout"] == lay and r["batch"] == B]))
+            for dt in ("f32", "bf16") for lay in ("bsf", "bsl") for B in (4096, 25088)
+            if any(r["dtype"] == dt and r["layout"] == lay and r["batch"] == B for r in points)},
+        "roofline": roofline,
+        "families": families,
+    }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline()
+    out["wall_s"] = time.time() - t_start
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -138,6 +138,21 @@ ks_status_t ks_plan_describe(int64_t a, int64_t b, int64_t c, int64_t d,
  */
 void ks_force_variant(int variant);
 
+/*
+ * Host-side check of the plan ks_matmul would use for these arguments (with
+ * 16-byte-aligned buffers and the variant forced on this thread, if any):
+ * replays every thread's address arithmetic on the CPU and checks that all
+ * reads and writes stay in bounds and that every element of Y is written
+ * exactly once (the row sets of Section 4.1 partition the output).  Enqueues
+ * nothing.  Cost is proportional to batch*M; meant for tests and tuning.
+ * Writes "ok" or the first violation into `report` (host, `len` bytes).
+ * Returns KS_OK, KS_ERR_UNSUPPORTED on a violation or missing plan, or the
+ * status ks_matmul would return for these arguments.
+ */
+ks_status_t ks_plan_verify(int64_t a, int64_t b, int64_t c, int64_t d,
+                           int64_t batch, int layout, int dtype,
+                           char *report, size_t len);
+
 #ifdef __cplusplus
 }
 #endif

@@ -17,7 +17,7 @@ import os
 __all__ = [
     "BSF", "BSL", "F32", "BF16", "F16", "KsError",
     "ks_matmul", "ks_chain", "ks_chain_workspace_bytes", "ks_status_string",
-    "ks_last_hip_error", "ks_plan_describe", "ks_force_variant",
+    "ks_last_hip_error", "ks_plan_describe", "ks_force_variant", "ks_plan_verify",
     "matmul", "chain", "library_path", "load_library", "EXPORTED_SYMBOLS",
 ]
 
@@ -33,7 +33,7 @@ STATUS_NAMES = {
 # Every function declared in include/ks.h.
 EXPORTED_SYMBOLS = (
     "ks_matmul", "ks_chain_workspace_bytes", "ks_chain", "ks_status_string",
-    "ks_last_hip_error", "ks_plan_describe", "ks_force_variant",
+    "ks_last_hip_error", "ks_plan_describe", "ks_force_variant", "ks_plan_verify",
 )
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -86,6 +86,8 @@ def load_library():
     lib.ks_plan_describe.restype = ci
     lib.ks_force_variant.argtypes = [ci]
     lib.ks_force_variant.restype = None
+    lib.ks_plan_verify.argtypes = [i64, i64, i64, i64, i64, ci, ci, ctypes.c_char_p, ctypes.c_size_t]
+    lib.ks_plan_verify.restype = ci
     _lib = lib
     return lib
 
@@ -141,6 +143,14 @@ def ks_plan_describe(a, b, c, d, batch, layout, dtype):
     if st != KS_OK:
         raise KsError(st, "ks_plan_describe")
     return buf.value.decode()
+
+
+def ks_plan_verify(a, b, c, d, batch, layout, dtype):
+    """Host-side replay of the planned launch; returns (status, report)."""
+    buf = ctypes.create_string_buffer(512)
+    st = load_library().ks_plan_verify(a, b, c, d, batch, _code(layout, _LAYOUTS, "layout"),
+                                       _code(dtype, _DTYPES, "dtype"), buf, 512)
+    return int(st), buf.value.decode()
 
 
 def ks_matmul(a, b, c, d, K_values, X, Y, batch, layout, dtype, stream=None, check=True):

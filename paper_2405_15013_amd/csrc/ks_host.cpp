@@ -372,3 +372,22 @@ namespace {
 bool plan_mfma(const Problem& p, bool al16, Plan* pl) { return plan_mfma_impl(p, al16, pl); }
 }  // namespace
 }  // namespace ks
+
+namespace ks {
+// Plan for stand-in aligned buffers (used by the host-side verifier).  Returns
+// false (with *st set) when there is nothing to launch or no plan.
+bool plan_for_verify(int64_t a, int64_t b, int64_t c, int64_t d, int64_t batch, int layout, int dtype, Problem* p,
+                     Plan* pl, ks_status_t* st) {
+  const uintptr_t base = uintptr_t(1) << 44;
+  const uintptr_t span = uintptr_t(1) << 40;
+  bool empty = false;
+  *st = validate(a, b, c, d, reinterpret_cast<const void*>(base), reinterpret_cast<const void*>(base + span),
+                 reinterpret_cast<void*>(base + 2 * span), batch, layout, dtype, p, &empty);
+  if (*st != KS_OK || empty) return false;
+  if (!get_plan(*p, true, pl)) {
+    *st = KS_ERR_UNSUPPORTED;
+    return false;
+  }
+  return true;
+}
+}  // namespace ks

@@ -167,3 +167,76 @@ def test_empty_batch(layout):
     x = torch.empty(0, device="cuda")
     y = torch.empty(0, device="cuda")
     assert ks.ks_matmul(2, 3, 3, 2, kd, x, y, 0, layout, "f32") == 0
+
+
+# --- the pattern sweep (every 50th pattern), sampled at full batch ------------
+
+def sweep_patterns():
+    return [(a, b, c, d) for a in (1, 2, 4, 8) for b in (16, 32, 48, 64, 96, 128) for c in (16, 32, 48, 64, 96, 128)
+            for d in (1, 2, 4, 8, 16) if a * b * d <= 8192 and a * c * d <= 8192]
+
+
+SWEEP_SAMPLE = sweep_patterns()[::50]
+
+
+def check_sampled(pattern, batch, dtype, layout, cfg, nsample=4096, variant=None):
+    """Run the full-size product on the GPU; compare a seeded sample of outputs
+    (always including the first and last batch rows) with the oracle, computed
+    one by one."""
+    a, b, c, d = pattern
+    M = a * b * d
+    x, kv, x64, kv64 = case(cfg, pattern, batch, dtype, "normal", "normal")
+    y = run_gpu(pattern, x, kv, batch, dtype, layout, variant=variant)
+    rng = np.random.default_rng(hash((pattern, batch, dtype, layout)) % (2 ** 32))
+    bi = np.concatenate([rng.integers(0, batch, nsample), np.zeros(M // 4 + 1, np.int64),
+                         np.full(M // 4 + 1, batch - 1)])
+    mi = np.concatenate([rng.integers(0, M, nsample), rng.integers(0, M, 2 * (M // 4 + 1))])
+    y64 = oracle.entries(pattern, kv64, x64, batch, "bsf", bi, mi)
+    assert np.all(np.isfinite(y)), "unwritten (NaN) outputs"
+    err = rel_err(y[bi, mi], y64)
+    assert err <= TOL[dtype], "%s B=%d %s %s: sampled rel err %.3e" % (pattern, batch, dtype, layout, err)
+
+
+@pytest.mark.parametrize("pattern", SWEEP_SAMPLE)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_sweep_sample_b4096(pattern, dtype, layout):
+    check_sampled(pattern, 4096, dtype, layout, cfg=7)
+
+
+@pytest.mark.parametrize("pattern", SWEEP_SAMPLE[::3])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_sweep_sample_b25088(pattern, dtype, layout):
+    check_sampled(pattern, 25088, dtype, layout, cfg=7)
+
+
+@pytest.mark.parametrize("pattern", SWEEP_SAMPLE)
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_sweep_ragged_batch_full(pattern, dtype, layout):
+    """Batches that leave a partial batch tile: full comparison."""
+    batch = 104 if dtype == "f32" else 120  # multiples of the 16-byte vector width, not of the tile
+    check(pattern, batch, dtype, layout, cfg=8, kdist="normal")
+
+
+@pytest.mark.parametrize("pattern", [(1, 32, 32, 32), (32, 32, 32, 1), (6, 64, 16, 8), (6, 16, 64, 8),
+                                     (2, 48, 80, 3), (1, 128, 16, 16), (8, 16, 128, 4)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_mfma_forced(pattern, dtype, layout):
+    import paper_2405_15013_amd as ks
+    desc = ks.ks_plan_describe(*pattern, 256, layout, dtype)
+    assert "name=mfma" in desc, desc
+    check(pattern, 256, dtype, layout, cfg=9, variant=3, kdist="normal")
+
+
+@pytest.mark.parametrize("pattern", [(1, 32, 32, 32), (6, 64, 16, 8), (4, 96, 48, 2)])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_mfma_generic_agree(pattern, layout):
+    """The MFMA and generic kernels agree on the same inputs (both within the
+    oracle tolerance, and close to each other)."""
+    x, kv, _, _ = case(10, pattern, 512, "f32", "normal", "normal")
+    y_m = run_gpu(pattern, x, kv, 512, "f32", layout, variant=3)
+    y_g = run_gpu(pattern, x, kv, 512, "f32", layout, variant=0)
+    assert rel_err(y_m, y_g) <= 1e-5

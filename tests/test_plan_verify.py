@@ -1,0 +1,59 @@
+"""Host-side replay of planned launches (ks_plan_verify): every global access
+of every thread stays in bounds, every LDS cell the MFMA reads was written,
+and every element of Y is written exactly once (the row sets of the paper's
+Section 4.1 partition the output, so no two workgroups may touch one element).
+Runs on the CPU; nothing is enqueued."""
+import pytest
+
+import paper_2405_15013_amd as ks
+
+
+def sweep_patterns():
+    return [(a, b, c, d) for a in (1, 2, 4, 8) for b in (16, 32, 48, 64, 96, 128) for c in (16, 32, 48, 64, 96, 128)
+            for d in (1, 2, 4, 8, 16) if a * b * d <= 8192 and a * c * d <= 8192]
+
+
+CONFIGS = ([(2, 4, 4, 2)] + [(2 ** (l - 1), 2, 2, 2 ** (10 - l)) for l in range(1, 11)]
+           + [(1, 32, 32, 32), (32, 32, 32, 1), (6, 64, 16, 8), (6, 16, 64, 8)])
+
+
+@pytest.mark.parametrize("pattern", sweep_patterns()[::23])
+@pytest.mark.parametrize("batch", [48, 1000, 4096])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_sweep_plans(pattern, batch, layout, dtype):
+    st, rep = ks.ks_plan_verify(*pattern, batch, layout, dtype)
+    assert st == 0, "%s B=%d %s %s: %s [%s]" % (pattern, batch, layout, dtype, rep,
+                                                ks.ks_plan_describe(*pattern, batch, layout, dtype))
+
+
+@pytest.mark.parametrize("pattern", CONFIGS)
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+def test_config_plans_small_batch(pattern, layout, dtype):
+    for batch in (1, 32, 104, 256):
+        st, rep = ks.ks_plan_verify(*pattern, batch, layout, dtype)
+        assert st == 0, "%s B=%d %s %s: %s" % (pattern, batch, layout, dtype, rep)
+
+
+@pytest.mark.parametrize("pattern,batch", [((1, 32, 32, 32), 16384), ((6, 64, 16, 8), 25088),
+                                           ((6, 16, 64, 8), 25088), ((1, 2, 2, 512), 4096)])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_full_size_plans(pattern, batch, layout):
+    st, rep = ks.ks_plan_verify(*pattern, batch, layout, "bf16")
+    assert st == 0, rep
+
+
+@pytest.mark.parametrize("variant", [0, 1, 2, 3])
+def test_forced_variants(variant):
+    """Every variant that accepts a shape produces a valid launch for it."""
+    ks.ks_force_variant(variant)
+    try:
+        for pattern, layout in [((2, 4, 4, 2), "bsl"), ((2, 4, 4, 2), "bsf"), ((1, 16, 16, 4), "bsf"),
+                                ((1, 16, 16, 4), "bsl"), ((3, 32, 48, 2), "bsf")]:
+            st, rep = ks.ks_plan_verify(*pattern, 64, layout, "f32")
+            assert st in (0, 5), rep
+            if st == 5:
+                assert rep == "no plan", rep
+    finally:
+        ks.ks_force_variant(None)
