@@ -15,13 +15,21 @@ the roof time is max(bytes / 8.0 TB/s, flops / peak) with peak = 157.3 TFLOP/s
 (fp32) or 2516.6 TFLOP/s (bf16 MFMA), and the point's fraction of roofline is
 roof time / measured time.
 
-Timing: every point gets a launch graph of L ks_matmul calls, each on its own
-buffer set taken from a rotating pool so that >= 768 MB (three times the
-256 MB Infinity Cache) pass between two uses of the same buffers (L capped at
-256 for the smallest points).  After --warmup untimed replays, --steps replays
-are bracketed by HIP events on the replay stream; the point's time is the
-elapsed time / (steps * L).  A "step" is one pass over the whole sweep, so
-ms_per_step is the sum of the per-point times.
+Timing: every point is timed over a rotation of buffer sets (one X and one Y
+region of two 3 GB pools per call) such that >= 768 MB, three times the 256 MB
+Infinity Cache, pass between two uses of the same buffers (at least 8 sets).
+One pass launches one ks_matmul per set; the passes are captured into HIP
+graphs of at most 512 calls, replayed --warmup times untimed and then --steps
+times between two HIP events recorded on the replay stream.  The point's time
+per call is the elapsed time / (steps * sets).  ms_per_step is the sum over the
+timed points of the time per call, i.e. the time of one pass over the sweep.
+
+The roofline object is computed for the dominant kernel instance (the one with
+the largest share of timed time): achieved = algorithmic bytes (or flops) of
+all its timed calls / their total time, and avg_launch_us = that total time /
+number of calls, which is what a profiler's per-kernel average duration
+reports for the same command (the event time also holds the gaps between
+launches inside the graph).
 
 Also reported: the same measurements for the other workload families (tiny,
 butterfly factors and 10-chain, Monarch factors and 2-chain, Transformer-MLP
@@ -46,8 +54,9 @@ HBM_BW = 8.0e12
 PEAK = {"f32": 157.3e12, "bf16": 2516.6e12, "f16": 2516.6e12}
 ESIZE = {"f32": 4, "bf16": 2, "f16": 2}
 POOL_BYTES = 3 << 30
-ROTATE_BYTES = 768 << 20
-MAX_LAUNCHES = 256
+ROTATE_BYTES = 768 << 20    # distinct buffer bytes between two uses of a buffer (3x the 256 MB MALL)
+MIN_SETS = 8
+GRAPH_LAUNCHES = 512
 
 
 def sweep_patterns():
@@ -71,12 +80,8 @@ def roof(pattern, batch, dtype):
     return nbytes, flops, max(t_hbm, t_flop), ("hbm" if t_hbm >= t_flop else "mfma")
 
 
-def kernel_key(desc, dtype, layout):
-    f = dict(kv.split("=", 1) for kv in desc.split())
-    name = f["name"]
-    if name == "mfma":
-        return "ks_mfma_kernel<%s,%s,NT=%s,MT=%s>" % (dtype, layout, f["waves_n"], f["waves_m"])
-    return "ks_%s_kernel<%s>" % (name, dtype)
+def plan_field(desc, key):
+    return dict(kv.split("=", 1) for kv in desc.split())[key]
 
 
 class Runner:
@@ -112,35 +117,46 @@ class Runner:
         torch.cuda.synchronize()
         self.filled = dtype
 
-    def time_calls(self, calls, set_bytes, launch):
-        """Capture a graph of L launches over rotating buffer sets, replay it.
-        `launch(r, stream_handle)` issues one call on buffer set r."""
+    def time_calls(self, set_bytes, nsets_pool, launch):
+        """Time one call per buffer set over a rotation of >= ROTATE_BYTES.
+
+        Every buffer set (one X and one Y region of the pools) is used once per
+        pass, so at least ROTATE_BYTES of distinct memory pass between two uses
+        of the same buffers.  The launches of a pass are captured into HIP
+        graphs of at most GRAPH_LAUNCHES calls; `warmup` untimed passes are
+        followed by `steps` timed passes, bracketed by HIP events recorded on
+        the replay stream (the stream the kernels run on).
+        `launch(r, stream_handle)` issues the call on buffer set r.
+        Returns (seconds per call, calls per pass)."""
         torch = self.torch
-        nsets = max(1, POOL_BYTES // max(1, set_bytes))
-        L = max(8, min(MAX_LAUNCHES, math.ceil(ROTATE_BYTES / max(1, set_bytes * calls))))
-        L = min(L, nsets)
+        nsets = max(MIN_SETS, math.ceil(ROTATE_BYTES / max(1, set_bytes)))
+        nsets = min(nsets, nsets_pool)
+        graphs = []
         with torch.cuda.stream(self.stream):
-            h = self.stream.cuda_stream
-            launch(0, h)  # eager call: plan creation outside the capture
+            launch(0, self.stream.cuda_stream)  # eager call: plan creation outside the capture
             torch.cuda.synchronize()
-            g = torch.cuda.CUDAGraph()
-            with torch.cuda.graph(g, stream=self.stream):
-                hc = torch.cuda.current_stream().cuda_stream
-                for r in range(L):
-                    launch(r % nsets, hc)
+            for g0 in range(0, nsets, GRAPH_LAUNCHES):
+                g = torch.cuda.CUDAGraph()
+                with torch.cuda.graph(g, stream=self.stream):
+                    hc = torch.cuda.current_stream().cuda_stream
+                    for r in range(g0, min(nsets, g0 + GRAPH_LAUNCHES)):
+                        launch(r, hc)
+                graphs.append(g)
             for _ in range(self.warmup):
-                g.replay()
+                for g in graphs:
+                    g.replay()
             e0 = torch.cuda.Event(enable_timing=True)
             e1 = torch.cuda.Event(enable_timing=True)
             self.stream.synchronize()
             e0.record(self.stream)
             for _ in range(self.steps):
-                g.replay()
+                for g in graphs:
+                    g.replay()
             e1.record(self.stream)
             e1.synchronize()
         ms = e0.elapsed_time(e1)
-        del g
-        return ms * 1e-3 / (self.steps * L), L
+        del graphs
+        return ms * 1e-3 / (self.steps * nsets), nsets
 
     def point(self, pattern, batch, dtype, layout):
         torch = self.torch
@@ -155,21 +171,21 @@ class Runner:
         lay = 0 if layout == "bsf" else 1
         dt = {"f32": 0, "bf16": 1, "f16": 2}[dtype]
         kp = kv.data_ptr()
-        nsets = max(1, POOL_BYTES // max(xb, yb))
+        nsets_pool = max(1, POOL_BYTES // max(xb, yb))
         lib = self.lib
 
         def launch(r, h):
-            st = lib.ks_matmul(a, b, c, d, kp, px + (r % nsets) * xb, py + (r % nsets) * yb, batch, lay, dt, h)
+            st = lib.ks_matmul(a, b, c, d, kp, px + r * xb, py + r * yb, batch, lay, dt, h)
             if st != 0:
                 raise RuntimeError("ks_matmul failed: %s" % self.ks.ks_status_string(st))
 
-        t, L = self.time_calls(1, xb + yb, launch)
+        t, nsets = self.time_calls(xb + yb, nsets_pool, launch)
         nbytes, flops, t_roof, bound = roof(pattern, batch, dtype)
         desc = self.ks.ks_plan_describe(a, b, c, d, batch, layout, dtype)
         return {"pattern": list(pattern), "batch": batch, "dtype": dtype, "layout": layout, "us": t * 1e6,
                 "gbps": nbytes / t / 1e9, "tflops": flops / t / 1e12, "frac": t_roof / t, "bound": bound,
-                "roof_us": t_roof * 1e6, "bytes": nbytes, "flops": flops, "launches": L,
-                "kernel": kernel_key(desc, dtype, layout), "plan": desc}
+                "roof_us": t_roof * 1e6, "bytes": nbytes, "flops": flops, "calls_per_pass": nsets,
+                "kernel": plan_field(desc, "kernel"), "plan": desc}
 
     def chain(self, patterns, batch, dtype, layout):
         torch = self.torch
@@ -186,13 +202,12 @@ class Runner:
         wsb = ks.ks_chain_workspace_bytes(factors, batch, dtype)
         ws = torch.empty(max(wsb, 1), dtype=torch.uint8, device=self.dev)
         px, py = self.pool_x.data_ptr(), self.pool_y.data_ptr()
-        nsets = max(1, POOL_BYTES // max(xb, yb))
+        nsets_pool = max(1, POOL_BYTES // max(xb, yb))
 
         def launch(r, h):
-            ks.ks_chain(factors, px + (r % nsets) * xb, py + (r % nsets) * yb, batch, layout, dtype, ws, wsb,
-                        stream=h)
+            ks.ks_chain(factors, px + r * xb, py + r * yb, batch, layout, dtype, ws, wsb, stream=h)
 
-        t, L = self.time_calls(len(patterns), xb + yb, launch)
+        t, _ = self.time_calls(xb + yb, nsets_pool, launch)
         unfused = sum(roof(p, batch, dtype)[0] for p in patterns)
         fused = (batch * (N + M) + sum(p[0] * p[1] * p[2] * p[3] for p in patterns)) * s
         flops = sum(roof(p, batch, dtype)[1] for p in patterns)
@@ -202,9 +217,11 @@ class Runner:
                 "fused_lower_bound_us": max(fused / HBM_BW, flops / PEAK[dtype]) * 1e6}
 
 
-def cpu_baseline(sample_every=50, batch=1024):
-    """fp64 oracle on a bounded sample of the sweep (every `sample_every`-th
-    pattern, fp32 inputs, batch `batch`, batch-size-first)."""
+def cpu_baseline(sample_every=7, batch=4096):
+    """The fp64 oracle timed on the host cores, on a bounded sample of the
+    sweep: every `sample_every`-th pattern (100 of the 700), batch `batch`,
+    fp32 inputs, both layouts.  Reported in the metric's unit (median fraction
+    of the MI355X roofline) and in GB/s of algorithmic traffic."""
     import numpy as np
     import oracle
     from paper_2405_15013_amd import inputs
@@ -214,26 +231,29 @@ def cpu_baseline(sample_every=50, batch=1024):
     for p in pats:
         x = inputs.to_f64(inputs.make_x(9, p, batch, "f32"), "f32")
         kv = inputs.to_f64(inputs.make_kv(9, p, batch, "f32", dist="normal"), "f32")
-        t0 = time.perf_counter()
-        oracle.matmul(p, kv, x, batch, "bsf")
-        t = time.perf_counter() - t0
-        total += t
-        nbytes, flops, t_roof, _ = roof(p, batch, "f32")
-        fracs.append(t_roof / t)
-        gbps.append(nbytes / t / 1e9)
-    return {"value": float(np.median(fracs)), "unit": "fraction of MI355X roofline (median over sampled patterns)",
+        for layout in ("bsf", "bsl"):
+            xl = inputs.to_layout(x, layout)
+            t0 = time.perf_counter()
+            oracle.matmul(p, kv, xl, batch, layout)
+            t = time.perf_counter() - t0
+            total += t
+            nbytes, flops, t_roof, _ = roof(p, batch, "f32")
+            fracs.append(t_roof / t)
+            gbps.append(nbytes / t / 1e9)
+    return {"value": float(np.median(fracs)), "unit": "fraction of MI355X roofline (median over sampled points)",
             "gbps_median": float(np.median(gbps)), "cores": oracle.threads(), "kind": "oracle",
             "seconds": total,
-            "sample": "%d of the 700 sweep patterns (every %dth), batch %d, fp32 values, BSF, fp64 arithmetic"
-                      % (len(pats), sample_every, batch)}
+            "sample": "%d of the 700 sweep patterns (every %dth) x {BSF, BSL}, batch %d, fp32 values, "
+                      "fp64 arithmetic" % (len(pats), sample_every, batch)}
 
 
 def main():
     ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=5)
-    ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--sample", type=int, default=1, help="time every S-th sweep point (1 = all 5600)")
+    ap.add_argument("--steps", type=int, default=3)
+    ap.add_argument("--warmup", type=int, default=1)
+    ap.add_argument("--sample", type=int, default=1,
+                    help="time a seeded 1/S subset of the sweep points (1 = all 5600)")
     ap.add_argument("--points-out", default=os.path.join(ROOT, "gpurun_out", "bench_points.jsonl"))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-families", action="store_true")
@@ -249,21 +269,21 @@ def main():
     run = Runner(args.steps, args.warmup)
     os.makedirs(os.path.dirname(args.points_out) or ".", exist_ok=True)
     pats = sweep_patterns()
+    grid = [(dtype, batch, layout, p) for dtype in ("f32", "bf16") for batch in (4096, 25088)
+            for layout in ("bsf", "bsl") for p in pats]
+    keep = np.random.default_rng(7).permutation(len(grid))[::args.sample]
+    keep = set(int(k) for k in keep)
     points = []
-    idx = 0
     with open(args.points_out, "w") as fout:
-        for dtype in ("f32", "bf16"):
+        for idx, (dtype, batch, layout, p) in enumerate(grid):
+            if idx not in keep:
+                continue
             run.fill(dtype)
-            for batch in (4096, 25088):
-                for layout in ("bsf", "bsl"):
-                    for p in pats:
-                        idx += 1
-                        if (idx - 1) % args.sample:
-                            continue
-                        r = run.point(p, batch, dtype, layout)
-                        points.append(r)
-                        fout.write(json.dumps(r) + "\n")
-                print("[bench] %s done: %d points, %.0f s" % (dtype, len(points), time.time() - t_start),
+            r = run.point(p, batch, dtype, layout)
+            points.append(r)
+            fout.write(json.dumps(r) + "\n")
+            if len(points) % 200 == 0:
+                print("[bench] %d/%d sweep points, %.0f s" % (len(points), len(keep), time.time() - t_start),
                       file=sys.stderr, flush=True)
         families = {}
         if not args.no_families:
@@ -303,29 +323,35 @@ def main():
                 "monarch_2chain_B16384_us": {"%s_%s" % (r["dtype"], r["layout"]): r["us"] for r in ch[1:]},
             }
     fr = np.array([r["frac"] for r in points])
-    # dominant kernel: largest share of the sweep's time
+    # Dominant kernel instance: the largest share of the sweep's timed time.
+    # Per instance, sums over its timed calls (each point contributes
+    # steps * calls_per_pass calls of the same duration).
     per_k = {}
     for r in points:
-        k = per_k.setdefault(r["kernel"], {"t": 0.0, "bytes": 0.0, "flops": 0.0, "n": 0, "t_hbm": 0.0, "t_flop": 0.0})
-        k["t"] += r["us"] * 1e-6
-        k["bytes"] += r["bytes"]
-        k["flops"] += r["flops"]
-        k["n"] += 1
-        k["t_hbm"] += r["bytes"] / HBM_BW
-        k["t_flop"] += r["flops"] / PEAK[r["dtype"]]
+        n = args.steps * r["calls_per_pass"]
+        k = per_k.setdefault(r["kernel"], {"t": 0.0, "bytes": 0.0, "flops": 0.0, "calls": 0, "points": 0,
+                                           "t_hbm": 0.0, "t_flop": 0.0, "dtype": r["dtype"]})
+        k["t"] += r["us"] * 1e-6 * n
+        k["bytes"] += r["bytes"] * n
+        k["flops"] += r["flops"] * n
+        k["calls"] += n
+        k["points"] += 1
+        k["t_hbm"] += r["bytes"] / HBM_BW * n
+        k["t_flop"] += r["flops"] / PEAK[r["dtype"]] * n
     dom_name, dom = max(per_k.items(), key=lambda kv: kv[1]["t"])
-    dtype_dom = "f32" if "<f32" in dom_name else "bf16"
     if dom["t_hbm"] >= dom["t_flop"]:
         achieved = dom["bytes"] / dom["t"] / 1e9
         roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_BW / 1e9, "unit": "GB/s",
                     "frac": achieved / (HBM_BW / 1e9), "traffic": None}
     else:
         achieved = dom["flops"] / dom["t"] / 1e12
-        roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK[dtype_dom] / 1e12, "unit": "TFLOP/s",
-                    "frac": achieved / (PEAK[dtype_dom] / 1e12), "traffic": None}
+        roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK[dom["dtype"]] / 1e12, "unit": "TFLOP/s",
+                    "frac": achieved / (PEAK[dom["dtype"]] / 1e12), "traffic": None}
     roofline["kernel"] = dom_name
-    roofline["points"] = dom["n"]
-    roofline["avg_launch_us"] = dom["t"] / dom["n"] * 1e6
+    roofline["points"] = dom["points"]
+    roofline["timed_calls"] = dom["calls"]
+    roofline["avg_launch_us"] = dom["t"] / dom["calls"] * 1e6
+    roofline["algorithmic_bytes_per_launch"] = dom["bytes"] / dom["calls"]
     roofline["share_of_sweep_time"] = dom["t"] / sum(v["t"] for v in per_k.values())
     ms_per_step = float(sum(r["us"] for r in points) * 1e-3)
     out = {
@@ -341,8 +367,8 @@ def main():
         "vs_baseline": None,
         "dtype": "f32+bf16 (fp32 accumulate)",
         "data": "synthetic: X, K i.i.d. N(0,1), seeded",
-        "config": {"workload": "KS pattern sweep a{1,2,4,8} x b,c{16..128} x d{1..16}, abd,acd<=8192 "
-                               "(700 patterns) x B{4096,25088} x {fp32,bf16} x {BSF,BSL}",
+        "config": {"workload": "KS pattern sweep a{1,2,4,8} x b,c{16,32,48,64,96,128} x d{1,2,4,8,16}, "
+                               "abd,acd<=8192 (700 patterns) x B{4096,25088} x {fp32,bf16} x {BSF,BSL}",
                    "points": len(points), "sample_every": args.sample, "parallelism": "single GPU"},
         "median_gbps": float(np.median([r["gbps"] for r in points])),
         "median_tflops": float(np.median([r["tflops"] for r in points])),

@@ -213,13 +213,40 @@ ks_status_t run_one(const Problem& p, hipStream_t s) {
   return KS_OK;
 }
 
-std::string describe(const Plan& pl) {
+// Name of the kernel instance a plan launches, written like the demangled
+// symbol without namespace, spaces or parameter list (profiler summaries are
+// matched against it).
+std::string kernel_name(const Problem& p, const Plan& pl) {
+  static const char* tnames[] = {"float", "unsigned short", "_Float16"};
+  const char* t = tnames[p.dtype];
+  const int m = p.b > p.c ? p.b : p.c;
+  const int mx = m <= 2 ? 2 : (m <= 4 ? 4 : (m <= 8 ? 8 : 16));
+  char buf[160];
+  switch (pl.variant) {
+    case V_GENERIC: snprintf(buf, sizeof buf, "ks_generic_kernel<%s>", t); break;
+    case V_VALU_BSL:
+      snprintf(buf, sizeof buf, "ks_valu_bsl_kernel<%s,%d,%d,%d,%d>", t, pl.vec, mx, mx, valu_bsl_unroll(p.b, p.c));
+      break;
+    case V_VALU_BSF: snprintf(buf, sizeof buf, "ks_valu_bsf_kernel<%s,%d,%d,%d>", t, pl.vec, mx, mx); break;
+    case V_MFMA:
+      snprintf(buf, sizeof buf, "ks_mfma_kernel<%s,%d,%d,%d>", t, p.layout, pl.waves_n, pl.waves_m);
+      break;
+    default: snprintf(buf, sizeof buf, "?");
+  }
+  std::string r(buf);
+  r.erase(std::remove(r.begin(), r.end(), ' '), r.end());
+  return r;
+}
+
+std::string describe(const Problem& p, const Plan& pl) {
   static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "mfma"};
   char buf[320];
   snprintf(buf, sizeof buf,
-           "variant=%d name=%s vec=%d bt=%d jg=%d unroll=%d waves_m=%d waves_n=%d lds=%d grid=%u block=%u xcd=%d",
+           "variant=%d name=%s vec=%d bt=%d jg=%d unroll=%d waves_m=%d waves_n=%d lds=%d grid=%u block=%u xcd=%d "
+           "kernel=%s",
            pl.variant, (pl.variant >= 0 && pl.variant < V_COUNT) ? names[pl.variant] : "?", pl.vec, pl.bt, pl.jg,
-           pl.unroll, pl.waves_m, pl.waves_n, pl.lds_bytes, pl.grid, pl.block, pl.xcd_remap);
+           pl.unroll, pl.waves_m, pl.waves_n, pl.lds_bytes, pl.grid, pl.block, pl.xcd_remap,
+           kernel_name(p, pl).c_str());
   return buf;
 }
 
@@ -358,7 +385,7 @@ ks_status_t ks_plan_describe(int64_t a, int64_t b, int64_t c, int64_t d, int64_t
   }
   Plan pl;
   if (!get_plan(p, true, &pl)) return KS_ERR_UNSUPPORTED;
-  snprintf(buf, len, "%s", describe(pl).c_str());
+  snprintf(buf, len, "%s", describe(p, pl).c_str());
   return KS_OK;
 }
 
