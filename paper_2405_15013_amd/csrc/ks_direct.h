@@ -1,0 +1,291 @@
+// Register-direct MFMA kernels for KS patterns whose blocks are dense
+// contractions (b and c multiples of 16).
+//
+// Output-stationary tiling of the paper (Section 4.1, Algorithm 2; kernel
+// sketch of Section 4.2), laid out for CDNA4 wavefronts: every wavefront is an
+// independent work item (see ks_direct_index.h) that streams the X values of
+// its tile from HBM straight into MFMA operand registers with nontemporal
+// vector loads of 4 elements (16 bytes fp32, 8 bytes 16-bit; no LDS, no
+// barriers), reads the packed b x c block(s) of K from L1/L2 as 16-byte A
+// operands, keeps the fp32 accumulators in registers
+// over the whole reduction over l, and stores each output once, directly in
+// the requested layout (BSL: 4-element runs along the batch; BSF: runs of
+// consecutive j, or of consecutive k and j when d <= 4).
+//
+// The products are Yt^T = Kblock * Xt^T on 16 x 16 MFMA tiles: A = 16 rows k
+// of the block, B = the lane's column of X (a batch vector in BSL, a batch row
+// in BSF), reduction over l.  The order of l inside a chunk is any fixed
+// assignment that A and B share: lane group g holds l = LPL*g .. LPL*g+LPL-1,
+// so both operands are contiguous in memory along l (K rows) or get
+// assembled from the lane's loaded vectors (X).
+//   fp32:    v_mfma_f32_16x16x4_f32, LPL = 4 (one MFMA per l of the lane);
+//   16-bit:  v_mfma_f32_16x16x32_{bf16,f16}, LPL = 8, plus one
+//            v_mfma_f32_16x16x16 step with LPL = 4 when c % 32 == 16.
+// The next chunk of l is loaded while the MFMAs of the current one run.
+#pragma once
+#include "ks_common.h"
+#include "ks_direct_index.h"
+#include "ks_internal.h"
+
+namespace ks {
+
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
+typedef short i16x4_t __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
+
+// One MFMA step: acc += A * B where each lane supplies LP values of l.
+template <typename T, int LP> struct DMma;
+template <> struct DMma<float, 4> {
+  // four 16x16x4 steps, one per l of the lane (component t of A and of B)
+  __device__ static __forceinline__ void run(const uint32_t* a, float bt, int t, f32x4& acc) {
+    acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a[t]), bt, acc, 0, 0, 0);
+  }
+};
+template <> struct DMma<bf16_t, 8> {
+  __device__ static __forceinline__ void run(const uint32_t* a, const uint32_t* b, f32x4& acc) {
+    const u32x4 av = {a[0], a[1], a[2], a[3]}, bv = {b[0], b[1], b[2], b[3]};
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, av), __builtin_bit_cast(bf16x8_t, bv),
+                                                  acc, 0, 0, 0);
+  }
+};
+template <> struct DMma<bf16_t, 4> {
+  __device__ static __forceinline__ void run(const uint32_t* a, const uint32_t* b, f32x4& acc) {
+    const u32x2 av = {a[0], a[1]}, bv = {b[0], b[1]};
+    acc = __builtin_amdgcn_mfma_f32_16x16x16bf16_1k(__builtin_bit_cast(i16x4_t, av), __builtin_bit_cast(i16x4_t, bv),
+                                                    acc, 0, 0, 0);
+  }
+};
+template <> struct DMma<_Float16, 8> {
+  __device__ static __forceinline__ void run(const uint32_t* a, const uint32_t* b, f32x4& acc) {
+    const u32x4 av = {a[0], a[1], a[2], a[3]}, bv = {b[0], b[1], b[2], b[3]};
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(__builtin_bit_cast(f16x8_t, av), __builtin_bit_cast(f16x8_t, bv),
+                                                 acc, 0, 0, 0);
+  }
+};
+template <> struct DMma<_Float16, 4> {
+  __device__ static __forceinline__ void run(const uint32_t* a, const uint32_t* b, f32x4& acc) {
+    const u32x2 av = {a[0], a[1]}, bv = {b[0], b[1]};
+    acc = __builtin_amdgcn_mfma_f32_16x16x16f16(__builtin_bit_cast(f16x4_t, av), __builtin_bit_cast(f16x4_t, bv),
+                                                acc, 0, 0, 0);
+  }
+};
+
+// Load NB bytes (16 or 8) at p into w[0 .. NB/4).
+template <int NB, bool NT>
+__device__ __forceinline__ void load_piece(const void* p, uint32_t* w) {
+  if constexpr (NB == 16) {
+    const u32x4 v = NT ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(p))
+                       : *reinterpret_cast<const u32x4*>(p);
+    w[0] = v[0]; w[1] = v[1]; w[2] = v[2]; w[3] = v[3];
+  } else {
+    static_assert(NB == 8, "pieces are 8 or 16 bytes");
+    const u32x2 v = NT ? __builtin_nontemporal_load(reinterpret_cast<const u32x2*>(p))
+                       : *reinterpret_cast<const u32x2*>(p);
+    w[0] = v[0]; w[1] = v[1];
+  }
+}
+
+template <int NB>
+__device__ __forceinline__ void store_piece(void* p, const uint32_t* w) {
+  if constexpr (NB == 16) {
+    const u32x4 v = {w[0], w[1], w[2], w[3]};
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x4*>(p));
+  } else {
+    static_assert(NB == 8, "pieces are 8 or 16 bytes");
+    const u32x2 v = {w[0], w[1]};
+    __builtin_nontemporal_store(v, reinterpret_cast<u32x2*>(p));
+  }
+}
+
+// 16-bit element f of a packed dword array.
+__device__ __forceinline__ uint32_t half_of(const uint32_t* w, int f) {
+  return (f & 1) ? (w[f >> 1] >> 16) : (w[f >> 1] & 0xffffu);
+}
+
+// One chunk of the reduction: LP values of l per lane group (4*LP per chunk).
+// Pointers passed to load() are the lane's bases (ks_direct_index.h).
+template <typename T, int LAYOUT, int V, bool STRIDED, int MT, int LP>
+struct DChunk {
+  static constexpr int S = sizeof(T);
+  static constexpr int VK = LAYOUT == BSL ? 1 : V;  // distinct K blocks per chunk
+  static constexpr int NXW = LP * V * S / 4;         // dwords of X per lane
+  static constexpr int KW = LP * S / 4;              // dwords of one A operand
+  static constexpr int PE = (LAYOUT == BSL || STRIDED) ? V : (LP * V * S < 16 ? LP * V : 16 / S);
+  static constexpr int NP = LP * V / PE;             // X pieces
+  static constexpr int PB = PE * S;                  // bytes per piece
+  uint32_t xw[NXW];
+  uint32_t kw[MT][VK][KW];
+
+  __device__ __forceinline__ void load(const T* __restrict__ xl, int64_t lstride, int64_t qstride,
+                                       const T* __restrict__ kl, int64_t kmstride, int64_t kestride, int l0) {
+    const T* xc = xl + (int64_t)l0 * lstride;
+#pragma unroll
+    for (int q = 0; q < NP; ++q) load_piece<PB, true>(xc + q * qstride, xw + q * (PB / 4));
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int e = 0; e < VK; ++e) load_piece<KW * 4, false>(kl + mt * kmstride + e * kestride + l0, kw[mt][e]);
+  }
+
+  __device__ __forceinline__ void mma(f32x4 (&acc)[MT][V]) const {
+    if constexpr (S == 4) {
+#pragma unroll
+      for (int t = 0; t < LP; ++t)
+#pragma unroll
+        for (int e = 0; e < V; ++e) {
+          const float bt = __uint_as_float(xw[t * V + e]);
+#pragma unroll
+          for (int mt = 0; mt < MT; ++mt) DMma<T, LP>::run(kw[mt][LAYOUT == BSL ? 0 : e], bt, t, acc[mt][e]);
+        }
+    } else {
+#pragma unroll
+      for (int e = 0; e < V; ++e) {
+        // B operand of chain e: the lane's LP values of l for column e,
+        // flat elements t*V + e, two per dword.
+        uint32_t bw[LP / 2];
+#pragma unroll
+        for (int q = 0; q < LP / 2; ++q) {
+          if constexpr (V == 1) {
+            bw[q] = xw[q];
+          } else {
+            bw[q] = half_of(xw, (2 * q) * V + e) | (half_of(xw, (2 * q + 1) * V + e) << 16);
+          }
+        }
+#pragma unroll
+        for (int mt = 0; mt < MT; ++mt) DMma<T, LP>::run(kw[mt][LAYOUT == BSL ? 0 : e], bw, acc[mt][e]);
+      }
+    }
+  }
+};
+
+template <typename T, int LAYOUT, int V, bool STRIDED, int MT>
+__global__ __launch_bounds__(256) void ks_direct_kernel(Problem p, DirectTile t) {
+  constexpr int S = sizeof(T);
+  constexpr int LP = S == 4 ? 4 : 8;
+  constexpr int CH = 4 * LP;  // l values per chunk
+  const int lane = threadIdx.x & 63;
+  const int item = blockIdx.x * t.waves + (threadIdx.x >> 6);
+  if (item >= t.items) return;  // wave-uniform
+  const int n = lane & 15, g = lane >> 4;
+  const DItem it = direct_item(p, t, V, MT, item);
+  const T* __restrict__ x = static_cast<const T*>(p.x);
+  const T* __restrict__ kv = static_cast<const T*>(p.kv);
+  T* __restrict__ y = static_cast<T*>(p.y);
+  const int c = p.c;
+  const int64_t lstride = direct_x_lstride(p);
+  const int64_t kmstride = (int64_t)16 * c, kestride = (int64_t)p.b * c;
+
+  f32x4 acc[MT][V];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int e = 0; e < V; ++e) acc[mt][e] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (c >= CH) {
+    const T* xl = x + direct_x_base(p, it, LP, V, n, g);
+    const T* kl = kv + direct_k_base(p, it, LP, n, g);
+    const int64_t qstride = direct_x_qstride(p, STRIDED, LP, V, S);
+    DChunk<T, LAYOUT, V, STRIDED, MT, LP> cur, nxt;
+    cur.load(xl, lstride, qstride, kl, kmstride, kestride, 0);
+    for (int l0 = 0; l0 + CH <= c; l0 += CH) {
+      const bool more = l0 + 2 * CH <= c;
+      if (more) nxt.load(xl, lstride, qstride, kl, kmstride, kestride, l0 + CH);
+      cur.mma(acc);
+      if (more) cur = nxt;
+    }
+  }
+  if constexpr (S == 2) {
+    if (c % CH) {  // c % 32 == 16: last 16 values of l with the 16x16x16 step
+      const T* xl = x + direct_x_base(p, it, 4, V, n, g);
+      const T* kl = kv + direct_k_base(p, it, 4, n, g);
+      const int64_t qstride = direct_x_qstride(p, STRIDED, 4, V, S);
+      DChunk<T, LAYOUT, V, STRIDED, MT, 4> tail;
+      tail.load(xl, lstride, qstride, kl, kmstride, kestride, c - 16);
+      tail.mma(acc);
+    }
+  }
+
+  // Epilogue: per M-tile the lane's 4 x V outputs, flat r*V + e, stored as
+  // pieces of YPE contiguous elements (ks_direct_index.h, direct_y_off).
+  if (!direct_lane_valid(p, it, V, n)) return;
+  constexpr int YPE = (LAYOUT == BSL || STRIDED) ? V : (4 * V * S < 16 ? 4 * V : 16 / S);
+  constexpr int YNP = 4 * V / YPE;
+  constexpr int YPB = YPE * S;
+  T* yl = y + direct_y_base(p, it, V, n, g);
+  const int64_t ymstride = direct_y_mstride(p), yqstride = direct_y_qstride(p, STRIDED, V, S);
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+#pragma unroll
+    for (int q = 0; q < YNP; ++q) {
+      uint32_t w[YPB / 4];
+      if constexpr (S == 4) {
+#pragma unroll
+        for (int u = 0; u < YPE; ++u) {
+          const int f = q * YPE + u;
+          w[u] = __float_as_uint(acc[mt][f % V][f / V]);
+        }
+      } else {
+#pragma unroll
+        for (int u = 0; u < YPE; u += 2) {
+          const int f0 = q * YPE + u, f1 = f0 + 1;
+          const uint32_t lo = __builtin_bit_cast(uint16_t, from_f32<T>(acc[mt][f0 % V][f0 / V]));
+          const uint32_t hi = __builtin_bit_cast(uint16_t, from_f32<T>(acc[mt][f1 % V][f1 / V]));
+          w[u / 2] = lo | (hi << 16);
+        }
+      }
+      store_piece<YPB>(yl + mt * ymstride + q * yqstride, w);
+    }
+  }
+}
+
+// Vector width along the batch (BSL) and largest j-run (BSF): 4 elements, i.e.
+// 16-byte fp32 or 8-byte 16-bit pieces.
+constexpr int kDirectVec = 4;
+
+// Largest M-tile count per wave for a (storage type, layout, V) instance set.
+constexpr int direct_mt_max(int esize, int layout, int V) {
+  return esize == 4 ? ((layout == BSL || V <= 2) ? 4 : 2) : ((layout == BSL || V <= 2) ? 4 : 2);
+}
+
+template <typename T, int LAYOUT, int V, bool STRIDED, int MT>
+hipError_t launch_direct_inst(const Problem& p, const DirectTile& t, unsigned grid, hipStream_t s) {
+  hipLaunchKernelGGL((ks_direct_kernel<T, LAYOUT, V, STRIDED, MT>), dim3(grid), dim3(64 * t.waves), 0, s, p, t);
+  return hipGetLastError();
+}
+
+template <typename T, int LAYOUT, int V, bool STRIDED>
+hipError_t launch_direct_mt(const Problem& p, const DirectTile& t, int mt, unsigned grid, hipStream_t s) {
+  constexpr int MX = direct_mt_max(sizeof(T), LAYOUT, V);
+  switch (mt) {
+    case 1: return launch_direct_inst<T, LAYOUT, V, STRIDED, 1>(p, t, grid, s);
+    case 2: if constexpr (MX >= 2) return launch_direct_inst<T, LAYOUT, V, STRIDED, 2>(p, t, grid, s); break;
+    case 3: if constexpr (MX >= 3) return launch_direct_inst<T, LAYOUT, V, STRIDED, 3>(p, t, grid, s); break;
+    case 4: if constexpr (MX >= 4) return launch_direct_inst<T, LAYOUT, V, STRIDED, 4>(p, t, grid, s); break;
+    default: break;
+  }
+  return hipErrorInvalidValue;
+}
+
+// All instances of one storage type.
+template <typename T>
+hipError_t launch_direct_type(const Problem& p, const DirectTile& t, int V, bool strided, int mt, unsigned grid,
+                              hipStream_t s) {
+  if (p.layout == BSL) {
+    if (V != kDirectVec || strided) return hipErrorInvalidValue;
+    return launch_direct_mt<T, BSL, kDirectVec, false>(p, t, mt, grid, s);
+  }
+  if (strided) {
+    if (V != kDirectVec) return hipErrorInvalidValue;
+    return launch_direct_mt<T, BSF, kDirectVec, true>(p, t, mt, grid, s);
+  }
+  switch (V) {
+    case 1: return launch_direct_mt<T, BSF, 1, false>(p, t, mt, grid, s);
+    case 2: return launch_direct_mt<T, BSF, 2, false>(p, t, mt, grid, s);
+    case 4: return launch_direct_mt<T, BSF, 4, false>(p, t, mt, grid, s);
+    default: break;
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace ks

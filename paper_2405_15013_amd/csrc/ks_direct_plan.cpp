@@ -1,0 +1,93 @@
+// Planner and launcher of the register-direct MFMA kernels (ks_direct.h).
+//
+// A plan fixes the vector width V (4 elements along the batch in BSL; the
+// j-run min(d, 4) in BSF), the number MT of 16-row M-tiles per wavefront,
+// and the wavefronts per workgroup.  MT trades X re-reads (b / (16*MT)
+// wavefronts read the same X tile) against registers and parallelism.
+#include "ks_direct_index.h"
+#include "ks_internal.h"
+
+namespace ks {
+
+hipError_t launch_direct_f32(const Problem& p, const DirectTile& t, int V, bool strided, int mt, unsigned grid,
+                             hipStream_t s);
+hipError_t launch_direct_bf16(const Problem& p, const DirectTile& t, int V, bool strided, int mt, unsigned grid,
+                              hipStream_t s);
+hipError_t launch_direct_f16(const Problem& p, const DirectTile& t, int V, bool strided, int mt, unsigned grid,
+                             hipStream_t s);
+
+// Largest MT instantiated for (storage size, layout, V); keep in sync with
+// direct_mt_max() in ks_direct.h.
+static int mt_max(int esize, int layout, int V) {
+  return esize == 4 ? ((layout == BSL || V <= 2) ? 4 : 2) : ((layout == BSL || V <= 2) ? 4 : 2);
+}
+
+DirectTile direct_tile(const Problem& p, const Plan& pl) {
+  DirectTile t;
+  const int V = pl.vec, MT = pl.waves_m;
+  t.kgroups = p.b / (16 * MT);
+  t.jgroups = p.layout == BSL ? p.d : p.d / V;
+  const int span = p.layout == BSL ? 16 * V : 16;
+  t.nbt = (p.batch + span - 1) / span;
+  t.items = t.nbt * p.a * t.jgroups * t.kgroups;
+  t.waves = (int)pl.block / 64;
+  return t;
+}
+
+bool plan_direct(const Problem& p, bool al16, Plan* pl) {
+  if (!al16 || p.b % 16 || p.c % 16) return false;
+  const int s = p.dtype == F32 ? 4 : 2;
+  const int vec = 4;  // kDirectVec in ks_direct.h
+  int V;
+  bool strided = false;
+  if (p.layout == BSL) {
+    V = vec;
+    if (p.batch % V) return false;
+  } else {
+    V = p.d < vec ? p.d : vec;
+    if (V != 1 && V != 2 && V != 4) return false;
+    if (p.d % V) return false;
+    strided = V < p.d;
+  }
+  const int kt = p.b / 16;  // M-tiles per block
+  const int span = p.layout == BSL ? 16 * V : 16;
+  const int64_t nbt = (p.batch + span - 1) / span;
+  const int64_t per_k = nbt * p.a * (p.layout == BSL ? p.d : p.d / V);
+  // Largest MT that still leaves >= 2048 wavefronts (8 per CU); otherwise the
+  // MT giving the most wavefronts.
+  int best = 0;
+  for (int mt = mt_max(s, p.layout, V); mt >= 1; --mt) {
+    if (kt % mt) continue;
+    best = mt;
+    if (per_k * (kt / mt) >= 2048) break;
+  }
+  const int64_t items = per_k * (kt / best);
+  const int waves = items >= 4096 ? 4 : (items >= 1024 ? 2 : 1);
+  const int64_t grid = (items + waves - 1) / waves;
+  if (items > 0x7fffffff || grid > 0x7fffffff) return false;
+  pl->variant = V_DIRECT;
+  pl->vec = V;
+  pl->unroll = strided ? 1 : 0;
+  pl->waves_m = best;
+  pl->waves_n = kt / best;
+  pl->bt = span;
+  pl->jg = p.layout == BSL ? 1 : V;
+  pl->lds_bytes = 0;
+  pl->block = 64u * waves;
+  pl->grid = (unsigned)grid;
+  pl->xcd_remap = 0;
+  return true;
+}
+
+hipError_t launch_direct(const Problem& p, const Plan& pl, hipStream_t s) {
+  const DirectTile t = direct_tile(p, pl);
+  const bool strided = pl.unroll != 0;
+  switch (p.dtype) {
+    case F32: return launch_direct_f32(p, t, pl.vec, strided, pl.waves_m, pl.grid, s);
+    case BF16: return launch_direct_bf16(p, t, pl.vec, strided, pl.waves_m, pl.grid, s);
+    case F16: return launch_direct_f16(p, t, pl.vec, strided, pl.waves_m, pl.grid, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace ks

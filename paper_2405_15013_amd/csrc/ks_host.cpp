@@ -104,12 +104,17 @@ bool plan_valu_bsf(const Problem& p, bool al16, Plan* pl) {
 
 bool plan_mfma(const Problem& p, bool al16, Plan* pl);
 
+}  // namespace
+bool plan_direct(const Problem& p, bool al16, Plan* pl);
+namespace {
+
 bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
   switch (v) {
     case V_GENERIC: return plan_generic(p, pl);
     case V_VALU_BSL: return plan_valu_bsl(p, al16, pl);
     case V_VALU_BSF: return plan_valu_bsf(p, al16, pl);
     case V_MFMA: return plan_mfma(p, al16, pl);
+    case V_DIRECT: return plan_direct(p, al16, pl);
     default: return false;
   }
 }
@@ -118,6 +123,7 @@ bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
 // dense contraction; VALU kernels for small blocks; the generic kernel for
 // whatever is left.
 bool plan_auto(const Problem& p, bool al16, Plan* pl) {
+  if (plan_direct(p, al16, pl)) return true;
   if (plan_mfma(p, al16, pl)) return true;
   if (p.layout == BSL && plan_valu_bsl(p, al16, pl)) return true;
   if (p.layout == BSF && plan_valu_bsf(p, al16, pl)) return true;
@@ -169,6 +175,7 @@ hipError_t launch(const Problem& p, const Plan& pl, hipStream_t s) {
     case V_VALU_BSL: return launch_valu_bsl(p, pl, s);
     case V_VALU_BSF: return launch_valu_bsf(p, pl, s);
     case V_MFMA: return launch_mfma(p, pl, s);
+    case V_DIRECT: return launch_direct(p, pl, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -231,6 +238,10 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
     case V_MFMA:
       snprintf(buf, sizeof buf, "ks_mfma_kernel<%s,%d,%d,%d>", t, p.layout, pl.waves_n, pl.waves_m);
       break;
+    case V_DIRECT:
+      snprintf(buf, sizeof buf, "ks_direct_kernel<%s,%d,%d,%s,%d>", t, p.layout, pl.vec, pl.unroll ? "true" : "false",
+               pl.waves_m);
+      break;
     default: snprintf(buf, sizeof buf, "?");
   }
   std::string r(buf);
@@ -239,7 +250,7 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
 }
 
 std::string describe(const Problem& p, const Plan& pl) {
-  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "mfma"};
+  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "mfma", "direct"};
   char buf[320];
   snprintf(buf, sizeof buf,
            "variant=%d name=%s vec=%d bt=%d jg=%d unroll=%d waves_m=%d waves_n=%d lds=%d grid=%u block=%u xcd=%d "

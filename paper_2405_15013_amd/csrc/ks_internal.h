@@ -1,5 +1,5 @@
 // Internal interface between the host planner (ks_host.cpp) and the HIP
-// kernels (ks_kernels.hip).  Not part of the public ABI.
+// kernels.  Not part of the public ABI.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <cstdint>
@@ -15,8 +15,9 @@ enum Variant : int {
   V_GENERIC = 0,   // one thread per output element, any pattern
   V_VALU_BSL = 1,  // VALU streaming, batch-size-last, small b and c
   V_VALU_BSF = 2,  // VALU, batch-size-first, small b and c
-  V_MFMA = 3,      // MFMA block GEMM, both layouts, b and c multiples of 16
-  V_COUNT = 4
+  V_MFMA = 3,      // MFMA block GEMM through LDS, both layouts, b and c multiples of 16
+  V_DIRECT = 4,    // register-direct MFMA, one work item per wavefront, b and c multiples of 16
+  V_COUNT = 5
 };
 
 // Problem description shared by all kernels.  Sizes fit in int32 (checked by
@@ -53,6 +54,7 @@ hipError_t launch_generic(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_valu_bsl(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_valu_bsf(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_mfma(const Problem& p, const Plan& pl, hipStream_t s);
+hipError_t launch_direct(const Problem& p, const Plan& pl, hipStream_t s);
 
 }  // namespace ks
 

@@ -14,8 +14,12 @@
 #include "../../include/ks.h"
 #include "ks_internal.h"
 #include "ks_mfma_index.h"
+#include "ks_direct_index.h"
 
 namespace ks {
+
+// Defined in ks_direct_plan.cpp.
+DirectTile direct_tile(const Problem& p, const Plan& pl);
 
 // Defined in ks_host.cpp.
 bool plan_for_verify(int64_t a, int64_t b, int64_t c, int64_t d, int64_t batch, int layout, int dtype, Problem* p,
@@ -192,6 +196,64 @@ bool verify_mfma(Checker& ck, const Plan& pl) {
   return ck.err.empty();
 }
 
+
+bool verify_direct(Checker& ck, const Plan& pl) {
+  const Problem& p = ck.p;
+  const DirectTile t = direct_tile(p, pl);
+  const int V = pl.vec, MT = pl.waves_m, S = p.dtype == F32 ? 4 : 2;
+  const bool strided = pl.unroll != 0;
+  const int LP = S == 4 ? 4 : 8, CH = 4 * LP;
+  if (t.kgroups * 16 * MT != p.b) return ck.fail("M-tiles do not cover b", p.b);
+  if (p.c % 16) return ck.fail("c not a multiple of 16", p.c);
+  if (t.waves < 1 || t.waves > 4 || (int)pl.block != 64 * t.waves) return ck.fail("bad workgroup size", pl.block);
+  if ((int64_t)pl.grid * t.waves < t.items) return ck.fail("grid does not cover the items", pl.grid);
+  if (p.layout == BSF && (p.d % V || (!strided && V != p.d))) return ck.fail("bad j-vector", V);
+  if (p.layout == BSL && p.batch % V) return ck.fail("batch not a multiple of the vector width", p.batch);
+  // chunks: (l0, values of l per lane group)
+  int chunks[16][2], nch = 0;
+  for (int l0 = 0; l0 + CH <= p.c; l0 += CH) { chunks[nch][0] = l0; chunks[nch][1] = LP; ++nch; }
+  if (S == 2 && p.c % CH) { chunks[nch][0] = p.c - 16; chunks[nch][1] = 4; ++nch; }
+  if (nch == 0) return ck.fail("no chunk covers c", p.c);
+  const int VK = p.layout == BSL ? 1 : V;
+  for (int item = 0; item < t.items && ck.err.empty(); ++item) {
+    const DItem it = direct_item(p, t, V, MT, item);
+    for (int ci = 0; ci < nch; ++ci) {
+      const int l0 = chunks[ci][0], lp = chunks[ci][1];
+      const int np = direct_x_pieces(p.layout, strided, lp, V, S);
+      const int pe = direct_x_piece_elems(p.layout, strided, lp, V, S);
+      if (pe * S != 16 && pe * S != 8) return ck.fail("X piece is not 8 or 16 bytes", pe * S);
+      if (np * pe != lp * V) return ck.fail("X pieces do not tile the lane block", np);
+      for (int lane = 0; lane < 64; ++lane) {
+        const int n = lane & 15, g = lane >> 4;
+        for (int q = 0; q < np; ++q) {
+          const int64_t off = direct_x_off(p, it, strided, lp, V, S, l0, n, g, q);
+          if (off < 0) continue;
+          if ((off * S) % (pe * S)) return ck.fail("X piece not aligned to its size", off);
+          ck.read_x(off, pe);
+        }
+        for (int mt = 0; mt < MT; ++mt)
+          for (int e = 0; e < VK; ++e) {
+            const int64_t off = direct_k_off(p, it, lp, l0, n, g, mt, e);
+            if ((off * S) % (lp * S)) return ck.fail("K operand not aligned to its size", off);
+            ck.read_k(off, lp);
+          }
+      }
+    }
+    const int ynp = direct_y_pieces(p.layout, strided, V, S);
+    const int ype = direct_y_piece_elems(p.layout, strided, V, S);
+    if (ype * S != 16 && ype * S != 8) return ck.fail("Y piece is not 8 or 16 bytes", ype * S);
+    for (int mt = 0; mt < MT; ++mt)
+      for (int lane = 0; lane < 64; ++lane)
+        for (int q = 0; q < ynp; ++q) {
+          const int64_t off = direct_y_off(p, it, strided, V, S, mt, lane & 15, lane >> 4, q);
+          if (off < 0) continue;
+          if ((off * S) % (ype * S)) return ck.fail("Y piece not aligned to its size", off);
+          ck.write_y(off, ype);
+        }
+  }
+  return ck.err.empty();
+}
+
 }  // namespace
 }  // namespace ks
 
@@ -214,6 +276,7 @@ extern "C" ks_status_t ks_plan_verify(int64_t a, int64_t b, int64_t c, int64_t d
     case V_VALU_BSL: ok = verify_valu_bsl(ck, pl); break;
     case V_VALU_BSF: ok = verify_valu_bsf(ck, pl); break;
     case V_MFMA: ok = verify_mfma(ck, pl); break;
+    case V_DIRECT: ok = verify_direct(ck, pl); break;
     default: ck.fail("unknown variant", pl.variant);
   }
   if (ok) ok = ck.coverage();

@@ -12,7 +12,7 @@ from parity_util import TOL, case, from_device, nan_tensor, oracle_y, rel_err, t
 
 pytestmark = pytest.mark.gpu
 
-VARIANTS = {"generic": 0, "valu_bsl": 1, "valu_bsf": 2, "mfma": 3}
+VARIANTS = {"generic": 0, "valu_bsl": 1, "valu_bsf": 2, "mfma": 3, "direct": 4}
 
 
 def run_gpu(pattern, x_logical, kv, batch, dtype, layout, variant=None, x_offset=0, y_offset=0):
@@ -169,14 +169,14 @@ def test_empty_batch(layout):
     assert ks.ks_matmul(2, 3, 3, 2, kd, x, y, 0, layout, "f32") == 0
 
 
-# --- the pattern sweep (every 50th pattern), sampled at full batch ------------
+# --- the pattern sweep (every 13th pattern), sampled at full batch ------------
 
 def sweep_patterns():
     return [(a, b, c, d) for a in (1, 2, 4, 8) for b in (16, 32, 48, 64, 96, 128) for c in (16, 32, 48, 64, 96, 128)
             for d in (1, 2, 4, 8, 16) if a * b * d <= 8192 and a * c * d <= 8192]
 
 
-SWEEP_SAMPLE = sweep_patterns()[::50]
+SWEEP_SAMPLE = sweep_patterns()[::13]
 
 
 def check_sampled(pattern, batch, dtype, layout, cfg, nsample=4096, variant=None):
@@ -225,18 +225,29 @@ def test_sweep_ragged_batch_full(pattern, dtype, layout):
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 @pytest.mark.parametrize("layout", ["bsf", "bsl"])
 def test_mfma_forced(pattern, dtype, layout):
-    import paper_2405_15013_amd as ks
-    desc = ks.ks_plan_describe(*pattern, 256, layout, dtype)
-    assert "name=mfma" in desc, desc
     check(pattern, 256, dtype, layout, cfg=9, variant=3, kdist="normal")
+
+
+@pytest.mark.parametrize("pattern", [(1, 32, 32, 32), (32, 32, 32, 1), (6, 64, 16, 8), (6, 16, 64, 8),
+                                     (2, 48, 80, 2), (1, 128, 16, 16), (8, 16, 128, 4), (3, 96, 48, 1),
+                                     (1, 16, 112, 8), (2, 64, 128, 2)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+@pytest.mark.parametrize("batch", [256, 72])
+def test_direct_forced(pattern, dtype, layout, batch):
+    """The register-direct MFMA kernel on every j-vector mode (d = 1, 2, 4 and
+    d > 4), c % 32 == 16 tails of the 16-bit path, and a ragged batch."""
+    check(pattern, batch, dtype, layout, cfg=11, variant=4, kdist="normal")
 
 
 @pytest.mark.parametrize("pattern", [(1, 32, 32, 32), (6, 64, 16, 8), (4, 96, 48, 2)])
 @pytest.mark.parametrize("layout", ["bsf", "bsl"])
 def test_mfma_generic_agree(pattern, layout):
-    """The MFMA and generic kernels agree on the same inputs (both within the
-    oracle tolerance, and close to each other)."""
+    """The MFMA, register-direct and generic kernels agree on the same inputs
+    (each within the oracle tolerance, and close to each other)."""
     x, kv, _, _ = case(10, pattern, 512, "f32", "normal", "normal")
     y_m = run_gpu(pattern, x, kv, 512, "f32", layout, variant=3)
+    y_d = run_gpu(pattern, x, kv, 512, "f32", layout, variant=4)
     y_g = run_gpu(pattern, x, kv, 512, "f32", layout, variant=0)
     assert rel_err(y_m, y_g) <= 1e-5
+    assert rel_err(y_d, y_g) <= 1e-5

@@ -44,7 +44,28 @@ def test_full_size_plans(pattern, batch, layout):
     assert st == 0, rep
 
 
-@pytest.mark.parametrize("variant", [0, 1, 2, 3])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_all_sweep_plans_ragged_batch(dtype, layout):
+    """Every sweep pattern, a batch that leaves a partial tile in both layouts."""
+    bad = []
+    for pattern in sweep_patterns():
+        st, rep = ks.ks_plan_verify(*pattern, 72, layout, dtype)
+        if st != 0:
+            bad.append((pattern, rep))
+    assert not bad, bad[:5]
+
+
+def test_sweep_plans_use_direct_kernel():
+    """The register-direct MFMA kernel covers the whole sweep (aligned buffers)."""
+    for pattern in sweep_patterns()[::7]:
+        for layout in ("bsf", "bsl"):
+            for dtype in ("f32", "bf16", "f16"):
+                desc = ks.ks_plan_describe(*pattern, 4096, layout, dtype)
+                assert "name=direct" in desc, (pattern, layout, dtype, desc)
+
+
+@pytest.mark.parametrize("variant", [0, 1, 2, 3, 4])
 def test_forced_variants(variant):
     """Every variant that accepts a shape produces a valid launch for it."""
     ks.ks_force_variant(variant)
