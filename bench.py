@@ -179,6 +179,10 @@ class Runner:
             if st != 0:
                 raise RuntimeError("ks_matmul failed: %s" % self.ks.ks_status_string(st))
 
+        try:
+            self.ks.ks_plan_describe(a, b, c, d, batch, layout, dtype)
+        except self.ks.KsError:
+            return None  # the forced variant cannot run this point
         t, nsets = self.time_calls(xb + yb, nsets_pool, launch)
         nbytes, flops, t_roof, bound = roof(pattern, batch, dtype)
         desc = self.ks.ks_plan_describe(a, b, c, d, batch, layout, dtype)
@@ -257,6 +261,8 @@ def main():
     ap.add_argument("--points-out", default=os.path.join(ROOT, "gpurun_out", "bench_points.jsonl"))
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-families", action="store_true")
+    ap.add_argument("--variant", type=int, default=-1,
+                    help="force a kernel variant for the sweep points (tuning; points it cannot run are skipped)")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the KS matmul path shards over the batch with no "
@@ -274,17 +280,23 @@ def main():
     keep = np.random.default_rng(7).permutation(len(grid))[::args.sample]
     keep = set(int(k) for k in keep)
     points = []
+    skipped = 0
     with open(args.points_out, "w") as fout:
+        run.ks.ks_force_variant(args.variant if args.variant >= 0 else None)
         for idx, (dtype, batch, layout, p) in enumerate(grid):
             if idx not in keep:
                 continue
             run.fill(dtype)
             r = run.point(p, batch, dtype, layout)
+            if r is None:
+                skipped += 1
+                continue
             points.append(r)
             fout.write(json.dumps(r) + "\n")
             if len(points) % 200 == 0:
                 print("[bench] %d/%d sweep points, %.0f s" % (len(points), len(keep), time.time() - t_start),
                       file=sys.stderr, flush=True)
+        run.ks.ks_force_variant(None)
         families = {}
         if not args.no_families:
             run.fill("f32")
@@ -370,6 +382,8 @@ def main():
         "config": {"workload": "KS pattern sweep a{1,2,4,8} x b,c{16,32,48,64,96,128} x d{1,2,4,8,16}, "
                                "abd,acd<=8192 (700 patterns) x B{4096,25088} x {fp32,bf16} x {BSF,BSL}",
                    "points": len(points), "sample_every": args.sample, "parallelism": "single GPU"},
+        "forced_variant": args.variant if args.variant >= 0 else None,
+        "skipped_points": skipped,
         "median_gbps": float(np.median([r["gbps"] for r in points])),
         "median_tflops": float(np.median([r["tflops"] for r in points])),
         "frac_quantiles_10_25_50_75_90": [float(np.quantile(fr, q)) for q in (0.1, 0.25, 0.5, 0.75, 0.9)],

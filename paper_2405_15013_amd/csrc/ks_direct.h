@@ -103,116 +103,52 @@ __device__ __forceinline__ uint32_t half_of(const uint32_t* w, int f) {
   return (f & 1) ? (w[f >> 1] >> 16) : (w[f >> 1] & 0xffffu);
 }
 
-// One chunk of the reduction: LP values of l per lane group (4*LP per chunk).
-// Pointers passed to load() are the lane's bases (ks_direct_index.h).
-template <typename T, int LAYOUT, int V, bool STRIDED, int MT, int LP>
-struct DChunk {
-  static constexpr int S = sizeof(T);
-  static constexpr int VK = LAYOUT == BSL ? 1 : V;  // distinct K blocks per chunk
-  static constexpr int NXW = LP * V * S / 4;         // dwords of X per lane
-  static constexpr int KW = LP * S / 4;              // dwords of one A operand
-  static constexpr int PE = (LAYOUT == BSL || STRIDED) ? V : (LP * V * S < 16 ? LP * V : 16 / S);
-  static constexpr int NP = LP * V / PE;             // X pieces
-  static constexpr int PB = PE * S;                  // bytes per piece
-  uint32_t xw[NXW];
-  uint32_t kw[MT][VK][KW];
-
-  __device__ __forceinline__ void load(const T* __restrict__ xl, int64_t lstride, int64_t qstride,
-                                       const T* __restrict__ kl, int64_t kmstride, int64_t kestride, int l0) {
-    const T* xc = xl + (int64_t)l0 * lstride;
+// MFMAs of one chunk: xw holds the lane's LP x V block of X (flat t*V + e),
+// kw[mt][e] the A operands (LP values of l of K row k0 + 16*mt + m; one block
+// in BSL, block j0 + e in BSF).
+template <typename T, int LAYOUT, int V, int MT, int LP>
+__device__ __forceinline__ void direct_mma(const uint32_t* xw, const uint32_t (&kw)[MT][LAYOUT == BSL ? 1 : V]
+                                           [LP * sizeof(T) / 4], f32x4 (&acc)[MT][V]) {
+  if constexpr (sizeof(T) == 4) {
 #pragma unroll
-    for (int q = 0; q < NP; ++q) load_piece<PB, true>(xc + q * qstride, xw + q * (PB / 4));
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int e = 0; e < VK; ++e) load_piece<KW * 4, false>(kl + mt * kmstride + e * kestride + l0, kw[mt][e]);
-  }
-
-  __device__ __forceinline__ void mma(f32x4 (&acc)[MT][V]) const {
-    if constexpr (S == 4) {
-#pragma unroll
-      for (int t = 0; t < LP; ++t)
-#pragma unroll
-        for (int e = 0; e < V; ++e) {
-          const float bt = __uint_as_float(xw[t * V + e]);
-#pragma unroll
-          for (int mt = 0; mt < MT; ++mt) DMma<T, LP>::run(kw[mt][LAYOUT == BSL ? 0 : e], bt, t, acc[mt][e]);
-        }
-    } else {
+    for (int t = 0; t < LP; ++t)
 #pragma unroll
       for (int e = 0; e < V; ++e) {
-        // B operand of chain e: the lane's LP values of l for column e,
-        // flat elements t*V + e, two per dword.
-        uint32_t bw[LP / 2];
+        const float bt = __uint_as_float(xw[t * V + e]);
 #pragma unroll
-        for (int q = 0; q < LP / 2; ++q) {
-          if constexpr (V == 1) {
-            bw[q] = xw[q];
-          } else {
-            bw[q] = half_of(xw, (2 * q) * V + e) | (half_of(xw, (2 * q + 1) * V + e) << 16);
-          }
-        }
-#pragma unroll
-        for (int mt = 0; mt < MT; ++mt) DMma<T, LP>::run(kw[mt][LAYOUT == BSL ? 0 : e], bw, acc[mt][e]);
+        for (int mt = 0; mt < MT; ++mt) DMma<T, LP>::run(kw[mt][LAYOUT == BSL ? 0 : e], bt, t, acc[mt][e]);
       }
+  } else {
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      // B operand of chain e: the lane's LP values of l for column e,
+      // flat elements t*V + e, two per dword.
+      uint32_t bw[LP / 2];
+#pragma unroll
+      for (int q = 0; q < LP / 2; ++q) {
+        if constexpr (V == 1) {
+          bw[q] = xw[q];
+        } else {
+          bw[q] = half_of(xw, (2 * q) * V + e) | (half_of(xw, (2 * q + 1) * V + e) << 16);
+        }
+      }
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) DMma<T, LP>::run(kw[mt][LAYOUT == BSL ? 0 : e], bw, acc[mt][e]);
     }
   }
-};
+}
 
+// Stores of the lane's outputs: per M-tile 4 x V values, flat r*V + e, as
+// pieces of YPE contiguous elements (ks_direct_index.h, direct_y_off).
 template <typename T, int LAYOUT, int V, bool STRIDED, int MT>
-__global__ __launch_bounds__(256) void ks_direct_kernel(Problem p, DirectTile t) {
+__device__ __forceinline__ void direct_store(const Problem& p, const DItem& it, int n, int g,
+                                             const f32x4 (&acc)[MT][V]) {
   constexpr int S = sizeof(T);
-  constexpr int LP = S == 4 ? 4 : 8;
-  constexpr int CH = 4 * LP;  // l values per chunk
-  const int lane = threadIdx.x & 63;
-  const int item = blockIdx.x * t.waves + (threadIdx.x >> 6);
-  if (item >= t.items) return;  // wave-uniform
-  const int n = lane & 15, g = lane >> 4;
-  const DItem it = direct_item(p, t, V, MT, item);
-  const T* __restrict__ x = static_cast<const T*>(p.x);
-  const T* __restrict__ kv = static_cast<const T*>(p.kv);
-  T* __restrict__ y = static_cast<T*>(p.y);
-  const int c = p.c;
-  const int64_t lstride = direct_x_lstride(p);
-  const int64_t kmstride = (int64_t)16 * c, kestride = (int64_t)p.b * c;
-
-  f32x4 acc[MT][V];
-#pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-    for (int e = 0; e < V; ++e) acc[mt][e] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  if (c >= CH) {
-    const T* xl = x + direct_x_base(p, it, LP, V, n, g);
-    const T* kl = kv + direct_k_base(p, it, LP, n, g);
-    const int64_t qstride = direct_x_qstride(p, STRIDED, LP, V, S);
-    DChunk<T, LAYOUT, V, STRIDED, MT, LP> cur, nxt;
-    cur.load(xl, lstride, qstride, kl, kmstride, kestride, 0);
-    for (int l0 = 0; l0 + CH <= c; l0 += CH) {
-      const bool more = l0 + 2 * CH <= c;
-      if (more) nxt.load(xl, lstride, qstride, kl, kmstride, kestride, l0 + CH);
-      cur.mma(acc);
-      if (more) cur = nxt;
-    }
-  }
-  if constexpr (S == 2) {
-    if (c % CH) {  // c % 32 == 16: last 16 values of l with the 16x16x16 step
-      const T* xl = x + direct_x_base(p, it, 4, V, n, g);
-      const T* kl = kv + direct_k_base(p, it, 4, n, g);
-      const int64_t qstride = direct_x_qstride(p, STRIDED, 4, V, S);
-      DChunk<T, LAYOUT, V, STRIDED, MT, 4> tail;
-      tail.load(xl, lstride, qstride, kl, kmstride, kestride, c - 16);
-      tail.mma(acc);
-    }
-  }
-
-  // Epilogue: per M-tile the lane's 4 x V outputs, flat r*V + e, stored as
-  // pieces of YPE contiguous elements (ks_direct_index.h, direct_y_off).
   if (!direct_lane_valid(p, it, V, n)) return;
   constexpr int YPE = (LAYOUT == BSL || STRIDED) ? V : (4 * V * S < 16 ? 4 * V : 16 / S);
   constexpr int YNP = 4 * V / YPE;
   constexpr int YPB = YPE * S;
-  T* yl = y + direct_y_base(p, it, V, n, g);
+  T* yl = static_cast<T*>(p.y) + direct_y_base(p, it, V, n, g);
   const int64_t ymstride = direct_y_mstride(p), yqstride = direct_y_qstride(p, STRIDED, V, S);
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
@@ -239,6 +175,152 @@ __global__ __launch_bounds__(256) void ks_direct_kernel(Problem p, DirectTile t)
   }
 }
 
+// One chunk of the reduction: LP values of l per lane group (4*LP per chunk).
+// Pointers passed to load() are the lane's bases (ks_direct_index.h).
+template <typename T, int LAYOUT, int V, bool STRIDED, int MT, int LP>
+struct DChunk {
+  static constexpr int S = sizeof(T);
+  static constexpr int VK = LAYOUT == BSL ? 1 : V;  // distinct K blocks per chunk
+  static constexpr int NXW = LP * V * S / 4;         // dwords of X per lane
+  static constexpr int KW = LP * S / 4;              // dwords of one A operand
+  static constexpr int PE = (LAYOUT == BSL || STRIDED) ? V : (LP * V * S < 16 ? LP * V : 16 / S);
+  static constexpr int NP = LP * V / PE;             // X pieces
+  static constexpr int PB = PE * S;                  // bytes per piece
+  uint32_t xw[NXW];
+  uint32_t kw[MT][VK][KW];
+
+  // ntx: X is read by this wavefront only (one k-group), so it is streamed
+  // with nontemporal loads; otherwise the k-group neighbours re-read it from
+  // the caches.
+  __device__ __forceinline__ void load(const T* __restrict__ xl, int64_t lstride, int64_t qstride,
+                                       const T* __restrict__ kl, int64_t kmstride, int64_t kestride, int l0, bool ntx) {
+    const T* xc = xl + (int64_t)l0 * lstride;
+    if (ntx) {
+#pragma unroll
+      for (int q = 0; q < NP; ++q) load_piece<PB, true>(xc + q * qstride, xw + q * (PB / 4));
+    } else {
+#pragma unroll
+      for (int q = 0; q < NP; ++q) load_piece<PB, false>(xc + q * qstride, xw + q * (PB / 4));
+    }
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int e = 0; e < VK; ++e) load_piece<KW * 4, false>(kl + mt * kmstride + e * kestride + l0, kw[mt][e]);
+  }
+
+  __device__ __forceinline__ void mma(f32x4 (&acc)[MT][V]) const { direct_mma<T, LAYOUT, V, MT, LP>(xw, kw, acc); }
+};
+
+template <typename T, int LAYOUT, int V, bool STRIDED, int MT>
+__global__ __launch_bounds__(256) void ks_direct_kernel(Problem p, DirectTile t) {
+  constexpr int S = sizeof(T);
+  constexpr int LP = S == 4 ? 4 : 8;
+  constexpr int CH = 4 * LP;  // l values per chunk
+  const int lane = threadIdx.x & 63;
+  const int item = blockIdx.x * t.waves + (threadIdx.x >> 6);
+  if (item >= t.items) return;  // wave-uniform
+  const int n = lane & 15, g = lane >> 4;
+  const DItem it = direct_item(p, t, V, MT, item);
+  const T* __restrict__ x = static_cast<const T*>(p.x);
+  const T* __restrict__ kv = static_cast<const T*>(p.kv);
+  const int c = p.c;
+  const int64_t lstride = direct_x_lstride(p);
+  const int64_t kmstride = (int64_t)16 * c, kestride = (int64_t)p.b * c;
+  const bool ntx = t.kgroups == 1;
+
+  f32x4 acc[MT][V];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int e = 0; e < V; ++e) acc[mt][e] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  if (c >= CH) {
+    const T* xl = x + direct_x_base(p, it, LP, V, n, g);
+    const T* kl = kv + direct_k_base(p, it, LP, n, g);
+    const int64_t qstride = direct_x_qstride(p, STRIDED, LP, V, S);
+    DChunk<T, LAYOUT, V, STRIDED, MT, LP> cur, nxt;
+    cur.load(xl, lstride, qstride, kl, kmstride, kestride, 0, ntx);
+    for (int l0 = 0; l0 + CH <= c; l0 += CH) {
+      const bool more = l0 + 2 * CH <= c;
+      if (more) nxt.load(xl, lstride, qstride, kl, kmstride, kestride, l0 + CH, ntx);
+      __builtin_amdgcn_sched_barrier(0);
+      cur.mma(acc);
+      if (more) cur = nxt;
+    }
+  }
+  if constexpr (S == 2) {
+    if (c % CH) {  // c % 32 == 16: last 16 values of l with the 16x16x16 step
+      const T* xl = x + direct_x_base(p, it, 4, V, n, g);
+      const T* kl = kv + direct_k_base(p, it, 4, n, g);
+      const int64_t qstride = direct_x_qstride(p, STRIDED, 4, V, S);
+      DChunk<T, LAYOUT, V, STRIDED, MT, 4> tail;
+      tail.load(xl, lstride, qstride, kl, kmstride, kestride, c - 16, ntx);
+      tail.mma(acc);
+    }
+  }
+
+  direct_store<T, LAYOUT, V, STRIDED, MT>(p, it, n, g, acc);
+}
+
+// The same work item with the reduction length fixed at compile time: NCH
+// full chunks (plus the 16-bit tail) are fully unrolled and the loads of up to
+// PD chunks ahead are in flight while a chunk is multiplied, PD chosen so the
+// chunks in flight take about 64 VGPRs.  A wavefront's time is then about one
+// memory latency plus its MFMAs, instead of one latency per chunk.
+template <typename T, int LAYOUT, int V, bool STRIDED, int MT, int NCH, bool TAIL>
+__global__ __launch_bounds__(256) void ks_direct_c_kernel(Problem p, DirectTile t) {
+  constexpr int S = sizeof(T);
+  constexpr int LP = S == 4 ? 4 : 8;
+  constexpr int CH = 4 * LP;
+  using Chunk = DChunk<T, LAYOUT, V, STRIDED, MT, LP>;
+  constexpr int R = Chunk::NXW + MT * Chunk::VK * Chunk::KW;  // VGPRs of one chunk
+  constexpr int PD0 = 64 / R;
+  constexpr int PD = NCH <= 1 ? 0 : (PD0 < 1 ? 1 : (PD0 > NCH - 1 ? NCH - 1 : PD0));
+  const int lane = threadIdx.x & 63;
+  const int item = blockIdx.x * t.waves + (threadIdx.x >> 6);
+  if (item >= t.items) return;  // wave-uniform
+  const int n = lane & 15, g = lane >> 4;
+  const DItem it = direct_item(p, t, V, MT, item);
+  const T* __restrict__ x = static_cast<const T*>(p.x);
+  const T* __restrict__ kv = static_cast<const T*>(p.kv);
+  const int c = p.c;
+  const int64_t lstride = direct_x_lstride(p);
+  const int64_t kmstride = (int64_t)16 * c, kestride = (int64_t)p.b * c;
+  const bool ntx = t.kgroups == 1;
+
+  f32x4 acc[MT][V];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int e = 0; e < V; ++e) acc[mt][e] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  const T* xl = x + direct_x_base(p, it, LP, V, n, g);
+  const T* kl = kv + direct_k_base(p, it, LP, n, g);
+  const int64_t qstride = direct_x_qstride(p, STRIDED, LP, V, S);
+  // sched_barrier(0) keeps the compiler's scheduler from sinking the loads
+  // next to their first use, which would serialise one memory latency per
+  // chunk.
+  Chunk ch[NCH > 0 ? NCH : 1];
+#pragma unroll
+  for (int q = 0; q <= PD && q < NCH; ++q) ch[q].load(xl, lstride, qstride, kl, kmstride, kestride, q * CH, ntx);
+  DChunk<T, LAYOUT, V, STRIDED, MT, 4> tl;
+  if constexpr (TAIL) {
+    tl.load(x + direct_x_base(p, it, 4, V, n, g), lstride, direct_x_qstride(p, STRIDED, 4, V, S),
+            kv + direct_k_base(p, it, 4, n, g), kmstride, kestride, c - 16, ntx);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+  for (int q = 0; q < NCH; ++q) {
+    if (q + PD + 1 < NCH)
+      ch[q + PD + 1].load(xl, lstride, qstride, kl, kmstride, kestride, (q + PD + 1) * CH, ntx);
+    __builtin_amdgcn_sched_barrier(0);
+    ch[q].mma(acc);
+  }
+  if constexpr (TAIL) tl.mma(acc);
+
+  direct_store<T, LAYOUT, V, STRIDED, MT>(p, it, n, g, acc);
+}
+
 // Vector width along the batch (BSL) and largest j-run (BSF): 4 elements, i.e.
 // 16-byte fp32 or 8-byte 16-bit pieces.
 constexpr int kDirectVec = 4;
@@ -250,7 +332,25 @@ constexpr int direct_mt_max(int esize, int layout, int V) {
 
 template <typename T, int LAYOUT, int V, bool STRIDED, int MT>
 hipError_t launch_direct_inst(const Problem& p, const DirectTile& t, unsigned grid, hipStream_t s) {
-  hipLaunchKernelGGL((ks_direct_kernel<T, LAYOUT, V, STRIDED, MT>), dim3(grid), dim3(64 * t.waves), 0, s, p, t);
+  int nch = 0;
+  bool tail = false;
+  const dim3 g(grid), b(64 * t.waves);
+  if (direct_c_specialised(sizeof(T), p.c, &nch, &tail)) {
+#define KS_DIRECT_C(N, TL)                                                                          \
+  if (nch == N && tail == TL) {                                                                    \
+    hipLaunchKernelGGL((ks_direct_c_kernel<T, LAYOUT, V, STRIDED, MT, N, TL>), g, b, 0, s, p, t); \
+    return hipGetLastError();                                                                      \
+  }
+    if constexpr (sizeof(T) == 4) {
+      KS_DIRECT_C(1, false) KS_DIRECT_C(2, false) KS_DIRECT_C(3, false)
+      KS_DIRECT_C(4, false) KS_DIRECT_C(6, false) KS_DIRECT_C(8, false)
+    } else {
+      KS_DIRECT_C(0, true) KS_DIRECT_C(1, false) KS_DIRECT_C(1, true)
+      KS_DIRECT_C(2, false) KS_DIRECT_C(3, false) KS_DIRECT_C(4, false)
+    }
+#undef KS_DIRECT_C
+  }
+  hipLaunchKernelGGL((ks_direct_kernel<T, LAYOUT, V, STRIDED, MT>), g, b, 0, s, p, t);
   return hipGetLastError();
 }
 

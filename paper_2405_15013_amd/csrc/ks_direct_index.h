@@ -43,6 +43,21 @@ struct DItem {
   int i, j0, k0, beta0;
 };
 
+// Reductions lengths with a specialised kernel instance (the chunk loop fully
+// unrolled, loads issued several chunks ahead): c / CH full chunks of
+// CH = 16 (fp32) or 32 (16-bit) values of l, plus a 16-value tail for 16-bit
+// storage when c % 32 == 16.  Other c use the runtime-length kernel.
+KS_HD bool direct_c_specialised(int esize, int c, int* nch, bool* tail) {
+  if (esize == 4) {
+    *nch = c / 16;
+    *tail = false;
+    return c % 16 == 0 && (*nch == 1 || *nch == 2 || *nch == 3 || *nch == 4 || *nch == 6 || *nch == 8);
+  }
+  *nch = c / 32;
+  *tail = c % 32 == 16;
+  return c % 16 == 0 && (c == 16 || c == 32 || c == 48 || c == 64 || c == 96 || c == 128);
+}
+
 // Item order: k-group fastest (items sharing X are neighbours, in the same
 // workgroup when possible), then j-group, then i, then the batch tile.
 KS_HD DItem direct_item(const Problem& p, const DirectTile& t, int V, int MT, int item) {

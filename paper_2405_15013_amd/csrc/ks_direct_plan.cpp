@@ -62,7 +62,12 @@ bool plan_direct(const Problem& p, bool al16, Plan* pl) {
     if (per_k * (kt / mt) >= 2048) break;
   }
   const int64_t items = per_k * (kt / best);
-  const int waves = items >= 4096 ? 4 : (items >= 1024 ? 2 : 1);
+  // Wavefronts per workgroup: 4 for large problems; fewer spread small ones
+  // over more CUs, but never fewer than the k-groups (up to 4) that share an X
+  // tile, so those read it through the same CU's caches.
+  int waves = items >= 4096 ? 4 : (items >= 1024 ? 2 : 1);
+  const int kg = kt / best;
+  if (waves < kg) waves = kg < 4 ? kg : 4;
   const int64_t grid = (items + waves - 1) / waves;
   if (items > 0x7fffffff || grid > 0x7fffffff) return false;
   pl->variant = V_DIRECT;

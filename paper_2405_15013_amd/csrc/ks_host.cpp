@@ -13,6 +13,7 @@
 #include <unordered_map>
 
 #include "../../include/ks.h"
+#include "ks_direct_index.h"
 #include "ks_internal.h"
 
 namespace ks {
@@ -102,10 +103,9 @@ bool plan_valu_bsf(const Problem& p, bool al16, Plan* pl) {
   return true;
 }
 
-bool plan_mfma(const Problem& p, bool al16, Plan* pl);
-
 }  // namespace
 bool plan_direct(const Problem& p, bool al16, Plan* pl);
+bool plan_staged(const Problem& p, bool al16, Plan* pl);
 namespace {
 
 bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
@@ -113,18 +113,19 @@ bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
     case V_GENERIC: return plan_generic(p, pl);
     case V_VALU_BSL: return plan_valu_bsl(p, al16, pl);
     case V_VALU_BSF: return plan_valu_bsf(p, al16, pl);
-    case V_MFMA: return plan_mfma(p, al16, pl);
     case V_DIRECT: return plan_direct(p, al16, pl);
+    case V_STAGED: return plan_staged(p, al16, pl);
     default: return false;
   }
 }
 
 // Automatic choice: MFMA block GEMM when b and c make each (i, j) block a real
-// dense contraction; VALU kernels for small blocks; the generic kernel for
-// whatever is left.
+// dense contraction (LDS-staged for batch-size-first with d >= 4, whose rows
+// interleave the blocks' inputs; register-direct otherwise); VALU kernels for
+// small blocks; the generic kernel for whatever is left.
 bool plan_auto(const Problem& p, bool al16, Plan* pl) {
+  if (p.layout == BSF && p.d >= 4 && plan_staged(p, al16, pl)) return true;
   if (plan_direct(p, al16, pl)) return true;
-  if (plan_mfma(p, al16, pl)) return true;
   if (p.layout == BSL && plan_valu_bsl(p, al16, pl)) return true;
   if (p.layout == BSF && plan_valu_bsf(p, al16, pl)) return true;
   return plan_generic(p, pl);
@@ -174,8 +175,8 @@ hipError_t launch(const Problem& p, const Plan& pl, hipStream_t s) {
     case V_GENERIC: return launch_generic(p, pl, s);
     case V_VALU_BSL: return launch_valu_bsl(p, pl, s);
     case V_VALU_BSF: return launch_valu_bsf(p, pl, s);
-    case V_MFMA: return launch_mfma(p, pl, s);
     case V_DIRECT: return launch_direct(p, pl, s);
+    case V_STAGED: return launch_staged(p, pl, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -235,12 +236,20 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
       snprintf(buf, sizeof buf, "ks_valu_bsl_kernel<%s,%d,%d,%d,%d>", t, pl.vec, mx, mx, valu_bsl_unroll(p.b, p.c));
       break;
     case V_VALU_BSF: snprintf(buf, sizeof buf, "ks_valu_bsf_kernel<%s,%d,%d,%d>", t, pl.vec, mx, mx); break;
-    case V_MFMA:
-      snprintf(buf, sizeof buf, "ks_mfma_kernel<%s,%d,%d,%d>", t, p.layout, pl.waves_n, pl.waves_m);
+    case V_DIRECT: {
+      int nch = 0;
+      bool tail = false;
+      if (direct_c_specialised(p.dtype == F32 ? 4 : 2, p.c, &nch, &tail))
+        snprintf(buf, sizeof buf, "ks_direct_c_kernel<%s,%d,%d,%s,%d,%d,%s>", t, p.layout, pl.vec,
+                 pl.unroll ? "true" : "false", pl.waves_m, nch, tail ? "true" : "false");
+      else
+        snprintf(buf, sizeof buf, "ks_direct_kernel<%s,%d,%d,%s,%d>", t, p.layout, pl.vec,
+                 pl.unroll ? "true" : "false", pl.waves_m);
       break;
-    case V_DIRECT:
-      snprintf(buf, sizeof buf, "ks_direct_kernel<%s,%d,%d,%s,%d>", t, p.layout, pl.vec, pl.unroll ? "true" : "false",
-               pl.waves_m);
+    }
+    case V_STAGED:
+      snprintf(buf, sizeof buf, "ks_staged_kernel<%s,%d,%d,%s,%d,%d>", t, p.layout, pl.vec,
+               pl.unroll ? "true" : "false", pl.waves_m, pl.cps);
       break;
     default: snprintf(buf, sizeof buf, "?");
   }
@@ -250,13 +259,13 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
 }
 
 std::string describe(const Problem& p, const Plan& pl) {
-  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "mfma", "direct"};
+  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "direct", "staged"};
   char buf[320];
   snprintf(buf, sizeof buf,
            "variant=%d name=%s vec=%d bt=%d jg=%d unroll=%d waves_m=%d waves_n=%d lds=%d grid=%u block=%u xcd=%d "
-           "kernel=%s",
+           "rs=%d kgw=%d lch=%d kernel=%s",
            pl.variant, (pl.variant >= 0 && pl.variant < V_COUNT) ? names[pl.variant] : "?", pl.vec, pl.bt, pl.jg,
-           pl.unroll, pl.waves_m, pl.waves_n, pl.lds_bytes, pl.grid, pl.block, pl.xcd_remap,
+           pl.unroll, pl.waves_m, pl.waves_n, pl.lds_bytes, pl.grid, pl.block, pl.xcd_remap, pl.rs, pl.kgw, pl.lch,
            kernel_name(p, pl).c_str());
   return buf;
 }
@@ -403,13 +412,6 @@ ks_status_t ks_plan_describe(int64_t a, int64_t b, int64_t c, int64_t d, int64_t
 void ks_force_variant(int variant) { g_forced_variant = variant < 0 ? -1 : variant; }
 
 }  // extern "C"
-
-namespace ks {
-bool plan_mfma_impl(const Problem& p, bool al16, Plan* pl);
-namespace {
-bool plan_mfma(const Problem& p, bool al16, Plan* pl) { return plan_mfma_impl(p, al16, pl); }
-}  // namespace
-}  // namespace ks
 
 namespace ks {
 // Plan for stand-in aligned buffers (used by the host-side verifier).  Returns

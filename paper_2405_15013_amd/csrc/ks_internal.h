@@ -15,8 +15,8 @@ enum Variant : int {
   V_GENERIC = 0,   // one thread per output element, any pattern
   V_VALU_BSL = 1,  // VALU streaming, batch-size-last, small b and c
   V_VALU_BSF = 2,  // VALU, batch-size-first, small b and c
-  V_MFMA = 3,      // MFMA block GEMM through LDS, both layouts, b and c multiples of 16
-  V_DIRECT = 4,    // register-direct MFMA, one work item per wavefront, b and c multiples of 16
+  V_DIRECT = 3,    // register-direct MFMA, one work item per wavefront, b and c multiples of 16
+  V_STAGED = 4,    // LDS-staged MFMA, 4 work items per workgroup share coalesced X stages
   V_COUNT = 5
 };
 
@@ -38,23 +38,28 @@ struct Plan {
   int variant = V_GENERIC;
   // variant-specific tile parameters
   int vec = 1;      // elements per memory vector along the contiguous dimension
-  int bt = 0;       // batch rows (BSF) / batch columns (BSL) per workgroup tile
-  int jg = 1;       // j values per workgroup (BSF MFMA / VALU)
+  int bt = 0;       // batch rows (BSF) / batch columns (BSL) per work item or tile
+  int jg = 1;       // j values per work item (direct) / j-groups per tile (staged)
   int unroll = 1;   // vectors per thread (VALU)
-  int waves_m = 1;  // MFMA: waves along the output-channel (k) dimension
-  int waves_n = 1;  // MFMA: waves along the batch dimension
+  int waves_m = 1;  // MFMA: 16-row M-tiles per wavefront (MT)
+  int waves_n = 1;  // MFMA: k-groups (direct) / k-group tiles (staged)
   int lds_bytes = 0;
   unsigned grid = 1;
   unsigned block = 256;
-  int xcd_remap = 0;  // remap blockIdx so neighbouring tiles share an XCD
+  int xcd_remap = 0;  // remap blockIdx so neighbouring tiles share an XCD (staged)
+  // LDS-staged MFMA
+  int rs = 1;       // row (BSF) / column (BSL) groups per tile
+  int kgw = 1;      // k-groups per tile
+  int lch = 0;      // values of l per stage
+  int cps = 1;      // MFMA chunks per stage
 };
 
 // Each launcher enqueues one kernel and returns the hipError_t of the launch.
 hipError_t launch_generic(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_valu_bsl(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_valu_bsf(const Problem& p, const Plan& pl, hipStream_t s);
-hipError_t launch_mfma(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_direct(const Problem& p, const Plan& pl, hipStream_t s);
+hipError_t launch_staged(const Problem& p, const Plan& pl, hipStream_t s);
 
 }  // namespace ks
 

@@ -1,0 +1,167 @@
+// Index arithmetic of the LDS-staged MFMA kernels (ks_staged.h), shared by the
+// kernels and by the host-side plan verifier (ks_plan_verify).
+//
+// A workgroup of 4 wavefronts owns one tile: the X values a set of 4 work
+// items share (paper Section 4.1, Algorithm 2: output-stationary, every output
+// written once).  The reduction over l is walked in stages of LCH values; the
+// workgroup loads a stage of X with coalesced 16-byte loads (consecutive
+// threads take consecutive 16-byte units of a contiguous run of memory) into a
+// double-buffered LDS tile, and each wavefront reads its MFMA operands from
+// LDS.
+//
+//  * batch-size-first: a tile is 16*RS batch rows of one i, all d values of j
+//    and KGW k-groups.  Stage rows are the runs X[beta, i*c*d + ls*d ..
+//    (ls + nl)*d) (all j of nl values of l, contiguous); LDS row r holds batch
+//    row beta0 + r with a 16-byte pad per row (bank spread).
+//  * batch-size-last: a tile is 16*V*RS batch entries of one (i, j) and KGW
+//    k-groups.  Stage rows are the input rows of l = ls .. ls + nl - 1, each
+//    16*V*RS contiguous batch entries.
+//
+// Wavefront w of the tile takes rs = w % RS, jg = (w / RS) % JG and
+// kgw = w / (RS * JG) (RS * JG * KGW == 4), i.e. the work item
+// (rows or columns group rs, j-group jg, k-group kt*KGW + kgw).
+#pragma once
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+#include "ks_internal.h"
+
+#define KS_HD __host__ __device__ __forceinline__
+
+namespace ks {
+
+struct StagedTile {
+  int RS;        // 16-row (BSF) or 16*V-column (BSL) groups per tile
+  int JG;        // j-groups per tile (BSF: d / V; BSL: 1)
+  int KGW;       // k-groups per tile
+  int kgt;       // k-group tiles: b / (16 * MT * KGW)
+  int nbt;       // batch tiles
+  int tiles;     // nbt * a * (BSL ? d : 1) * kgt
+  int LCH;       // l values per stage (a multiple of 16)
+  int pitch;     // LDS row pitch, bytes
+  int stage;     // LDS bytes of one stage buffer
+  int remap;     // XCD-aware tile order (tiles % 8 == 0)
+  int ypitch;    // BSF: LDS row pitch of the staged output tile, bytes
+  int lds;       // LDS bytes per workgroup: max(2 * stage, BSF output tile)
+};
+
+struct STile {
+  int i, j, kt, bt;  // j: BSL only
+};
+
+// Workgroup g runs on XCD g % 8; give each XCD a contiguous range of logical
+// tiles so that tiles sharing X (neighbouring k-group tiles) share an L2.
+KS_HD int staged_remap(int g, int tiles) { return (g & 7) * (tiles >> 3) + (g >> 3); }
+
+KS_HD STile staged_tile(const Problem& p, const StagedTile& t, int block) {
+  const int tile = t.remap ? staged_remap(block, t.tiles) : block;
+  STile s;
+  int rest = tile;
+  s.kt = rest % t.kgt;
+  rest /= t.kgt;
+  if (p.layout == BSL) {
+    s.j = rest % p.d;
+    rest /= p.d;
+  } else {
+    s.j = 0;
+  }
+  s.i = rest % p.a;
+  s.bt = rest / p.a;
+  return s;
+}
+
+// Number of batch entries a tile spans.
+KS_HD int staged_span(const Problem& p, const StagedTile& t, int V) {
+  return p.layout == BSL ? 16 * V * t.RS : 16 * t.RS;
+}
+
+// ---- stage loads ----------------------------------------------------------
+// Stage rows and 16-byte units per row for a stage of nl values of l.
+KS_HD int staged_rows(const Problem& p, const StagedTile& t, int nl) { return p.layout == BSL ? nl : 16 * t.RS; }
+KS_HD int staged_units_per_row(const Problem& p, const StagedTile& t, int V, int esize, int nl) {
+  return p.layout == BSL ? (16 * V * t.RS * esize) / 16 : (nl * p.d * esize) / 16;
+}
+// Element offset in X of unit v of stage row r (stage starting at l = ls);
+// rows or columns beyond the batch read the last valid one instead.
+KS_HD int64_t staged_x_unit(const Problem& p, const StagedTile& t, const STile& s, int V, int esize, int ls, int r,
+                            int v) {
+  const int ue = 16 / esize;  // elements per unit
+  const int c = p.c, d = p.d;
+  if (p.layout == BSL) {
+    int beta = s.bt * 16 * V * t.RS + v * ue;
+    if (beta >= p.batch) beta = p.batch - ue;
+    const int64_t row = (int64_t)s.i * c * d + (int64_t)(ls + r) * d + s.j;
+    return row * p.batch + beta;
+  }
+  int beta = s.bt * 16 * t.RS + r;
+  if (beta >= p.batch) beta = p.batch - 1;
+  return (int64_t)beta * p.N + (int64_t)s.i * c * d + (int64_t)ls * d + (int64_t)v * ue;
+}
+// LDS byte offset of unit v of stage row r within a stage buffer.
+KS_HD int staged_lds_unit(const StagedTile& t, int r, int v) { return r * t.pitch + v * 16; }
+
+// ---- operand reads from LDS -----------------------------------------------
+// Work item of wavefront w in tile s.
+struct SItem {
+  int rs, jg, kgw;
+  int j0, k0, beta0;
+};
+KS_HD SItem staged_item(const Problem& p, const StagedTile& t, const STile& s, int V, int MT, int w) {
+  SItem it;
+  it.rs = w % t.RS;
+  it.jg = (w / t.RS) % t.JG;
+  it.kgw = w / (t.RS * t.JG);
+  it.k0 = (s.kt * t.KGW + it.kgw) * 16 * MT;
+  if (p.layout == BSL) {
+    it.j0 = s.j;
+    it.beta0 = s.bt * 16 * V * t.RS + it.rs * 16 * V;
+  } else {
+    it.j0 = it.jg * V;
+    it.beta0 = s.bt * 16 * t.RS + it.rs * 16;
+  }
+  return it;
+}
+// A lane's operand block of an MFMA chunk at l = l0 (relative to the stage
+// start) is LP x V elements (flat t*V + e), read as pieces of PE elements:
+// piece q at LDS byte offset base + q * qstride (+ l0 * lstride).
+//   BSL:            row LP*g + q (l), columns 16*V*rs + V*n .. + V;
+//   BSF strided:    row 16*rs + n, elements (LP*g + q)*d + j0 .. + V;
+//   BSF contiguous: row 16*rs + n, elements (LP*g)*d + q*PE .. + PE (V == d).
+KS_HD int staged_op_base(const Problem& p, const StagedTile& t, const SItem& it, int LP, int V, int esize, int n,
+                         int g) {
+  if (p.layout == BSL) return (LP * g) * t.pitch + (it.rs * 16 * V + V * n) * esize;
+  return (it.rs * 16 + n) * t.pitch + ((LP * g) * p.d + it.j0) * esize;
+}
+KS_HD int staged_op_lstride(const Problem& p, const StagedTile& t, int esize) {
+  return p.layout == BSL ? t.pitch : p.d * esize;
+}
+KS_HD int staged_op_qstride(const Problem& p, const StagedTile& t, bool strided, int pe, int esize) {
+  if (p.layout == BSL) return t.pitch;
+  return strided ? p.d * esize : pe * esize;
+}
+
+// ---- batch-size-first output tile ------------------------------------------
+// In BSF the tile's outputs of a batch row are the contiguous run
+// Y[beta, i*b*d + kb*d .. i*b*d + (kb + KR)*d) with kb = kt*KGW*16*MT and
+// KR = 16*MT*KGW (all j of KR consecutive k).  The wavefronts write their
+// accumulators into an LDS copy of the tile (row r at r * ypitch) and the
+// workgroup stores it with coalesced 16-byte units ("structured epilogue").
+KS_HD int staged_y_kr(const StagedTile& t, int MT) { return 16 * MT * t.KGW; }
+// LDS byte offset of output element (row r, k, j) of the tile.
+KS_HD int staged_y_lds(const Problem& p, const StagedTile& t, const STile& s, int MT, int esize, int r, int k, int j) {
+  const int kb = s.kt * t.KGW * 16 * MT;
+  return r * t.ypitch + ((k - kb) * p.d + j) * esize;
+}
+// 16-byte units per row of the output tile and the Y offset (elements) of
+// unit v of tile row r, or -1 beyond the batch.
+KS_HD int staged_y_units_per_row(const Problem& p, const StagedTile& t, int MT, int esize) {
+  return staged_y_kr(t, MT) * p.d * esize / 16;
+}
+KS_HD int64_t staged_y_unit(const Problem& p, const StagedTile& t, const STile& s, int MT, int esize, int r, int v) {
+  const int beta = s.bt * 16 * t.RS + r;
+  if (beta >= p.batch) return -1;
+  const int kb = s.kt * t.KGW * 16 * MT;
+  return (int64_t)beta * p.M + (int64_t)s.i * p.b * p.d + (int64_t)kb * p.d + (int64_t)v * (16 / esize);
+}
+
+}  // namespace ks

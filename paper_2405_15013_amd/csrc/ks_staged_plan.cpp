@@ -1,0 +1,142 @@
+// Planner and launcher of the LDS-staged MFMA kernels (ks_staged.h).
+//
+// A plan fixes the vector width V (4 along the batch in BSL, min(d, 4) of j
+// in BSF), the M-tiles per wavefront MT, and how the 4 wavefronts of a tile
+// split the work: JG j-groups (BSF: d / V) x KGW k-groups x RS row/column
+// groups with JG * KGW * RS == 4.  A stage of X is at most 1024 16-byte units
+// (16 KB), so every thread stages at most 4 units and a workgroup needs two
+// stage buffers of LDS.
+#include "ks_staged_index.h"
+#include "ks_internal.h"
+
+namespace ks {
+
+hipError_t launch_staged_f32(const Problem& p, const StagedTile& t, int V, bool strided, int mt, int cps,
+                             hipStream_t s);
+hipError_t launch_staged_bf16(const Problem& p, const StagedTile& t, int V, bool strided, int mt, int cps,
+                              hipStream_t s);
+hipError_t launch_staged_f16(const Problem& p, const StagedTile& t, int V, bool strided, int mt, int cps,
+                             hipStream_t s);
+
+namespace {
+constexpr int kMaxStageUnits = 1024;  // 256 threads x kStagedUnitsPerThread (ks_staged.h)
+
+// Largest MT instantiated; keep in sync with direct_mt_max() in ks_direct.h.
+int mt_max(int esize, int layout, int V) {
+  (void)esize;
+  return (layout == BSL || V <= 2) ? 4 : 2;
+}
+}  // namespace
+
+StagedTile staged_tile_of(const Problem& p, const Plan& pl) {
+  StagedTile t;
+  const int S = p.dtype == F32 ? 4 : 2, V = pl.vec, MT = pl.waves_m;
+  t.RS = pl.rs;
+  t.JG = p.layout == BSL ? 1 : p.d / V;
+  t.KGW = pl.kgw;
+  t.kgt = p.b / (16 * MT * t.KGW);
+  const int span = p.layout == BSL ? 16 * V * t.RS : 16 * t.RS;
+  t.nbt = (p.batch + span - 1) / span;
+  t.tiles = t.nbt * p.a * (p.layout == BSL ? p.d : 1) * t.kgt;
+  t.LCH = pl.lch;
+  if (p.layout == BSL) {
+    t.pitch = 16 * V * t.RS * S;
+    t.stage = t.LCH * t.pitch;
+  } else {
+    t.pitch = t.LCH * p.d * S + 16;
+    t.stage = 16 * t.RS * t.pitch;
+  }
+  t.remap = pl.xcd_remap;
+  t.ypitch = 0;
+  t.lds = 2 * t.stage;
+  if (p.layout == BSF) {
+    t.ypitch = 16 * MT * t.KGW * p.d * S + 16;
+    const int ytile = 16 * t.RS * t.ypitch;
+    if (ytile > t.lds) t.lds = ytile;
+  }
+  return t;
+}
+
+bool plan_staged(const Problem& p, bool al16, Plan* pl) {
+  if (!al16 || p.b % 16 || p.c % 16) return false;
+  const int S = p.dtype == F32 ? 4 : 2;
+  const int UE = 16 / S, CH = S == 4 ? 16 : 32;
+  int V, JG;
+  bool strided = false;
+  if (p.layout == BSL) {
+    V = 4;
+    if (p.batch % UE) return false;
+    JG = 1;
+  } else {
+    V = p.d < 4 ? p.d : 4;
+    if ((V != 1 && V != 2 && V != 4) || p.d % V) return false;
+    strided = V < p.d;
+    JG = p.d / V;
+    if (JG > 4) return false;
+  }
+  const int lch = (p.layout == BSF && CH * p.d * S < 128) ? 2 * CH : CH;
+  const int KT = p.b / 16;
+  bool found = false;
+  int64_t best_tiles = 0;
+  int best_kgt = 0, best_mt = 0, best_kgw = 0, best_rs = 0;
+  for (int mt = mt_max(S, p.layout, V); mt >= 1; --mt) {
+    if (KT % mt) continue;
+    const int kgroups = KT / mt;
+    for (int kgw : {4, 2, 1}) {
+      if (kgw * JG > 4 || kgroups % kgw) continue;
+      const int rs = 4 / (JG * kgw);
+      const int64_t units = p.layout == BSL ? (int64_t)lch * (16 * V * rs * S / 16)
+                                            : (int64_t)16 * rs * (lch * p.d * S / 16);
+      if (units > kMaxStageUnits) continue;
+      const int kgt = kgroups / kgw;
+      const int span = p.layout == BSL ? 16 * V * rs : 16 * rs;
+      const int64_t tiles = (int64_t)((p.batch + span - 1) / span) * p.a * (p.layout == BSL ? p.d : 1) * kgt;
+      if (tiles > 0x7fffffff) continue;
+      // Enough workgroups first (4 per CU), then fewest re-reads of X, then
+      // the largest MT.
+      const int64_t tcap = tiles < 1024 ? tiles : 1024;
+      const int64_t bcap = best_tiles < 1024 ? best_tiles : 1024;
+      bool better = !found || tcap > bcap || (tcap == bcap && (kgt < best_kgt || (kgt == best_kgt && mt > best_mt)));
+      if (better) {
+        found = true;
+        best_tiles = tiles;
+        best_kgt = kgt;
+        best_mt = mt;
+        best_kgw = kgw;
+        best_rs = rs;
+      }
+    }
+  }
+  if (!found) return false;
+  pl->variant = V_STAGED;
+  pl->vec = V;
+  pl->unroll = strided ? 1 : 0;
+  pl->waves_m = best_mt;
+  pl->waves_n = best_kgt;
+  pl->jg = JG;
+  pl->rs = best_rs;
+  pl->kgw = best_kgw;
+  pl->lch = lch;
+  pl->cps = lch / CH;
+  pl->bt = p.layout == BSL ? 16 * V * best_rs : 16 * best_rs;
+  pl->block = 256;
+  pl->grid = (unsigned)best_tiles;
+  pl->xcd_remap = (best_kgt > 1 && best_tiles % 8 == 0) ? 1 : 0;
+  const StagedTile t = staged_tile_of(p, *pl);
+  if (t.lds > 64 * 1024) return false;
+  pl->lds_bytes = t.lds;
+  return true;
+}
+
+hipError_t launch_staged(const Problem& p, const Plan& pl, hipStream_t s) {
+  const StagedTile t = staged_tile_of(p, pl);
+  const bool strided = pl.unroll != 0;
+  switch (p.dtype) {
+    case F32: return launch_staged_f32(p, t, pl.vec, strided, pl.waves_m, pl.cps, s);
+    case BF16: return launch_staged_bf16(p, t, pl.vec, strided, pl.waves_m, pl.cps, s);
+    case F16: return launch_staged_f16(p, t, pl.vec, strided, pl.waves_m, pl.cps, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace ks

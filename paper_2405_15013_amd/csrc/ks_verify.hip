@@ -1,9 +1,10 @@
 // Host-side plan verifier: replays, on the CPU, the address arithmetic every
 // thread of the planned launch would perform, and checks that all global reads
-// and writes stay inside their tensors, that every LDS cell a tile reads has
-// been written, and that every element of Y is written exactly once (the
-// partition property of the row/col index sets, paper Section 4.1).  Nothing is
-// enqueued on a GPU.
+// and writes stay inside their tensors, that every MFMA operand element a lane
+// reads (from memory or from an LDS stage written in the same stage) is the X
+// value the product needs, and that every element of Y is written exactly once
+// (the partition property of the row/col index sets, paper Section 4.1).
+// Nothing is enqueued on a GPU.
 #include <hip/hip_runtime.h>
 
 #include <cstdio>
@@ -13,13 +14,14 @@
 
 #include "../../include/ks.h"
 #include "ks_internal.h"
-#include "ks_mfma_index.h"
 #include "ks_direct_index.h"
+#include "ks_staged_index.h"
 
 namespace ks {
 
-// Defined in ks_direct_plan.cpp.
+// Defined in ks_direct_plan.cpp and ks_staged_plan.cpp.
 DirectTile direct_tile(const Problem& p, const Plan& pl);
+StagedTile staged_tile_of(const Problem& p, const Plan& pl);
 
 // Defined in ks_host.cpp.
 bool plan_for_verify(int64_t a, int64_t b, int64_t c, int64_t d, int64_t batch, int layout, int dtype, Problem* p,
@@ -103,99 +105,16 @@ bool verify_valu_bsf(Checker& ck, const Plan& pl) {
   return ck.err.empty();
 }
 
-bool verify_mfma(Checker& ck, const Plan& pl) {
-  const Problem& p = ck.p;
-  MfmaTile t;
-  t.bt = pl.bt;
-  t.jg = pl.jg;
-  t.njg = p.d / pl.jg;
-  t.nbt = (p.batch + pl.bt - 1) / pl.bt;
-  t.mode = pl.unroll;
-  t.remap = pl.xcd_remap;
-  t.vec = pl.vec;
-  const int MT = pl.waves_m, NT = pl.waves_n, V = t.vec, s = p.dtype == F32 ? 4 : 2;
-  const int KC = s == 4 ? 16 : 32;
-  const int P = x_pitch(p, t), PY = y_pitch(p, t);
-  const int xs_cells = t.jg * t.bt * P;
-  if (t.njg * t.jg != p.d) return ck.fail("j-group does not divide d", t.jg);
-  if (t.bt % (16 * MT)) return ck.fail("batch tile not a multiple of 16*MT", t.bt);
-  if ((p.b / 16) % NT) return ck.fail("NT does not divide b/16", NT);
-  if (x_chunks(p, t) > 256 * kMaxChunks) return ck.fail("too many X chunks per thread", x_chunks(p, t));
-  int64_t lds_need = (int64_t)xs_cells * s + (p.layout == BSF ? (int64_t)t.bt * PY * s : 0);
-  if (lds_need > pl.lds_bytes) return ck.fail("LDS allocation too small", lds_need);
-  if ((int64_t)t.nbt * p.a * t.njg != (int64_t)pl.grid) return ck.fail("grid does not match the tiles", pl.grid);
-  if (t.remap && pl.grid % 8) return ck.fail("XCD remap needs a grid multiple of 8", pl.grid);
-  std::vector<uint8_t> seen_tile(pl.grid, 0);
-  std::vector<uint8_t> xs(xs_cells), ys;
-  for (unsigned blk = 0; blk < pl.grid && ck.err.empty(); ++blk) {
-    const TileCoord tc = tile_coord(p, t, blk, pl.grid);
-    const int logical = t.remap ? xcd_remap(blk, pl.grid) : (int)blk;
-    if (seen_tile[logical]++) return ck.fail("tile visited twice", logical);
-    std::fill(xs.begin(), xs.end(), 0);
-    const int total = x_chunks(p, t);
-    for (int q = 0; q < total; ++q) {
-      const int64_t src = x_chunk_src(p, t, tc, q);
-      if (src >= 0) ck.read_x(src, V);
-      if (src >= 0 && (src % V)) ck.fail("X chunk not vector aligned", src);
-      for (int e = 0; e < V; ++e) {
-        const int li = x_chunk_lds(p, t, q, e);
-        if (li < 0 || li >= xs_cells) return ck.fail("Xs write out of bounds", li);
-        if (xs[li]++) return ck.fail("Xs cell written twice", li);
-      }
-    }
-    // every cell the MFMA reads must have been written
-    for (int jj = 0; jj < t.jg; ++jj)
-      for (int r = 0; r < t.bt; ++r)
-        for (int l = 0; l < p.c; ++l)
-          if (!xs[(jj * t.bt + r) * P + l]) return ck.fail("Xs cell read but never written", (jj * t.bt + r) * P + l);
-    if (p.layout == BSF) ys.assign((size_t)t.bt * PY, 0);
-    const int items = mfma_items(p, t, MT, NT);
-    for (int it = 0; it < items; ++it) {
-      const Item itm = mfma_item(p, t, MT, NT, it);
-      for (int lane = 0; lane < 64; ++lane) {
-        const int n = lane & 15, g = lane >> 4;
-        for (int nt = 0; nt < NT; ++nt) {
-          const int k = (itm.ngi * NT + nt) * 16 + n;
-          const int64_t krow = ((int64_t)(tc.i * p.d + tc.j0 + itm.jj) * p.b + k) * p.c;
-          ck.read_k(krow, p.c);
-          for (int mt = 0; mt < MT; ++mt) {
-            const int bl = (itm.mgi * MT + mt) * 16 + 4 * g;
-            const int arow = itm.jj * t.bt + (itm.mgi * MT + mt) * 16 + n;
-            if (arow >= t.jg * t.bt) return ck.fail("A operand row out of range", arow);
-            if (p.layout == BSL) {
-              const int beta = tc.beta0 + bl;
-              if (beta < p.batch) {
-                if (beta + 4 > p.batch) return ck.fail("BSL store straddles the batch end", beta);
-                ck.write_y((int64_t)(tc.i * p.b * p.d + k * p.d + tc.j0 + itm.jj) * p.batch + beta, 4);
-              }
-            } else {
-              for (int r = 0; r < 4; ++r) {
-                const int yi = (bl + r) * PY + k * t.jg + itm.jj;
-                if (yi >= (int)ys.size()) return ck.fail("Ys write out of bounds", yi);
-                if (ys[yi]++) return ck.fail("Ys cell written twice", yi);
-              }
-            }
-          }
-        }
-      }
-    }
-    (void)KC;
-    if (p.layout == BSF) {
-      const int ych = y_chunks(p, t);
-      for (int q = 0; q < ych; ++q) {
-        int lds;
-        const int64_t dst = y_chunk_dst(p, t, tc, q, &lds);
-        if (dst < 0) continue;
-        for (int e = 0; e < V; ++e)
-          if (!ys[lds + e]) return ck.fail("Ys cell stored but never written", lds + e);
-        if (dst % V) return ck.fail("Y chunk not vector aligned", dst);
-        ck.write_y(dst, V);
-      }
-    }
-  }
-  return ck.err.empty();
+// X element (offset) that flat element f = t*V + e of a lane's operand block
+// must hold: l = l0 + LP*g + t and column e (batch V*n + e in BSL, j0 + e in
+// BSF), from the definition of the product (Section 4.1 index sets).
+int64_t expected_x(const Problem& p, const DItem& it, int V, int LP, int l0, int n, int g, int f) {
+  const int t = f / V, e = f % V;
+  const int64_t l = l0 + LP * g + t;
+  if (p.layout == BSL)
+    return ((int64_t)it.i * p.c * p.d + l * p.d + it.j0) * p.batch + it.beta0 + V * n + e;
+  return (int64_t)(it.beta0 + n) * p.N + (int64_t)it.i * p.c * p.d + l * p.d + it.j0 + e;
 }
-
 
 bool verify_direct(Checker& ck, const Plan& pl) {
   const Problem& p = ck.p;
@@ -225,11 +144,14 @@ bool verify_direct(Checker& ck, const Plan& pl) {
       if (np * pe != lp * V) return ck.fail("X pieces do not tile the lane block", np);
       for (int lane = 0; lane < 64; ++lane) {
         const int n = lane & 15, g = lane >> 4;
+        const bool valid = direct_lane_valid(p, it, V, n);
         for (int q = 0; q < np; ++q) {
           const int64_t off = direct_x_off(p, it, strided, lp, V, S, l0, n, g, q);
-          if (off < 0) continue;
           if ((off * S) % (pe * S)) return ck.fail("X piece not aligned to its size", off);
           ck.read_x(off, pe);
+          for (int e = 0; valid && e < pe; ++e)
+            if (off + e != expected_x(p, it, V, lp, l0, n, g, q * pe + e))
+              return ck.fail("operand element is not the X value the product needs", off + e);
         }
         for (int mt = 0; mt < MT; ++mt)
           for (int e = 0; e < VK; ++e) {
@@ -250,6 +172,143 @@ bool verify_direct(Checker& ck, const Plan& pl) {
           if ((off * S) % (ype * S)) return ck.fail("Y piece not aligned to its size", off);
           ck.write_y(off, ype);
         }
+  }
+  return ck.err.empty();
+}
+
+bool verify_staged(Checker& ck, const Plan& pl) {
+  const Problem& p = ck.p;
+  const StagedTile t = staged_tile_of(p, pl);
+  const int V = pl.vec, MT = pl.waves_m, S = p.dtype == F32 ? 4 : 2;
+  const bool strided = pl.unroll != 0;
+  const int LP = S == 4 ? 4 : 8, CH = 4 * LP, UE = 16 / S;
+  if (t.RS * t.JG * t.KGW != 4) return ck.fail("waves do not split the tile 4 ways", t.RS * t.JG * t.KGW);
+  if (t.kgt * t.KGW * 16 * MT != p.b) return ck.fail("k-groups do not cover b", p.b);
+  if (t.LCH % CH || t.LCH / CH != pl.cps) return ck.fail("stage is not a whole number of chunks", t.LCH);
+  if ((int)pl.grid != t.tiles || pl.block != 256) return ck.fail("grid does not match the tiles", pl.grid);
+  if (pl.lds_bytes != t.lds || t.lds < 2 * t.stage) return ck.fail("LDS allocation does not hold two stages", pl.lds_bytes);
+  if (p.layout == BSF && t.lds < 16 * t.RS * t.ypitch) return ck.fail("LDS allocation does not hold the output tile", t.lds);
+  if (t.remap && t.tiles % 8) return ck.fail("XCD remap needs a multiple of 8 tiles", t.tiles);
+  if (p.layout == BSF && (p.d % V || (!strided && V != p.d) || t.JG != p.d / V)) return ck.fail("bad j-vector", V);
+  if (p.layout == BSL && p.batch % UE) return ck.fail("batch not a multiple of the 16-byte unit", p.batch);
+  std::vector<uint8_t> seen(t.tiles, 0);
+  std::vector<int64_t> shadow((size_t)t.stage / S);
+  const int nstages = (p.c + t.LCH - 1) / t.LCH;
+  for (int blk = 0; blk < t.tiles && ck.err.empty(); ++blk) {
+    const STile st = staged_tile(p, t, blk);
+    const int logical = t.remap ? staged_remap(blk, t.tiles) : blk;
+    if (logical < 0 || logical >= t.tiles || seen[logical]++) return ck.fail("tile visited twice", logical);
+    for (int s = 0; s < nstages; ++s) {
+      const int ls = s * t.LCH, nl = p.c - ls < t.LCH ? p.c - ls : t.LCH;
+      std::fill(shadow.begin(), shadow.end(), (int64_t)-1);
+      const int ur = staged_units_per_row(p, t, V, S, nl);
+      const int nunits = staged_rows(p, t, nl) * ur;
+      if (nunits > 1024) return ck.fail("stage has more than 1024 units", nunits);
+      for (int u = 0; u < nunits; ++u) {
+        const int r = u / ur, v = u % ur;
+        const int64_t off = staged_x_unit(p, t, st, V, S, ls, r, v);
+        if ((off * S) % 16) return ck.fail("X unit not 16-byte aligned", off);
+        ck.read_x(off, UE);
+        const int lo = staged_lds_unit(t, r, v);
+        if (lo < 0 || lo + 16 > t.stage) return ck.fail("LDS unit out of the stage buffer", lo);
+        for (int e = 0; e < UE; ++e) {
+          int64_t& cell = shadow[(size_t)(lo / S + e)];
+          if (cell != -1) return ck.fail("LDS cell written twice in a stage", lo);
+          cell = off + e;
+        }
+      }
+      for (int w = 0; w < 4; ++w) {
+        const SItem si = staged_item(p, t, st, V, MT, w);
+        DItem it;
+        it.i = st.i; it.j0 = si.j0; it.k0 = si.k0; it.beta0 = si.beta0;
+        // MFMA chunks of this stage: full chunks, then the 16-bit tail
+        int chunks[8][2], nch = 0;
+        for (int q = 0; (q + 1) * CH <= nl; ++q) { chunks[nch][0] = q * CH; chunks[nch][1] = LP; ++nch; }
+        if (nl % CH) {
+          if (S != 2 || nl % CH != 16) return ck.fail("stage leaves values of l uncovered", nl);
+          chunks[nch][0] = nl - 16; chunks[nch][1] = 4; ++nch;
+        }
+        for (int ci = 0; ci < nch; ++ci) {
+          const int l0 = chunks[ci][0], lp = chunks[ci][1];
+          const int pe = direct_x_piece_elems(p.layout, strided, lp, V, S);
+          const int np = lp * V / pe, pb = pe * S;
+          if (pb != 16 && pb != 8) return ck.fail("operand piece is not 8 or 16 bytes", pb);
+          const int olstride = staged_op_lstride(p, t, S), oqstride = staged_op_qstride(p, t, strided, pe, S);
+          for (int lane = 0; lane < 64; ++lane) {
+            const int n = lane & 15, g = lane >> 4;
+            const bool valid = direct_lane_valid(p, it, V, n);
+            const int ob = staged_op_base(p, t, si, lp, V, S, n, g);
+            for (int q = 0; q < np; ++q) {
+              const int o = ob + l0 * olstride + q * oqstride;
+              if (o < 0 || o + pb > t.stage || o % pb) return ck.fail("operand read outside the stage or unaligned", o);
+              for (int e = 0; e < pe; ++e) {
+                const int64_t have = shadow[(size_t)(o / S + e)];
+                if (have < 0) return ck.fail("operand read of an LDS cell not written in this stage", o);
+                if (valid && have != expected_x(p, it, V, lp, ls + l0, n, g, q * pe + e))
+                  return ck.fail("operand element is not the X value the product needs", have);
+              }
+            }
+            for (int mt = 0; mt < MT; ++mt)
+              for (int e = 0; e < (p.layout == BSL ? 1 : V); ++e) {
+                const int64_t off = direct_k_off(p, it, lp, ls + l0, n, g, mt, e);
+                if ((off * S) % (lp * S)) return ck.fail("K operand not aligned to its size", off);
+                ck.read_k(off, lp);
+              }
+          }
+        }
+      }
+    }
+    if (p.layout == BSL) {
+      for (int w = 0; w < 4; ++w) {
+        const SItem si = staged_item(p, t, st, V, MT, w);
+        DItem it;
+        it.i = st.i; it.j0 = si.j0; it.k0 = si.k0; it.beta0 = si.beta0;
+        const int ynp = direct_y_pieces(p.layout, strided, V, S);
+        const int ype = direct_y_piece_elems(p.layout, strided, V, S);
+        for (int mt = 0; mt < MT; ++mt)
+          for (int lane = 0; lane < 64; ++lane)
+            for (int q = 0; q < ynp; ++q) {
+              const int64_t off = direct_y_off(p, it, strided, V, S, mt, lane & 15, lane >> 4, q);
+              if (off < 0) continue;
+              if ((off * S) % (ype * S)) return ck.fail("Y piece not aligned to its size", off);
+              ck.write_y(off, ype);
+            }
+      }
+    } else {
+      // Structured epilogue: every cell of the LDS output tile is written once
+      // by the lane holding that output, then stored by its 16-byte unit.
+      const int kr = staged_y_kr(t, MT), rows = 16 * t.RS;
+      std::vector<int64_t> ytile((size_t)rows * t.ypitch / S, -1);
+      for (int w = 0; w < 4; ++w) {
+        const SItem si = staged_item(p, t, st, V, MT, w);
+        for (int lane = 0; lane < 64; ++lane) {
+          const int n = lane & 15, g = lane >> 4, r = 16 * si.rs + n;
+          for (int mt = 0; mt < MT; ++mt)
+            for (int r4 = 0; r4 < 4; ++r4)
+              for (int e = 0; e < V; ++e) {
+                const int k = si.k0 + 16 * mt + 4 * g + r4, j = si.j0 + e;
+                const int o = staged_y_lds(p, t, st, MT, S, r, k, j);
+                if (e == 0 && o % (V * S)) return ck.fail("output tile write not aligned to its size", o);
+                if (o < 0 || o + S > rows * t.ypitch) return ck.fail("output tile write out of range", o);
+                int64_t& cell = ytile[(size_t)(o / S)];
+                if (cell != -1) return ck.fail("output tile cell written twice", o);
+                cell = (int64_t)(st.bt * 16 * t.RS + r) * p.M + (int64_t)st.i * p.b * p.d + (int64_t)k * p.d + j;
+              }
+        }
+      }
+      const int uy = staged_y_units_per_row(p, t, MT, S);
+      if (uy * 16 != kr * p.d * S) return ck.fail("output row is not a whole number of units", kr);
+      for (int r = 0; r < rows; ++r)
+        for (int v = 0; v < uy; ++v) {
+          const int64_t off = staged_y_unit(p, t, st, MT, S, r, v);
+          if (off < 0) continue;
+          if ((off * S) % 16) return ck.fail("Y unit not 16-byte aligned", off);
+          for (int e = 0; e < 16 / S; ++e)
+            if (ytile[(size_t)((r * t.ypitch + v * 16) / S + e)] != off + e)
+              return ck.fail("Y unit does not hold the outputs it is stored to", off + e);
+          ck.write_y(off, 16 / S);
+        }
+    }
   }
   return ck.err.empty();
 }
@@ -275,8 +334,8 @@ extern "C" ks_status_t ks_plan_verify(int64_t a, int64_t b, int64_t c, int64_t d
     case V_GENERIC: ok = verify_generic(ck, pl); break;
     case V_VALU_BSL: ok = verify_valu_bsl(ck, pl); break;
     case V_VALU_BSF: ok = verify_valu_bsf(ck, pl); break;
-    case V_MFMA: ok = verify_mfma(ck, pl); break;
     case V_DIRECT: ok = verify_direct(ck, pl); break;
+    case V_STAGED: ok = verify_staged(ck, pl); break;
     default: ck.fail("unknown variant", pl.variant);
   }
   if (ok) ok = ck.coverage();

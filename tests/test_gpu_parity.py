@@ -12,7 +12,7 @@ from parity_util import TOL, case, from_device, nan_tensor, oracle_y, rel_err, t
 
 pytestmark = pytest.mark.gpu
 
-VARIANTS = {"generic": 0, "valu_bsl": 1, "valu_bsf": 2, "mfma": 3, "direct": 4}
+VARIANTS = {"generic": 0, "valu_bsl": 1, "valu_bsf": 2, "direct": 3, "staged": 4}
 
 
 def run_gpu(pattern, x_logical, kv, batch, dtype, layout, variant=None, x_offset=0, y_offset=0):
@@ -220,34 +220,41 @@ def test_sweep_ragged_batch_full(pattern, dtype, layout):
     check(pattern, batch, dtype, layout, cfg=8, kdist="normal")
 
 
-@pytest.mark.parametrize("pattern", [(1, 32, 32, 32), (32, 32, 32, 1), (6, 64, 16, 8), (6, 16, 64, 8),
-                                     (2, 48, 80, 3), (1, 128, 16, 16), (8, 16, 128, 4)])
-@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
-@pytest.mark.parametrize("layout", ["bsf", "bsl"])
-def test_mfma_forced(pattern, dtype, layout):
-    check(pattern, 256, dtype, layout, cfg=9, variant=3, kdist="normal")
+MFMA_SHAPES = [(1, 32, 32, 32), (32, 32, 32, 1), (6, 64, 16, 8), (6, 16, 64, 8), (2, 48, 80, 2), (1, 128, 16, 16),
+               (8, 16, 128, 4), (3, 96, 48, 1), (1, 16, 112, 8), (2, 64, 128, 2)]
 
 
-@pytest.mark.parametrize("pattern", [(1, 32, 32, 32), (32, 32, 32, 1), (6, 64, 16, 8), (6, 16, 64, 8),
-                                     (2, 48, 80, 2), (1, 128, 16, 16), (8, 16, 128, 4), (3, 96, 48, 1),
-                                     (1, 16, 112, 8), (2, 64, 128, 2)])
+@pytest.mark.parametrize("pattern", MFMA_SHAPES)
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 @pytest.mark.parametrize("layout", ["bsf", "bsl"])
 @pytest.mark.parametrize("batch", [256, 72])
 def test_direct_forced(pattern, dtype, layout, batch):
     """The register-direct MFMA kernel on every j-vector mode (d = 1, 2, 4 and
     d > 4), c % 32 == 16 tails of the 16-bit path, and a ragged batch."""
-    check(pattern, batch, dtype, layout, cfg=11, variant=4, kdist="normal")
+    check(pattern, batch, dtype, layout, cfg=11, variant=VARIANTS["direct"], kdist="normal")
+
+
+@pytest.mark.parametrize("pattern", [s for s in MFMA_SHAPES if s[3] <= 16])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+@pytest.mark.parametrize("batch", [256, 72, 1000])
+def test_staged_forced(pattern, dtype, layout, batch):
+    """The LDS-staged MFMA kernel: the same shapes, ragged batches, several
+    stages of l (c up to 128) and the 16-bit c % 32 == 16 tail."""
+    if layout == "bsl" and batch % (4 if dtype == "f32" else 8):
+        pytest.skip("BSL staging needs the batch to be a multiple of a 16-byte unit")
+    check(pattern, batch, dtype, layout, cfg=12, variant=VARIANTS["staged"], kdist="normal")
 
 
 @pytest.mark.parametrize("pattern", [(1, 32, 32, 32), (6, 64, 16, 8), (4, 96, 48, 2)])
 @pytest.mark.parametrize("layout", ["bsf", "bsl"])
 def test_mfma_generic_agree(pattern, layout):
-    """The MFMA, register-direct and generic kernels agree on the same inputs
-    (each within the oracle tolerance, and close to each other)."""
+    """The LDS-staged, register-direct and generic kernels agree on the same
+    inputs (each within the oracle tolerance, and close to each other)."""
     x, kv, _, _ = case(10, pattern, 512, "f32", "normal", "normal")
-    y_m = run_gpu(pattern, x, kv, 512, "f32", layout, variant=3)
-    y_d = run_gpu(pattern, x, kv, 512, "f32", layout, variant=4)
-    y_g = run_gpu(pattern, x, kv, 512, "f32", layout, variant=0)
-    assert rel_err(y_m, y_g) <= 1e-5
+    y_d = run_gpu(pattern, x, kv, 512, "f32", layout, variant=VARIANTS["direct"])
+    y_g = run_gpu(pattern, x, kv, 512, "f32", layout, variant=VARIANTS["generic"])
     assert rel_err(y_d, y_g) <= 1e-5
+    if layout == "bsl" or pattern[3] <= 16:  # BSF staging takes d <= 16 (at most 4 j-groups per tile)
+        y_s = run_gpu(pattern, x, kv, 512, "f32", layout, variant=VARIANTS["staged"])
+        assert rel_err(y_s, y_g) <= 1e-5

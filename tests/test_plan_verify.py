@@ -56,13 +56,34 @@ def test_all_sweep_plans_ragged_batch(dtype, layout):
     assert not bad, bad[:5]
 
 
-def test_sweep_plans_use_direct_kernel():
-    """The register-direct MFMA kernel covers the whole sweep (aligned buffers)."""
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+@pytest.mark.parametrize("batch,every", [(72, 1), (1000, 5)])
+def test_all_sweep_plans_staged(dtype, layout, batch, every):
+    """The LDS-staged kernel on every sweep pattern (forced): bounds, LDS cells
+    written before they are read, every operand element the right X value,
+    every output written once."""
+    bad = []
+    ks.ks_force_variant(4)
+    try:
+        for pattern in sweep_patterns()[::every]:
+            st, rep = ks.ks_plan_verify(*pattern, batch, layout, dtype)
+            if st != 0 and not (rep == "no plan" and layout == "bsl" and batch % (16 // (4 if dtype == "f32" else 2))):
+                bad.append((pattern, rep))
+    finally:
+        ks.ks_force_variant(None)
+    assert not bad, bad[:5]
+
+
+def test_sweep_plans_use_mfma_kernels():
+    """The whole sweep runs on the MFMA kernels (aligned buffers): LDS-staged
+    for batch-size-first with d >= 4, register-direct otherwise."""
     for pattern in sweep_patterns()[::7]:
         for layout in ("bsf", "bsl"):
             for dtype in ("f32", "bf16", "f16"):
                 desc = ks.ks_plan_describe(*pattern, 4096, layout, dtype)
-                assert "name=direct" in desc, (pattern, layout, dtype, desc)
+                want = "name=staged" if (layout == "bsf" and pattern[3] >= 4) else "name=direct"
+                assert want in desc, (pattern, layout, dtype, desc)
 
 
 @pytest.mark.parametrize("variant", [0, 1, 2, 3, 4])
