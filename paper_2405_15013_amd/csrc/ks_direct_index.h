@@ -59,16 +59,18 @@ KS_HD bool direct_c_specialised(int esize, int c, int* nch, bool* tail) {
 }
 
 // Item order: k-group fastest (items sharing X are neighbours, in the same
-// workgroup when possible), then j-group, then i, then the batch tile.
+// workgroup when possible), then the batch tile (wavefronts running together
+// stream neighbouring runs of the same rows of X and Y and share a K block),
+// then j-group, then i.
 KS_HD DItem direct_item(const Problem& p, const DirectTile& t, int V, int MT, int item) {
   DItem it;
   int rest = item;
   const int kg = rest % t.kgroups;
   rest /= t.kgroups;
+  const int bt = rest % t.nbt;
+  rest /= t.nbt;
   const int jg = rest % t.jgroups;
-  rest /= t.jgroups;
-  it.i = rest % p.a;
-  const int bt = rest / p.a;
+  it.i = rest / t.jgroups;
   it.k0 = kg * 16 * MT;
   if (p.layout == BSL) {
     it.j0 = jg;

@@ -53,20 +53,24 @@ struct STile {
 // tiles so that tiles sharing X (neighbouring k-group tiles) share an L2.
 KS_HD int staged_remap(int g, int tiles) { return (g & 7) * (tiles >> 3) + (g >> 3); }
 
+// Tile order: k-group tile fastest, then the batch tile (tiles running
+// together read neighbouring rows or runs of X and share K), then j (BSL),
+// then i.
 KS_HD STile staged_tile(const Problem& p, const StagedTile& t, int block) {
   const int tile = t.remap ? staged_remap(block, t.tiles) : block;
   STile s;
   int rest = tile;
   s.kt = rest % t.kgt;
   rest /= t.kgt;
+  s.bt = rest % t.nbt;
+  rest /= t.nbt;
   if (p.layout == BSL) {
     s.j = rest % p.d;
     rest /= p.d;
   } else {
     s.j = 0;
   }
-  s.i = rest % p.a;
-  s.bt = rest / p.a;
+  s.i = rest;
   return s;
 }
 
