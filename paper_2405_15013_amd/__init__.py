@@ -70,6 +70,11 @@ def load_library():
     if not os.path.exists(_LIB_PATH):
         raise RuntimeError("libks.so is not built (expected at %s); run "
                            "`python -m paper_2405_15013_amd.build`" % _LIB_PATH)
+    # libks.so and PyTorch must share one HIP runtime (the buffers and streams
+    # passed in are PyTorch's).  PyTorch bundles its own libamdhip64 under the
+    # same soname, and whichever is loaded first serves both, so PyTorch is
+    # loaded before the library.
+    import torch  # noqa: F401
     lib = ctypes.CDLL(_LIB_PATH)
     i64, vp, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
     lib.ks_matmul.argtypes = [i64, i64, i64, i64, vp, vp, vp, i64, ci, ci, vp]

@@ -106,6 +106,7 @@ bool plan_valu_bsf(const Problem& p, bool al16, Plan* pl) {
 }  // namespace
 bool plan_direct(const Problem& p, bool al16, Plan* pl);
 bool plan_staged(const Problem& p, bool al16, Plan* pl);
+bool plan_stream(const Problem& p, bool al16, Plan* pl);
 namespace {
 
 bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
@@ -115,6 +116,7 @@ bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
     case V_VALU_BSF: return plan_valu_bsf(p, al16, pl);
     case V_DIRECT: return plan_direct(p, al16, pl);
     case V_STAGED: return plan_staged(p, al16, pl);
+    case V_STREAM: return plan_stream(p, al16, pl);
     default: return false;
   }
 }
@@ -177,6 +179,7 @@ hipError_t launch(const Problem& p, const Plan& pl, hipStream_t s) {
     case V_VALU_BSF: return launch_valu_bsf(p, pl, s);
     case V_DIRECT: return launch_direct(p, pl, s);
     case V_STAGED: return launch_staged(p, pl, s);
+    case V_STREAM: return launch_stream(p, pl, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -251,6 +254,10 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
       snprintf(buf, sizeof buf, "ks_staged_kernel<%s,%d,%d,%s,%d,%d>", t, p.layout, pl.vec,
                pl.unroll ? "true" : "false", pl.waves_m, pl.cps);
       break;
+    case V_STREAM:
+      snprintf(buf, sizeof buf, "ks_stream_kernel<%s,%d,%d,%s,%d>", t, p.layout, pl.vec, pl.unroll ? "true" : "false",
+               pl.waves_m);
+      break;
     default: snprintf(buf, sizeof buf, "?");
   }
   std::string r(buf);
@@ -259,7 +266,7 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
 }
 
 std::string describe(const Problem& p, const Plan& pl) {
-  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "direct", "staged"};
+  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "direct", "staged", "stream"};
   char buf[320];
   snprintf(buf, sizeof buf,
            "variant=%d name=%s vec=%d bt=%d jg=%d unroll=%d waves_m=%d waves_n=%d lds=%d grid=%u block=%u xcd=%d "

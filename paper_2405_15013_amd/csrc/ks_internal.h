@@ -17,7 +17,8 @@ enum Variant : int {
   V_VALU_BSF = 2,  // VALU, batch-size-first, small b and c
   V_DIRECT = 3,    // register-direct MFMA, one work item per wavefront, b and c multiples of 16
   V_STAGED = 4,    // LDS-staged MFMA, 4 work items per workgroup share coalesced X stages
-  V_COUNT = 5
+  V_STREAM = 5,    // register-direct MFMA, each wavefront streams a run of batch tiles
+  V_COUNT = 6
 };
 
 // Problem description shared by all kernels.  Sizes fit in int32 (checked by
@@ -38,7 +39,7 @@ struct Plan {
   int variant = V_GENERIC;
   // variant-specific tile parameters
   int vec = 1;      // elements per memory vector along the contiguous dimension
-  int bt = 0;       // batch rows (BSF) / batch columns (BSL) per work item or tile
+  int bt = 0;       // batch rows (BSF) / batch columns (BSL) per work item or tile; stream: tiles per wavefront
   int jg = 1;       // j values per work item (direct) / j-groups per tile (staged)
   int unroll = 1;   // vectors per thread (VALU)
   int waves_m = 1;  // MFMA: 16-row M-tiles per wavefront (MT)
@@ -60,6 +61,7 @@ hipError_t launch_valu_bsl(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_valu_bsf(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_direct(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_staged(const Problem& p, const Plan& pl, hipStream_t s);
+hipError_t launch_stream(const Problem& p, const Plan& pl, hipStream_t s);
 
 }  // namespace ks
 

@@ -86,33 +86,47 @@ __global__ __launch_bounds__(256) void ks_staged_kernel(Problem p, StagedTile t)
   // ---- stage loads: units tid + 256*k of the stage -------------------------
   // X is streamed with nontemporal loads unless other tiles (k-group tiles)
   // read the same stage.
+  //
+  // Units of a stage: thread tid takes units tid + 256*k.  A unit's X offset
+  // is linear in the stage start (ls * d elements in BSF, ls * d * batch in
+  // BSL) and its LDS offset does not depend on the stage, so both are
+  // computed once for the full stages and once more for a shorter last stage.
   uint32_t stg[UPT][4];
   const bool ntx = t.kgt == 1;
-  auto gload = [&](int ls) {
-    const int nl = c - ls < LCH ? c - ls : LCH;
+  const int64_t xls = p.layout == BSL ? (int64_t)p.d * p.batch : p.d;  // X elements per value of l
+  int64_t uoff[UPT];
+  int ulds[UPT];
+  int nunits = 0;
+  auto units_for = [&](int nl) {
     const int ur = staged_units_per_row(p, t, V, S, nl);
-    const int nunits = staged_rows(p, t, nl) * ur;
+    nunits = staged_rows(p, t, nl) * ur;
 #pragma unroll
     for (int k = 0; k < UPT; ++k) {
       const int u = tid + 256 * k;
-      if (u < nunits) {
-        const T* src = x + staged_x_unit(p, t, st, V, S, ls, u / ur, u % ur);
-        if (ntx) load_piece<16, true>(src, stg[k]);
-        else load_piece<16, false>(src, stg[k]);
+      const int r = u / ur, v = u - (u / ur) * ur;
+      uoff[k] = u < nunits ? staged_x_unit(p, t, st, V, S, 0, r, v) : 0;
+      ulds[k] = staged_lds_unit(t, r, v);
+    }
+  };
+  units_for(c < LCH ? c : LCH);
+  auto gload = [&](int ls) {
+    if (c - ls < LCH && ls > 0) units_for(c - ls);  // shorter last stage
+    const T* xs = x + (int64_t)ls * xls;
+#pragma unroll
+    for (int k = 0; k < UPT; ++k) {
+      if (tid + 256 * k < nunits) {
+        if (ntx) load_piece<16, true>(xs + uoff[k], stg[k]);
+        else load_piece<16, false>(xs + uoff[k], stg[k]);
       }
     }
   };
-  auto lstore = [&](int buf, int ls) {
-    const int nl = c - ls < LCH ? c - ls : LCH;
-    const int ur = staged_units_per_row(p, t, V, S, nl);
-    const int nunits = staged_rows(p, t, nl) * ur;
+  auto lstore = [&](int buf) {
     char* base = smem + buf * t.stage;
 #pragma unroll
     for (int k = 0; k < UPT; ++k) {
-      const int u = tid + 256 * k;
-      if (u < nunits) {
+      if (tid + 256 * k < nunits) {
         const u32x4 v = {stg[k][0], stg[k][1], stg[k][2], stg[k][3]};
-        *reinterpret_cast<u32x4*>(base + staged_lds_unit(t, u / ur, u % ur)) = v;
+        *reinterpret_cast<u32x4*>(base + ulds[k]) = v;
       }
     }
   };
@@ -131,7 +145,7 @@ __global__ __launch_bounds__(256) void ks_staged_kernel(Problem p, StagedTile t)
 
   SChunk<T, LAYOUT, V, STRIDED, MT, LP> kc[CPS], kn[CPS];
   gload(0);
-  lstore(0, 0);
+  lstore(0);
   if (nstages > 1) gload(LCH);
 #pragma unroll
   for (int q = 0; q < CPS; ++q)
@@ -163,7 +177,7 @@ __global__ __launch_bounds__(256) void ks_staged_kernel(Problem p, StagedTile t)
       }
     }
     if (more) {
-      lstore((s + 1) & 1, ls + LCH);
+      lstore((s + 1) & 1);
       if (s + 2 < nstages) gload(ls + 2 * LCH);
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll

@@ -16,12 +16,14 @@
 #include "ks_internal.h"
 #include "ks_direct_index.h"
 #include "ks_staged_index.h"
+#include "ks_stream_index.h"
 
 namespace ks {
 
 // Defined in ks_direct_plan.cpp and ks_staged_plan.cpp.
 DirectTile direct_tile(const Problem& p, const Plan& pl);
 StagedTile staged_tile_of(const Problem& p, const Plan& pl);
+StreamTile stream_tile_of(const Problem& p, const Plan& pl);
 
 // Defined in ks_host.cpp.
 bool plan_for_verify(int64_t a, int64_t b, int64_t c, int64_t d, int64_t batch, int layout, int dtype, Problem* p,
@@ -116,6 +118,50 @@ int64_t expected_x(const Problem& p, const DItem& it, int V, int LP, int l0, int
   return (int64_t)(it.beta0 + n) * p.N + (int64_t)it.i * p.c * p.d + l * p.d + it.j0 + e;
 }
 
+// X and K reads and Y writes of one register-direct work item, for the
+// chunks (l0, values of l per lane group) listed.
+bool verify_item(Checker& ck, const DItem& it, bool strided, int V, int MT, int S, const int (*chunks)[2], int nch) {
+  const Problem& p = ck.p;
+  const int VK = p.layout == BSL ? 1 : V;
+  for (int ci = 0; ci < nch; ++ci) {
+    const int l0 = chunks[ci][0], lp = chunks[ci][1];
+    const int np = direct_x_pieces(p.layout, strided, lp, V, S);
+    const int pe = direct_x_piece_elems(p.layout, strided, lp, V, S);
+    if (pe * S != 16 && pe * S != 8) return ck.fail("X piece is not 8 or 16 bytes", pe * S);
+    if (np * pe != lp * V) return ck.fail("X pieces do not tile the lane block", np);
+    for (int lane = 0; lane < 64; ++lane) {
+      const int n = lane & 15, g = lane >> 4;
+      const bool valid = direct_lane_valid(p, it, V, n);
+      for (int q = 0; q < np; ++q) {
+        const int64_t off = direct_x_off(p, it, strided, lp, V, S, l0, n, g, q);
+        if ((off * S) % (pe * S)) return ck.fail("X piece not aligned to its size", off);
+        ck.read_x(off, pe);
+        for (int e = 0; valid && e < pe; ++e)
+          if (off + e != expected_x(p, it, V, lp, l0, n, g, q * pe + e))
+            return ck.fail("operand element is not the X value the product needs", off + e);
+      }
+      for (int mt = 0; mt < MT; ++mt)
+        for (int e = 0; e < VK; ++e) {
+          const int64_t off = direct_k_off(p, it, lp, l0, n, g, mt, e);
+          if ((off * S) % (lp * S)) return ck.fail("K operand not aligned to its size", off);
+          ck.read_k(off, lp);
+        }
+    }
+  }
+  const int ynp = direct_y_pieces(p.layout, strided, V, S);
+  const int ype = direct_y_piece_elems(p.layout, strided, V, S);
+  if (ype * S != 16 && ype * S != 8) return ck.fail("Y piece is not 8 or 16 bytes", ype * S);
+  for (int mt = 0; mt < MT; ++mt)
+    for (int lane = 0; lane < 64; ++lane)
+      for (int q = 0; q < ynp; ++q) {
+        const int64_t off = direct_y_off(p, it, strided, V, S, mt, lane & 15, lane >> 4, q);
+        if (off < 0) continue;
+        if ((off * S) % (ype * S)) return ck.fail("Y piece not aligned to its size", off);
+        ck.write_y(off, ype);
+      }
+  return ck.err.empty();
+}
+
 bool verify_direct(Checker& ck, const Plan& pl) {
   const Problem& p = ck.p;
   const DirectTile t = direct_tile(p, pl);
@@ -128,51 +174,38 @@ bool verify_direct(Checker& ck, const Plan& pl) {
   if ((int64_t)pl.grid * t.waves < t.items) return ck.fail("grid does not cover the items", pl.grid);
   if (p.layout == BSF && (p.d % V || (!strided && V != p.d))) return ck.fail("bad j-vector", V);
   if (p.layout == BSL && p.batch % V) return ck.fail("batch not a multiple of the vector width", p.batch);
-  // chunks: (l0, values of l per lane group)
   int chunks[16][2], nch = 0;
   for (int l0 = 0; l0 + CH <= p.c; l0 += CH) { chunks[nch][0] = l0; chunks[nch][1] = LP; ++nch; }
   if (S == 2 && p.c % CH) { chunks[nch][0] = p.c - 16; chunks[nch][1] = 4; ++nch; }
   if (nch == 0) return ck.fail("no chunk covers c", p.c);
-  const int VK = p.layout == BSL ? 1 : V;
-  for (int item = 0; item < t.items && ck.err.empty(); ++item) {
-    const DItem it = direct_item(p, t, V, MT, item);
-    for (int ci = 0; ci < nch; ++ci) {
-      const int l0 = chunks[ci][0], lp = chunks[ci][1];
-      const int np = direct_x_pieces(p.layout, strided, lp, V, S);
-      const int pe = direct_x_piece_elems(p.layout, strided, lp, V, S);
-      if (pe * S != 16 && pe * S != 8) return ck.fail("X piece is not 8 or 16 bytes", pe * S);
-      if (np * pe != lp * V) return ck.fail("X pieces do not tile the lane block", np);
-      for (int lane = 0; lane < 64; ++lane) {
-        const int n = lane & 15, g = lane >> 4;
-        const bool valid = direct_lane_valid(p, it, V, n);
-        for (int q = 0; q < np; ++q) {
-          const int64_t off = direct_x_off(p, it, strided, lp, V, S, l0, n, g, q);
-          if ((off * S) % (pe * S)) return ck.fail("X piece not aligned to its size", off);
-          ck.read_x(off, pe);
-          for (int e = 0; valid && e < pe; ++e)
-            if (off + e != expected_x(p, it, V, lp, l0, n, g, q * pe + e))
-              return ck.fail("operand element is not the X value the product needs", off + e);
-        }
-        for (int mt = 0; mt < MT; ++mt)
-          for (int e = 0; e < VK; ++e) {
-            const int64_t off = direct_k_off(p, it, lp, l0, n, g, mt, e);
-            if ((off * S) % (lp * S)) return ck.fail("K operand not aligned to its size", off);
-            ck.read_k(off, lp);
-          }
-      }
-    }
-    const int ynp = direct_y_pieces(p.layout, strided, V, S);
-    const int ype = direct_y_piece_elems(p.layout, strided, V, S);
-    if (ype * S != 16 && ype * S != 8) return ck.fail("Y piece is not 8 or 16 bytes", ype * S);
-    for (int mt = 0; mt < MT; ++mt)
-      for (int lane = 0; lane < 64; ++lane)
-        for (int q = 0; q < ynp; ++q) {
-          const int64_t off = direct_y_off(p, it, strided, V, S, mt, lane & 15, lane >> 4, q);
-          if (off < 0) continue;
-          if ((off * S) % (ype * S)) return ck.fail("Y piece not aligned to its size", off);
-          ck.write_y(off, ype);
-        }
+  for (int item = 0; item < t.items && ck.err.empty(); ++item)
+    if (!verify_item(ck, direct_item(p, t, V, MT, item), strided, V, MT, S, chunks, nch)) return false;
+  return ck.err.empty();
+}
+
+bool verify_stream(Checker& ck, const Plan& pl) {
+  const Problem& p = ck.p;
+  const StreamTile t = stream_tile_of(p, pl);
+  const int V = pl.vec, MT = pl.waves_m, S = p.dtype == F32 ? 4 : 2;
+  const bool strided = pl.unroll != 0;
+  if (t.kgroups * 16 * MT != p.b) return ck.fail("M-tiles do not cover b", p.b);
+  if (p.c % 16) return ck.fail("c not a multiple of 16", p.c);
+  if (t.nwaves < 1 || t.nwaves > t.tiles) return ck.fail("bad number of wavefronts", t.nwaves);
+  if (p.layout == BSF && (p.d % V || (!strided && V != p.d))) return ck.fail("bad j-vector", V);
+  if (p.layout == BSL && p.batch % V) return ck.fail("batch not a multiple of the vector width", p.batch);
+  int chunks[64][2], nch = 0;
+  if (p.c / 16 > 64) return ck.fail("c too large for the verifier", p.c);
+  for (int l0 = 0; l0 < p.c; l0 += 16) { chunks[nch][0] = l0; chunks[nch][1] = 4; ++nch; }
+  int next = 0;  // the shares must tile [0, tiles) in order
+  for (int w = 0; w < t.nwaves && ck.err.empty(); ++w) {
+    int first, count;
+    stream_share(t, w, &first, &count);
+    if (first != next || count < 0) return ck.fail("wavefront shares do not tile the tiles", w);
+    next = first + count;
+    for (int q = 0; q < count; ++q)
+      if (!verify_item(ck, stream_item(p, t, V, MT, first + q), strided, V, MT, S, chunks, nch)) return false;
   }
+  if (next != t.tiles) return ck.fail("wavefront shares do not cover the tiles", next);
   return ck.err.empty();
 }
 
@@ -204,9 +237,13 @@ bool verify_staged(Checker& ck, const Plan& pl) {
       const int ur = staged_units_per_row(p, t, V, S, nl);
       const int nunits = staged_rows(p, t, nl) * ur;
       if (nunits > 1024) return ck.fail("stage has more than 1024 units", nunits);
+      const int64_t xls = p.layout == BSL ? (int64_t)p.d * p.batch : p.d;
       for (int u = 0; u < nunits; ++u) {
         const int r = u / ur, v = u % ur;
         const int64_t off = staged_x_unit(p, t, st, V, S, ls, r, v);
+        // the kernel computes the offset once at ls = 0 and shifts it per stage
+        if (off != staged_x_unit(p, t, st, V, S, 0, r, v) + (int64_t)ls * xls)
+          return ck.fail("X unit offset is not linear in the stage start", off);
         if ((off * S) % 16) return ck.fail("X unit not 16-byte aligned", off);
         ck.read_x(off, UE);
         const int lo = staged_lds_unit(t, r, v);
@@ -336,6 +373,7 @@ extern "C" ks_status_t ks_plan_verify(int64_t a, int64_t b, int64_t c, int64_t d
     case V_VALU_BSF: ok = verify_valu_bsf(ck, pl); break;
     case V_DIRECT: ok = verify_direct(ck, pl); break;
     case V_STAGED: ok = verify_staged(ck, pl); break;
+    case V_STREAM: ok = verify_stream(ck, pl); break;
     default: ck.fail("unknown variant", pl.variant);
   }
   if (ok) ok = ck.coverage();

@@ -12,7 +12,7 @@ from parity_util import TOL, case, from_device, nan_tensor, oracle_y, rel_err, t
 
 pytestmark = pytest.mark.gpu
 
-VARIANTS = {"generic": 0, "valu_bsl": 1, "valu_bsf": 2, "direct": 3, "staged": 4}
+VARIANTS = {"generic": 0, "valu_bsl": 1, "valu_bsf": 2, "direct": 3, "staged": 4, "stream": 5}
 
 
 def run_gpu(pattern, x_logical, kv, batch, dtype, layout, variant=None, x_offset=0, y_offset=0):
@@ -232,6 +232,16 @@ def test_direct_forced(pattern, dtype, layout, batch):
     """The register-direct MFMA kernel on every j-vector mode (d = 1, 2, 4 and
     d > 4), c % 32 == 16 tails of the 16-bit path, and a ragged batch."""
     check(pattern, batch, dtype, layout, cfg=11, variant=VARIANTS["direct"], kdist="normal")
+
+
+@pytest.mark.parametrize("pattern", MFMA_SHAPES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+@pytest.mark.parametrize("batch", [256, 72, 25088])
+def test_stream_forced(pattern, dtype, layout, batch):
+    """The streaming kernel: one tile per wavefront (small batches) and runs of
+    tiles per wavefront (full batch), every j-vector mode, ragged batches."""
+    check(pattern, batch, dtype, layout, cfg=13, variant=VARIANTS["stream"], kdist="normal")
 
 
 @pytest.mark.parametrize("pattern", [s for s in MFMA_SHAPES if s[3] <= 16])

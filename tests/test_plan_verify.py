@@ -75,6 +75,24 @@ def test_all_sweep_plans_staged(dtype, layout, batch, every):
     assert not bad, bad[:5]
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+@pytest.mark.parametrize("batch,every", [(72, 1), (25088, 17)])
+def test_all_sweep_plans_stream(dtype, layout, batch, every):
+    """The streaming kernel on the sweep patterns (forced), including full
+    batches where a wavefront walks several batch tiles."""
+    bad = []
+    ks.ks_force_variant(5)
+    try:
+        for pattern in sweep_patterns()[::every]:
+            st, rep = ks.ks_plan_verify(*pattern, batch, layout, dtype)
+            if st != 0:
+                bad.append((pattern, rep))
+    finally:
+        ks.ks_force_variant(None)
+    assert not bad, bad[:5]
+
+
 def test_sweep_plans_use_mfma_kernels():
     """The whole sweep runs on the MFMA kernels (aligned buffers): LDS-staged
     for batch-size-first with d >= 4, register-direct otherwise."""
@@ -86,7 +104,7 @@ def test_sweep_plans_use_mfma_kernels():
                 assert want in desc, (pattern, layout, dtype, desc)
 
 
-@pytest.mark.parametrize("variant", [0, 1, 2, 3, 4])
+@pytest.mark.parametrize("variant", [0, 1, 2, 3, 4, 5])
 def test_forced_variants(variant):
     """Every variant that accepts a shape produces a valid launch for it."""
     ks.ks_force_variant(variant)
