@@ -21,7 +21,8 @@
 
 namespace ks {
 
-constexpr int kStagedUnitsPerThread = 4;  // 16-byte units of a stage per thread (<= 1024 per stage)
+constexpr int kStagedMaxLds = 128 * 1024;  // LDS per workgroup (of the CU's 160 KB)
+constexpr int kStagedUnitsPerThread = 4;  // 16-byte units of a stage per thread (<= 256 per wavefront)
 
 template <int NB>
 __device__ __forceinline__ void lds_read_piece(const char* p, uint32_t* w) {
@@ -62,13 +63,14 @@ struct SChunk {
 };
 
 template <typename T, int LAYOUT, int V, bool STRIDED, int MT, int CPS>
-__global__ __launch_bounds__(256) void ks_staged_kernel(Problem p, StagedTile t) {
+__global__ __launch_bounds__(512) void ks_staged_kernel(Problem p, StagedTile t) {
   constexpr int S = sizeof(T);
   constexpr int LP = S == 4 ? 4 : 8;
   constexpr int CH = 4 * LP;
   constexpr int UPT = kStagedUnitsPerThread;
   extern __shared__ __attribute__((aligned(16))) char smem[];
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
+  const int nthr = 64 * t.W;
   const int n = lane & 15, g = lane >> 4;
   const STile st = staged_tile(p, t, blockIdx.x);
   const SItem si = staged_item(p, t, st, V, MT, w);
@@ -83,11 +85,11 @@ __global__ __launch_bounds__(256) void ks_staged_kernel(Problem p, StagedTile t)
   const int LCH = t.LCH;
   const int nstages = (c + LCH - 1) / LCH;
 
-  // ---- stage loads: units tid + 256*k of the stage -------------------------
+  // ---- stage loads: units tid + nthr*k of the stage ------------------------
   // X is streamed with nontemporal loads unless other tiles (k-group tiles)
   // read the same stage.
   //
-  // Units of a stage: thread tid takes units tid + 256*k.  A unit's X offset
+  // Units of a stage: thread tid takes units tid + nthr*k.  A unit's X offset
   // is linear in the stage start (ls * d elements in BSF, ls * d * batch in
   // BSL) and its LDS offset does not depend on the stage, so both are
   // computed once for the full stages and once more for a shorter last stage.
@@ -102,7 +104,7 @@ __global__ __launch_bounds__(256) void ks_staged_kernel(Problem p, StagedTile t)
     nunits = staged_rows(p, t, nl) * ur;
 #pragma unroll
     for (int k = 0; k < UPT; ++k) {
-      const int u = tid + 256 * k;
+      const int u = tid + nthr * k;
       const int r = u / ur, v = u - (u / ur) * ur;
       uoff[k] = u < nunits ? staged_x_unit(p, t, st, V, S, 0, r, v) : 0;
       ulds[k] = staged_lds_unit(t, r, v);
@@ -114,7 +116,7 @@ __global__ __launch_bounds__(256) void ks_staged_kernel(Problem p, StagedTile t)
     const T* xs = x + (int64_t)ls * xls;
 #pragma unroll
     for (int k = 0; k < UPT; ++k) {
-      if (tid + 256 * k < nunits) {
+      if (tid + nthr * k < nunits) {
         if (ntx) load_piece<16, true>(xs + uoff[k], stg[k]);
         else load_piece<16, false>(xs + uoff[k], stg[k]);
       }
@@ -124,7 +126,7 @@ __global__ __launch_bounds__(256) void ks_staged_kernel(Problem p, StagedTile t)
     char* base = smem + buf * t.stage;
 #pragma unroll
     for (int k = 0; k < UPT; ++k) {
-      if (tid + 256 * k < nunits) {
+      if (tid + nthr * k < nunits) {
         const u32x4 v = {stg[k][0], stg[k][1], stg[k][2], stg[k][3]};
         *reinterpret_cast<u32x4*>(base + ulds[k]) = v;
       }
@@ -231,7 +233,7 @@ __global__ __launch_bounds__(256) void ks_staged_kernel(Problem p, StagedTile t)
     const int uy = staged_y_units_per_row(p, t, MT, S);
     const int nunits = 16 * t.RS * uy;
     T* __restrict__ y = static_cast<T*>(p.y);
-    for (int u = tid; u < nunits; u += 256) {
+    for (int u = tid; u < nunits; u += nthr) {
       const int row = u / uy, v = u % uy;
       const int64_t off = staged_y_unit(p, t, st, MT, S, row, v);
       if (off < 0) continue;
@@ -243,7 +245,18 @@ __global__ __launch_bounds__(256) void ks_staged_kernel(Problem p, StagedTile t)
 
 template <typename T, int LAYOUT, int V, bool STRIDED, int MT, int CPS>
 hipError_t launch_staged_inst(const Problem& p, const StagedTile& t, hipStream_t s) {
-  hipLaunchKernelGGL((ks_staged_kernel<T, LAYOUT, V, STRIDED, MT, CPS>), dim3(t.tiles), dim3(256), t.lds, s, p, t);
+  if (t.lds > 64 * 1024) {
+    // Opt in to more than 64 KB of dynamic LDS (once per instance).
+    static bool raised = false;
+    if (!raised) {
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ks_staged_kernel<T, LAYOUT, V, STRIDED, MT, CPS>),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, kStagedMaxLds);
+      if (e != hipSuccess) return e;
+      raised = true;
+    }
+  }
+  hipLaunchKernelGGL((ks_staged_kernel<T, LAYOUT, V, STRIDED, MT, CPS>), dim3(t.tiles), dim3(64 * t.W), t.lds, s, p,
+                     t);
   return hipGetLastError();
 }
 

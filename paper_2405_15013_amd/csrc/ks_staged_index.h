@@ -1,7 +1,7 @@
 // Index arithmetic of the LDS-staged MFMA kernels (ks_staged.h), shared by the
 // kernels and by the host-side plan verifier (ks_plan_verify).
 //
-// A workgroup of 4 wavefronts owns one tile: the X values a set of 4 work
+// A workgroup of W wavefronts owns one tile: the X values a set of W work
 // items share (paper Section 4.1, Algorithm 2: output-stationary, every output
 // written once).  The reduction over l is walked in stages of LCH values; the
 // workgroup loads a stage of X with coalesced 16-byte loads (consecutive
@@ -18,7 +18,7 @@
 //    16*V*RS contiguous batch entries.
 //
 // Wavefront w of the tile takes rs = w % RS, jg = (w / RS) % JG and
-// kgw = w / (RS * JG) (RS * JG * KGW == 4), i.e. the work item
+// kgw = w / (RS * JG) (W = RS * JG * KGW <= 8), i.e. the work item
 // (rows or columns group rs, j-group jg, k-group kt*KGW + kgw).
 #pragma once
 #include <hip/hip_runtime.h>
@@ -31,6 +31,7 @@
 namespace ks {
 
 struct StagedTile {
+  int W;         // wavefronts per workgroup: RS * JG * KGW
   int RS;        // 16-row (BSF) or 16*V-column (BSL) groups per tile
   int JG;        // j-groups per tile (BSF: d / V; BSL: 1)
   int KGW;       // k-groups per tile

@@ -1,11 +1,14 @@
 // Planner and launcher of the LDS-staged MFMA kernels (ks_staged.h).
 //
 // A plan fixes the vector width V (4 along the batch in BSL, min(d, 4) of j
-// in BSF), the M-tiles per wavefront MT, and how the 4 wavefronts of a tile
-// split the work: JG j-groups (BSF: d / V) x KGW k-groups x RS row/column
-// groups with JG * KGW * RS == 4.  A stage of X is at most 1024 16-byte units
-// (16 KB), so every thread stages at most 4 units and a workgroup needs two
-// stage buffers of LDS.
+// in BSF), the M-tiles per wavefront MT, and how the W <= 8 wavefronts of a
+// tile split the work: JG j-groups (BSF: d / V) x KGW k-groups x RS row/column
+// groups, with W = 4 (8 when d / V = 8: eight j-groups).  Larger tiles cut
+// the re-reads of K and X but leave fewer workgroups resident per CU, which
+// measured slower.  Preferred: enough tiles for the chip, then the fewest
+// re-reads of X, then the largest MT.  A stage of X is at most 256 16-byte
+// units per wavefront (4 per thread) and a workgroup needs two stage buffers
+// of LDS.
 #include "ks_staged_index.h"
 #include "ks_internal.h"
 
@@ -19,7 +22,8 @@ hipError_t launch_staged_f16(const Problem& p, const StagedTile& t, int V, bool 
                              hipStream_t s);
 
 namespace {
-constexpr int kMaxStageUnits = 1024;  // 256 threads x kStagedUnitsPerThread (ks_staged.h)
+constexpr int kUnitsPerWave = 256;  // 64 threads x kStagedUnitsPerThread (ks_staged.h)
+constexpr int kMaxLds = 128 * 1024;  // kStagedMaxLds (ks_staged.h)
 
 // Largest MT instantiated; keep in sync with direct_mt_max() in ks_direct.h.
 int mt_max(int esize, int layout, int V) {
@@ -31,6 +35,7 @@ int mt_max(int esize, int layout, int V) {
 StagedTile staged_tile_of(const Problem& p, const Plan& pl) {
   StagedTile t;
   const int S = p.dtype == F32 ? 4 : 2, V = pl.vec, MT = pl.waves_m;
+  t.W = (int)pl.block / 64;
   t.RS = pl.rs;
   t.JG = p.layout == BSL ? 1 : p.d / V;
   t.KGW = pl.kgw;
@@ -72,7 +77,7 @@ bool plan_staged(const Problem& p, bool al16, Plan* pl) {
     if ((V != 1 && V != 2 && V != 4) || p.d % V) return false;
     strided = V < p.d;
     JG = p.d / V;
-    if (JG > 4) return false;
+    if (JG > 8) return false;
   }
   const int lch = (p.layout == BSF && CH * p.d * S < 128) ? 2 * CH : CH;
   const int KT = p.b / 16;
@@ -82,28 +87,47 @@ bool plan_staged(const Problem& p, bool al16, Plan* pl) {
   for (int mt = mt_max(S, p.layout, V); mt >= 1; --mt) {
     if (KT % mt) continue;
     const int kgroups = KT / mt;
-    for (int kgw : {4, 2, 1}) {
-      if (kgw * JG > 4 || kgroups % kgw) continue;
-      const int rs = 4 / (JG * kgw);
-      const int64_t units = p.layout == BSL ? (int64_t)lch * (16 * V * rs * S / 16)
-                                            : (int64_t)16 * rs * (lch * p.d * S / 16);
-      if (units > kMaxStageUnits) continue;
-      const int kgt = kgroups / kgw;
-      const int span = p.layout == BSL ? 16 * V * rs : 16 * rs;
-      const int64_t tiles = (int64_t)((p.batch + span - 1) / span) * p.a * (p.layout == BSL ? p.d : 1) * kgt;
-      if (tiles > 0x7fffffff) continue;
-      // Enough workgroups first (4 per CU), then fewest re-reads of X, then
-      // the largest MT.
-      const int64_t tcap = tiles < 1024 ? tiles : 1024;
-      const int64_t bcap = best_tiles < 1024 ? best_tiles : 1024;
-      bool better = !found || tcap > bcap || (tcap == bcap && (kgt < best_kgt || (kgt == best_kgt && mt > best_mt)));
-      if (better) {
-        found = true;
-        best_tiles = tiles;
-        best_kgt = kgt;
-        best_mt = mt;
-        best_kgw = kgw;
-        best_rs = rs;
+    for (int kgw = 1; kgw <= 8; ++kgw) {
+      if (kgroups % kgw || kgw * JG > 8) continue;
+      for (int rs = 1; rs * kgw * JG <= 8; rs *= 2) {
+        const int w = rs * kgw * JG;
+        // Four wavefronts per tile (smaller tiles keep more workgroups resident
+        // per CU); eight only when there are eight j-groups.
+        if (w != (JG > 4 ? 8 : 4)) continue;
+        const int64_t units = p.layout == BSL ? (int64_t)lch * (16 * V * rs * S / 16)
+                                              : (int64_t)16 * rs * (lch * p.d * S / 16);
+        if (units > (int64_t)kUnitsPerWave * w) continue;
+        const int kgt = kgroups / kgw;
+        const int span = p.layout == BSL ? 16 * V * rs : 16 * rs;
+        const int64_t tiles = (int64_t)((p.batch + span - 1) / span) * p.a * (p.layout == BSL ? p.d : 1) * kgt;
+        if (tiles > 0x7fffffff) continue;
+        // LDS: two stages, and the BSF output tile
+        const int64_t pitch = p.layout == BSL ? (int64_t)16 * V * rs * S : (int64_t)lch * p.d * S + 16;
+        const int64_t stage = p.layout == BSL ? lch * pitch : 16 * rs * pitch;
+        int64_t lds = 2 * stage;
+        if (p.layout == BSF) {
+          const int64_t ytile = 16 * rs * ((int64_t)16 * mt * kgw * p.d * S + 16);
+          if (ytile > lds) lds = ytile;
+        }
+        if (lds > kMaxLds) continue;
+        // Enough tiles (4 per CU) first, then the fewest re-reads of X, then
+        // the largest MT.
+        const int64_t tcap = tiles < 1024 ? tiles : 1024;
+        const int64_t bcap = best_tiles < 1024 ? best_tiles : 1024;
+        bool better = !found;
+        if (!better) {
+          if (tcap != bcap) better = tcap > bcap;
+          else if (kgt != best_kgt) better = kgt < best_kgt;
+          else better = mt > best_mt;
+        }
+        if (better) {
+          found = true;
+          best_tiles = tiles;
+          best_kgt = kgt;
+          best_mt = mt;
+          best_kgw = kgw;
+          best_rs = rs;
+        }
       }
     }
   }
@@ -119,11 +143,11 @@ bool plan_staged(const Problem& p, bool al16, Plan* pl) {
   pl->lch = lch;
   pl->cps = lch / CH;
   pl->bt = p.layout == BSL ? 16 * V * best_rs : 16 * best_rs;
-  pl->block = 256;
+  pl->block = 64u * (unsigned)(best_rs * best_kgw * JG);
   pl->grid = (unsigned)best_tiles;
   pl->xcd_remap = (best_kgt > 1 && best_tiles % 8 == 0) ? 1 : 0;
   const StagedTile t = staged_tile_of(p, *pl);
-  if (t.lds > 64 * 1024) return false;
+  if (t.lds > kMaxLds) return false;
   pl->lds_bytes = t.lds;
   return true;
 }

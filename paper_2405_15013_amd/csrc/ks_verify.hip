@@ -215,10 +215,10 @@ bool verify_staged(Checker& ck, const Plan& pl) {
   const int V = pl.vec, MT = pl.waves_m, S = p.dtype == F32 ? 4 : 2;
   const bool strided = pl.unroll != 0;
   const int LP = S == 4 ? 4 : 8, CH = 4 * LP, UE = 16 / S;
-  if (t.RS * t.JG * t.KGW != 4) return ck.fail("waves do not split the tile 4 ways", t.RS * t.JG * t.KGW);
+  if (t.RS * t.JG * t.KGW != t.W || t.W < 1 || t.W > 8) return ck.fail("waves do not split the tile", t.W);
   if (t.kgt * t.KGW * 16 * MT != p.b) return ck.fail("k-groups do not cover b", p.b);
   if (t.LCH % CH || t.LCH / CH != pl.cps) return ck.fail("stage is not a whole number of chunks", t.LCH);
-  if ((int)pl.grid != t.tiles || pl.block != 256) return ck.fail("grid does not match the tiles", pl.grid);
+  if ((int)pl.grid != t.tiles || (int)pl.block != 64 * t.W) return ck.fail("grid does not match the tiles", pl.grid);
   if (pl.lds_bytes != t.lds || t.lds < 2 * t.stage) return ck.fail("LDS allocation does not hold two stages", pl.lds_bytes);
   if (p.layout == BSF && t.lds < 16 * t.RS * t.ypitch) return ck.fail("LDS allocation does not hold the output tile", t.lds);
   if (t.remap && t.tiles % 8) return ck.fail("XCD remap needs a multiple of 8 tiles", t.tiles);
@@ -236,7 +236,7 @@ bool verify_staged(Checker& ck, const Plan& pl) {
       std::fill(shadow.begin(), shadow.end(), (int64_t)-1);
       const int ur = staged_units_per_row(p, t, V, S, nl);
       const int nunits = staged_rows(p, t, nl) * ur;
-      if (nunits > 1024) return ck.fail("stage has more than 1024 units", nunits);
+      if (nunits > 256 * t.W) return ck.fail("stage has more than 4 units per thread", nunits);
       const int64_t xls = p.layout == BSL ? (int64_t)p.d * p.batch : p.d;
       for (int u = 0; u < nunits; ++u) {
         const int r = u / ur, v = u % ur;
@@ -254,7 +254,7 @@ bool verify_staged(Checker& ck, const Plan& pl) {
           cell = off + e;
         }
       }
-      for (int w = 0; w < 4; ++w) {
+      for (int w = 0; w < t.W; ++w) {
         const SItem si = staged_item(p, t, st, V, MT, w);
         DItem it;
         it.i = st.i; it.j0 = si.j0; it.k0 = si.k0; it.beta0 = si.beta0;
@@ -296,7 +296,7 @@ bool verify_staged(Checker& ck, const Plan& pl) {
       }
     }
     if (p.layout == BSL) {
-      for (int w = 0; w < 4; ++w) {
+      for (int w = 0; w < t.W; ++w) {
         const SItem si = staged_item(p, t, st, V, MT, w);
         DItem it;
         it.i = st.i; it.j0 = si.j0; it.k0 = si.k0; it.beta0 = si.beta0;
@@ -316,7 +316,7 @@ bool verify_staged(Checker& ck, const Plan& pl) {
       // by the lane holding that output, then stored by its 16-byte unit.
       const int kr = staged_y_kr(t, MT), rows = 16 * t.RS;
       std::vector<int64_t> ytile((size_t)rows * t.ypitch / S, -1);
-      for (int w = 0; w < 4; ++w) {
+      for (int w = 0; w < t.W; ++w) {
         const SItem si = staged_item(p, t, st, V, MT, w);
         for (int lane = 0; lane < 64; ++lane) {
           const int n = lane & 15, g = lane >> 4, r = 16 * si.rs + n;
