@@ -84,8 +84,163 @@ def plan_field(desc, key):
     return dict(kv.split("=", 1) for kv in desc.split())[key]
 
 
+def kernel_sources_sha1():
+    """Hash of the sources the kernels are built from (and their build
+    script): a traffic record taken from profiler counters is used only while
+    this hash is unchanged."""
+    import hashlib
+    h = hashlib.sha1()
+    csrc = os.path.join(ROOT, "paper_2405_15013_amd", "csrc")
+    names = sorted(f for f in os.listdir(csrc) if f.endswith((".h", ".hip", ".cpp")) and f != "ks_verify.hip")
+    for f in names + ["../build.py"]:
+        with open(os.path.join(csrc, f), "rb") as fh:
+            h.update(f.encode() + b"\0" + fh.read())
+    return h.hexdigest()
+
+
+TRAFFIC_TAG = "traffic-record: "
+
+
+def traffic_record(kernel, sample_every):
+    """HBM bytes per launch of `kernel` from a committed counter summary
+    (profiles/*.md), or None when there is none for the current sources and
+    the same sweep sample."""
+    pdir = os.path.join(ROOT, "profiles")
+    if not os.path.isdir(pdir):
+        return None
+    sha = kernel_sources_sha1()
+    for f in sorted(os.listdir(pdir)):
+        if not f.endswith(".md"):
+            continue
+        with open(os.path.join(pdir, f)) as fh:
+            for line in fh:
+                if line.startswith(TRAFFIC_TAG):
+                    rec = json.loads(line[len(TRAFFIC_TAG):])
+                    if (rec.get("kernel") == kernel and rec.get("sources_sha1") == sha
+                            and rec.get("sample_every") == sample_every):
+                        return rec
+    return None
+
+
+def counter_per_dispatch(csv_path, counter, name_filter=None):
+    """Per-dispatch totals of one counter from a rocprofv3 counter_collection
+    CSV (rows of one dispatch are summed over the counter's instances), for
+    the dispatches whose kernel name (spaces removed, lower case) contains
+    `name_filter`."""
+    import csv
+    per = {}
+    names = {}
+    with open(csv_path) as fh:
+        for r in csv.DictReader(fh):
+            if r["Counter_Name"] != counter:
+                continue
+            if name_filter is not None and name_filter not in r["Kernel_Name"].replace(" ", "").lower():
+                continue
+            per[r["Dispatch_Id"]] = per.get(r["Dispatch_Id"], 0.0) + float(r["Counter_Value"])
+            names[r["Kernel_Name"]] = names.get(r["Kernel_Name"], 0) + 1
+    return per, names
+
+
+def copy_calibration(nbytes=64 << 20, pairs=8, reps=20):
+    """A plain device-to-device copy of `nbytes`, `reps` times over `pairs`
+    buffer pairs: the profiler's FETCH_SIZE / WRITE_SIZE of these dispatches
+    against the known nbytes give the counters' scale."""
+    import torch
+    src = [torch.ones(nbytes, dtype=torch.uint8, device="cuda:0") for _ in range(pairs)]
+    dst = [torch.zeros(nbytes, dtype=torch.uint8, device="cuda:0") for _ in range(pairs)]
+    torch.cuda.synchronize()
+    for r in range(reps):
+        dst[r % pairs].copy_(src[r % pairs])
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": nbytes, "dispatches": reps}), flush=True)
+
+
+def trace_summary(stats_csv, bench_json, out_md, command_lines, top=25):
+    """Write the kernel-trace summary (rocprofv3 --kernel-trace --stats) of a
+    bench run, with the dominant kernel's profiler average beside the
+    bench's own avg_launch_us.  `bench_json` is the bench line of the same
+    command run without the profiler (the tracer adds a per-dispatch cost
+    that changes which instance dominates among microsecond-sized calls)."""
+    import csv
+    with open(bench_json) as fh:
+        bench = json.loads(fh.read().strip().splitlines()[-1])
+    dom = bench["roofline"]["kernel"]
+    rows = list(csv.DictReader(open(stats_csv)))
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    drow = [r for r in rows if dom in r["Name"].replace(" ", "")]
+    lines = ["# Kernel-trace summary: KS pattern sweep bench (all kernels)", "",
+             "Workload: %s, %d timed sweep points plus the context families; %d timed + %d warmup passes per point "
+             "over a >= 768 MB buffer rotation, launched through HIP graphs." % (
+                 bench["config"]["workload"], bench["config"]["points"], bench["steps"], bench["warmup"]), "",
+             "Command (from the repository root):", "", "```"] + command_lines + ["```", "",
+             "Bench line of the same command without the profiler: median fraction of roofline %.4f "
+             "(sources sha1 %s)." % (
+                 bench["value"], bench["sources_sha1"][:12]), "",
+             "Dominant kernel (largest share of timed sweep time, %.1f %%): `%s`." % (
+                 100 * bench["roofline"]["share_of_sweep_time"], dom)]
+    if drow:
+        r = drow[0]
+        lines.append("bench.py (HIP events on the replay stream, timed calls only): avg_launch_us = %.2f; "
+                     "rocprofv3 average over all its dispatches: %.2f us (%s calls, incl. warmup and eager calls)." % (
+                         bench["roofline"]["avg_launch_us"], float(r["AverageNs"]) / 1e3, r["Calls"]))
+    lines += ["", "| Kernel | Calls | Total ms | Avg us | % |", "|---|---:|---:|---:|---:|"]
+    for r in rows[:top]:
+        name = r["Name"].replace("void ", "").split("(")[0]
+        lines.append("| `%s` | %s | %.1f | %.2f | %.2f |" % (name, r["Calls"], float(r["TotalDurationNs"]) / 1e6,
+                                                          float(r["AverageNs"]) / 1e3, float(r["Percentage"])))
+    lines.append("")
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
+
+
+def pmc_summary(pdir, out_md, command_lines):
+    """Write the traffic summary of the dominant kernel from four counter
+    passes in `pdir` (fetch.csv, write.csv: the kernel's sweep points;
+    copy_fetch.csv, copy_write.csv: the copy calibration) and the bench line
+    of the kernel's points (bench.json)."""
+    with open(os.path.join(pdir, "bench.json")) as fh:
+        bench = json.loads(fh.read().strip().splitlines()[-1])
+    kernel = bench["roofline"]["kernel"]
+    cal_bytes = 64 << 20
+    # The copy's dispatches only (the buffers' fill kernels run in the same pass).
+    cf, cfn = counter_per_dispatch(os.path.join(pdir, "copy_fetch.csv"), "FETCH_SIZE", "copy")
+    cw, cwn = counter_per_dispatch(os.path.join(pdir, "copy_write.csv"), "WRITE_SIZE", "copy")
+    import numpy as np
+    f_cal = float(np.median(list(cf.values()))) * 1024.0
+    w_cal = float(np.median(list(cw.values()))) * 1024.0
+    f_scale, w_scale = cal_bytes / f_cal, cal_bytes / w_cal
+    kf, kfn = counter_per_dispatch(os.path.join(pdir, "fetch.csv"), "FETCH_SIZE", kernel.lower())
+    kw, kwn = counter_per_dispatch(os.path.join(pdir, "write.csv"), "WRITE_SIZE", kernel.lower())
+    fetch = float(np.mean(list(kf.values()))) * 1024.0 * f_scale
+    write = float(np.mean(list(kw.values()))) * 1024.0 * w_scale
+    alg = bench["roofline"]["algorithmic_bytes_per_launch"]
+    rec = {"kernel": kernel, "sources_sha1": bench["sources_sha1"], "sample_every": bench["config"]["sample_every"],
+           "dispatches": [len(kf), len(kw)], "timed_calls": bench["roofline"]["timed_calls"],
+           "fetch_scale": f_scale, "write_scale": w_scale,
+           "fetch_bytes_per_launch": fetch, "write_bytes_per_launch": write,
+           "traffic_bytes_per_launch": fetch + write, "algorithmic_bytes_per_launch": alg}
+    lines = ["# HBM traffic of %s over its sweep points" % kernel, "",
+             "Counter passes (rocprofv3 --pmc, one counter per run), each command run from the repository root:", "",
+             "```"] + command_lines + ["```", "",
+             "| | value |", "|---|---|",
+             "| copy calibration kernel | %s |" % ", ".join(sorted(cfn)),
+             "| copy of 64 MiB: FETCH_SIZE (median per dispatch) | %.1f MiB -> scale x%.3f |" % (f_cal / 2**20, f_scale),
+             "| copy of 64 MiB: WRITE_SIZE (median per dispatch) | %.1f MiB -> scale x%.3f |" % (w_cal / 2**20, w_scale),
+             "| kernel dispatches counted (fetch, write) | %d, %d |" % (len(kf), len(kw)),
+             "| sweep points of the kernel | %d |" % bench["roofline"]["points"],
+             "| algorithmic bytes per launch (X + K + Y once) | %.4g |" % alg,
+             "| fetched bytes per launch (scaled) | %.4g (%.3f of the algorithmic bytes) |" % (fetch, fetch / max(1.0, alg)),
+             "| written bytes per launch (scaled) | %.4g |" % write,
+             "| HBM traffic per launch | %.4g (%.3f x algorithmic) |" % (fetch + write, (fetch + write) / max(1.0, alg)),
+             "", TRAFFIC_TAG + json.dumps(rec), ""]
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
+
+
 class Runner:
-    def __init__(self, steps, warmup):
+    def __init__(self, steps, warmup, eager=False):
         import torch
         import paper_2405_15013_amd as ks
         if not os.path.exists(ks.library_path()):
@@ -101,6 +256,7 @@ class Runner:
         self.pool_y = torch.empty(POOL_BYTES, dtype=torch.uint8, device=self.dev)
         self.stream = torch.cuda.Stream(device=self.dev)
         self.filled = None
+        self.eager = eager
 
     def fill(self, dtype):
         """Fill the input pool with N(0,1) values of the storage dtype."""
@@ -131,6 +287,8 @@ class Runner:
         torch = self.torch
         nsets = max(MIN_SETS, math.ceil(ROTATE_BYTES / max(1, set_bytes)))
         nsets = min(nsets, nsets_pool)
+        if self.eager:
+            return self.time_eager(nsets, launch), nsets
         graphs = []
         with torch.cuda.stream(self.stream):
             launch(0, self.stream.cuda_stream)  # eager call: plan creation outside the capture
@@ -158,7 +316,27 @@ class Runner:
         del graphs
         return ms * 1e-3 / (self.steps * nsets), nsets
 
-    def point(self, pattern, batch, dtype, layout):
+    def time_eager(self, nsets, launch):
+        """The same rotation launched call by call (no graphs), for profiler
+        counter passes, which count per dispatch."""
+        torch = self.torch
+        with torch.cuda.stream(self.stream):
+            h = self.stream.cuda_stream
+            for _ in range(self.warmup):
+                for r in range(nsets):
+                    launch(r, h)
+            self.stream.synchronize()
+            e0 = torch.cuda.Event(enable_timing=True)
+            e1 = torch.cuda.Event(enable_timing=True)
+            e0.record(self.stream)
+            for _ in range(self.steps):
+                for r in range(nsets):
+                    launch(r, h)
+            e1.record(self.stream)
+            e1.synchronize()
+        return e0.elapsed_time(e1) * 1e-3 / (self.steps * nsets)
+
+    def point(self, pattern, batch, dtype, layout, only_kernel=None):
         torch = self.torch
         a, b, c, d = pattern
         s = ESIZE[dtype]
@@ -180,9 +358,11 @@ class Runner:
                 raise RuntimeError("ks_matmul failed: %s" % self.ks.ks_status_string(st))
 
         try:
-            self.ks.ks_plan_describe(a, b, c, d, batch, layout, dtype)
+            desc0 = self.ks.ks_plan_describe(a, b, c, d, batch, layout, dtype)
         except self.ks.KsError:
             return None  # the forced variant cannot run this point
+        if only_kernel is not None and plan_field(desc0, "kernel") != only_kernel:
+            return None
         t, nsets = self.time_calls(xb + yb, nsets_pool, launch)
         nbytes, flops, t_roof, bound = roof(pattern, batch, dtype)
         desc = self.ks.ks_plan_describe(a, b, c, d, batch, layout, dtype)
@@ -263,7 +443,24 @@ def main():
     ap.add_argument("--no-families", action="store_true")
     ap.add_argument("--variant", type=int, default=-1,
                     help="force a kernel variant for the sweep points (tuning; points it cannot run are skipped)")
+    ap.add_argument("--kernel", default=None,
+                    help="time only the sweep points whose plan runs this kernel instance (counter passes)")
+    ap.add_argument("--eager", action="store_true", help="launch call by call instead of through HIP graphs")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only run the plain 64 MiB copy used to scale the profiler's byte counters")
+    ap.add_argument("--pmc-summary", nargs=2, metavar=("DIR", "OUT_MD"),
+                    help="summarise counter passes in DIR into OUT_MD (no GPU)")
+    ap.add_argument("--trace-summary", nargs=3, metavar=("STATS_CSV", "BENCH_JSON", "OUT_MD"),
+                    help="summarise a rocprofv3 kernel_stats.csv of a bench run into OUT_MD (no GPU)")
+    ap.add_argument("--pmc-command", action="append", default=[],
+                    help="command line recorded in the --pmc-summary / --trace-summary output (repeatable)")
     args = ap.parse_args()
+    if args.pmc_summary:
+        pmc_summary(args.pmc_summary[0], args.pmc_summary[1], args.pmc_command)
+        return
+    if args.trace_summary:
+        trace_summary(*args.trace_summary, args.pmc_command)
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the KS matmul path shards over the batch with no "
               "communication, so there is no multi-GPU step to time (got --gpus %d)" % args.gpus, file=sys.stderr)
@@ -271,8 +468,11 @@ def main():
     import numpy as np
     import torch
     assert torch.cuda.is_available(), "bench.py needs a GPU"
+    if args.copy_calibration:
+        copy_calibration()
+        return
     t_start = time.time()
-    run = Runner(args.steps, args.warmup)
+    run = Runner(args.steps, args.warmup, eager=args.eager)
     os.makedirs(os.path.dirname(args.points_out) or ".", exist_ok=True)
     pats = sweep_patterns()
     grid = [(dtype, batch, layout, p) for dtype in ("f32", "bf16") for batch in (4096, 25088)
@@ -287,7 +487,7 @@ def main():
             if idx not in keep:
                 continue
             run.fill(dtype)
-            r = run.point(p, batch, dtype, layout)
+            r = run.point(p, batch, dtype, layout, only_kernel=args.kernel)
             if r is None:
                 skipped += 1
                 continue
@@ -298,7 +498,7 @@ def main():
                       file=sys.stderr, flush=True)
         run.ks.ks_force_variant(None)
         families = {}
-        if not args.no_families:
+        if not args.no_families and args.kernel is None:
             run.fill("f32")
             fam = []
             for layout in ("bsf", "bsl"):
@@ -365,6 +565,11 @@ def main():
     roofline["avg_launch_us"] = dom["t"] / dom["calls"] * 1e6
     roofline["algorithmic_bytes_per_launch"] = dom["bytes"] / dom["calls"]
     roofline["share_of_sweep_time"] = dom["t"] / sum(v["t"] for v in per_k.values())
+    sha = kernel_sources_sha1()
+    rec = traffic_record(dom_name, args.sample) if args.kernel is None and not args.eager else None
+    if rec is not None:
+        roofline["traffic"] = rec["traffic_bytes_per_launch"]
+        roofline["traffic_unit"] = "HBM bytes per launch (FETCH_SIZE + WRITE_SIZE, copy-calibrated)"
     ms_per_step = float(sum(r["us"] for r in points) * 1e-3)
     out = {
         "metric": METRIC,
@@ -383,6 +588,9 @@ def main():
                                "abd,acd<=8192 (700 patterns) x B{4096,25088} x {fp32,bf16} x {BSF,BSL}",
                    "points": len(points), "sample_every": args.sample, "parallelism": "single GPU"},
         "forced_variant": args.variant if args.variant >= 0 else None,
+        "only_kernel": args.kernel,
+        "eager": args.eager,
+        "sources_sha1": sha,
         "skipped_points": skipped,
         "median_gbps": float(np.median([r["gbps"] for r in points])),
         "median_tflops": float(np.median([r["tflops"] for r in points])),
@@ -395,7 +603,7 @@ def main():
         "roofline": roofline,
         "families": families,
     }
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and args.kernel is None:
         out["cpu_baseline"] = cpu_baseline()
     out["wall_s"] = time.time() - t_start
     print(json.dumps(out), flush=True)

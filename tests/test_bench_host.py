@@ -1,0 +1,93 @@
+"""Host-side pieces of bench.py: the roofline of a point, the profiler
+counter parsing and the traffic record lookup (no GPU)."""
+import json
+import os
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+
+def test_sweep_has_700_patterns():
+    pats = bench.sweep_patterns()
+    assert len(pats) == 700
+    assert all(a * b * d <= 8192 and a * c * d <= 8192 for a, b, c, d in pats)
+
+
+def test_roof_bytes_and_bound():
+    # fp32, (1, 64, 64, 1), batch 4096: X, Y 4096*64 each, K 64*64 (paper Section 4.3 traffic).
+    nbytes, flops, t, bound = bench.roof((1, 64, 64, 1), 4096, "f32")
+    assert nbytes == (4096 * 64 * 2 + 64 * 64) * 4
+    assert flops == 2.0 * 4096 * 64 * 64
+    assert bound == "hbm" and abs(t - nbytes / bench.HBM_BW) < 1e-15
+    # bf16 with large b*c stays HBM-bound on the MFMA peak.
+    assert bench.roof((1, 128, 128, 64), 25088, "bf16")[3] == "hbm"
+
+
+def _write_counter_csv(path, rows):
+    with open(path, "w") as fh:
+        fh.write('"Dispatch_Id","Kernel_Name","Counter_Name","Counter_Value"\n')
+        for did, name, ctr, val in rows:
+            fh.write('%d,"%s","%s",%s\n' % (did, name, ctr, val))
+
+
+def test_counter_per_dispatch_sums_instances_and_filters(tmp_path):
+    p = tmp_path / "c.csv"
+    _write_counter_csv(p, [
+        (1, "void ks::ks_staged_kernel<float, 0, 4, true, 2, 1>(ks::Problem, ks::StagedTile)", "FETCH_SIZE", 10),
+        (1, "void ks::ks_staged_kernel<float, 0, 4, true, 2, 1>(ks::Problem, ks::StagedTile)", "FETCH_SIZE", 5),
+        (2, "void ks::ks_staged_kernel<float, 0, 4, true, 1, 1>(ks::Problem, ks::StagedTile)", "FETCH_SIZE", 7),
+        (3, "__amd_rocclr_copyBuffer", "FETCH_SIZE", 3),
+    ])
+    per, names = bench.counter_per_dispatch(str(p), "FETCH_SIZE", "ks_staged_kernel<float,0,4,true,2,1>")
+    assert per == {"1": 15.0}
+    per, _ = bench.counter_per_dispatch(str(p), "FETCH_SIZE", "copy")
+    assert per == {"3": 3.0}
+    assert len(bench.counter_per_dispatch(str(p), "FETCH_SIZE")[0]) == 3
+
+
+def test_pmc_summary_scales_by_copy_calibration(tmp_path):
+    k = "ks_staged_kernel<float,0,4,true,2,1>"
+    kname = "void ks::ks_staged_kernel<float, 0, 4, true, 2, 1>(ks::Problem, ks::StagedTile)"
+    fill = "void at::native::vectorized_elementwise_kernel<16, FillFunctor>"
+    cal_kib = 64 * 1024  # 64 MiB
+    _write_counter_csv(tmp_path / "copy_fetch.csv", [(i, "__amd_rocclr_copyBuffer", "FETCH_SIZE", cal_kib / 2)
+                                                     for i in range(5)] + [(9 + i, fill, "FETCH_SIZE", 0)
+                                                                           for i in range(8)])
+    _write_counter_csv(tmp_path / "copy_write.csv", [(i, "__amd_rocclr_copyBuffer", "WRITE_SIZE", cal_kib)
+                                                     for i in range(5)])
+    # Two dispatches, 1000 and 3000 KiB fetched (counter) -> mean 2000 KiB x2 scale.
+    _write_counter_csv(tmp_path / "fetch.csv", [(1, kname, "FETCH_SIZE", 600), (1, kname, "FETCH_SIZE", 400),
+                                                (2, kname, "FETCH_SIZE", 3000)])
+    _write_counter_csv(tmp_path / "write.csv", [(1, kname, "WRITE_SIZE", 100), (2, kname, "WRITE_SIZE", 300)])
+    line = {"config": {"sample_every": 1}, "sources_sha1": "abc",
+            "roofline": {"kernel": k, "algorithmic_bytes_per_launch": 4.0e6, "timed_calls": 6, "points": 1}}
+    (tmp_path / "bench.json").write_text("[bench] progress\n" + json.dumps(line) + "\n")
+    out = tmp_path / "t.md"
+    bench.pmc_summary(str(tmp_path), str(out), ["cmd"])
+    rec = [json.loads(x[len(bench.TRAFFIC_TAG):]) for x in out.read_text().splitlines()
+           if x.startswith(bench.TRAFFIC_TAG)][0]
+    assert abs(rec["fetch_scale"] - 2.0) < 1e-12 and abs(rec["write_scale"] - 1.0) < 1e-12
+    assert rec["fetch_bytes_per_launch"] == 2000 * 1024 * 2.0
+    assert rec["write_bytes_per_launch"] == 200 * 1024
+    assert rec["dispatches"] == [2, 2]
+
+
+def test_traffic_record_needs_current_sources(tmp_path, monkeypatch):
+    k = "ks_x_kernel<float>"
+    pdir = tmp_path / "profiles"
+    pdir.mkdir()
+    rec = {"kernel": k, "sources_sha1": bench.kernel_sources_sha1(), "sample_every": 1,
+           "traffic_bytes_per_launch": 123.0}
+    (pdir / "a.md").write_text("# x\n" + bench.TRAFFIC_TAG + json.dumps(rec) + "\n")
+    stale = dict(rec, kernel="ks_y_kernel<float>", sources_sha1="0" * 40)
+    (pdir / "b.md").write_text(bench.TRAFFIC_TAG + json.dumps(stale) + "\n")
+    # The records are read from ROOT/profiles; the hash stays the real tree's.
+    sha = rec["sources_sha1"]
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    monkeypatch.setattr(bench, "kernel_sources_sha1", lambda: sha)
+    assert bench.traffic_record(k, 1)["traffic_bytes_per_launch"] == 123.0
+    assert bench.traffic_record(k, 2) is None
+    assert bench.traffic_record("ks_y_kernel<float>", 1) is None
