@@ -1,0 +1,305 @@
+// LDS-DMA MFMA kernels for batch-size-first KS patterns with d >= 4.
+//
+// Same output-stationary tiles and products as the LDS-staged kernels (paper
+// Section 4.1, Algorithm 2; tile and item mapping in ks_staged_index.h), with
+// the X stages moved from HBM to LDS by the memory unit itself
+// (global_load_lds_dwordx4: every lane's 16 bytes land at M0 + 16 * lane), so
+// the bytes in flight occupy no registers.  Three stage buffers per
+// workgroup: while stage s is multiplied, stages s+1 and s+2 are in flight.
+// The paper's weak batch-size-first case (Section 4.2) again becomes
+// contiguous row runs: each stage row is X[beta, i*c*d + ls*d .. (ls+LCH)*d).
+//
+// Synchronisation, per stage s:
+//   1. wait until at most UD vector-memory operations are outstanding (the
+//      DMAs of stage s+1), so this wavefront's DMAs of stage s and its K loads
+//      of stage s have completed;
+//   2. s_barrier: every wavefront's DMAs of stage s are in LDS, and every
+//      wavefront has finished reading stage s-1, whose buffer is refilled next;
+//   3. load K of stage s+1 (registers), then DMA stage s+2;
+//   4. read the operands of stage s from LDS and run the MFMAs.
+// The vector-memory issue order of step 3 (K loads, then DMAs) is pinned with
+// scheduling barriers, which is what makes the count of step 1 exact.  The
+// operand reads are issued as inline assembly with their own wait: the
+// compiler cannot tell which LDS bytes a DMA writes and would otherwise wait
+// for every DMA in flight before using any LDS value.
+//
+// Outputs leave through the structured epilogue of the staged kernel (LDS
+// copy of the output tile, coalesced 16-byte stores; Appendix D.3).
+#pragma once
+#include <type_traits>
+
+#include "ks_direct.h"
+#include "ks_staged_index.h"
+
+namespace ks {
+
+typedef __attribute__((address_space(3))) void lds_void_t;
+constexpr int kDmaMaxLds = 128 * 1024;
+
+// vmcnt(N) on gfx9: vmcnt in bits 3:0 and 15:14, expcnt (bits 6:4) and
+// lgkmcnt (bits 11:8) left at their maxima (no wait).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is six bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// Workgroup barrier without a memory fence (a fence would wait for every DMA
+// in flight); the empty asm statements keep the compiler from moving memory
+// accesses across it, the scheduling barriers keep the scheduler from doing so.
+__device__ __forceinline__ void dma_barrier() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// One LDS read of NB bytes at LDS byte address addr, outside the compiler's
+// tracking (the caller waits with lds_wait before using the value).
+template <int NB> struct LdsVec;
+template <> struct LdsVec<16> {
+  typedef u32x4 type;
+  __device__ static __forceinline__ type read(uint32_t addr) {
+    type v;
+    asm volatile("ds_read_b128 %0, %1" : "=v"(v) : "v"(addr));
+    return v;
+  }
+};
+template <> struct LdsVec<8> {
+  typedef u32x2 type;
+  __device__ static __forceinline__ type read(uint32_t addr) {
+    type v;
+    asm volatile("ds_read_b64 %0, %1" : "=v"(v) : "v"(addr));
+    return v;
+  }
+};
+
+// The K operands of one chunk (one stage): MT x V blocks of LP values of l.
+template <typename T, int MT, int LP>
+struct DmaK {
+  static constexpr int KW = LP * (int)sizeof(T) / 4;
+  uint32_t kw[MT][4][KW];
+  __device__ __forceinline__ void load(const T* __restrict__ kl, int64_t kmstride, int64_t kestride, int l) {
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) load_piece<KW * 4, false>(kl + mt * kmstride + e * kestride + l, kw[mt][e]);
+  }
+};
+
+template <typename T, bool STRIDED, int MT, int LP, int UD>
+__global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
+  constexpr int S = sizeof(T);
+  constexpr int V = 4;
+  constexpr int CH = 4 * LP;  // values of l per stage
+  constexpr int PE = STRIDED ? V : 16 / S;
+  constexpr int NP = LP * V / PE;
+  constexpr int PB = PE * S;
+  using Piece = LdsVec<PB>;
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 15, g = lane >> 4;
+  const STile st = staged_tile(p, t, blockIdx.x);
+  const SItem si = staged_item(p, t, st, V, MT, w);
+  DItem it;
+  it.i = st.i;
+  it.j0 = si.j0;
+  it.k0 = si.k0;
+  it.beta0 = si.beta0;
+  const T* __restrict__ kv = static_cast<const T*>(p.kv);
+  const int nst = p.c / CH;
+  const int stage = t.stage;
+  const uint32_t lds0 = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) char*)smem;
+
+  // DMA sources: instruction m of this wavefront fills physical units
+  // (m*W + w)*64 + lane; the lane loads the logical unit stored there (rows
+  // beyond the batch read the last row instead).
+  const T* __restrict__ xi = static_cast<const T*>(p.x) + (int64_t)st.i * p.c * p.d;
+  int soff[UD];
+#pragma unroll
+  for (int m = 0; m < UD; ++m) {
+    int r, v;
+    dma_unit_of(t, dma_phys_unit(t, m, w, lane), &r, &v);
+    int beta = st.bt * 16 * t.RS + r;
+    if (beta >= p.batch) beta = p.batch - 1;
+    soff[m] = beta * p.N + v * (16 / S);
+  }
+  const int64_t xstage = (int64_t)CH * p.d;  // X elements per stage along a row
+  auto dma = [&](int s) {
+    const T* xs = xi + s * xstage;
+    char* dst = smem + (s % 3) * stage + w * 1024;
+#pragma unroll
+    for (int m = 0; m < UD; ++m)
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(xs + soff[m]),
+                                       (lds_void_t*)(dst + m * t.W * 1024), 16, 0, 0);
+  };
+
+  // Operand pieces of this lane: LDS byte offsets within a stage buffer.
+  uint32_t ooff[NP];
+  {
+    const int r = 16 * si.rs + n;
+#pragma unroll
+    for (int q = 0; q < NP; ++q)
+      ooff[q] = lds0 + dma_lds_byte(t, r, dma_op_byte(p, si, LP, V, STRIDED, PE, S, 0, g, q));
+  }
+
+  const int64_t kmstride = (int64_t)16 * p.c, kestride = (int64_t)p.b * p.c;
+  const T* kl = kv + direct_k_base(p, it, LP, n, g);
+
+  f32x4 acc[MT][V];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int e = 0; e < V; ++e) acc[mt][e] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  // One stage.  MODE 2: K of stage s+1 and DMA of stage s+2 (steady state);
+  // MODE 1: K of stage s+1 only (stage nst-2); MODE 0: nothing (last stage).
+  // The modes are separate straight-line code so that the compiler's own
+  // wait before the MFMAs sees a fixed number of operations after each K load.
+  auto step = [&](auto mode, int s, DmaK<T, MT, LP>& kc, DmaK<T, MT, LP>& kn) {
+    constexpr int MODE = decltype(mode)::value;
+    // 1-2: stage s (and its K) complete in every wavefront; stage s-1 read.
+    // (The scheduling barrier keeps the wait from being hoisted into the
+    // previous stage's MFMAs.)
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (MODE == 0) wait_vmcnt<0>();
+    else wait_vmcnt<UD>();
+    dma_barrier();
+    // 3: K of stage s+1, then the DMAs of stage s+2 (this order is what the
+    // count of step 1 relies on).
+    if constexpr (MODE >= 1) kn.load(kl, kmstride, kestride, (s + 1) * CH);
+    __builtin_amdgcn_sched_barrier(0);
+    if constexpr (MODE == 2) dma(s + 2);
+    __builtin_amdgcn_sched_barrier(0);
+    // 4: operands from LDS, then the MFMAs.
+    const uint32_t base = (uint32_t)((s % 3) * stage);
+    typename Piece::type pc[NP];
+#pragma unroll
+    for (int q = 0; q < NP; ++q) pc[q] = Piece::read(ooff[q] + base);
+    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+    uint32_t xw[LP * V * S / 4];
+#pragma unroll
+    for (int q = 0; q < NP; ++q) {
+      asm volatile("" : "+v"(pc[q]));  // ordered after the wait above
+#pragma unroll
+      for (int u = 0; u < PB / 4; ++u) xw[q * (PB / 4) + u] = pc[q][u];
+    }
+    direct_mma<T, BSF, V, MT, LP>(xw, kc.kw, acc);
+  };
+  using M0 = std::integral_constant<int, 0>;
+  using M1 = std::integral_constant<int, 1>;
+  using M2 = std::integral_constant<int, 2>;
+
+  DmaK<T, MT, LP> ka, kb;
+  ka.load(kl, kmstride, kestride, 0);
+  __builtin_amdgcn_sched_barrier(0);
+  dma(0);
+  if (nst > 1) dma(1);
+  __builtin_amdgcn_sched_barrier(0);
+  int s = 0;
+  for (; s + 3 < nst; s += 2) {  // both steps are steady-state steps
+    step(M2(), s, ka, kb);
+    step(M2(), s + 1, kb, ka);
+  }
+  // The last 1-3 stages (s even, so ka holds K of stage s).
+  const int left = nst - s;
+  if (left == 3) {
+    step(M2(), s, ka, kb);
+    step(M1(), s + 1, kb, ka);
+    step(M0(), s + 2, ka, kb);
+  } else if (left == 2) {
+    step(M1(), s, ka, kb);
+    step(M0(), s + 1, kb, ka);
+  } else {
+    step(M0(), s, ka, kb);
+  }
+
+  // Structured epilogue: accumulators -> LDS output tile -> contiguous runs.
+  __syncthreads();  // every wavefront is done with the stage buffers
+  const int r = 16 * si.rs + n;
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int r4 = 0; r4 < 4; ++r4) {
+      const int k = it.k0 + 16 * mt + 4 * g + r4;
+      char* cell = smem + staged_y_lds(p, t, st, MT, S, r, k, it.j0);
+      if constexpr (S == 4) {
+        *reinterpret_cast<f32x4*>(cell) = f32x4{acc[mt][0][r4], acc[mt][1][r4], acc[mt][2][r4], acc[mt][3][r4]};
+      } else {
+        uint32_t wv[2];
+#pragma unroll
+        for (int e = 0; e < V; e += 2) {
+          const uint32_t lo = __builtin_bit_cast(uint16_t, from_f32<T>(acc[mt][e][r4]));
+          const uint32_t hi = __builtin_bit_cast(uint16_t, from_f32<T>(acc[mt][e + 1][r4]));
+          wv[e / 2] = lo | (hi << 16);
+        }
+        *reinterpret_cast<u32x2*>(cell) = u32x2{wv[0], wv[1]};
+      }
+    }
+  __syncthreads();
+  const int uy = staged_y_units_per_row(p, t, MT, S);
+  const int nunits = 16 * t.RS * uy;
+  T* __restrict__ y = static_cast<T*>(p.y);
+  for (int u = tid; u < nunits; u += 64 * t.W) {
+    const int row = u / uy, v = u % uy;
+    const int64_t off = staged_y_unit(p, t, st, MT, S, row, v);
+    if (off < 0) continue;
+    const u32x4 val = *reinterpret_cast<const u32x4*>(smem + row * t.ypitch + v * 16);
+    __builtin_nontemporal_store(val, reinterpret_cast<u32x4*>(y + off));
+  }
+}
+
+template <typename T, bool STRIDED, int MT, int LP, int UD>
+hipError_t launch_dma_inst(const Problem& p, const StagedTile& t, hipStream_t s) {
+  if (t.lds > 64 * 1024) {
+    static bool raised = false;  // opt in to more than 64 KB of dynamic LDS, once per instance
+    if (!raised) {
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ks_dma_kernel<T, STRIDED, MT, LP, UD>),
+                                         hipFuncAttributeMaxDynamicSharedMemorySize, kDmaMaxLds);
+      if (e != hipSuccess) return e;
+      raised = true;
+    }
+  }
+  hipLaunchKernelGGL((ks_dma_kernel<T, STRIDED, MT, LP, UD>), dim3(t.tiles), dim3(256), t.lds, s, p, t);
+  return hipGetLastError();
+}
+
+template <typename T, bool STRIDED, int LP, int UD>
+hipError_t launch_dma_mt(const Problem& p, const StagedTile& t, int mt, hipStream_t s) {
+  switch (mt) {
+    case 1: return launch_dma_inst<T, STRIDED, 1, LP, UD>(p, t, s);
+    case 2: return launch_dma_inst<T, STRIDED, 2, LP, UD>(p, t, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// Instances of one storage type: strided (d >= 8) or contiguous (d == 4)
+// operands, MT in {1, 2}, LP (4 for fp32; 8, or 4 when c % 32 == 16, for
+// 16-bit types), 2 or 4 DMA instructions per wavefront per stage.
+template <typename T>
+hipError_t launch_dma_type(const Problem& p, const StagedTile& t, bool strided, int mt, int lp, hipStream_t s) {
+  if (t.W != 4) return hipErrorInvalidValue;
+  if constexpr (sizeof(T) == 4) {
+    if (lp != 4) return hipErrorInvalidValue;
+  }
+#define KS_DMA_UD(STR, LPV)                                                         \
+  switch (t.UD) {                                                                   \
+    case 2: return launch_dma_mt<T, STR, LPV, 2>(p, t, mt, s);                      \
+    case 4: return launch_dma_mt<T, STR, LPV, 4>(p, t, mt, s);                      \
+    default: return hipErrorInvalidValue;                                           \
+  }
+  if (lp == 4) {
+    if (strided) { KS_DMA_UD(true, 4) } else { KS_DMA_UD(false, 4) }
+  }
+  if constexpr (sizeof(T) == 2) {
+    if (lp == 8) {
+      if (strided) { KS_DMA_UD(true, 8) } else { KS_DMA_UD(false, 8) }
+    }
+  }
+#undef KS_DMA_UD
+  return hipErrorInvalidValue;
+}
+
+}  // namespace ks

@@ -1,0 +1,11 @@
+// Instances of the LDS-DMA MFMA kernels (ks_dma.h) for bf16_t storage.
+// One file per storage type so the instances compile in parallel.
+#include "ks_dma.h"
+
+namespace ks {
+
+hipError_t launch_dma_bf16(const Problem& p, const StagedTile& t, bool strided, int mt, int lp, hipStream_t s) {
+  return launch_dma_type<bf16_t>(p, t, strided, mt, lp, s);
+}
+
+}  // namespace ks

@@ -107,6 +107,7 @@ bool plan_valu_bsf(const Problem& p, bool al16, Plan* pl) {
 bool plan_direct(const Problem& p, bool al16, Plan* pl);
 bool plan_staged(const Problem& p, bool al16, Plan* pl);
 bool plan_stream(const Problem& p, bool al16, Plan* pl);
+bool plan_dma(const Problem& p, bool al16, Plan* pl);
 namespace {
 
 bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
@@ -117,15 +118,18 @@ bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
     case V_DIRECT: return plan_direct(p, al16, pl);
     case V_STAGED: return plan_staged(p, al16, pl);
     case V_STREAM: return plan_stream(p, al16, pl);
+    case V_DMA: return plan_dma(p, al16, pl);
     default: return false;
   }
 }
 
 // Automatic choice: MFMA block GEMM when b and c make each (i, j) block a real
-// dense contraction (LDS-staged for batch-size-first with d >= 4, whose rows
-// interleave the blocks' inputs; register-direct otherwise); VALU kernels for
-// small blocks; the generic kernel for whatever is left.
+// dense contraction (batch-size-first with d >= 4, whose rows interleave the
+// blocks' inputs, through LDS: DMA-fed for d <= 16, register-staged beyond;
+// register-direct otherwise); VALU kernels for small blocks; the generic
+// kernel for whatever is left.
 bool plan_auto(const Problem& p, bool al16, Plan* pl) {
+  if (p.layout == BSF && p.d >= 4 && plan_dma(p, al16, pl)) return true;
   if (p.layout == BSF && p.d >= 4 && plan_staged(p, al16, pl)) return true;
   if (plan_direct(p, al16, pl)) return true;
   if (p.layout == BSL && plan_valu_bsl(p, al16, pl)) return true;
@@ -180,6 +184,7 @@ hipError_t launch(const Problem& p, const Plan& pl, hipStream_t s) {
     case V_DIRECT: return launch_direct(p, pl, s);
     case V_STAGED: return launch_staged(p, pl, s);
     case V_STREAM: return launch_stream(p, pl, s);
+    case V_DMA: return launch_dma(p, pl, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -258,6 +263,12 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
       snprintf(buf, sizeof buf, "ks_stream_kernel<%s,%d,%d,%s,%d>", t, p.layout, pl.vec, pl.unroll ? "true" : "false",
                pl.waves_m);
       break;
+    case V_DMA:
+      // DMA instructions per wavefront per stage: 16*rs rows of lch*d*esize
+      // bytes over four wavefronts of 64 16-byte lanes.
+      snprintf(buf, sizeof buf, "ks_dma_kernel<%s,%s,%d,%d,%d>", t, pl.unroll ? "true" : "false", pl.waves_m, pl.cps,
+               (int)(pl.rs * pl.lch * p.d * (p.dtype == F32 ? 4 : 2) / 256));
+      break;
     default: snprintf(buf, sizeof buf, "?");
   }
   std::string r(buf);
@@ -266,7 +277,7 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
 }
 
 std::string describe(const Problem& p, const Plan& pl) {
-  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "direct", "staged", "stream"};
+  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "direct", "staged", "stream", "dma"};
   char buf[320];
   snprintf(buf, sizeof buf,
            "variant=%d name=%s vec=%d bt=%d jg=%d unroll=%d waves_m=%d waves_n=%d lds=%d grid=%u block=%u xcd=%d "

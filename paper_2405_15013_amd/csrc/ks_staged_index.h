@@ -44,6 +44,9 @@ struct StagedTile {
   int remap;     // XCD-aware tile order (tiles % 8 == 0)
   int ypitch;    // BSF: LDS row pitch of the staged output tile, bytes
   int lds;       // LDS bytes per workgroup: max(2 * stage, BSF output tile)
+  // LDS-DMA kernel (ks_dma.h) only, 0 otherwise:
+  int UR;        // 16-byte units per stage row (LCH * d * esize / 16, a power of two)
+  int UD;        // DMA instructions (64 units each) per wavefront per stage
 };
 
 struct STile {
@@ -167,6 +170,34 @@ KS_HD int64_t staged_y_unit(const Problem& p, const StagedTile& t, const STile& 
   if (beta >= p.batch) return -1;
   const int kb = s.kt * t.KGW * 16 * MT;
   return (int64_t)beta * p.M + (int64_t)s.i * p.b * p.d + (int64_t)kb * p.d + (int64_t)v * (16 / esize);
+}
+
+// ---- LDS-DMA stages (ks_dma.h) ---------------------------------------------
+// Batch-size-first only.  A stage buffer holds 16*RS rows of UR 16-byte units
+// with no padding; logical unit v of row r sits at physical unit
+// v ^ (r & (min(UR, 16) - 1)) of that row (spreads the 16 rows an operand
+// read touches over distinct banks).  DMA instruction m of wavefront w writes
+// the 64 consecutive physical units (m*W + w)*64 + lane, so each lane loads
+// the logical unit that lands there.
+KS_HD int dma_swizzle(const StagedTile& t, int r) { return r & ((t.UR < 16 ? t.UR : 16) - 1); }
+// Physical unit P of a stage buffer -> row r and logical unit v.
+KS_HD void dma_unit_of(const StagedTile& t, int P, int* r, int* v) {
+  *r = P / t.UR;
+  *v = (P % t.UR) ^ dma_swizzle(t, *r);
+}
+// Physical unit written by lane `lane` of DMA instruction m of wavefront w.
+KS_HD int dma_phys_unit(const StagedTile& t, int m, int w, int lane) { return (m * t.W + w) * 64 + lane; }
+// LDS byte offset (within a stage buffer) of logical byte b of row r.
+KS_HD int dma_lds_byte(const StagedTile& t, int r, int b) {
+  return (r * t.UR + ((b >> 4) ^ dma_swizzle(t, r))) * 16 + (b & 15);
+}
+// Byte (within its stage row) of piece q of chunk l0 for lane (n, g), item it
+// (the operand layout of staged_op_base: strided pieces of V elements at
+// stride d, contiguous pieces of PE elements).
+KS_HD int dma_op_byte(const Problem& p, const SItem& it, int LP, int V, bool strided, int pe, int esize, int l0, int g,
+                      int q) {
+  if (strided) return ((l0 + LP * g + q) * p.d + it.j0) * esize;
+  return ((l0 + LP * g) * p.d + it.j0) * esize + q * pe * esize;
 }
 
 }  // namespace ks

@@ -20,6 +20,9 @@ hipError_t launch_staged_bf16(const Problem& p, const StagedTile& t, int V, bool
                               hipStream_t s);
 hipError_t launch_staged_f16(const Problem& p, const StagedTile& t, int V, bool strided, int mt, int cps,
                              hipStream_t s);
+hipError_t launch_dma_f32(const Problem& p, const StagedTile& t, bool strided, int mt, int lp, hipStream_t s);
+hipError_t launch_dma_bf16(const Problem& p, const StagedTile& t, bool strided, int mt, int lp, hipStream_t s);
+hipError_t launch_dma_f16(const Problem& p, const StagedTile& t, bool strided, int mt, int lp, hipStream_t s);
 
 namespace {
 constexpr int kUnitsPerWave = 256;  // 64 threads x kStagedUnitsPerThread (ks_staged.h)
@@ -53,7 +56,17 @@ StagedTile staged_tile_of(const Problem& p, const Plan& pl) {
   }
   t.remap = pl.xcd_remap;
   t.ypitch = 0;
+  t.UR = 0;
+  t.UD = 0;
   t.lds = 2 * t.stage;
+  if (pl.variant == V_DMA) {
+    // Unpadded, swizzled rows of UR units; three stage buffers.
+    t.UR = t.LCH * p.d * S / 16;
+    t.pitch = t.UR * 16;
+    t.stage = 16 * t.RS * t.pitch;
+    t.UD = t.stage / 16 / (64 * t.W);
+    t.lds = 3 * t.stage;
+  }
   if (p.layout == BSF) {
     t.ypitch = 16 * MT * t.KGW * p.d * S + 16;
     const int ytile = 16 * t.RS * t.ypitch;
@@ -150,6 +163,89 @@ bool plan_staged(const Problem& p, bool al16, Plan* pl) {
   if (t.lds > kMaxLds) return false;
   pl->lds_bytes = t.lds;
   return true;
+}
+
+// LDS-DMA kernel (ks_dma.h): batch-size-first, d in {4, 8, 16} (four
+// j values per lane: d / 4 j-groups), four wavefronts per tile, one MFMA chunk
+// per stage (16 values of l for fp32; 32, or 16 when c % 32 == 16, for 16-bit
+// types), a stage of 2 or 4 DMA instructions per wavefront, three stage
+// buffers.  Same preference order as the staged kernel.
+bool plan_dma(const Problem& p, bool al16, Plan* pl) {
+  if (!al16 || p.layout != BSF || p.b % 16 || p.c % 16) return false;
+  if (p.d != 4 && p.d != 8 && p.d != 16) return false;
+  const int S = p.dtype == F32 ? 4 : 2;
+  const int LP = (S == 4 || p.c % 32) ? 4 : 8, CH = 4 * LP;
+  const int V = 4, JG = p.d / V, W = 4;
+  const int UR = CH * p.d * S / 16;
+  const int KT = p.b / 16;
+  bool found = false;
+  int64_t best_tiles = 0;
+  int best_kgt = 0, best_mt = 0, best_kgw = 0, best_rs = 0;
+  for (int mt = 2; mt >= 1; --mt) {
+    if (KT % mt) continue;
+    const int kgroups = KT / mt;
+    for (int kgw = 1; kgw * JG <= W; ++kgw) {
+      if (kgroups % kgw || W % (kgw * JG)) continue;
+      const int rs = W / (kgw * JG);
+      const int64_t units = (int64_t)16 * rs * UR;
+      if (units % (64 * W)) continue;
+      const int64_t ud = units / (64 * W);
+      if (ud != 2 && ud != 4) continue;
+      const int64_t stage = units * 16;
+      const int64_t ytile = 16 * rs * ((int64_t)16 * mt * kgw * p.d * S + 16);
+      const int64_t lds = 3 * stage > ytile ? 3 * stage : ytile;
+      if (lds > kMaxLds) continue;
+      const int kgt = kgroups / kgw;
+      const int64_t tiles = (int64_t)((p.batch + 16 * rs - 1) / (16 * rs)) * p.a * kgt;
+      if (tiles > 0x7fffffff) continue;
+      const int64_t tcap = tiles < 1024 ? tiles : 1024;
+      const int64_t bcap = best_tiles < 1024 ? best_tiles : 1024;
+      bool better = !found;
+      if (!better) {
+        if (tcap != bcap) better = tcap > bcap;
+        else if (kgt != best_kgt) better = kgt < best_kgt;
+        else better = mt > best_mt;
+      }
+      if (better) {
+        found = true;
+        best_tiles = tiles;
+        best_kgt = kgt;
+        best_mt = mt;
+        best_kgw = kgw;
+        best_rs = rs;
+      }
+    }
+  }
+  if (!found) return false;
+  pl->variant = V_DMA;
+  pl->vec = V;
+  pl->unroll = p.d > V ? 1 : 0;
+  pl->waves_m = best_mt;
+  pl->waves_n = best_kgt;
+  pl->jg = JG;
+  pl->rs = best_rs;
+  pl->kgw = best_kgw;
+  pl->lch = CH;
+  pl->cps = LP;  // MFMA lane depth (4 or 8 values of l per lane group)
+  pl->bt = 16 * best_rs;
+  pl->block = 64u * W;
+  pl->grid = (unsigned)best_tiles;
+  pl->xcd_remap = (best_kgt > 1 && best_tiles % 8 == 0) ? 1 : 0;
+  const StagedTile t = staged_tile_of(p, *pl);
+  if (t.lds > kMaxLds || t.UD * 64 * W * 16 != t.stage) return false;
+  pl->lds_bytes = t.lds;
+  return true;
+}
+
+hipError_t launch_dma(const Problem& p, const Plan& pl, hipStream_t s) {
+  const StagedTile t = staged_tile_of(p, pl);
+  const bool strided = pl.unroll != 0;
+  switch (p.dtype) {
+    case F32: return launch_dma_f32(p, t, strided, pl.waves_m, pl.cps, s);
+    case BF16: return launch_dma_bf16(p, t, strided, pl.waves_m, pl.cps, s);
+    case F16: return launch_dma_f16(p, t, strided, pl.waves_m, pl.cps, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_staged(const Problem& p, const Plan& pl, hipStream_t s) {

@@ -209,6 +209,45 @@ bool verify_stream(Checker& ck, const Plan& pl) {
   return ck.err.empty();
 }
 
+// Structured epilogue of the batch-size-first staged and DMA kernels: every
+// cell of the LDS output tile is written once by the lane holding that output,
+// then stored by its 16-byte unit.
+bool verify_bsf_epilogue(Checker& ck, const StagedTile& t, const STile& st, int V, int MT, int S) {
+  const Problem& p = ck.p;
+  const int kr = staged_y_kr(t, MT), rows = 16 * t.RS;
+  std::vector<int64_t> ytile((size_t)rows * t.ypitch / S, -1);
+  for (int w = 0; w < t.W; ++w) {
+    const SItem si = staged_item(p, t, st, V, MT, w);
+    for (int lane = 0; lane < 64; ++lane) {
+      const int n = lane & 15, g = lane >> 4, r = 16 * si.rs + n;
+      for (int mt = 0; mt < MT; ++mt)
+        for (int r4 = 0; r4 < 4; ++r4)
+          for (int e = 0; e < V; ++e) {
+            const int k = si.k0 + 16 * mt + 4 * g + r4, j = si.j0 + e;
+            const int o = staged_y_lds(p, t, st, MT, S, r, k, j);
+            if (e == 0 && o % (V * S)) return ck.fail("output tile write not aligned to its size", o);
+            if (o < 0 || o + S > rows * t.ypitch) return ck.fail("output tile write out of range", o);
+            int64_t& cell = ytile[(size_t)(o / S)];
+            if (cell != -1) return ck.fail("output tile cell written twice", o);
+            cell = (int64_t)(st.bt * 16 * t.RS + r) * p.M + (int64_t)st.i * p.b * p.d + (int64_t)k * p.d + j;
+          }
+    }
+  }
+  const int uy = staged_y_units_per_row(p, t, MT, S);
+  if (uy * 16 != kr * p.d * S) return ck.fail("output row is not a whole number of units", kr);
+  for (int r = 0; r < rows; ++r)
+    for (int v = 0; v < uy; ++v) {
+      const int64_t off = staged_y_unit(p, t, st, MT, S, r, v);
+      if (off < 0) continue;
+      if ((off * S) % 16) return ck.fail("Y unit not 16-byte aligned", off);
+      for (int e = 0; e < 16 / S; ++e)
+        if (ytile[(size_t)((r * t.ypitch + v * 16) / S + e)] != off + e)
+          return ck.fail("Y unit does not hold the outputs it is stored to", off + e);
+      ck.write_y(off, 16 / S);
+    }
+  return true;
+}
+
 bool verify_staged(Checker& ck, const Plan& pl) {
   const Problem& p = ck.p;
   const StagedTile t = staged_tile_of(p, pl);
@@ -311,41 +350,95 @@ bool verify_staged(Checker& ck, const Plan& pl) {
               ck.write_y(off, ype);
             }
       }
-    } else {
-      // Structured epilogue: every cell of the LDS output tile is written once
-      // by the lane holding that output, then stored by its 16-byte unit.
-      const int kr = staged_y_kr(t, MT), rows = 16 * t.RS;
-      std::vector<int64_t> ytile((size_t)rows * t.ypitch / S, -1);
+    } else if (!verify_bsf_epilogue(ck, t, st, V, MT, S)) {
+      return false;
+    }
+  }
+  return ck.err.empty();
+}
+
+// LDS-DMA kernel (ks_dma.h): every lane of every DMA instruction of a stage
+// fills one 16-byte unit of the stage buffer (all units exactly once) from an
+// in-bounds, 16-byte aligned X address; every operand piece a lane reads from
+// the swizzled stage holds the X values its products need; K, the output
+// tile and the Y stores as in the staged kernel.
+bool verify_dma(Checker& ck, const Plan& pl) {
+  const Problem& p = ck.p;
+  const StagedTile t = staged_tile_of(p, pl);
+  const int V = pl.vec, MT = pl.waves_m, S = p.dtype == F32 ? 4 : 2, LP = pl.cps, CH = 4 * LP, UE = 16 / S;
+  const bool strided = pl.unroll != 0;
+  if (p.layout != BSF || V != 4 || p.d % V || strided != (p.d > V)) return ck.fail("bad j-vector", V);
+  if (LP != 4 && !(S == 2 && LP == 8)) return ck.fail("bad MFMA lane depth", LP);
+  if (t.W != 4 || t.RS * t.JG * t.KGW != t.W || t.JG != p.d / V) return ck.fail("waves do not split the tile", t.W);
+  if (t.kgt * t.KGW * 16 * MT != p.b) return ck.fail("k-groups do not cover b", p.b);
+  if (t.LCH != CH || p.c % CH) return ck.fail("stages do not cover c", t.LCH);
+  if (t.UR * 16 != CH * p.d * S || (t.UR & (t.UR - 1))) return ck.fail("stage row is not a power-of-two of units", t.UR);
+  if (t.stage != 16 * t.RS * t.UR * 16 || t.UD * 64 * t.W * 16 != t.stage || (t.UD != 2 && t.UD != 4))
+    return ck.fail("stage is not a whole number of DMA instructions per wavefront", t.stage);
+  if ((int)pl.grid != t.tiles || (int)pl.block != 64 * t.W) return ck.fail("grid does not match the tiles", pl.grid);
+  if (pl.lds_bytes != t.lds || t.lds < 3 * t.stage) return ck.fail("LDS allocation does not hold three stages", t.lds);
+  if (t.lds < 16 * t.RS * t.ypitch) return ck.fail("LDS allocation does not hold the output tile", t.lds);
+  if (t.remap && t.tiles % 8) return ck.fail("XCD remap needs a multiple of 8 tiles", t.tiles);
+  const int pe = strided ? V : UE, np = LP * V / pe, pb = pe * S;
+  std::vector<uint8_t> seen(t.tiles, 0);
+  std::vector<int64_t> shadow((size_t)t.stage / S);
+  const int nst = p.c / CH;
+  for (int blk = 0; blk < t.tiles && ck.err.empty(); ++blk) {
+    const STile st = staged_tile(p, t, blk);
+    const int logical = t.remap ? staged_remap(blk, t.tiles) : blk;
+    if (logical < 0 || logical >= t.tiles || seen[logical]++) return ck.fail("tile visited twice", logical);
+    for (int s = 0; s < nst; ++s) {
+      std::fill(shadow.begin(), shadow.end(), (int64_t)-1);
+      for (int w = 0; w < t.W; ++w)
+        for (int m = 0; m < t.UD; ++m)
+          for (int lane = 0; lane < 64; ++lane) {
+            const int P = dma_phys_unit(t, m, w, lane);
+            if (P < 0 || (P + 1) * 16 > t.stage) return ck.fail("DMA writes outside the stage buffer", P);
+            int r, v;
+            dma_unit_of(t, P, &r, &v);
+            if (r < 0 || r >= 16 * t.RS || v < 0 || v >= t.UR) return ck.fail("DMA unit outside the stage rows", P);
+            int beta = st.bt * 16 * t.RS + r;
+            if (beta >= p.batch) beta = p.batch - 1;
+            // the kernel's form: row base i*c*d, stage offset s*CH*d, lane offset beta*N + v*UE
+            const int64_t off = (int64_t)st.i * p.c * p.d + (int64_t)s * CH * p.d + ((int64_t)beta * p.N + v * UE);
+            if ((off * S) % 16) return ck.fail("DMA source not 16-byte aligned", off);
+            if ((int64_t)beta * p.N + v * UE > 0x7fffffff) return ck.fail("DMA lane offset exceeds 32 bits", beta);
+            ck.read_x(off, UE);
+            for (int e = 0; e < UE; ++e) {
+              int64_t& cell = shadow[(size_t)(P * 16 / S + e)];
+              if (cell != -1) return ck.fail("LDS cell written twice in a stage", P);
+              cell = off + e;
+            }
+          }
       for (int w = 0; w < t.W; ++w) {
         const SItem si = staged_item(p, t, st, V, MT, w);
+        DItem it;
+        it.i = st.i; it.j0 = si.j0; it.k0 = si.k0; it.beta0 = si.beta0;
         for (int lane = 0; lane < 64; ++lane) {
           const int n = lane & 15, g = lane >> 4, r = 16 * si.rs + n;
+          const bool valid = direct_lane_valid(p, it, V, n);
+          for (int q = 0; q < np; ++q) {
+            const int b = dma_op_byte(p, si, LP, V, strided, pe, S, 0, g, q);
+            if ((b & 15) + pb > 16 || b % pb) return ck.fail("operand piece crosses a 16-byte unit", b);
+            const int o = dma_lds_byte(t, r, b);
+            if (o < 0 || o + pb > t.stage || o % pb) return ck.fail("operand read outside the stage or unaligned", o);
+            for (int e = 0; e < pe; ++e) {
+              const int64_t have = shadow[(size_t)(o / S + e)];
+              if (have < 0) return ck.fail("operand read of an LDS cell not written in this stage", o);
+              if (valid && have != expected_x(p, it, V, LP, s * CH, n, g, q * pe + e))
+                return ck.fail("operand element is not the X value the product needs", have);
+            }
+          }
           for (int mt = 0; mt < MT; ++mt)
-            for (int r4 = 0; r4 < 4; ++r4)
-              for (int e = 0; e < V; ++e) {
-                const int k = si.k0 + 16 * mt + 4 * g + r4, j = si.j0 + e;
-                const int o = staged_y_lds(p, t, st, MT, S, r, k, j);
-                if (e == 0 && o % (V * S)) return ck.fail("output tile write not aligned to its size", o);
-                if (o < 0 || o + S > rows * t.ypitch) return ck.fail("output tile write out of range", o);
-                int64_t& cell = ytile[(size_t)(o / S)];
-                if (cell != -1) return ck.fail("output tile cell written twice", o);
-                cell = (int64_t)(st.bt * 16 * t.RS + r) * p.M + (int64_t)st.i * p.b * p.d + (int64_t)k * p.d + j;
-              }
+            for (int e = 0; e < V; ++e) {
+              const int64_t off = direct_k_off(p, it, LP, s * CH, n, g, mt, e);
+              if ((off * S) % (LP * S)) return ck.fail("K operand not aligned to its size", off);
+              ck.read_k(off, LP);
+            }
         }
       }
-      const int uy = staged_y_units_per_row(p, t, MT, S);
-      if (uy * 16 != kr * p.d * S) return ck.fail("output row is not a whole number of units", kr);
-      for (int r = 0; r < rows; ++r)
-        for (int v = 0; v < uy; ++v) {
-          const int64_t off = staged_y_unit(p, t, st, MT, S, r, v);
-          if (off < 0) continue;
-          if ((off * S) % 16) return ck.fail("Y unit not 16-byte aligned", off);
-          for (int e = 0; e < 16 / S; ++e)
-            if (ytile[(size_t)((r * t.ypitch + v * 16) / S + e)] != off + e)
-              return ck.fail("Y unit does not hold the outputs it is stored to", off + e);
-          ck.write_y(off, 16 / S);
-        }
     }
+    if (!verify_bsf_epilogue(ck, t, st, V, MT, S)) return false;
   }
   return ck.err.empty();
 }
@@ -374,6 +467,7 @@ extern "C" ks_status_t ks_plan_verify(int64_t a, int64_t b, int64_t c, int64_t d
     case V_DIRECT: ok = verify_direct(ck, pl); break;
     case V_STAGED: ok = verify_staged(ck, pl); break;
     case V_STREAM: ok = verify_stream(ck, pl); break;
+    case V_DMA: ok = verify_dma(ck, pl); break;
     default: ck.fail("unknown variant", pl.variant);
   }
   if (ok) ok = ck.coverage();

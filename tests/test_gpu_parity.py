@@ -12,7 +12,7 @@ from parity_util import TOL, case, from_device, nan_tensor, oracle_y, rel_err, t
 
 pytestmark = pytest.mark.gpu
 
-VARIANTS = {"generic": 0, "valu_bsl": 1, "valu_bsf": 2, "direct": 3, "staged": 4, "stream": 5}
+VARIANTS = {"generic": 0, "valu_bsl": 1, "valu_bsf": 2, "direct": 3, "staged": 4, "stream": 5, "dma": 6}
 
 
 def run_gpu(pattern, x_logical, kv, batch, dtype, layout, variant=None, x_offset=0, y_offset=0):
@@ -256,6 +256,29 @@ def test_staged_forced(pattern, dtype, layout, batch):
     check(pattern, batch, dtype, layout, cfg=12, variant=VARIANTS["staged"], kdist="normal")
 
 
+DMA_SHAPES = ([s for s in MFMA_SHAPES if s[3] in (4, 8, 16)]
+              + [(2, 128, 128, 16), (4, 48, 96, 4), (1, 32, 48, 16), (1, 16, 32, 8), (3, 64, 80, 4), (2, 96, 16, 16)])
+
+
+@pytest.mark.parametrize("pattern", DMA_SHAPES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("batch", [256, 72, 1000])
+def test_dma_forced(pattern, dtype, batch):
+    """The LDS-DMA kernel (batch-size-first, d in {4, 8, 16}): strided and
+    contiguous j-vectors, one to eight stages of l (the 1-, 2- and 3-stage
+    tails of its pipeline), the 16-bit c % 32 == 16 lane depth, ragged
+    batches."""
+    check(pattern, batch, dtype, "bsf", cfg=14, variant=VARIANTS["dma"], kdist="normal")
+
+
+@pytest.mark.parametrize("pattern", [(6, 64, 16, 8), (2, 128, 128, 16), (8, 16, 128, 4)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_dma_full_batch(pattern, dtype):
+    """The LDS-DMA kernel at the full batch of 25088 rows (thousands of tiles,
+    XCD remap)."""
+    check(pattern, 25088, dtype, "bsf", cfg=15, variant=VARIANTS["dma"], kdist="normal")
+
+
 @pytest.mark.parametrize("pattern", [(1, 32, 32, 32), (6, 64, 16, 8), (4, 96, 48, 2)])
 @pytest.mark.parametrize("layout", ["bsf", "bsl"])
 def test_mfma_generic_agree(pattern, layout):
@@ -268,3 +291,6 @@ def test_mfma_generic_agree(pattern, layout):
     if layout == "bsl" or pattern[3] <= 16:  # BSF staging takes d <= 16 (at most 4 j-groups per tile)
         y_s = run_gpu(pattern, x, kv, 512, "f32", layout, variant=VARIANTS["staged"])
         assert rel_err(y_s, y_g) <= 1e-5
+    if layout == "bsf" and pattern[3] in (4, 8, 16):
+        y_m = run_gpu(pattern, x, kv, 512, "f32", layout, variant=VARIANTS["dma"])
+        assert rel_err(y_m, y_g) <= 1e-5

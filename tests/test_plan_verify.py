@@ -76,6 +76,27 @@ def test_all_sweep_plans_staged(dtype, layout, batch, every):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("batch,every", [(72, 1), (1000, 3), (25088, 29)])
+def test_all_sweep_plans_dma(dtype, batch, every):
+    """The LDS-DMA kernel (forced) on every batch-size-first sweep pattern it
+    accepts (d >= 4): every DMA lane fills one unit of the stage from an
+    in-bounds address, every swizzled operand read holds the right X value,
+    every output written once.  It must accept every d >= 4 pattern."""
+    bad = []
+    ks.ks_force_variant(6)
+    try:
+        for pattern in [p for p in sweep_patterns() if p[3] >= 4][::every]:
+            st, rep = ks.ks_plan_verify(*pattern, batch, "bsf", dtype)
+            if st != 0:
+                bad.append((pattern, rep))
+            else:
+                assert "name=dma" in ks.ks_plan_describe(*pattern, batch, "bsf", dtype)
+    finally:
+        ks.ks_force_variant(None)
+    assert not bad, bad[:5]
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 @pytest.mark.parametrize("layout", ["bsf", "bsl"])
 @pytest.mark.parametrize("batch,every", [(72, 1), (25088, 17)])
 def test_all_sweep_plans_stream(dtype, layout, batch, every):
@@ -94,17 +115,17 @@ def test_all_sweep_plans_stream(dtype, layout, batch, every):
 
 
 def test_sweep_plans_use_mfma_kernels():
-    """The whole sweep runs on the MFMA kernels (aligned buffers): LDS-staged
-    for batch-size-first with d >= 4, register-direct otherwise."""
+    """The whole sweep runs on the MFMA kernels (aligned buffers): LDS-DMA for
+    batch-size-first with d >= 4, register-direct otherwise."""
     for pattern in sweep_patterns()[::7]:
         for layout in ("bsf", "bsl"):
             for dtype in ("f32", "bf16", "f16"):
                 desc = ks.ks_plan_describe(*pattern, 4096, layout, dtype)
-                want = "name=staged" if (layout == "bsf" and pattern[3] >= 4) else "name=direct"
+                want = "name=dma" if (layout == "bsf" and pattern[3] >= 4) else "name=direct"
                 assert want in desc, (pattern, layout, dtype, desc)
 
 
-@pytest.mark.parametrize("variant", [0, 1, 2, 3, 4, 5])
+@pytest.mark.parametrize("variant", [0, 1, 2, 3, 4, 5, 6])
 def test_forced_variants(variant):
     """Every variant that accepts a shape produces a valid launch for it."""
     ks.ks_force_variant(variant)
