@@ -88,7 +88,7 @@ struct DmaK {
   }
 };
 
-template <typename T, bool STRIDED, int MT, int LP, int UD>
+template <typename T, bool STRIDED, int MT, int LP, int UD, int NT>
 __global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
   constexpr int S = sizeof(T);
   constexpr int V = 4;
@@ -122,7 +122,7 @@ __global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
   for (int m = 0; m < UD; ++m) {
     int r, v;
     dma_unit_of(t, dma_phys_unit(t, m, w, lane), &r, &v);
-    int beta = st.bt * 16 * t.RS + r;
+    int beta = st.bt * 16 * t.RS * NT + r;
     if (beta >= p.batch) beta = p.batch - 1;
     soff[m] = beta * p.N + v * (16 / S);
   }
@@ -136,10 +136,13 @@ __global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
                                        (lds_void_t*)(dst + m * t.W * 1024), 16, 0, 0);
   };
 
-  // Operand pieces of this lane: LDS byte offsets within a stage buffer.
+  // Operand pieces of this lane: LDS byte offsets within a stage buffer (row
+  // group 0 of the wavefront; group u is 16*u rows further, and the swizzle
+  // depends on the row modulo 16 only).
   uint32_t ooff[NP];
+  const uint32_t ugroup = 16 * t.UR * 16;  // bytes of 16 stage rows
   {
-    const int r = 16 * si.rs + n;
+    const int r = 16 * NT * si.rs + n;
 #pragma unroll
     for (int q = 0; q < NP; ++q)
       ooff[q] = lds0 + dma_lds_byte(t, r, dma_op_byte(p, si, LP, V, STRIDED, PE, S, 0, g, q));
@@ -148,11 +151,13 @@ __global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
   const int64_t kmstride = (int64_t)16 * p.c, kestride = (int64_t)p.b * p.c;
   const T* kl = kv + direct_k_base(p, it, LP, n, g);
 
-  f32x4 acc[MT][V];
+  f32x4 acc[NT][MT][V];
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
+  for (int u = 0; u < NT; ++u)
 #pragma unroll
-    for (int e = 0; e < V; ++e) acc[mt][e] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int e = 0; e < V; ++e) acc[u][mt][e] = f32x4{0.f, 0.f, 0.f, 0.f};
 
   // One stage.  MODE 2: K of stage s+1 and DMA of stage s+2 (steady state);
   // MODE 1: K of stage s+1 only (stage nst-2); MODE 0: nothing (last stage).
@@ -173,20 +178,24 @@ __global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
     __builtin_amdgcn_sched_barrier(0);
     if constexpr (MODE == 2) dma(s + 2);
     __builtin_amdgcn_sched_barrier(0);
-    // 4: operands from LDS, then the MFMAs.
+    // 4: per row group, operands from LDS, then the MFMAs (the K operands
+    // serve all NT groups).
     const uint32_t base = (uint32_t)((s % 3) * stage);
-    typename Piece::type pc[NP];
 #pragma unroll
-    for (int q = 0; q < NP; ++q) pc[q] = Piece::read(ooff[q] + base);
-    asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-    uint32_t xw[LP * V * S / 4];
+    for (int u = 0; u < NT; ++u) {
+      typename Piece::type pc[NP];
 #pragma unroll
-    for (int q = 0; q < NP; ++q) {
-      asm volatile("" : "+v"(pc[q]));  // ordered after the wait above
+      for (int q = 0; q < NP; ++q) pc[q] = Piece::read(ooff[q] + base + u * ugroup);
+      asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+      uint32_t xw[LP * V * S / 4];
 #pragma unroll
-      for (int u = 0; u < PB / 4; ++u) xw[q * (PB / 4) + u] = pc[q][u];
+      for (int q = 0; q < NP; ++q) {
+        asm volatile("" : "+v"(pc[q]));  // ordered after the wait above
+#pragma unroll
+        for (int w2 = 0; w2 < PB / 4; ++w2) xw[q * (PB / 4) + w2] = pc[q][w2];
+      }
+      direct_mma<T, BSF, V, MT, LP>(xw, kc.kw, acc[u]);
     }
-    direct_mma<T, BSF, V, MT, LP>(xw, kc.kw, acc);
   };
   using M0 = std::integral_constant<int, 0>;
   using M1 = std::integral_constant<int, 1>;
@@ -218,29 +227,33 @@ __global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
 
   // Structured epilogue: accumulators -> LDS output tile -> contiguous runs.
   __syncthreads();  // every wavefront is done with the stage buffers
-  const int r = 16 * si.rs + n;
 #pragma unroll
-  for (int mt = 0; mt < MT; ++mt)
+  for (int u = 0; u < NT; ++u) {
+    const int r = 16 * (NT * si.rs + u) + n;
 #pragma unroll
-    for (int r4 = 0; r4 < 4; ++r4) {
-      const int k = it.k0 + 16 * mt + 4 * g + r4;
-      char* cell = smem + staged_y_lds(p, t, st, MT, S, r, k, it.j0);
-      if constexpr (S == 4) {
-        *reinterpret_cast<f32x4*>(cell) = f32x4{acc[mt][0][r4], acc[mt][1][r4], acc[mt][2][r4], acc[mt][3][r4]};
-      } else {
-        uint32_t wv[2];
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-        for (int e = 0; e < V; e += 2) {
-          const uint32_t lo = __builtin_bit_cast(uint16_t, from_f32<T>(acc[mt][e][r4]));
-          const uint32_t hi = __builtin_bit_cast(uint16_t, from_f32<T>(acc[mt][e + 1][r4]));
-          wv[e / 2] = lo | (hi << 16);
+      for (int r4 = 0; r4 < 4; ++r4) {
+        const int k = it.k0 + 16 * mt + 4 * g + r4;
+        char* cell = smem + staged_y_lds(p, t, st, MT, S, r, k, it.j0);
+        if constexpr (S == 4) {
+          *reinterpret_cast<f32x4*>(cell) =
+              f32x4{acc[u][mt][0][r4], acc[u][mt][1][r4], acc[u][mt][2][r4], acc[u][mt][3][r4]};
+        } else {
+          uint32_t wv[2];
+#pragma unroll
+          for (int e = 0; e < V; e += 2) {
+            const uint32_t lo = __builtin_bit_cast(uint16_t, from_f32<T>(acc[u][mt][e][r4]));
+            const uint32_t hi = __builtin_bit_cast(uint16_t, from_f32<T>(acc[u][mt][e + 1][r4]));
+            wv[e / 2] = lo | (hi << 16);
+          }
+          *reinterpret_cast<u32x2*>(cell) = u32x2{wv[0], wv[1]};
         }
-        *reinterpret_cast<u32x2*>(cell) = u32x2{wv[0], wv[1]};
       }
-    }
+  }
   __syncthreads();
   const int uy = staged_y_units_per_row(p, t, MT, S);
-  const int nunits = 16 * t.RS * uy;
+  const int nunits = 16 * t.RS * NT * uy;
   T* __restrict__ y = static_cast<T*>(p.y);
   for (int u = tid; u < nunits; u += 64 * t.W) {
     const int row = u / uy, v = u % uy;
@@ -251,33 +264,37 @@ __global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
   }
 }
 
-template <typename T, bool STRIDED, int MT, int LP, int UD>
+template <typename T, bool STRIDED, int MT, int LP, int UD, int NT>
 hipError_t launch_dma_inst(const Problem& p, const StagedTile& t, hipStream_t s) {
   if (t.lds > 64 * 1024) {
     static bool raised = false;  // opt in to more than 64 KB of dynamic LDS, once per instance
     if (!raised) {
-      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ks_dma_kernel<T, STRIDED, MT, LP, UD>),
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ks_dma_kernel<T, STRIDED, MT, LP, UD, NT>),
                                          hipFuncAttributeMaxDynamicSharedMemorySize, kDmaMaxLds);
       if (e != hipSuccess) return e;
       raised = true;
     }
   }
-  hipLaunchKernelGGL((ks_dma_kernel<T, STRIDED, MT, LP, UD>), dim3(t.tiles), dim3(256), t.lds, s, p, t);
+  hipLaunchKernelGGL((ks_dma_kernel<T, STRIDED, MT, LP, UD, NT>), dim3(t.tiles), dim3(256), t.lds, s, p, t);
   return hipGetLastError();
 }
 
+// (MT, NT) pairs instantiated: MT * NT <= 4.
 template <typename T, bool STRIDED, int LP, int UD>
 hipError_t launch_dma_mt(const Problem& p, const StagedTile& t, int mt, hipStream_t s) {
-  switch (mt) {
-    case 1: return launch_dma_inst<T, STRIDED, 1, LP, UD>(p, t, s);
-    case 2: return launch_dma_inst<T, STRIDED, 2, LP, UD>(p, t, s);
-    default: return hipErrorInvalidValue;
-  }
+  const int nt = t.NT;
+  if (mt == 1 && nt == 1) return launch_dma_inst<T, STRIDED, 1, LP, UD, 1>(p, t, s);
+  if (mt == 2 && nt == 1) return launch_dma_inst<T, STRIDED, 2, LP, UD, 1>(p, t, s);
+  if (mt == 1 && nt == 2) return launch_dma_inst<T, STRIDED, 1, LP, UD, 2>(p, t, s);
+  if (mt == 2 && nt == 2) return launch_dma_inst<T, STRIDED, 2, LP, UD, 2>(p, t, s);
+  if (mt == 1 && nt == 4) return launch_dma_inst<T, STRIDED, 1, LP, UD, 4>(p, t, s);
+  return hipErrorInvalidValue;
 }
 
 // Instances of one storage type: strided (d >= 8) or contiguous (d == 4)
-// operands, MT in {1, 2}, LP (4 for fp32; 8, or 4 when c % 32 == 16, for
-// 16-bit types), 2 or 4 DMA instructions per wavefront per stage.
+// operands, (MT, NT) with MT * NT <= 4, LP (4 for fp32; 8, or 4 when
+// c % 32 == 16, for 16-bit types), 2, 4 or 8 DMA instructions per wavefront
+// per stage.
 template <typename T>
 hipError_t launch_dma_type(const Problem& p, const StagedTile& t, bool strided, int mt, int lp, hipStream_t s) {
   if (t.W != 4) return hipErrorInvalidValue;
@@ -288,6 +305,7 @@ hipError_t launch_dma_type(const Problem& p, const StagedTile& t, bool strided, 
   switch (t.UD) {                                                                   \
     case 2: return launch_dma_mt<T, STR, LPV, 2>(p, t, mt, s);                      \
     case 4: return launch_dma_mt<T, STR, LPV, 4>(p, t, mt, s);                      \
+    case 8: return launch_dma_mt<T, STR, LPV, 8>(p, t, mt, s);                      \
     default: return hipErrorInvalidValue;                                           \
   }
   if (lp == 4) {

@@ -266,8 +266,8 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
     case V_DMA:
       // DMA instructions per wavefront per stage: 16*rs rows of lch*d*esize
       // bytes over four wavefronts of 64 16-byte lanes.
-      snprintf(buf, sizeof buf, "ks_dma_kernel<%s,%s,%d,%d,%d>", t, pl.unroll ? "true" : "false", pl.waves_m, pl.cps,
-               (int)(pl.rs * pl.lch * p.d * (p.dtype == F32 ? 4 : 2) / 256));
+      snprintf(buf, sizeof buf, "ks_dma_kernel<%s,%s,%d,%d,%d,%d>", t, pl.unroll ? "true" : "false", pl.waves_m,
+               pl.cps, (int)(pl.rs * pl.nt * pl.lch * p.d * (p.dtype == F32 ? 4 : 2) / 256), pl.nt);
       break;
     default: snprintf(buf, sizeof buf, "?");
   }
@@ -281,10 +281,10 @@ std::string describe(const Problem& p, const Plan& pl) {
   char buf[320];
   snprintf(buf, sizeof buf,
            "variant=%d name=%s vec=%d bt=%d jg=%d unroll=%d waves_m=%d waves_n=%d lds=%d grid=%u block=%u xcd=%d "
-           "rs=%d kgw=%d lch=%d kernel=%s",
+           "rs=%d kgw=%d lch=%d nt=%d kernel=%s",
            pl.variant, (pl.variant >= 0 && pl.variant < V_COUNT) ? names[pl.variant] : "?", pl.vec, pl.bt, pl.jg,
            pl.unroll, pl.waves_m, pl.waves_n, pl.lds_bytes, pl.grid, pl.block, pl.xcd_remap, pl.rs, pl.kgw, pl.lch,
-           kernel_name(p, pl).c_str());
+           pl.nt, kernel_name(p, pl).c_str());
   return buf;
 }
 

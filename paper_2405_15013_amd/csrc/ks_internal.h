@@ -53,7 +53,8 @@ struct Plan {
   int rs = 1;       // row (BSF) / column (BSL) groups per tile
   int kgw = 1;      // k-groups per tile
   int lch = 0;      // values of l per stage
-  int cps = 1;      // MFMA chunks per stage
+  int cps = 1;      // MFMA chunks per stage (LDS-DMA: MFMA lane depth LP)
+  int nt = 1;       // LDS-DMA: 16-row groups per wavefront (each K operand serves 16*nt batch rows)
 };
 
 // Each launcher enqueues one kernel and returns the hipError_t of the launch.

@@ -19,7 +19,10 @@
 //
 // Wavefront w of the tile takes rs = w % RS, jg = (w / RS) % JG and
 // kgw = w / (RS * JG) (W = RS * JG * KGW <= 8), i.e. the work item
-// (rows or columns group rs, j-group jg, k-group kt*KGW + kgw).
+// (rows or columns group rs, j-group jg, k-group kt*KGW + kgw).  In the
+// batch-size-first DMA kernel a wavefront's rows group is NT consecutive
+// groups of 16 rows (tile rows 16*RS*NT), so each K operand it loads serves
+// 16*NT rows.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <cstdint>
@@ -47,6 +50,7 @@ struct StagedTile {
   // LDS-DMA kernel (ks_dma.h) only, 0 otherwise:
   int UR;        // 16-byte units per stage row (LCH * d * esize / 16, a power of two)
   int UD;        // DMA instructions (64 units each) per wavefront per stage
+  int NT;        // batch-size-first: 16-row groups per wavefront (1 except in the DMA kernel)
 };
 
 struct STile {
@@ -80,12 +84,14 @@ KS_HD STile staged_tile(const Problem& p, const StagedTile& t, int block) {
 
 // Number of batch entries a tile spans.
 KS_HD int staged_span(const Problem& p, const StagedTile& t, int V) {
-  return p.layout == BSL ? 16 * V * t.RS : 16 * t.RS;
+  return p.layout == BSL ? 16 * V * t.RS : 16 * t.RS * t.NT;
 }
 
 // ---- stage loads ----------------------------------------------------------
 // Stage rows and 16-byte units per row for a stage of nl values of l.
-KS_HD int staged_rows(const Problem& p, const StagedTile& t, int nl) { return p.layout == BSL ? nl : 16 * t.RS; }
+KS_HD int staged_rows(const Problem& p, const StagedTile& t, int nl) {
+  return p.layout == BSL ? nl : 16 * t.RS * t.NT;
+}
 KS_HD int staged_units_per_row(const Problem& p, const StagedTile& t, int V, int esize, int nl) {
   return p.layout == BSL ? (16 * V * t.RS * esize) / 16 : (nl * p.d * esize) / 16;
 }
@@ -101,7 +107,7 @@ KS_HD int64_t staged_x_unit(const Problem& p, const StagedTile& t, const STile& 
     const int64_t row = (int64_t)s.i * c * d + (int64_t)(ls + r) * d + s.j;
     return row * p.batch + beta;
   }
-  int beta = s.bt * 16 * t.RS + r;
+  int beta = s.bt * 16 * t.RS * t.NT + r;
   if (beta >= p.batch) beta = p.batch - 1;
   return (int64_t)beta * p.N + (int64_t)s.i * c * d + (int64_t)ls * d + (int64_t)v * ue;
 }
@@ -125,7 +131,7 @@ KS_HD SItem staged_item(const Problem& p, const StagedTile& t, const STile& s, i
     it.beta0 = s.bt * 16 * V * t.RS + it.rs * 16 * V;
   } else {
     it.j0 = it.jg * V;
-    it.beta0 = s.bt * 16 * t.RS + it.rs * 16;
+    it.beta0 = (s.bt * t.RS + it.rs) * 16 * t.NT;
   }
   return it;
 }
@@ -166,7 +172,7 @@ KS_HD int staged_y_units_per_row(const Problem& p, const StagedTile& t, int MT, 
   return staged_y_kr(t, MT) * p.d * esize / 16;
 }
 KS_HD int64_t staged_y_unit(const Problem& p, const StagedTile& t, const STile& s, int MT, int esize, int r, int v) {
-  const int beta = s.bt * 16 * t.RS + r;
+  const int beta = s.bt * 16 * t.RS * t.NT + r;
   if (beta >= p.batch) return -1;
   const int kb = s.kt * t.KGW * 16 * MT;
   return (int64_t)beta * p.M + (int64_t)s.i * p.b * p.d + (int64_t)kb * p.d + (int64_t)v * (16 / esize);

@@ -43,7 +43,8 @@ StagedTile staged_tile_of(const Problem& p, const Plan& pl) {
   t.JG = p.layout == BSL ? 1 : p.d / V;
   t.KGW = pl.kgw;
   t.kgt = p.b / (16 * MT * t.KGW);
-  const int span = p.layout == BSL ? 16 * V * t.RS : 16 * t.RS;
+  t.NT = (pl.variant == V_DMA) ? pl.nt : 1;
+  const int span = p.layout == BSL ? 16 * V * t.RS : 16 * t.RS * t.NT;
   t.nbt = (p.batch + span - 1) / span;
   t.tiles = t.nbt * p.a * (p.layout == BSL ? p.d : 1) * t.kgt;
   t.LCH = pl.lch;
@@ -63,13 +64,13 @@ StagedTile staged_tile_of(const Problem& p, const Plan& pl) {
     // Unpadded, swizzled rows of UR units; three stage buffers.
     t.UR = t.LCH * p.d * S / 16;
     t.pitch = t.UR * 16;
-    t.stage = 16 * t.RS * t.pitch;
+    t.stage = 16 * t.RS * t.NT * t.pitch;
     t.UD = t.stage / 16 / (64 * t.W);
     t.lds = 3 * t.stage;
   }
   if (p.layout == BSF) {
     t.ypitch = 16 * MT * t.KGW * p.d * S + 16;
-    const int ytile = 16 * t.RS * t.ypitch;
+    const int ytile = 16 * t.RS * t.NT * t.ypitch;
     if (ytile > t.lds) t.lds = ytile;
   }
   return t;
@@ -168,51 +169,63 @@ bool plan_staged(const Problem& p, bool al16, Plan* pl) {
 // LDS-DMA kernel (ks_dma.h): batch-size-first, d in {4, 8, 16} (four
 // j values per lane: d / 4 j-groups), four wavefronts per tile, one MFMA chunk
 // per stage (16 values of l for fp32; 32, or 16 when c % 32 == 16, for 16-bit
-// types), a stage of 2 or 4 DMA instructions per wavefront, three stage
-// buffers.  Same preference order as the staged kernel.
+// types), a stage of 2, 4 or 8 DMA instructions per wavefront, three stage
+// buffers, NT groups of 16 rows per wavefront (MT * NT <= 4).
+struct DmaChoice {
+  int lp, mt, nt, kgw, rs, kgt;
+  int64_t tiles, lds;
+};
+// Preference: at most 64 KB of LDS (two workgroups per CU), then enough tiles
+// for the chip (1024), then the most batch rows per K operand (NT: K is read
+// from L2 once per 16*NT rows), then the fewest re-reads of X (k-group
+// tiles), then the largest MT, then the deeper MFMA (LP).
+constexpr int64_t kDmaLdsPref = 64 * 1024;
+bool dma_better(const DmaChoice& c, const DmaChoice& b) {
+  if ((c.lds <= kDmaLdsPref) != (b.lds <= kDmaLdsPref)) return c.lds <= kDmaLdsPref;
+  const int64_t tc = c.tiles < 1024 ? c.tiles : 1024, tb = b.tiles < 1024 ? b.tiles : 1024;
+  if (tc != tb) return tc > tb;
+  if (c.nt != b.nt) return c.nt > b.nt;
+  if (c.kgt != b.kgt) return c.kgt < b.kgt;
+  if (c.mt != b.mt) return c.mt > b.mt;
+  return c.lp > b.lp;
+}
 bool plan_dma(const Problem& p, bool al16, Plan* pl) {
   if (!al16 || p.layout != BSF || p.b % 16 || p.c % 16) return false;
   if (p.d != 4 && p.d != 8 && p.d != 16) return false;
   const int S = p.dtype == F32 ? 4 : 2;
-  const int LP = (S == 4 || p.c % 32) ? 4 : 8, CH = 4 * LP;
   const int V = 4, JG = p.d / V, W = 4;
-  const int UR = CH * p.d * S / 16;
   const int KT = p.b / 16;
   bool found = false;
-  int64_t best_tiles = 0;
-  int best_kgt = 0, best_mt = 0, best_kgw = 0, best_rs = 0;
-  for (int mt = 2; mt >= 1; --mt) {
-    if (KT % mt) continue;
-    const int kgroups = KT / mt;
-    for (int kgw = 1; kgw * JG <= W; ++kgw) {
-      if (kgroups % kgw || W % (kgw * JG)) continue;
-      const int rs = W / (kgw * JG);
-      const int64_t units = (int64_t)16 * rs * UR;
-      if (units % (64 * W)) continue;
-      const int64_t ud = units / (64 * W);
-      if (ud != 2 && ud != 4) continue;
-      const int64_t stage = units * 16;
-      const int64_t ytile = 16 * rs * ((int64_t)16 * mt * kgw * p.d * S + 16);
-      const int64_t lds = 3 * stage > ytile ? 3 * stage : ytile;
-      if (lds > kMaxLds) continue;
-      const int kgt = kgroups / kgw;
-      const int64_t tiles = (int64_t)((p.batch + 16 * rs - 1) / (16 * rs)) * p.a * kgt;
-      if (tiles > 0x7fffffff) continue;
-      const int64_t tcap = tiles < 1024 ? tiles : 1024;
-      const int64_t bcap = best_tiles < 1024 ? best_tiles : 1024;
-      bool better = !found;
-      if (!better) {
-        if (tcap != bcap) better = tcap > bcap;
-        else if (kgt != best_kgt) better = kgt < best_kgt;
-        else better = mt > best_mt;
-      }
-      if (better) {
-        found = true;
-        best_tiles = tiles;
-        best_kgt = kgt;
-        best_mt = mt;
-        best_kgw = kgw;
-        best_rs = rs;
+  DmaChoice best{};
+  // 16-bit types: 16x16x32 MFMAs (LP = 8, stages of 32 values of l) when
+  // c % 32 == 0, or 16x16x16 (LP = 4, stages of 16: half the stage size).
+  for (int LP = (S == 2 && p.c % 32 == 0) ? 8 : 4; LP >= 4; LP /= 2) {
+    const int CH = 4 * LP, UR = CH * p.d * S / 16;
+    for (int mt = 2; mt >= 1; --mt) {
+      if (KT % mt) continue;
+      const int kgroups = KT / mt;
+      for (int nt = 1; nt * mt <= 4; nt *= 2) {
+        for (int kgw = 1; kgw * JG <= W; ++kgw) {
+          if (kgroups % kgw || W % (kgw * JG)) continue;
+          const int rs = W / (kgw * JG);
+          const int64_t units = (int64_t)16 * rs * nt * UR;
+          if (units % (64 * W)) continue;
+          const int64_t ud = units / (64 * W);
+          if (ud != 2 && ud != 4 && ud != 8) continue;
+          const int64_t stage = units * 16;
+          const int64_t ytile = 16 * rs * nt * ((int64_t)16 * mt * kgw * p.d * S + 16);
+          const int64_t lds = 3 * stage > ytile ? 3 * stage : ytile;
+          if (lds > kMaxLds) continue;
+          const int kgt = kgroups / kgw;
+          const int span = 16 * rs * nt;
+          const int64_t tiles = (int64_t)((p.batch + span - 1) / span) * p.a * kgt;
+          if (tiles > 0x7fffffff) continue;
+          const DmaChoice c{LP, mt, nt, kgw, rs, kgt, tiles, lds};
+          if (!found || dma_better(c, best)) {
+            found = true;
+            best = c;
+          }
+        }
       }
     }
   }
@@ -220,17 +233,18 @@ bool plan_dma(const Problem& p, bool al16, Plan* pl) {
   pl->variant = V_DMA;
   pl->vec = V;
   pl->unroll = p.d > V ? 1 : 0;
-  pl->waves_m = best_mt;
-  pl->waves_n = best_kgt;
+  pl->waves_m = best.mt;
+  pl->waves_n = best.kgt;
   pl->jg = JG;
-  pl->rs = best_rs;
-  pl->kgw = best_kgw;
-  pl->lch = CH;
-  pl->cps = LP;  // MFMA lane depth (4 or 8 values of l per lane group)
-  pl->bt = 16 * best_rs;
+  pl->rs = best.rs;
+  pl->kgw = best.kgw;
+  pl->nt = best.nt;
+  pl->lch = 4 * best.lp;
+  pl->cps = best.lp;  // MFMA lane depth (4 or 8 values of l per lane group)
+  pl->bt = 16 * best.rs * best.nt;
   pl->block = 64u * W;
-  pl->grid = (unsigned)best_tiles;
-  pl->xcd_remap = (best_kgt > 1 && best_tiles % 8 == 0) ? 1 : 0;
+  pl->grid = (unsigned)best.tiles;
+  pl->xcd_remap = (best.kgt > 1 && best.tiles % 8 == 0) ? 1 : 0;
   const StagedTile t = staged_tile_of(p, *pl);
   if (t.lds > kMaxLds || t.UD * 64 * W * 16 != t.stage) return false;
   pl->lds_bytes = t.lds;

@@ -214,12 +214,15 @@ bool verify_stream(Checker& ck, const Plan& pl) {
 // then stored by its 16-byte unit.
 bool verify_bsf_epilogue(Checker& ck, const StagedTile& t, const STile& st, int V, int MT, int S) {
   const Problem& p = ck.p;
-  const int kr = staged_y_kr(t, MT), rows = 16 * t.RS;
+  const int kr = staged_y_kr(t, MT), rows = 16 * t.RS * t.NT;
   std::vector<int64_t> ytile((size_t)rows * t.ypitch / S, -1);
   for (int w = 0; w < t.W; ++w) {
     const SItem si = staged_item(p, t, st, V, MT, w);
-    for (int lane = 0; lane < 64; ++lane) {
-      const int n = lane & 15, g = lane >> 4, r = 16 * si.rs + n;
+    for (int lu = 0; lu < 64 * t.NT; ++lu) {
+      const int lane = lu & 63, u = lu >> 6;
+      const int n = lane & 15, g = lane >> 4, r = 16 * (t.NT * si.rs + u) + n;
+      if (si.beta0 + 16 * u != st.bt * 16 * t.RS * t.NT + 16 * (t.NT * si.rs + u))
+        return ck.fail("row group base does not match the tile", si.beta0);
       for (int mt = 0; mt < MT; ++mt)
         for (int r4 = 0; r4 < 4; ++r4)
           for (int e = 0; e < V; ++e) {
@@ -229,7 +232,7 @@ bool verify_bsf_epilogue(Checker& ck, const StagedTile& t, const STile& st, int 
             if (o < 0 || o + S > rows * t.ypitch) return ck.fail("output tile write out of range", o);
             int64_t& cell = ytile[(size_t)(o / S)];
             if (cell != -1) return ck.fail("output tile cell written twice", o);
-            cell = (int64_t)(st.bt * 16 * t.RS + r) * p.M + (int64_t)st.i * p.b * p.d + (int64_t)k * p.d + j;
+            cell = (int64_t)(st.bt * 16 * t.RS * t.NT + r) * p.M + (int64_t)st.i * p.b * p.d + (int64_t)k * p.d + j;
           }
     }
   }
@@ -373,11 +376,13 @@ bool verify_dma(Checker& ck, const Plan& pl) {
   if (t.kgt * t.KGW * 16 * MT != p.b) return ck.fail("k-groups do not cover b", p.b);
   if (t.LCH != CH || p.c % CH) return ck.fail("stages do not cover c", t.LCH);
   if (t.UR * 16 != CH * p.d * S || (t.UR & (t.UR - 1))) return ck.fail("stage row is not a power-of-two of units", t.UR);
-  if (t.stage != 16 * t.RS * t.UR * 16 || t.UD * 64 * t.W * 16 != t.stage || (t.UD != 2 && t.UD != 4))
+  if (t.NT != pl.nt || (t.NT != 1 && t.NT != 2 && t.NT != 4) || MT * t.NT > 4) return ck.fail("bad row groups per wavefront", t.NT);
+  if (t.stage != 16 * t.RS * t.NT * t.UR * 16 || t.UD * 64 * t.W * 16 != t.stage ||
+      (t.UD != 2 && t.UD != 4 && t.UD != 8))
     return ck.fail("stage is not a whole number of DMA instructions per wavefront", t.stage);
   if ((int)pl.grid != t.tiles || (int)pl.block != 64 * t.W) return ck.fail("grid does not match the tiles", pl.grid);
   if (pl.lds_bytes != t.lds || t.lds < 3 * t.stage) return ck.fail("LDS allocation does not hold three stages", t.lds);
-  if (t.lds < 16 * t.RS * t.ypitch) return ck.fail("LDS allocation does not hold the output tile", t.lds);
+  if (t.lds < 16 * t.RS * t.NT * t.ypitch) return ck.fail("LDS allocation does not hold the output tile", t.lds);
   if (t.remap && t.tiles % 8) return ck.fail("XCD remap needs a multiple of 8 tiles", t.tiles);
   const int pe = strided ? V : UE, np = LP * V / pe, pb = pe * S;
   std::vector<uint8_t> seen(t.tiles, 0);
@@ -396,8 +401,8 @@ bool verify_dma(Checker& ck, const Plan& pl) {
             if (P < 0 || (P + 1) * 16 > t.stage) return ck.fail("DMA writes outside the stage buffer", P);
             int r, v;
             dma_unit_of(t, P, &r, &v);
-            if (r < 0 || r >= 16 * t.RS || v < 0 || v >= t.UR) return ck.fail("DMA unit outside the stage rows", P);
-            int beta = st.bt * 16 * t.RS + r;
+            if (r < 0 || r >= 16 * t.RS * t.NT || v < 0 || v >= t.UR) return ck.fail("DMA unit outside the stage rows", P);
+            int beta = st.bt * 16 * t.RS * t.NT + r;
             if (beta >= p.batch) beta = p.batch - 1;
             // the kernel's form: row base i*c*d, stage offset s*CH*d, lane offset beta*N + v*UE
             const int64_t off = (int64_t)st.i * p.c * p.d + (int64_t)s * CH * p.d + ((int64_t)beta * p.N + v * UE);
@@ -414,21 +419,28 @@ bool verify_dma(Checker& ck, const Plan& pl) {
         const SItem si = staged_item(p, t, st, V, MT, w);
         DItem it;
         it.i = st.i; it.j0 = si.j0; it.k0 = si.k0; it.beta0 = si.beta0;
-        for (int lane = 0; lane < 64; ++lane) {
-          const int n = lane & 15, g = lane >> 4, r = 16 * si.rs + n;
-          const bool valid = direct_lane_valid(p, it, V, n);
+        for (int lu = 0; lu < 64 * t.NT; ++lu) {
+          // lane of row group u: the kernel reads group 0's offset + u * (16 rows)
+          const int lane = lu & 63, u = lu >> 6;
+          const int n = lane & 15, g = lane >> 4, r = 16 * (t.NT * si.rs + u) + n;
+          DItem itu = it;
+          itu.beta0 = it.beta0 + 16 * u;
+          const bool valid = direct_lane_valid(p, itu, V, n);
           for (int q = 0; q < np; ++q) {
             const int b = dma_op_byte(p, si, LP, V, strided, pe, S, 0, g, q);
             if ((b & 15) + pb > 16 || b % pb) return ck.fail("operand piece crosses a 16-byte unit", b);
             const int o = dma_lds_byte(t, r, b);
+            if (o != dma_lds_byte(t, 16 * t.NT * si.rs + n, b) + u * 16 * t.UR * 16)
+              return ck.fail("row group operand offset is not group 0's plus 16 rows", o);
             if (o < 0 || o + pb > t.stage || o % pb) return ck.fail("operand read outside the stage or unaligned", o);
             for (int e = 0; e < pe; ++e) {
               const int64_t have = shadow[(size_t)(o / S + e)];
               if (have < 0) return ck.fail("operand read of an LDS cell not written in this stage", o);
-              if (valid && have != expected_x(p, it, V, LP, s * CH, n, g, q * pe + e))
+              if (valid && have != expected_x(p, itu, V, LP, s * CH, n, g, q * pe + e))
                 return ck.fail("operand element is not the X value the product needs", have);
             }
           }
+          if (u > 0) continue;
           for (int mt = 0; mt < MT; ++mt)
             for (int e = 0; e < V; ++e) {
               const int64_t off = direct_k_off(p, it, LP, s * CH, n, g, mt, e);

@@ -9,6 +9,7 @@ import oracle
 import paper_2405_15013_amd as ks
 from paper_2405_15013_amd import inputs
 from parity_util import TOL, case, from_device, nan_tensor, oracle_y, rel_err, to_device
+from shapes import DMA_ROW_GROUP_SHAPES, DMA_SHAPES, MFMA_SHAPES
 
 pytestmark = pytest.mark.gpu
 
@@ -220,9 +221,6 @@ def test_sweep_ragged_batch_full(pattern, dtype, layout):
     check(pattern, batch, dtype, layout, cfg=8, kdist="normal")
 
 
-MFMA_SHAPES = [(1, 32, 32, 32), (32, 32, 32, 1), (6, 64, 16, 8), (6, 16, 64, 8), (2, 48, 80, 2), (1, 128, 16, 16),
-               (8, 16, 128, 4), (3, 96, 48, 1), (1, 16, 112, 8), (2, 64, 128, 2)]
-
 
 @pytest.mark.parametrize("pattern", MFMA_SHAPES)
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
@@ -256,8 +254,6 @@ def test_staged_forced(pattern, dtype, layout, batch):
     check(pattern, batch, dtype, layout, cfg=12, variant=VARIANTS["staged"], kdist="normal")
 
 
-DMA_SHAPES = ([s for s in MFMA_SHAPES if s[3] in (4, 8, 16)]
-              + [(2, 128, 128, 16), (4, 48, 96, 4), (1, 32, 48, 16), (1, 16, 32, 8), (3, 64, 80, 4), (2, 96, 16, 16)])
 
 
 @pytest.mark.parametrize("pattern", DMA_SHAPES)
@@ -269,6 +265,15 @@ def test_dma_forced(pattern, dtype, batch):
     tails of its pipeline), the 16-bit c % 32 == 16 lane depth, ragged
     batches."""
     check(pattern, batch, dtype, "bsf", cfg=14, variant=VARIANTS["dma"], kdist="normal")
+
+
+@pytest.mark.parametrize("pattern", DMA_ROW_GROUP_SHAPES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("batch", [4096, 4000])
+def test_dma_row_groups(pattern, dtype, batch):
+    """The LDS-DMA kernel with several 16-row groups per wavefront (each K
+    operand reused for 32 or 64 batch rows), full and ragged last tiles."""
+    check(pattern, batch, dtype, "bsf", cfg=16, variant=VARIANTS["dma"], kdist="normal")
 
 
 @pytest.mark.parametrize("pattern", [(6, 64, 16, 8), (2, 128, 128, 16), (8, 16, 128, 4)])

@@ -6,6 +6,7 @@ Runs on the CPU; nothing is enqueued."""
 import pytest
 
 import paper_2405_15013_amd as ks
+from shapes import DMA_ROW_GROUP_SHAPES, DMA_SHAPES
 
 
 def sweep_patterns():
@@ -138,3 +139,22 @@ def test_forced_variants(variant):
                 assert rep == "no plan", rep
     finally:
         ks.ks_force_variant(None)
+
+
+def test_dma_row_group_plans_covered():
+    """The GPU parity shapes of the DMA kernel reach every (MT, NT, stage
+    length, strided) plan its planner makes on sweep-like patterns at batch
+    4096, and each of those plans passes the replay."""
+    def key(p, dt):
+        f = dict(kv.split("=", 1) for kv in ks.ks_plan_describe(*p, 4096, "bsf", dt).split())
+        return (dt, f["waves_m"], f["nt"], f["lch"], f["unroll"])
+    have = {key(p, dt) for p in DMA_ROW_GROUP_SHAPES + DMA_SHAPES for dt in ("f32", "bf16")}
+    want = {key(p, dt) for p in [(a, b, c, d) for a in (1, 2, 4, 8) for b in (16, 32, 64, 128) for c in (16, 32, 64)
+                                  for d in (4, 8, 16) if a * b * d <= 8192 and a * c * d <= 8192]
+            for dt in ("f32", "bf16")}
+    assert want <= have, sorted(want - have)
+    for p in DMA_ROW_GROUP_SHAPES:
+        for dt in ("f32", "bf16"):
+            for batch in (4096, 4000):
+                st, rep = ks.ks_plan_verify(*p, batch, "bsf", dt)
+                assert st == 0, (p, dt, batch, rep)
