@@ -76,24 +76,25 @@ template <> struct LdsVec<8> {
 };
 
 // The K operands of one chunk (one stage): MT x V blocks of LP values of l.
-template <typename T, int MT, int LP>
+template <typename T, int V, int MT, int LP>
 struct DmaK {
   static constexpr int KW = LP * (int)sizeof(T) / 4;
-  uint32_t kw[MT][4][KW];
+  uint32_t kw[MT][V][KW];
   __device__ __forceinline__ void load(const T* __restrict__ kl, int64_t kmstride, int64_t kestride, int l) {
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int e = 0; e < 4; ++e) load_piece<KW * 4, false>(kl + mt * kmstride + e * kestride + l, kw[mt][e]);
+      for (int e = 0; e < V; ++e) load_piece<KW * 4, false>(kl + mt * kmstride + e * kestride + l, kw[mt][e]);
   }
 };
 
-template <typename T, bool STRIDED, int MT, int LP, int UD, int NT>
+// V j values per lane (V = min(d, 4)): STRIDED when d > V (pieces of V
+// elements at stride d), otherwise the lane's LP x V block is contiguous.
+template <typename T, int V, bool STRIDED, int MT, int LP, int UD, int NT>
 __global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
   constexpr int S = sizeof(T);
-  constexpr int V = 4;
   constexpr int CH = 4 * LP;  // values of l per stage
-  constexpr int PE = STRIDED ? V : 16 / S;
+  constexpr int PE = STRIDED ? V : (LP * V * S < 16 ? LP * V : 16 / S);
   constexpr int NP = LP * V / PE;
   constexpr int PB = PE * S;
   using Piece = LdsVec<PB>;
@@ -163,7 +164,7 @@ __global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
   // MODE 1: K of stage s+1 only (stage nst-2); MODE 0: nothing (last stage).
   // The modes are separate straight-line code so that the compiler's own
   // wait before the MFMAs sees a fixed number of operations after each K load.
-  auto step = [&](auto mode, int s, DmaK<T, MT, LP>& kc, DmaK<T, MT, LP>& kn) {
+  auto step = [&](auto mode, int s, DmaK<T, V, MT, LP>& kc, DmaK<T, V, MT, LP>& kn) {
     constexpr int MODE = decltype(mode)::value;
     // 1-2: stage s (and its K) complete in every wavefront; stage s-1 read.
     // (The scheduling barrier keeps the wait from being hoisted into the
@@ -201,7 +202,7 @@ __global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
   using M1 = std::integral_constant<int, 1>;
   using M2 = std::integral_constant<int, 2>;
 
-  DmaK<T, MT, LP> ka, kb;
+  DmaK<T, V, MT, LP> ka, kb;
   ka.load(kl, kmstride, kestride, 0);
   __builtin_amdgcn_sched_barrier(0);
   dma(0);
@@ -234,20 +235,26 @@ __global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
+        // V consecutive j of output row k
         const int k = it.k0 + 16 * mt + 4 * g + r4;
         char* cell = smem + staged_y_lds(p, t, st, MT, S, r, k, it.j0);
-        if constexpr (S == 4) {
-          *reinterpret_cast<f32x4*>(cell) =
-              f32x4{acc[u][mt][0][r4], acc[u][mt][1][r4], acc[u][mt][2][r4], acc[u][mt][3][r4]};
-        } else {
-          uint32_t wv[2];
+        if constexpr (V == 4) {
+          if constexpr (S == 4) {
+            *reinterpret_cast<f32x4*>(cell) =
+                f32x4{acc[u][mt][0][r4], acc[u][mt][1][r4], acc[u][mt][2][r4], acc[u][mt][3][r4]};
+          } else {
+            uint32_t wv[2];
 #pragma unroll
-          for (int e = 0; e < V; e += 2) {
-            const uint32_t lo = __builtin_bit_cast(uint16_t, from_f32<T>(acc[u][mt][e][r4]));
-            const uint32_t hi = __builtin_bit_cast(uint16_t, from_f32<T>(acc[u][mt][e + 1][r4]));
-            wv[e / 2] = lo | (hi << 16);
+            for (int e = 0; e < V; e += 2) {
+              const uint32_t lo = __builtin_bit_cast(uint16_t, from_f32<T>(acc[u][mt][e][r4]));
+              const uint32_t hi = __builtin_bit_cast(uint16_t, from_f32<T>(acc[u][mt][e + 1][r4]));
+              wv[e / 2] = lo | (hi << 16);
+            }
+            *reinterpret_cast<u32x2*>(cell) = u32x2{wv[0], wv[1]};
           }
-          *reinterpret_cast<u32x2*>(cell) = u32x2{wv[0], wv[1]};
+        } else {
+#pragma unroll
+          for (int e = 0; e < V; ++e) reinterpret_cast<T*>(cell)[e] = from_f32<T>(acc[u][mt][e][r4]);
         }
       }
   }
@@ -264,57 +271,53 @@ __global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
   }
 }
 
-template <typename T, bool STRIDED, int MT, int LP, int UD, int NT>
+template <typename T, int V, bool STRIDED, int MT, int LP, int UD, int NT>
 hipError_t launch_dma_inst(const Problem& p, const StagedTile& t, hipStream_t s) {
   if (t.lds > 64 * 1024) {
     static bool raised = false;  // opt in to more than 64 KB of dynamic LDS, once per instance
     if (!raised) {
-      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ks_dma_kernel<T, STRIDED, MT, LP, UD, NT>),
+      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ks_dma_kernel<T, V, STRIDED, MT, LP, UD, NT>),
                                          hipFuncAttributeMaxDynamicSharedMemorySize, kDmaMaxLds);
       if (e != hipSuccess) return e;
       raised = true;
     }
   }
-  hipLaunchKernelGGL((ks_dma_kernel<T, STRIDED, MT, LP, UD, NT>), dim3(t.tiles), dim3(256), t.lds, s, p, t);
+  hipLaunchKernelGGL((ks_dma_kernel<T, V, STRIDED, MT, LP, UD, NT>), dim3(t.tiles), dim3(256), t.lds, s, p, t);
   return hipGetLastError();
 }
 
 // (MT, NT) pairs instantiated: MT * NT <= 4.
-template <typename T, bool STRIDED, int LP, int UD>
+template <typename T, int V, bool STRIDED, int LP, int UD>
 hipError_t launch_dma_mt(const Problem& p, const StagedTile& t, int mt, hipStream_t s) {
   const int nt = t.NT;
-  if (mt == 1 && nt == 1) return launch_dma_inst<T, STRIDED, 1, LP, UD, 1>(p, t, s);
-  if (mt == 2 && nt == 1) return launch_dma_inst<T, STRIDED, 2, LP, UD, 1>(p, t, s);
-  if (mt == 1 && nt == 2) return launch_dma_inst<T, STRIDED, 1, LP, UD, 2>(p, t, s);
-  if (mt == 2 && nt == 2) return launch_dma_inst<T, STRIDED, 2, LP, UD, 2>(p, t, s);
-  if (mt == 1 && nt == 4) return launch_dma_inst<T, STRIDED, 1, LP, UD, 4>(p, t, s);
+  if (mt == 1 && nt == 1) return launch_dma_inst<T, V, STRIDED, 1, LP, UD, 1>(p, t, s);
+  if (mt == 2 && nt == 1) return launch_dma_inst<T, V, STRIDED, 2, LP, UD, 1>(p, t, s);
+  if (mt == 1 && nt == 2) return launch_dma_inst<T, V, STRIDED, 1, LP, UD, 2>(p, t, s);
+  if (mt == 2 && nt == 2) return launch_dma_inst<T, V, STRIDED, 2, LP, UD, 2>(p, t, s);
+  if (mt == 1 && nt == 4) return launch_dma_inst<T, V, STRIDED, 1, LP, UD, 4>(p, t, s);
   return hipErrorInvalidValue;
 }
 
-// Instances of one storage type: strided (d >= 8) or contiguous (d == 4)
-// operands, (MT, NT) with MT * NT <= 4, LP (4 for fp32; 8, or 4 when
-// c % 32 == 16, for 16-bit types), 2, 4 or 8 DMA instructions per wavefront
-// per stage.
-template <typename T>
-hipError_t launch_dma_type(const Problem& p, const StagedTile& t, bool strided, int mt, int lp, hipStream_t s) {
+// Instances of one storage type and j-vector mode (V, STRIDED): (MT, NT) with
+// MT * NT <= 4, LP (4 for fp32; 8, or 4, for 16-bit types), 2, 4 or 8 DMA
+// instructions per wavefront per stage.  One source file per storage type
+// and mode, so the instances compile in parallel.
+template <typename T, int V, bool STRIDED>
+hipError_t launch_dma_mode(const Problem& p, const StagedTile& t, int mt, int lp, hipStream_t s) {
   if (t.W != 4) return hipErrorInvalidValue;
   if constexpr (sizeof(T) == 4) {
     if (lp != 4) return hipErrorInvalidValue;
   }
-#define KS_DMA_UD(STR, LPV)                                                         \
+#define KS_DMA_UD(LPV)                                                              \
   switch (t.UD) {                                                                   \
-    case 2: return launch_dma_mt<T, STR, LPV, 2>(p, t, mt, s);                      \
-    case 4: return launch_dma_mt<T, STR, LPV, 4>(p, t, mt, s);                      \
-    case 8: return launch_dma_mt<T, STR, LPV, 8>(p, t, mt, s);                      \
+    case 2: return launch_dma_mt<T, V, STRIDED, LPV, 2>(p, t, mt, s);               \
+    case 4: return launch_dma_mt<T, V, STRIDED, LPV, 4>(p, t, mt, s);               \
+    case 8: return launch_dma_mt<T, V, STRIDED, LPV, 8>(p, t, mt, s);               \
     default: return hipErrorInvalidValue;                                           \
   }
-  if (lp == 4) {
-    if (strided) { KS_DMA_UD(true, 4) } else { KS_DMA_UD(false, 4) }
-  }
+  if (lp == 4) { KS_DMA_UD(4) }
   if constexpr (sizeof(T) == 2) {
-    if (lp == 8) {
-      if (strided) { KS_DMA_UD(true, 8) } else { KS_DMA_UD(false, 8) }
-    }
+    if (lp == 8) { KS_DMA_UD(8) }
   }
 #undef KS_DMA_UD
   return hipErrorInvalidValue;

@@ -1,0 +1,10 @@
+// Instances of the LDS-DMA MFMA kernel (ks_dma.h) for float storage, d > 4: four j values per lane at stride d.
+#include "ks_dma.h"
+
+namespace ks {
+
+hipError_t launch_dma_f32_v4s(const Problem& p, const StagedTile& t, int mt, int lp, hipStream_t s) {
+  return launch_dma_mode<float, 4, true>(p, t, mt, lp, s);
+}
+
+}  // namespace ks

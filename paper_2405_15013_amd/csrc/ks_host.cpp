@@ -124,12 +124,15 @@ bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
 }
 
 // Automatic choice: MFMA block GEMM when b and c make each (i, j) block a real
-// dense contraction (batch-size-first with d >= 4, whose rows interleave the
-// blocks' inputs, through LDS: DMA-fed for d <= 16, register-staged beyond;
-// register-direct otherwise); VALU kernels for small blocks; the generic
+// dense contraction (batch-size-first through LDS: DMA-fed for d <= 16,
+// register-staged beyond; register-direct for batch-size-last and small
+// batch-size-first problems); VALU kernels for small blocks; the generic
 // kernel for whatever is left.
 bool plan_auto(const Problem& p, bool al16, Plan* pl) {
-  if (p.layout == BSF && p.d >= 4 && plan_dma(p, al16, pl)) return true;
+  // Batch-size-first with d <= 2: the DMA kernel from 8 MB of X + Y up
+  // (measured: below that the register-direct items' shorter latency wins).
+  const int64_t xy_bytes = (int64_t)p.batch * (p.N + p.M) * (p.dtype == F32 ? 4 : 2);
+  if (p.layout == BSF && (p.d >= 4 || xy_bytes >= (8 << 20)) && plan_dma(p, al16, pl)) return true;
   if (p.layout == BSF && p.d >= 4 && plan_staged(p, al16, pl)) return true;
   if (plan_direct(p, al16, pl)) return true;
   if (p.layout == BSL && plan_valu_bsl(p, al16, pl)) return true;

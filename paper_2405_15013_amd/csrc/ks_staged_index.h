@@ -179,13 +179,16 @@ KS_HD int64_t staged_y_unit(const Problem& p, const StagedTile& t, const STile& 
 }
 
 // ---- LDS-DMA stages (ks_dma.h) ---------------------------------------------
-// Batch-size-first only.  A stage buffer holds 16*RS rows of UR 16-byte units
-// with no padding; logical unit v of row r sits at physical unit
-// v ^ (r & (min(UR, 16) - 1)) of that row (spreads the 16 rows an operand
-// read touches over distinct banks).  DMA instruction m of wavefront w writes
-// the 64 consecutive physical units (m*W + w)*64 + lane, so each lane loads
-// the logical unit that lands there.
-KS_HD int dma_swizzle(const StagedTile& t, int r) { return r & ((t.UR < 16 ? t.UR : 16) - 1); }
+// Batch-size-first only.  A stage buffer holds 16*RS*NT rows of UR 16-byte
+// units with no padding; logical unit v of row r sits at physical unit
+// v ^ swizzle(r) of that row, which puts the same logical unit of 16
+// consecutive rows (what an operand read touches) at 16 distinct 16-byte
+// positions of a 256-byte bank line: swizzle(r) = r mod 16 for rows of 16
+// units or more, else the row's index among the rows sharing a position,
+// (r * UR / 16) mod UR.  DMA instruction m of wavefront w writes the 64
+// consecutive physical units (m*W + w)*64 + lane, so each lane loads the
+// logical unit that lands there.
+KS_HD int dma_swizzle(const StagedTile& t, int r) { return t.UR >= 16 ? (r & 15) : ((r * t.UR / 16) & (t.UR - 1)); }
 // Physical unit P of a stage buffer -> row r and logical unit v.
 KS_HD void dma_unit_of(const StagedTile& t, int P, int* r, int* v) {
   *r = P / t.UR;

@@ -20,9 +20,12 @@ hipError_t launch_staged_bf16(const Problem& p, const StagedTile& t, int V, bool
                               hipStream_t s);
 hipError_t launch_staged_f16(const Problem& p, const StagedTile& t, int V, bool strided, int mt, int cps,
                              hipStream_t s);
-hipError_t launch_dma_f32(const Problem& p, const StagedTile& t, bool strided, int mt, int lp, hipStream_t s);
-hipError_t launch_dma_bf16(const Problem& p, const StagedTile& t, bool strided, int mt, int lp, hipStream_t s);
-hipError_t launch_dma_f16(const Problem& p, const StagedTile& t, bool strided, int mt, int lp, hipStream_t s);
+#define KS_DMA_DECL(T, M) \
+  hipError_t launch_dma_##T##_##M(const Problem& p, const StagedTile& t, int mt, int lp, hipStream_t s);
+KS_DMA_DECL(f32, v4s) KS_DMA_DECL(f32, v4c) KS_DMA_DECL(f32, v2) KS_DMA_DECL(f32, v1)
+KS_DMA_DECL(bf16, v4s) KS_DMA_DECL(bf16, v4c) KS_DMA_DECL(bf16, v2) KS_DMA_DECL(bf16, v1)
+KS_DMA_DECL(f16, v4s) KS_DMA_DECL(f16, v4c) KS_DMA_DECL(f16, v2) KS_DMA_DECL(f16, v1)
+#undef KS_DMA_DECL
 
 namespace {
 constexpr int kUnitsPerWave = 256;  // 64 threads x kStagedUnitsPerThread (ks_staged.h)
@@ -166,8 +169,8 @@ bool plan_staged(const Problem& p, bool al16, Plan* pl) {
   return true;
 }
 
-// LDS-DMA kernel (ks_dma.h): batch-size-first, d in {4, 8, 16} (four
-// j values per lane: d / 4 j-groups), four wavefronts per tile, one MFMA chunk
+// LDS-DMA kernel (ks_dma.h): batch-size-first, d in {1, 2, 4, 8, 16}
+// (V = min(d, 4) j values per lane: d / V j-groups), four wavefronts per tile, one MFMA chunk
 // per stage (16 values of l for fp32; 32, or 16 when c % 32 == 16, for 16-bit
 // types), a stage of 2, 4 or 8 DMA instructions per wavefront, three stage
 // buffers, NT groups of 16 rows per wavefront (MT * NT <= 4).
@@ -191,9 +194,9 @@ bool dma_better(const DmaChoice& c, const DmaChoice& b) {
 }
 bool plan_dma(const Problem& p, bool al16, Plan* pl) {
   if (!al16 || p.layout != BSF || p.b % 16 || p.c % 16) return false;
-  if (p.d != 4 && p.d != 8 && p.d != 16) return false;
+  if (p.d != 1 && p.d != 2 && p.d != 4 && p.d != 8 && p.d != 16) return false;
   const int S = p.dtype == F32 ? 4 : 2;
-  const int V = 4, JG = p.d / V, W = 4;
+  const int V = p.d < 4 ? p.d : 4, JG = p.d / V, W = 4;
   const int KT = p.b / 16;
   bool found = false;
   DmaChoice best{};
@@ -253,13 +256,22 @@ bool plan_dma(const Problem& p, bool al16, Plan* pl) {
 
 hipError_t launch_dma(const Problem& p, const Plan& pl, hipStream_t s) {
   const StagedTile t = staged_tile_of(p, pl);
-  const bool strided = pl.unroll != 0;
+  const int mode = pl.unroll ? 0 : (pl.vec == 4 ? 1 : (pl.vec == 2 ? 2 : 3));  // v4s, v4c, v2, v1
+  if ((pl.unroll && pl.vec != 4) || (!pl.unroll && pl.vec != p.d)) return hipErrorInvalidValue;
+#define KS_DMA_CALL(T)                                                 \
+  switch (mode) {                                                      \
+    case 0: return launch_dma_##T##_v4s(p, t, pl.waves_m, pl.cps, s);  \
+    case 1: return launch_dma_##T##_v4c(p, t, pl.waves_m, pl.cps, s);  \
+    case 2: return launch_dma_##T##_v2(p, t, pl.waves_m, pl.cps, s);   \
+    default: return launch_dma_##T##_v1(p, t, pl.waves_m, pl.cps, s);  \
+  }
   switch (p.dtype) {
-    case F32: return launch_dma_f32(p, t, strided, pl.waves_m, pl.cps, s);
-    case BF16: return launch_dma_bf16(p, t, strided, pl.waves_m, pl.cps, s);
-    case F16: return launch_dma_f16(p, t, strided, pl.waves_m, pl.cps, s);
+    case F32: KS_DMA_CALL(f32)
+    case BF16: KS_DMA_CALL(bf16)
+    case F16: KS_DMA_CALL(f16)
     default: return hipErrorInvalidValue;
   }
+#undef KS_DMA_CALL
 }
 
 hipError_t launch_staged(const Problem& p, const Plan& pl, hipStream_t s) {

@@ -370,7 +370,7 @@ bool verify_dma(Checker& ck, const Plan& pl) {
   const StagedTile t = staged_tile_of(p, pl);
   const int V = pl.vec, MT = pl.waves_m, S = p.dtype == F32 ? 4 : 2, LP = pl.cps, CH = 4 * LP, UE = 16 / S;
   const bool strided = pl.unroll != 0;
-  if (p.layout != BSF || V != 4 || p.d % V || strided != (p.d > V)) return ck.fail("bad j-vector", V);
+  if (p.layout != BSF || V != (p.d < 4 ? p.d : 4) || p.d % V || strided != (p.d > V)) return ck.fail("bad j-vector", V);
   if (LP != 4 && !(S == 2 && LP == 8)) return ck.fail("bad MFMA lane depth", LP);
   if (t.W != 4 || t.RS * t.JG * t.KGW != t.W || t.JG != p.d / V) return ck.fail("waves do not split the tile", t.W);
   if (t.kgt * t.KGW * 16 * MT != p.b) return ck.fail("k-groups do not cover b", p.b);
@@ -384,7 +384,7 @@ bool verify_dma(Checker& ck, const Plan& pl) {
   if (pl.lds_bytes != t.lds || t.lds < 3 * t.stage) return ck.fail("LDS allocation does not hold three stages", t.lds);
   if (t.lds < 16 * t.RS * t.NT * t.ypitch) return ck.fail("LDS allocation does not hold the output tile", t.lds);
   if (t.remap && t.tiles % 8) return ck.fail("XCD remap needs a multiple of 8 tiles", t.tiles);
-  const int pe = strided ? V : UE, np = LP * V / pe, pb = pe * S;
+  const int pe = direct_x_piece_elems(BSF, strided, LP, V, S), np = LP * V / pe, pb = pe * S;
   std::vector<uint8_t> seen(t.tiles, 0);
   std::vector<int64_t> shadow((size_t)t.stage / S);
   const int nst = p.c / CH;

@@ -79,14 +79,14 @@ def test_all_sweep_plans_staged(dtype, layout, batch, every):
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 @pytest.mark.parametrize("batch,every", [(72, 1), (1000, 3), (25088, 29)])
 def test_all_sweep_plans_dma(dtype, batch, every):
-    """The LDS-DMA kernel (forced) on every batch-size-first sweep pattern it
-    accepts (d >= 4): every DMA lane fills one unit of the stage from an
-    in-bounds address, every swizzled operand read holds the right X value,
-    every output written once.  It must accept every d >= 4 pattern."""
+    """The LDS-DMA kernel (forced) on every batch-size-first sweep pattern:
+    every DMA lane fills one unit of the stage from an in-bounds address, every
+    swizzled operand read holds the right X value, every output written once.
+    It must accept every pattern of the sweep."""
     bad = []
     ks.ks_force_variant(6)
     try:
-        for pattern in [p for p in sweep_patterns() if p[3] >= 4][::every]:
+        for pattern in sweep_patterns()[::every]:
             st, rep = ks.ks_plan_verify(*pattern, batch, "bsf", dtype)
             if st != 0:
                 bad.append((pattern, rep))
@@ -117,12 +117,15 @@ def test_all_sweep_plans_stream(dtype, layout, batch, every):
 
 def test_sweep_plans_use_mfma_kernels():
     """The whole sweep runs on the MFMA kernels (aligned buffers): LDS-DMA for
-    batch-size-first with d >= 4, register-direct otherwise."""
+    batch-size-first with d >= 4 or at least 8 MB of X and Y, register-direct
+    otherwise."""
     for pattern in sweep_patterns()[::7]:
         for layout in ("bsf", "bsl"):
             for dtype in ("f32", "bf16", "f16"):
                 desc = ks.ks_plan_describe(*pattern, 4096, layout, dtype)
-                want = "name=dma" if (layout == "bsf" and pattern[3] >= 4) else "name=direct"
+                a, b, c, d = pattern
+                big = 4096 * (a * c * d + a * b * d) * (4 if dtype == "f32" else 2) >= 8 << 20
+                want = "name=dma" if (layout == "bsf" and (d >= 4 or big)) else "name=direct"
                 assert want in desc, (pattern, layout, dtype, desc)
 
 
@@ -150,7 +153,7 @@ def test_dma_row_group_plans_covered():
         return (dt, f["waves_m"], f["nt"], f["lch"], f["unroll"])
     have = {key(p, dt) for p in DMA_ROW_GROUP_SHAPES + DMA_SHAPES for dt in ("f32", "bf16")}
     want = {key(p, dt) for p in [(a, b, c, d) for a in (1, 2, 4, 8) for b in (16, 32, 64, 128) for c in (16, 32, 64)
-                                  for d in (4, 8, 16) if a * b * d <= 8192 and a * c * d <= 8192]
+                                  for d in (1, 2, 4, 8, 16) if a * b * d <= 8192 and a * c * d <= 8192]
             for dt in ("f32", "bf16")}
     assert want <= have, sorted(want - have)
     for p in DMA_ROW_GROUP_SHAPES:
