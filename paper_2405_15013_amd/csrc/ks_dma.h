@@ -90,8 +90,12 @@ struct DmaK {
 
 // V j values per lane (V = min(d, 4)): STRIDED when d > V (pieces of V
 // elements at stride d), otherwise the lane's LP x V block is contiguous.
+// Register budget per instance: the smallest tiles (MT = NT = 1) are fitted
+// to four waves per SIMD (four workgroups per CU), NT = 2 to three, the rest
+// to two (the accumulators then live in VGPRs instead of AGPRs).
 template <typename T, int V, bool STRIDED, int MT, int LP, int UD, int NT>
-__global__ __launch_bounds__(256) void ks_dma_kernel(Problem p, StagedTile t) {
+__global__ __launch_bounds__(256) __attribute__((amdgpu_waves_per_eu(MT * NT == 1 ? 4 : ((MT == 1 && NT == 2) ? 3 : 2))))
+void ks_dma_kernel(Problem p, StagedTile t) {
   constexpr int S = sizeof(T);
   constexpr int CH = 4 * LP;  // values of l per stage
   constexpr int PE = STRIDED ? V : (LP * V * S < 16 ? LP * V : 16 / S);
