@@ -1,4 +1,4 @@
-// LDS-DMA MFMA kernels for batch-size-first KS patterns with d >= 4.
+// LDS-DMA MFMA kernels for batch-size-first KS patterns.
 //
 // Same output-stationary tiles and products as the LDS-staged kernels (paper
 // Section 4.1, Algorithm 2; tile and item mapping in ks_staged_index.h), with
