@@ -16,10 +16,12 @@ __device__ __forceinline__ float to_f32(_Float16 v) { return (float)v; }
 template <typename T> __device__ __forceinline__ T from_f32(float v);
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
 // fp32 -> bfloat16, round to nearest even; NaNs stay quiet NaNs.
+// (Branch-free: both results are formed and one is selected.)
 template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) {
-  uint32_t u = __float_as_uint(v);
-  if ((u & 0x7fffffffu) > 0x7f800000u) return (bf16_t)((u >> 16) | 0x40u);
-  return (bf16_t)((u + 0x7fffu + ((u >> 16) & 1u)) >> 16);
+  const uint32_t u = __float_as_uint(v);
+  const uint32_t rne = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
+  const uint32_t qnan = (u >> 16) | 0x40u;
+  return (bf16_t)((u & 0x7fffffffu) > 0x7f800000u ? qnan : rne);
 }
 // fp32 -> fp16; the conversion instruction rounds to nearest even.
 template <> __device__ __forceinline__ _Float16 from_f32<_Float16>(float v) { return (_Float16)v; }

@@ -106,8 +106,8 @@ void ks_dma_kernel(Problem p, StagedTile t) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, g = lane >> 4;
-  const STile st = staged_tile(p, t, blockIdx.x);
-  const SItem si = staged_item(p, t, st, V, MT, w);
+  const STile st = dma_tile(t, blockIdx.x);
+  const SItem si = dma_item(t, st, V, MT, w);
   DItem it;
   it.i = st.i;
   it.j0 = si.j0;
@@ -126,15 +126,15 @@ void ks_dma_kernel(Problem p, StagedTile t) {
 #pragma unroll
   for (int m = 0; m < UD; ++m) {
     int r, v;
-    dma_unit_of(t, dma_phys_unit(t, m, w, lane), &r, &v);
+    dma_unit_of_fast(t, dma_phys_unit(t, m, w, lane), &r, &v);
     int beta = st.bt * 16 * t.RS * NT + r;
     if (beta >= p.batch) beta = p.batch - 1;
     soff[m] = beta * p.N + v * (16 / S);
   }
-  const int64_t xstage = (int64_t)CH * p.d;  // X elements per stage along a row
-  auto dma = [&](int s) {
-    const T* xs = xi + s * xstage;
-    char* dst = smem + (s % 3) * stage + w * 1024;
+  const int xstage = CH * p.d;  // X elements per stage along a row
+  // DMA of the stage whose row runs start at xs, into stage buffer buf.
+  auto dma = [&](const T* xs, int buf) {
+    char* dst = smem + buf * stage + w * 1024;
 #pragma unroll
     for (int m = 0; m < UD; ++m)
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(xs + soff[m]),
@@ -168,6 +168,10 @@ void ks_dma_kernel(Problem p, StagedTile t) {
   // MODE 1: K of stage s+1 only (stage nst-2); MODE 0: nothing (last stage).
   // The modes are separate straight-line code so that the compiler's own
   // wait before the MFMAs sees a fixed number of operations after each K load.
+  // Stage s uses buffer cur = s % 3 (kept incrementally), the DMAs of stage
+  // s+2 go to buffer (s+2) % 3 from the row runs at xnext.
+  int cur = 0;
+  const T* xnext = xi + 2 * xstage;
   auto step = [&](auto mode, int s, DmaK<T, V, MT, LP>& kc, DmaK<T, V, MT, LP>& kn) {
     constexpr int MODE = decltype(mode)::value;
     // 1-2: stage s (and its K) complete in every wavefront; stage s-1 read.
@@ -181,11 +185,15 @@ void ks_dma_kernel(Problem p, StagedTile t) {
     // count of step 1 relies on).
     if constexpr (MODE >= 1) kn.load(kl, kmstride, kestride, (s + 1) * CH);
     __builtin_amdgcn_sched_barrier(0);
-    if constexpr (MODE == 2) dma(s + 2);
+    if constexpr (MODE == 2) {
+      dma(xnext, cur == 0 ? 2 : cur - 1);
+      xnext += xstage;
+    }
     __builtin_amdgcn_sched_barrier(0);
     // 4: per row group, operands from LDS, then the MFMAs (the K operands
     // serve all NT groups).
-    const uint32_t base = (uint32_t)((s % 3) * stage);
+    const uint32_t base = (uint32_t)(cur * stage);
+    cur = cur == 2 ? 0 : cur + 1;
 #pragma unroll
     for (int u = 0; u < NT; ++u) {
       typename Piece::type pc[NP];
@@ -209,8 +217,8 @@ void ks_dma_kernel(Problem p, StagedTile t) {
   DmaK<T, V, MT, LP> ka, kb;
   ka.load(kl, kmstride, kestride, 0);
   __builtin_amdgcn_sched_barrier(0);
-  dma(0);
-  if (nst > 1) dma(1);
+  dma(xi, 0);
+  if (nst > 1) dma(xi + xstage, 1);
   __builtin_amdgcn_sched_barrier(0);
   int s = 0;
   for (; s + 3 < nst; s += 2) {  // both steps are steady-state steps
@@ -232,16 +240,15 @@ void ks_dma_kernel(Problem p, StagedTile t) {
 
   // Structured epilogue: accumulators -> LDS output tile -> contiguous runs.
   __syncthreads();  // every wavefront is done with the stage buffers
+  char* ycell0 = smem + dma_y_lds_lane(p, t, si, MT, S, n, g);
 #pragma unroll
-  for (int u = 0; u < NT; ++u) {
-    const int r = 16 * (NT * si.rs + u) + n;
+  for (int u = 0; u < NT; ++u)
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
       for (int r4 = 0; r4 < 4; ++r4) {
-        // V consecutive j of output row k
-        const int k = it.k0 + 16 * mt + 4 * g + r4;
-        char* cell = smem + staged_y_lds(p, t, st, MT, S, r, k, it.j0);
+        // V consecutive j of output row k = k0 + 16*mt + 4*g + r4
+        char* cell = ycell0 + u * 16 * t.ypitch + (16 * mt + r4) * p.d * S;
         if constexpr (V == 4) {
           if constexpr (S == 4) {
             *reinterpret_cast<f32x4*>(cell) =
@@ -261,17 +268,17 @@ void ks_dma_kernel(Problem p, StagedTile t) {
           for (int e = 0; e < V; ++e) reinterpret_cast<T*>(cell)[e] = from_f32<T>(acc[u][mt][e][r4]);
         }
       }
-  }
   __syncthreads();
-  const int uy = staged_y_units_per_row(p, t, MT, S);
-  const int nunits = 16 * t.RS * NT * uy;
-  T* __restrict__ y = static_cast<T*>(p.y);
+  // 16-byte units of the output tile (uy = 2^lUY per row): rows beyond the
+  // batch are not stored.
+  const int nunits = (16 * t.RS * NT) << t.lUY;
+  const int rows_valid = p.batch - st.bt * 16 * t.RS * NT;
+  T* __restrict__ ytile = static_cast<T*>(p.y) + dma_y_tile_base(p, t, st, MT);
   for (int u = tid; u < nunits; u += 64 * t.W) {
-    const int row = u / uy, v = u % uy;
-    const int64_t off = staged_y_unit(p, t, st, MT, S, row, v);
-    if (off < 0) continue;
+    const int row = u >> t.lUY, v = u & ((1 << t.lUY) - 1);
+    if (row >= rows_valid) continue;
     const u32x4 val = *reinterpret_cast<const u32x4*>(smem + row * t.ypitch + v * 16);
-    __builtin_nontemporal_store(val, reinterpret_cast<u32x4*>(y + off));
+    __builtin_nontemporal_store(val, reinterpret_cast<u32x4*>(ytile + dma_y_row(p, row, v, S)));
   }
 }
 

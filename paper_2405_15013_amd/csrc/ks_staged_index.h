@@ -51,7 +51,23 @@ struct StagedTile {
   int UR;        // 16-byte units per stage row (LCH * d * esize / 16, a power of two)
   int UD;        // DMA instructions (64 units each) per wavefront per stage
   int NT;        // batch-size-first: 16-row groups per wavefront (1 except in the DMA kernel)
+  // DMA kernel: log2 of the power-of-two sizes, and multiply-shift constants
+  // for the divisions of the tile decode (dma_div).
+  int lUR, lRS, lJG, lUY;
+  uint32_t mkgt, mnbt;
+  int skgt, snbt;
 };
+
+// Division by a runtime constant as a multiply and a shift: for d >= 1 take
+// l = ceil(log2 d), m = ceil(2^(31+l) / d) (< 2^32) and s = 31 + l; then
+// floor(n / d) = (n * m) >> s for every 0 <= n < 2^31 (m*d - 2^(31+l) < d <= 2^l).
+inline void dma_magic(uint32_t d, uint32_t* m, int* s) {
+  int l = 0;
+  while ((1u << l) < d) ++l;
+  *s = 31 + l;
+  *m = (uint32_t)((((uint64_t)1 << (31 + l)) + d - 1) / d);
+}
+KS_HD uint32_t dma_div(uint32_t n, uint32_t m, int s) { return (uint32_t)(((uint64_t)n * m) >> s); }
 
 struct STile {
   int i, j, kt, bt;  // j: BSL only
@@ -188,7 +204,9 @@ KS_HD int64_t staged_y_unit(const Problem& p, const StagedTile& t, const STile& 
 // (r * UR / 16) mod UR.  DMA instruction m of wavefront w writes the 64
 // consecutive physical units (m*W + w)*64 + lane, so each lane loads the
 // logical unit that lands there.
-KS_HD int dma_swizzle(const StagedTile& t, int r) { return t.UR >= 16 ? (r & 15) : ((r * t.UR / 16) & (t.UR - 1)); }
+KS_HD int dma_swizzle(const StagedTile& t, int r) {
+  return t.UR >= 16 ? (r & 15) : (int)((((uint32_t)r * (uint32_t)t.UR) >> 4) & (uint32_t)(t.UR - 1));
+}
 // Physical unit P of a stage buffer -> row r and logical unit v.
 KS_HD void dma_unit_of(const StagedTile& t, int P, int* r, int* v) {
   *r = P / t.UR;
@@ -208,5 +226,47 @@ KS_HD int dma_op_byte(const Problem& p, const SItem& it, int LP, int V, bool str
   if (strided) return ((l0 + LP * g + q) * p.d + it.j0) * esize;
   return ((l0 + LP * g) * p.d + it.j0) * esize + q * pe * esize;
 }
+
+// Tile and work item of the DMA kernel: staged_tile and staged_item computed
+// with the multiply-shift divisions and the power-of-two shifts above (the
+// plan verifier checks both against the plain forms for every tile).
+KS_HD STile dma_tile(const StagedTile& t, int block) {
+  const uint32_t tile = t.remap ? (uint32_t)staged_remap(block, t.tiles) : (uint32_t)block;
+  STile s;
+  const uint32_t q1 = dma_div(tile, t.mkgt, t.skgt);
+  s.kt = (int)(tile - q1 * (uint32_t)t.kgt);
+  const uint32_t q2 = dma_div(q1, t.mnbt, t.snbt);
+  s.bt = (int)(q1 - q2 * (uint32_t)t.nbt);
+  s.j = 0;
+  s.i = (int)q2;
+  return s;
+}
+KS_HD SItem dma_item(const StagedTile& t, const STile& s, int V, int MT, int w) {
+  SItem it;
+  it.rs = w & (t.RS - 1);
+  it.jg = (w >> t.lRS) & (t.JG - 1);
+  it.kgw = w >> (t.lRS + t.lJG);
+  it.k0 = (s.kt * t.KGW + it.kgw) * 16 * MT;
+  it.j0 = it.jg * V;
+  it.beta0 = (s.bt * t.RS + it.rs) * 16 * t.NT;
+  return it;
+}
+// Physical unit P of a stage buffer -> row r and logical unit v (UR a power of two).
+KS_HD void dma_unit_of_fast(const StagedTile& t, int P, int* r, int* v) {
+  *r = (int)((uint32_t)P >> t.lUR);
+  *v = (int)(((uint32_t)P & (uint32_t)(t.UR - 1)) ^ (uint32_t)dma_swizzle(t, *r));
+}
+
+// Output tile of the DMA kernel: LDS byte offset of the lane's first output
+// (row group 0, M-tile 0, r = 0); output (u, mt, r) is u*16*ypitch +
+// (16*mt + r)*d*esize further.  Y element offset of output-tile row `row`
+// relative to the tile's first row, and that first row's offset.
+KS_HD int dma_y_lds_lane(const Problem& p, const StagedTile& t, const SItem& it, int MT, int esize, int n, int g) {
+  return (16 * t.NT * it.rs + n) * t.ypitch + ((it.kgw * 16 * MT + 4 * g) * p.d + it.j0) * esize;
+}
+KS_HD int64_t dma_y_tile_base(const Problem& p, const StagedTile& t, const STile& s, int MT) {
+  return (int64_t)s.bt * 16 * t.RS * t.NT * p.M + (int64_t)s.i * p.b * p.d + (int64_t)s.kt * t.KGW * 16 * MT * p.d;
+}
+KS_HD int dma_y_row(const Problem& p, int row, int v, int esize) { return row * p.M + v * (16 / esize); }
 
 }  // namespace ks

@@ -62,6 +62,9 @@ StagedTile staged_tile_of(const Problem& p, const Plan& pl) {
   t.ypitch = 0;
   t.UR = 0;
   t.UD = 0;
+  t.lUR = t.lRS = t.lJG = t.lUY = 0;
+  t.mkgt = t.mnbt = 0;
+  t.skgt = t.snbt = 0;
   t.lds = 2 * t.stage;
   if (pl.variant == V_DMA) {
     // Unpadded, swizzled rows of UR units; three stage buffers.
@@ -70,6 +73,13 @@ StagedTile staged_tile_of(const Problem& p, const Plan& pl) {
     t.stage = 16 * t.RS * t.NT * t.pitch;
     t.UD = t.stage / 16 / (64 * t.W);
     t.lds = 3 * t.stage;
+    auto log2i = [](int v) { int l = 0; while ((1 << l) < v) ++l; return l; };
+    t.lUR = log2i(t.UR);
+    t.lRS = log2i(t.RS);
+    t.lJG = log2i(t.JG);
+    t.lUY = log2i(MT * t.KGW * p.d * S);  // 16-byte units per output tile row
+    dma_magic((uint32_t)t.kgt, &t.mkgt, &t.skgt);
+    dma_magic((uint32_t)t.nbt, &t.mnbt, &t.snbt);
   }
   if (p.layout == BSF) {
     t.ypitch = 16 * MT * t.KGW * p.d * S + 16;

@@ -388,10 +388,22 @@ bool verify_dma(Checker& ck, const Plan& pl) {
   std::vector<uint8_t> seen(t.tiles, 0);
   std::vector<int64_t> shadow((size_t)t.stage / S);
   const int nst = p.c / CH;
+  if ((1 << t.lUR) != t.UR || (1 << t.lRS) != t.RS || (1 << t.lJG) != t.JG ||
+      (16 << t.lUY) != staged_y_kr(t, MT) * p.d * S)
+    return ck.fail("tile sizes are not the powers of two the kernel shifts by", t.UR);
   for (int blk = 0; blk < t.tiles && ck.err.empty(); ++blk) {
     const STile st = staged_tile(p, t, blk);
     const int logical = t.remap ? staged_remap(blk, t.tiles) : blk;
     if (logical < 0 || logical >= t.tiles || seen[logical]++) return ck.fail("tile visited twice", logical);
+    // The kernel's decode (multiply-shift divisions, shifts) gives the same tile and items.
+    const STile sf = dma_tile(t, blk);
+    if (sf.i != st.i || sf.bt != st.bt || sf.kt != st.kt) return ck.fail("fast tile decode differs", blk);
+    for (int w = 0; w < t.W; ++w) {
+      const SItem a1 = staged_item(p, t, st, V, MT, w), a2 = dma_item(t, st, V, MT, w);
+      if (a1.rs != a2.rs || a1.jg != a2.jg || a1.kgw != a2.kgw || a1.j0 != a2.j0 || a1.k0 != a2.k0 ||
+          a1.beta0 != a2.beta0)
+        return ck.fail("fast work-item decode differs", w);
+    }
     for (int s = 0; s < nst; ++s) {
       std::fill(shadow.begin(), shadow.end(), (int64_t)-1);
       for (int w = 0; w < t.W; ++w)
@@ -399,8 +411,10 @@ bool verify_dma(Checker& ck, const Plan& pl) {
           for (int lane = 0; lane < 64; ++lane) {
             const int P = dma_phys_unit(t, m, w, lane);
             if (P < 0 || (P + 1) * 16 > t.stage) return ck.fail("DMA writes outside the stage buffer", P);
-            int r, v;
+            int r, v, r2, v2;
             dma_unit_of(t, P, &r, &v);
+            dma_unit_of_fast(t, P, &r2, &v2);
+            if (r2 != r || v2 != v) return ck.fail("fast DMA unit mapping differs", P);
             if (r < 0 || r >= 16 * t.RS * t.NT || v < 0 || v >= t.UR) return ck.fail("DMA unit outside the stage rows", P);
             int beta = st.bt * 16 * t.RS * t.NT + r;
             if (beta >= p.batch) beta = p.batch - 1;
@@ -451,6 +465,28 @@ bool verify_dma(Checker& ck, const Plan& pl) {
       }
     }
     if (!verify_bsf_epilogue(ck, t, st, V, MT, S)) return false;
+    // The kernel's own epilogue offsets: per-lane LDS base plus constants, and
+    // Y = tile base + row offset for rows inside the batch.
+    for (int w = 0; w < t.W; ++w) {
+      const SItem si = staged_item(p, t, st, V, MT, w);
+      for (int lane = 0; lane < 64; ++lane) {
+        const int n = lane & 15, g = lane >> 4;
+        for (int u = 0; u < t.NT; ++u)
+          for (int mt = 0; mt < MT; ++mt)
+            for (int r4 = 0; r4 < 4; ++r4) {
+              const int k = si.k0 + 16 * mt + 4 * g + r4, r = 16 * (t.NT * si.rs + u) + n;
+              const int o = dma_y_lds_lane(p, t, si, MT, S, n, g) + u * 16 * t.ypitch + (16 * mt + r4) * p.d * S;
+              if (o != staged_y_lds(p, t, st, MT, S, r, k, si.j0)) return ck.fail("output tile offset differs", o);
+            }
+      }
+    }
+    const int uy = 1 << t.lUY, rows_valid = p.batch - st.bt * 16 * t.RS * t.NT;
+    for (int r = 0; r < 16 * t.RS * t.NT; ++r)
+      for (int v = 0; v < uy; ++v) {
+        const int64_t want = staged_y_unit(p, t, st, MT, S, r, v);
+        const int64_t have = r < rows_valid ? dma_y_tile_base(p, t, st, MT) + dma_y_row(p, r, v, S) : -1;
+        if (want != have) return ck.fail("output store offset differs", r);
+      }
   }
   return ck.err.empty();
 }
