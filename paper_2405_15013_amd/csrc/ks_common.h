@@ -15,16 +15,24 @@ __device__ __forceinline__ float to_f32(_Float16 v) { return (float)v; }
 
 template <typename T> __device__ __forceinline__ T from_f32(float v);
 template <> __device__ __forceinline__ float from_f32<float>(float v) { return v; }
-// fp32 -> bfloat16, round to nearest even; NaNs stay quiet NaNs.
-// (Branch-free: both results are formed and one is selected.)
+// fp32 -> bfloat16 and fp16: the conversion instructions (v_cvt_pk_bf16_f32,
+// v_cvt_f16_f32) round to nearest even; NaNs stay NaNs.
 template <> __device__ __forceinline__ bf16_t from_f32<bf16_t>(float v) {
-  const uint32_t u = __float_as_uint(v);
-  const uint32_t rne = (u + 0x7fffu + ((u >> 16) & 1u)) >> 16;
-  const uint32_t qnan = (u >> 16) | 0x40u;
-  return (bf16_t)((u & 0x7fffffffu) > 0x7f800000u ? qnan : rne);
+  return __builtin_bit_cast(uint16_t, (__bf16)v);
 }
-// fp32 -> fp16; the conversion instruction rounds to nearest even.
 template <> __device__ __forceinline__ _Float16 from_f32<_Float16>(float v) { return (_Float16)v; }
+
+// Two fp32 values rounded to the 16-bit storage type T and packed into one
+// dword (lo in bits 0..15): one packed conversion for bfloat16.
+typedef float f32x2_t __attribute__((ext_vector_type(2)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+template <typename T> __device__ __forceinline__ uint32_t pack2_f32(float lo, float hi);
+template <> __device__ __forceinline__ uint32_t pack2_f32<bf16_t>(float lo, float hi) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{lo, hi}, bf16x2_t));
+}
+template <> __device__ __forceinline__ uint32_t pack2_f32<_Float16>(float lo, float hi) {
+  return (uint32_t)__builtin_bit_cast(uint16_t, (_Float16)lo) | ((uint32_t)__builtin_bit_cast(uint16_t, (_Float16)hi) << 16);
+}
 
 // 16-byte vector type used for global memory traffic.
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));

@@ -165,9 +165,7 @@ __device__ __forceinline__ void direct_store(const Problem& p, const DItem& it, 
 #pragma unroll
         for (int u = 0; u < YPE; u += 2) {
           const int f0 = q * YPE + u, f1 = f0 + 1;
-          const uint32_t lo = __builtin_bit_cast(uint16_t, from_f32<T>(acc[mt][f0 % V][f0 / V]));
-          const uint32_t hi = __builtin_bit_cast(uint16_t, from_f32<T>(acc[mt][f1 % V][f1 / V]));
-          w[u / 2] = lo | (hi << 16);
+          w[u / 2] = pack2_f32<T>(acc[mt][f0 % V][f0 / V], acc[mt][f1 % V][f1 / V]);
         }
       }
       store_piece<YPB>(yl + mt * ymstride + q * yqstride, w);
@@ -217,10 +215,10 @@ __global__ __launch_bounds__(256) void ks_direct_kernel(Problem p, DirectTile t)
   constexpr int LP = S == 4 ? 4 : 8;
   constexpr int CH = 4 * LP;  // l values per chunk
   const int lane = threadIdx.x & 63;
-  const int item = blockIdx.x * t.waves + (threadIdx.x >> 6);
+  const int item = blockIdx.x * t.waves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (item >= t.items) return;  // wave-uniform
   const int n = lane & 15, g = lane >> 4;
-  const DItem it = direct_item(p, t, V, MT, item);
+  const DItem it = direct_item_fast(p, t, V, MT, item);
   const T* __restrict__ x = static_cast<const T*>(p.x);
   const T* __restrict__ kv = static_cast<const T*>(p.kv);
   const int c = p.c;
@@ -277,10 +275,10 @@ __global__ __launch_bounds__(256) void ks_direct_c_kernel(Problem p, DirectTile 
   constexpr int PD0 = 64 / R;
   constexpr int PD = NCH <= 1 ? 0 : (PD0 < 1 ? 1 : (PD0 > NCH - 1 ? NCH - 1 : PD0));
   const int lane = threadIdx.x & 63;
-  const int item = blockIdx.x * t.waves + (threadIdx.x >> 6);
+  const int item = blockIdx.x * t.waves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (item >= t.items) return;  // wave-uniform
   const int n = lane & 15, g = lane >> 4;
-  const DItem it = direct_item(p, t, V, MT, item);
+  const DItem it = direct_item_fast(p, t, V, MT, item);
   const T* __restrict__ x = static_cast<const T*>(p.x);
   const T* __restrict__ kv = static_cast<const T*>(p.kv);
   const int c = p.c;

@@ -25,6 +25,7 @@
 #include <hip/hip_runtime.h>
 #include <cstdint>
 
+#include "ks_divide.h"
 #include "ks_internal.h"
 
 #define KS_HD __host__ __device__ __forceinline__
@@ -37,6 +38,8 @@ struct DirectTile {
   int nbt;       // batch tiles (16*V entries in BSL, 16 rows in BSF)
   int items;     // nbt * a * jgroups * kgroups
   int waves;     // wavefronts per workgroup (1, 2 or 4)
+  uint32_t mkg, mnbt, mjg;  // multiply-shift constants of the item decode (ks_divide.h)
+  int skg, snbt, sjg;
 };
 
 struct DItem {
@@ -71,6 +74,28 @@ KS_HD DItem direct_item(const Problem& p, const DirectTile& t, int V, int MT, in
   rest /= t.nbt;
   const int jg = rest % t.jgroups;
   it.i = rest / t.jgroups;
+  it.k0 = kg * 16 * MT;
+  if (p.layout == BSL) {
+    it.j0 = jg;
+    it.beta0 = bt * 16 * V;
+  } else {
+    it.j0 = jg * V;
+    it.beta0 = bt * 16;
+  }
+  return it;
+}
+
+// direct_item with the divisions done by multiply and shift (the kernels'
+// form; the plan verifier checks it against direct_item for every item).
+KS_HD DItem direct_item_fast(const Problem& p, const DirectTile& t, int V, int MT, int item) {
+  DItem it;
+  const uint32_t q1 = div_fast((uint32_t)item, t.mkg, t.skg);
+  const int kg = item - (int)q1 * t.kgroups;
+  const uint32_t q2 = div_fast(q1, t.mnbt, t.snbt);
+  const int bt = (int)q1 - (int)q2 * t.nbt;
+  const uint32_t q3 = div_fast(q2, t.mjg, t.sjg);
+  const int jg = (int)q2 - (int)q3 * t.jgroups;
+  it.i = (int)q3;
   it.k0 = kg * 16 * MT;
   if (p.layout == BSL) {
     it.j0 = jg;

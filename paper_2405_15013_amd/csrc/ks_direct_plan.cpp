@@ -31,6 +31,9 @@ DirectTile direct_tile(const Problem& p, const Plan& pl) {
   t.nbt = (p.batch + span - 1) / span;
   t.items = t.nbt * p.a * t.jgroups * t.kgroups;
   t.waves = (int)pl.block / 64;
+  div_magic((uint32_t)t.kgroups, &t.mkg, &t.skg);
+  div_magic((uint32_t)t.nbt, &t.mnbt, &t.snbt);
+  div_magic((uint32_t)t.jgroups, &t.mjg, &t.sjg);
   return t;
 }
 

@@ -257,9 +257,7 @@ void ks_dma_kernel(Problem p, StagedTile t) {
             uint32_t wv[2];
 #pragma unroll
             for (int e = 0; e < V; e += 2) {
-              const uint32_t lo = __builtin_bit_cast(uint16_t, from_f32<T>(acc[u][mt][e][r4]));
-              const uint32_t hi = __builtin_bit_cast(uint16_t, from_f32<T>(acc[u][mt][e + 1][r4]));
-              wv[e / 2] = lo | (hi << 16);
+              wv[e / 2] = pack2_f32<T>(acc[u][mt][e][r4], acc[u][mt][e + 1][r4]);
             }
             *reinterpret_cast<u32x2*>(cell) = u32x2{wv[0], wv[1]};
           }

@@ -27,6 +27,7 @@
 #include <hip/hip_runtime.h>
 #include <cstdint>
 
+#include "ks_divide.h"
 #include "ks_internal.h"
 
 #define KS_HD __host__ __device__ __forceinline__
@@ -52,22 +53,13 @@ struct StagedTile {
   int UD;        // DMA instructions (64 units each) per wavefront per stage
   int NT;        // batch-size-first: 16-row groups per wavefront (1 except in the DMA kernel)
   // DMA kernel: log2 of the power-of-two sizes, and multiply-shift constants
-  // for the divisions of the tile decode (dma_div).
+  // for the divisions of the tile decode (div_fast, ks_divide.h).
   int lUR, lRS, lJG, lUY;
   uint32_t mkgt, mnbt;
   int skgt, snbt;
 };
 
-// Division by a runtime constant as a multiply and a shift: for d >= 1 take
-// l = ceil(log2 d), m = ceil(2^(31+l) / d) (< 2^32) and s = 31 + l; then
-// floor(n / d) = (n * m) >> s for every 0 <= n < 2^31 (m*d - 2^(31+l) < d <= 2^l).
-inline void dma_magic(uint32_t d, uint32_t* m, int* s) {
-  int l = 0;
-  while ((1u << l) < d) ++l;
-  *s = 31 + l;
-  *m = (uint32_t)((((uint64_t)1 << (31 + l)) + d - 1) / d);
-}
-KS_HD uint32_t dma_div(uint32_t n, uint32_t m, int s) { return (uint32_t)(((uint64_t)n * m) >> s); }
+
 
 struct STile {
   int i, j, kt, bt;  // j: BSL only
@@ -233,9 +225,9 @@ KS_HD int dma_op_byte(const Problem& p, const SItem& it, int LP, int V, bool str
 KS_HD STile dma_tile(const StagedTile& t, int block) {
   const uint32_t tile = t.remap ? (uint32_t)staged_remap(block, t.tiles) : (uint32_t)block;
   STile s;
-  const uint32_t q1 = dma_div(tile, t.mkgt, t.skgt);
+  const uint32_t q1 = div_fast(tile, t.mkgt, t.skgt);
   s.kt = (int)(tile - q1 * (uint32_t)t.kgt);
-  const uint32_t q2 = dma_div(q1, t.mnbt, t.snbt);
+  const uint32_t q2 = div_fast(q1, t.mnbt, t.snbt);
   s.bt = (int)(q1 - q2 * (uint32_t)t.nbt);
   s.j = 0;
   s.i = (int)q2;

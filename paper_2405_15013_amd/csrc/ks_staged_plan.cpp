@@ -78,8 +78,8 @@ StagedTile staged_tile_of(const Problem& p, const Plan& pl) {
     t.lRS = log2i(t.RS);
     t.lJG = log2i(t.JG);
     t.lUY = log2i(MT * t.KGW * p.d * S);  // 16-byte units per output tile row
-    dma_magic((uint32_t)t.kgt, &t.mkgt, &t.skgt);
-    dma_magic((uint32_t)t.nbt, &t.mnbt, &t.snbt);
+    div_magic((uint32_t)t.kgt, &t.mkgt, &t.skgt);
+    div_magic((uint32_t)t.nbt, &t.mnbt, &t.snbt);
   }
   if (p.layout == BSF) {
     t.ypitch = 16 * MT * t.KGW * p.d * S + 16;

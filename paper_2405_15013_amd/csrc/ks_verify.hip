@@ -178,8 +178,13 @@ bool verify_direct(Checker& ck, const Plan& pl) {
   for (int l0 = 0; l0 + CH <= p.c; l0 += CH) { chunks[nch][0] = l0; chunks[nch][1] = LP; ++nch; }
   if (S == 2 && p.c % CH) { chunks[nch][0] = p.c - 16; chunks[nch][1] = 4; ++nch; }
   if (nch == 0) return ck.fail("no chunk covers c", p.c);
-  for (int item = 0; item < t.items && ck.err.empty(); ++item)
-    if (!verify_item(ck, direct_item(p, t, V, MT, item), strided, V, MT, S, chunks, nch)) return false;
+  for (int item = 0; item < t.items && ck.err.empty(); ++item) {
+    // The kernels decode items with multiply-shift divisions: same item.
+    const DItem a1 = direct_item(p, t, V, MT, item), a2 = direct_item_fast(p, t, V, MT, item);
+    if (a1.i != a2.i || a1.j0 != a2.j0 || a1.k0 != a2.k0 || a1.beta0 != a2.beta0)
+      return ck.fail("fast item decode differs", item);
+    if (!verify_item(ck, a1, strided, V, MT, S, chunks, nch)) return false;
+  }
   return ck.err.empty();
 }
 
