@@ -56,21 +56,21 @@ bool plan_direct(const Problem& p, bool al16, Plan* pl) {
   const int span = p.layout == BSL ? 16 * V : 16;
   const int64_t nbt = (p.batch + span - 1) / span;
   const int64_t per_k = nbt * p.a * (p.layout == BSL ? p.d : p.d / V);
-  // Largest MT that still leaves >= 2048 wavefronts (8 per CU); otherwise the
-  // MT giving the most wavefronts.
+  // Largest MT that still leaves >= 768 wavefronts (three per CU); otherwise
+  // the MT giving the most wavefronts.  Fewer k-groups mean fewer re-reads of
+  // each X tile, which measured worth more than extra wavefronts down to
+  // about three per CU.
   int best = 0;
   for (int mt = mt_max(s, p.layout, V); mt >= 1; --mt) {
     if (kt % mt) continue;
     best = mt;
-    if (per_k * (kt / mt) >= 2048) break;
+    if (per_k * (kt / mt) >= 768) break;
   }
   const int64_t items = per_k * (kt / best);
-  // Wavefronts per workgroup: 4 for large problems; fewer spread small ones
-  // over more CUs, but never fewer than the k-groups (up to 4) that share an X
-  // tile, so those read it through the same CU's caches.
-  int waves = items >= 4096 ? 4 : (items >= 1024 ? 2 : 1);
-  const int kg = kt / best;
-  if (waves < kg) waves = kg < 4 ? kg : 4;
+  // Four wavefronts per workgroup at every size: consecutive items (the
+  // k-groups of one X tile first) share a CU's caches, and spreading small
+  // problems over more, smaller workgroups measured slower.
+  const int waves = 4;
   const int64_t grid = (items + waves - 1) / waves;
   if (items > 0x7fffffff || grid > 0x7fffffff) return false;
   pl->variant = V_DIRECT;

@@ -189,13 +189,17 @@ struct DmaChoice {
   int64_t tiles, lds;
 };
 // Preference: at most 64 KB of LDS (two workgroups per CU), then enough tiles
-// for the chip (1024), then the most batch rows per K operand (NT: K is read
+// for one per CU (256), then the most batch rows per K operand (NT: K is read
 // from L2 once per 16*NT rows), then the fewest re-reads of X (k-group
-// tiles), then the largest MT, then the deeper MFMA (LP).
+// tiles), then the largest MT, then the deeper MFMA (LP).  Asking for more
+// tiles than CUs (smaller tiles, more k-group tiles) measured slower over the
+// pattern sweep: the extra K and X re-reads cost more than the parallelism.
 constexpr int64_t kDmaLdsPref = 64 * 1024;
+constexpr int64_t kDmaTileTarget = 256;
 bool dma_better(const DmaChoice& c, const DmaChoice& b) {
   if ((c.lds <= kDmaLdsPref) != (b.lds <= kDmaLdsPref)) return c.lds <= kDmaLdsPref;
-  const int64_t tc = c.tiles < 1024 ? c.tiles : 1024, tb = b.tiles < 1024 ? b.tiles : 1024;
+  const int64_t tc = c.tiles < kDmaTileTarget ? c.tiles : kDmaTileTarget;
+  const int64_t tb = b.tiles < kDmaTileTarget ? b.tiles : kDmaTileTarget;
   if (tc != tb) return tc > tb;
   if (c.nt != b.nt) return c.nt > b.nt;
   if (c.kgt != b.kgt) return c.kgt < b.kgt;

@@ -12,7 +12,9 @@ DMA_SHAPES = ([s for s in MFMA_SHAPES if s[3] <= 16]
                  (1, 16, 16, 1), (2, 32, 48, 2), (8, 128, 96, 1)])
 
 # Batch 4096 shapes whose DMA plans take 2 or 4 row groups per wavefront (NT),
-# 16x16x16 stages of 16-bit types with c % 32 == 0, strided and contiguous.
+# 16x16x16 stages of 16-bit types with c % 32 == 0, strided and contiguous, and
+# whose register-direct plans take 2 or 4 M-tiles per wavefront (d = 1).
 DMA_ROW_GROUP_SHAPES = [(1, 128, 16, 16), (4, 128, 32, 4), (2, 128, 32, 8), (8, 128, 16, 4), (8, 128, 32, 4),
                         (4, 128, 16, 4), (2, 64, 64, 16), (4, 128, 16, 8), (4, 128, 64, 1), (8, 64, 32, 2),
-                        (2, 48, 64, 1), (8, 128, 16, 2)]
+                        (2, 48, 64, 1), (8, 128, 16, 2), (1, 16, 16, 4), (1, 16, 32, 4), (1, 64, 32, 8),
+                        (1, 128, 32, 4), (1, 128, 16, 1), (2, 128, 16, 1)]
