@@ -323,6 +323,10 @@ __global__ __launch_bounds__(256) void ks_direct_c_kernel(Problem p, DirectTile 
 // 16-byte fp32 or 8-byte 16-bit pieces.
 constexpr int kDirectVec = 4;
 
+// Batch entries per lane of the batch-size-last kernels for 16-bit storage:
+// 8 (one 16-byte vector per row of X or Y) when the batch is a multiple of 8.
+constexpr int kDirectVecBsl16 = 8;
+
 // Largest M-tile count per wave for a (storage type, layout, V) instance set.
 constexpr int direct_mt_max(int esize, int layout, int V) {
   return esize == 4 ? ((layout == BSL || V <= 2) ? 4 : 2) : ((layout == BSL || V <= 2) ? 4 : 2);
@@ -370,7 +374,11 @@ template <typename T>
 hipError_t launch_direct_type(const Problem& p, const DirectTile& t, int V, bool strided, int mt, unsigned grid,
                               hipStream_t s) {
   if (p.layout == BSL) {
-    if (V != kDirectVec || strided) return hipErrorInvalidValue;
+    if (strided) return hipErrorInvalidValue;
+    if constexpr (sizeof(T) == 2) {
+      if (V == kDirectVecBsl16) return launch_direct_mt<T, BSL, kDirectVecBsl16, false>(p, t, mt, grid, s);
+    }
+    if (V != kDirectVec) return hipErrorInvalidValue;
     return launch_direct_mt<T, BSL, kDirectVec, false>(p, t, mt, grid, s);
   }
   if (strided) {

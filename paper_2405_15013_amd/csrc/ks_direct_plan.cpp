@@ -44,7 +44,9 @@ bool plan_direct(const Problem& p, bool al16, Plan* pl) {
   int V;
   bool strided = false;
   if (p.layout == BSL) {
-    V = vec;
+    // 16-bit storage: 8 batch entries per lane (16-byte loads and stores)
+    // when the batch allows it (kDirectVecBsl16 in ks_direct.h).
+    V = (s == 2 && p.batch % 8 == 0) ? 8 : vec;
     if (p.batch % V) return false;
   } else {
     V = p.d < vec ? p.d : vec;

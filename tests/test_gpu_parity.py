@@ -225,10 +225,11 @@ def test_sweep_ragged_batch_full(pattern, dtype, layout):
 @pytest.mark.parametrize("pattern", MFMA_SHAPES)
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
 @pytest.mark.parametrize("layout", ["bsf", "bsl"])
-@pytest.mark.parametrize("batch", [256, 72])
+@pytest.mark.parametrize("batch", [256, 72, 68])
 def test_direct_forced(pattern, dtype, layout, batch):
     """The register-direct MFMA kernel on every j-vector mode (d = 1, 2, 4 and
-    d > 4), c % 32 == 16 tails of the 16-bit path, and a ragged batch."""
+    d > 4), c % 32 == 16 tails of the 16-bit path, and ragged batches (68: the
+    16-bit batch-size-last path with 4 instead of 8 batch entries per lane)."""
     check(pattern, batch, dtype, layout, cfg=11, variant=VARIANTS["direct"], kdist="normal")
 
 
