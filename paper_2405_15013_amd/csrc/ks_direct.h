@@ -263,8 +263,10 @@ __global__ __launch_bounds__(256) void ks_direct_kernel(Problem p, DirectTile t)
 // The same work item with the reduction length fixed at compile time: NCH
 // full chunks (plus the 16-bit tail) are fully unrolled and the loads of up to
 // PD chunks ahead are in flight while a chunk is multiplied, PD chosen so the
-// chunks in flight take about 64 VGPRs.  A wavefront's time is then about one
-// memory latency plus its MFMAs, instead of one latency per chunk.
+// chunks in flight take about 32 VGPRs (at least one chunk ahead).  A
+// wavefront's time is then about one memory latency plus its MFMAs, instead
+// of one latency per chunk; a deeper prefetch (64 VGPRs) measured slower for
+// fp32 (fewer resident wavefronts) and the same for 16-bit storage.
 template <typename T, int LAYOUT, int V, bool STRIDED, int MT, int NCH, bool TAIL>
 __global__ __launch_bounds__(256) void ks_direct_c_kernel(Problem p, DirectTile t) {
   constexpr int S = sizeof(T);
@@ -272,7 +274,7 @@ __global__ __launch_bounds__(256) void ks_direct_c_kernel(Problem p, DirectTile 
   constexpr int CH = 4 * LP;
   using Chunk = DChunk<T, LAYOUT, V, STRIDED, MT, LP>;
   constexpr int R = Chunk::NXW + MT * Chunk::VK * Chunk::KW;  // VGPRs of one chunk
-  constexpr int PD0 = 64 / R;
+  constexpr int PD0 = 32 / R;
   constexpr int PD = NCH <= 1 ? 0 : (PD0 < 1 ? 1 : (PD0 > NCH - 1 ? NCH - 1 : PD0));
   const int lane = threadIdx.x & 63;
   const int item = blockIdx.x * t.waves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);

@@ -269,8 +269,8 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
     case V_DMA:
       // DMA instructions per wavefront per stage: 16*rs rows of lch*d*esize
       // bytes over four wavefronts of 64 16-byte lanes.
-      snprintf(buf, sizeof buf, "ks_dma_kernel<%s,%s,%d,%d,%d,%d>", t, pl.unroll ? "true" : "false", pl.waves_m,
-               pl.cps, (int)(pl.rs * pl.nt * pl.lch * p.d * (p.dtype == F32 ? 4 : 2) / 256), pl.nt);
+      snprintf(buf, sizeof buf, "ks_dma_kernel<%s,%d,%s,%d,%d,%d,%d>", t, pl.vec, pl.unroll ? "true" : "false",
+               pl.waves_m, pl.cps, (int)(pl.rs * pl.nt * pl.lch * p.d * (p.dtype == F32 ? 4 : 2) / 256), pl.nt);
       break;
     default: snprintf(buf, sizeof buf, "?");
   }

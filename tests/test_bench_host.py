@@ -91,3 +91,30 @@ def test_traffic_record_needs_current_sources(tmp_path, monkeypatch):
     assert bench.traffic_record(k, 1)["traffic_bytes_per_launch"] == 123.0
     assert bench.traffic_record(k, 2) is None
     assert bench.traffic_record("ks_y_kernel<float>", 1) is None
+
+
+def test_plan_kernel_names_are_library_symbols():
+    """The kernel= field of ks_plan_describe names a kernel instance that the
+    library contains (profiler summaries and counter passes select dispatches
+    by that name), for every variant the automatic planner picks on a sample
+    of the sweep."""
+    import shutil
+    import subprocess
+    import pytest
+    import paper_2405_15013_amd as ks
+    nm = shutil.which("nm")
+    if nm is None or not os.path.exists(ks.library_path()):
+        pytest.skip("needs nm and the built library")
+    out = subprocess.run([nm, "-C", ks.library_path()], capture_output=True, text=True, check=True).stdout
+    syms = {line.split(" ", 2)[2].replace(" ", "").split("(")[0].replace("voidks::", "")
+            for line in out.splitlines() if " ks::ks_" in line and "__device_stub" not in line}
+    seen = set()
+    for p in bench.sweep_patterns()[::9] + [(2, 4, 4, 2), (16, 2, 2, 32), (3, 5, 7, 2)]:
+        for layout in ("bsf", "bsl"):
+            for dtype in ("f32", "bf16"):
+                for batch in (4096, 25088, 100):
+                    name = bench.plan_field(ks.ks_plan_describe(*p, batch, layout, dtype), "kernel")
+                    seen.add(name)
+    missing = sorted(n for n in seen if n not in syms)
+    assert not missing, missing[:5]
+    assert any(n.startswith("ks_dma_kernel<") for n in seen) and any(n.startswith("ks_direct_c_kernel<") for n in seen)
