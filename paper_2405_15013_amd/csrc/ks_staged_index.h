@@ -219,6 +219,12 @@ KS_HD int dma_op_byte(const Problem& p, const SItem& it, int LP, int V, bool str
   return ((l0 + LP * g) * p.d + it.j0) * esize + q * pe * esize;
 }
 
+// Stage buffers the DMA kernel uses for nst stages of l: three (stage s is
+// multiplied while s+1 and s+2 are in flight), or one per stage when there
+// are fewer; with one or two stages no DMA targets the third buffer, so it is
+// not allocated (more workgroups fit in a CU's LDS).
+KS_HD int dma_stage_buffers(int nst) { return nst < 3 ? nst : 3; }
+
 // Tile and work item of the DMA kernel: staged_tile and staged_item computed
 // with the multiply-shift divisions and the power-of-two shifts above (the
 // plan verifier checks both against the plain forms for every tile).

@@ -67,12 +67,13 @@ StagedTile staged_tile_of(const Problem& p, const Plan& pl) {
   t.skgt = t.snbt = 0;
   t.lds = 2 * t.stage;
   if (pl.variant == V_DMA) {
-    // Unpadded, swizzled rows of UR units; three stage buffers.
+    // Unpadded, swizzled rows of UR units; three stage buffers, or one per
+    // stage when there are fewer stages (dma_stage_buffers).
     t.UR = t.LCH * p.d * S / 16;
     t.pitch = t.UR * 16;
     t.stage = 16 * t.RS * t.NT * t.pitch;
     t.UD = t.stage / 16 / (64 * t.W);
-    t.lds = 3 * t.stage;
+    t.lds = dma_stage_buffers(p.c / t.LCH) * t.stage;
     auto log2i = [](int v) { int l = 0; while ((1 << l) < v) ++l; return l; };
     t.lUR = log2i(t.UR);
     t.lRS = log2i(t.RS);
@@ -240,7 +241,8 @@ bool plan_dma(const Problem& p, bool al16, Plan* pl) {
           if (ud != 2 && ud != 4 && ud != 8) continue;
           const int64_t stage = units * 16;
           const int64_t ytile = 16 * rs * nt * ((int64_t)16 * mt * kgw * p.d * S + 16);
-          const int64_t lds = 3 * stage > ytile ? 3 * stage : ytile;
+          const int64_t sbuf = dma_stage_buffers(p.c / CH) * stage;
+          const int64_t lds = sbuf > ytile ? sbuf : ytile;
           if (lds > kMaxLds) continue;
           const int kgt = kgroups / kgw;
           const int span = 16 * rs * nt;

@@ -386,7 +386,16 @@ bool verify_dma(Checker& ck, const Plan& pl) {
       (t.UD != 2 && t.UD != 4 && t.UD != 8))
     return ck.fail("stage is not a whole number of DMA instructions per wavefront", t.stage);
   if ((int)pl.grid != t.tiles || (int)pl.block != 64 * t.W) return ck.fail("grid does not match the tiles", pl.grid);
-  if (pl.lds_bytes != t.lds || t.lds < 3 * t.stage) return ck.fail("LDS allocation does not hold three stages", t.lds);
+  // The kernel's stage s reads buffer s % 3 and the DMAs of stage s + 2
+  // (issued only when s + 2 < nst) write buffer (s + 2) % 3: buffers
+  // 0 .. min(nst, 3) - 1 are touched.
+  {
+    const int nst_v = p.c / CH;
+    int top = 0;
+    for (int s = 0; s < nst_v; ++s) top = std::max(top, s % 3);
+    if (pl.lds_bytes != t.lds || t.lds < (int64_t)(top + 1) * t.stage || dma_stage_buffers(nst_v) != top + 1)
+      return ck.fail("LDS allocation does not hold the stage buffers the kernel touches", t.lds);
+  }
   if (t.lds < 16 * t.RS * t.NT * t.ypitch) return ck.fail("LDS allocation does not hold the output tile", t.lds);
   if (t.remap && t.tiles % 8) return ck.fail("XCD remap needs a multiple of 8 tiles", t.tiles);
   const int pe = direct_x_piece_elems(BSF, strided, LP, V, S), np = LP * V / pe, pb = pe * S;
