@@ -1,7 +1,8 @@
 // Planner and launcher of the register-direct MFMA kernels (ks_direct.h).
 //
-// A plan fixes the vector width V (4 elements along the batch in BSL; the
-// j-run min(d, 4) in BSF), the number MT of 16-row M-tiles per wavefront,
+// A plan fixes the vector width V (along the batch in BSL: 8 elements for
+// 16-bit storage when the batch allows it, else 4; the j-run min(d, 4) in
+// BSF), the number MT of 16-row M-tiles per wavefront,
 // and the wavefronts per workgroup.  MT trades X re-reads (b / (16*MT)
 // wavefronts read the same X tile) against registers and parallelism.
 #include "ks_direct_index.h"

@@ -191,9 +191,10 @@ struct DmaChoice {
 };
 // Preference: at most 64 KB of LDS (two workgroups per CU; see dma_lds_pref
 // for the one exception), then enough tiles
-// for one per CU (256), then the most batch rows per K operand (NT: K is read
+// for one per CU (256), then the deeper MFMA (LP: 16x16x32 steps for 16-bit
+// types when c allows), then the most batch rows per K operand (NT: K is read
 // from L2 once per 16*NT rows), then the fewest re-reads of X (k-group
-// tiles), then the largest MT, then the deeper MFMA (LP).  Asking for more
+// tiles), then the largest MT.  Asking for more
 // tiles than CUs (smaller tiles, more k-group tiles) measured slower over the
 // pattern sweep: the extra K and X re-reads cost more than the parallelism.
 constexpr int64_t kDmaLdsPref = 64 * 1024;
@@ -211,10 +212,10 @@ bool dma_better(const DmaChoice& c, const DmaChoice& b, int64_t lds_pref) {
   const int64_t tc = c.tiles < kDmaTileTarget ? c.tiles : kDmaTileTarget;
   const int64_t tb = b.tiles < kDmaTileTarget ? b.tiles : kDmaTileTarget;
   if (tc != tb) return tc > tb;
+  if (c.lp != b.lp) return c.lp > b.lp;
   if (c.nt != b.nt) return c.nt > b.nt;
   if (c.kgt != b.kgt) return c.kgt < b.kgt;
-  if (c.mt != b.mt) return c.mt > b.mt;
-  return c.lp > b.lp;
+  return c.mt > b.mt;
 }
 bool plan_dma(const Problem& p, bool al16, Plan* pl) {
   if (!al16 || p.layout != BSF || p.b % 16 || p.c % 16) return false;
