@@ -601,6 +601,10 @@ def main():
             for dt in ("f32", "bf16") for lay in ("bsf", "bsl") for B in (4096, 25088)
             if any(r["dtype"] == dt and r["layout"] == lay and r["batch"] == B for r in points)},
         "roofline": roofline,
+        "top_kernels": [{"kernel": k, "share_of_sweep_time": v["t"] / sum(x["t"] for x in per_k.values()),
+                         "points": v["points"], "avg_launch_us": v["t"] / v["calls"] * 1e6,
+                         "gbps": v["bytes"] / v["t"] / 1e9}
+                        for k, v in sorted(per_k.items(), key=lambda kv: -kv[1]["t"])[:5]],
         "families": families,
     }
     if not args.no_cpu_baseline and args.kernel is None:
