@@ -438,7 +438,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=1)
     ap.add_argument("--sample", type=int, default=1,
                     help="time a seeded 1/S subset of the sweep points (1 = all 5600)")
-    ap.add_argument("--points-out", default=os.path.join(ROOT, "gpurun_out", "bench_points.jsonl"))
+    ap.add_argument("--points-out", default=None,
+                    help="also write every timed point as one JSON line to this file")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-families", action="store_true")
     ap.add_argument("--variant", type=int, default=-1,
@@ -473,7 +474,8 @@ def main():
         return
     t_start = time.time()
     run = Runner(args.steps, args.warmup, eager=args.eager)
-    os.makedirs(os.path.dirname(args.points_out) or ".", exist_ok=True)
+    if args.points_out:
+        os.makedirs(os.path.dirname(args.points_out) or ".", exist_ok=True)
     pats = sweep_patterns()
     grid = [(dtype, batch, layout, p) for dtype in ("f32", "bf16") for batch in (4096, 25088)
             for layout in ("bsf", "bsl") for p in pats]
@@ -481,7 +483,7 @@ def main():
     keep = set(int(k) for k in keep)
     points = []
     skipped = 0
-    with open(args.points_out, "w") as fout:
+    with open(args.points_out or os.devnull, "w") as fout:
         run.ks.ks_force_variant(args.variant if args.variant >= 0 else None)
         for idx, (dtype, batch, layout, p) in enumerate(grid):
             if idx not in keep:
