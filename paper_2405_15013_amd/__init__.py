@@ -213,44 +213,104 @@ def _check_tensor(t, name):
         raise ValueError("%s must be contiguous" % name)
 
 
+def _check_values(kv, pattern, dtype, device, name="K_values"):
+    """The packed values of a factor: a*d*b*c contiguous elements of the
+    storage dtype on the same device (the library reads exactly that many)."""
+    a, b, c, d = pattern
+    _check_tensor(kv, name)
+    if kv.dtype != dtype:
+        raise TypeError("%s has dtype %s, expected %s" % (name, kv.dtype, dtype))
+    if kv.device != device:
+        raise ValueError("%s is on %s, expected %s" % (name, kv.device, device))
+    if kv.numel() != a * b * c * d:
+        raise ValueError("%s has %d elements, pattern %s needs a*b*c*d = %d"
+                         % (name, kv.numel(), tuple(pattern), a * b * c * d))
+
+
+def _check_batch(X, N, lay):
+    """Batch size of an input of width N in layout `lay` (2-D tensors must
+    have the layout's shape; flat ones any multiple of N)."""
+    if X.numel() % N:
+        raise ValueError("X has %d elements, not a multiple of N = %d" % (X.numel(), N))
+    batch = X.numel() // N
+    want = (batch, N) if lay == BSF else (N, batch)
+    if X.dim() == 2 and tuple(X.shape) != want:
+        raise ValueError("X has shape %s, expected %s" % (tuple(X.shape), want))
+    if X.dim() not in (1, 2):
+        raise ValueError("X must be 1-D or 2-D, got %d dimensions" % X.dim())
+    return batch
+
+
+def _check_out(out, shape, X):
+    """A caller-supplied output: contiguous, of X's dtype and device, with
+    exactly batch*M elements (the library writes all of them)."""
+    _check_tensor(out, "out")
+    if out.dtype != X.dtype:
+        raise TypeError("out has dtype %s, expected %s" % (out.dtype, X.dtype))
+    if out.device != X.device:
+        raise ValueError("out is on %s, expected %s" % (out.device, X.device))
+    n = shape[0] * shape[1]
+    if out.numel() != n or (out.dim() == 2 and tuple(out.shape) != tuple(shape)):
+        raise ValueError("out has shape %s, expected %s" % (tuple(out.shape), tuple(shape)))
+
+
 def matmul(X, K_values, pattern, layout="bsl", out=None):
-    """Allocate Y and run ks_matmul.  X is (batch, a*c*d) for BSF or (a*c*d, batch)
-    for BSL; K_values is (a*d, b, c) or flat; all three share one dtype."""
+    """Allocate Y (unless `out` is given) and run ks_matmul.  X is
+    (batch, a*c*d) for BSF or (a*c*d, batch) for BSL; K_values is (a*d, b, c)
+    or flat; all three share one dtype and device.  Every argument is checked
+    on the host before the call (the C ABI sees only pointers)."""
     import torch
     a, b, c, d = (int(v) for v in pattern)
     lay = _code(layout, _LAYOUTS, "layout")
     _check_tensor(X, "X")
-    _check_tensor(K_values, "K_values")
-    if X.dtype != K_values.dtype:
-        raise TypeError("X and K_values must share a dtype")
+    dt = _dtype_of(X)
+    _check_values(K_values, (a, b, c, d), X.dtype, X.device)
     N, M = a * c * d, a * b * d
-    if X.numel() % N:
-        raise ValueError("X has %d elements, not a multiple of N = %d" % (X.numel(), N))
-    batch = X.numel() // N
-    if X.dim() == 2 and X.shape != ((batch, N) if lay == BSF else (N, batch)):
-        raise ValueError("X has shape %s, expected %s" % (tuple(X.shape), (batch, N) if lay == BSF else (N, batch)))
+    batch = _check_batch(X, N, lay)
     shape = (batch, M) if lay == BSF else (M, batch)
     if out is None:
         out = torch.empty(shape, dtype=X.dtype, device=X.device)
-    ks_matmul(a, b, c, d, K_values, X, out, batch, lay, _dtype_of(X))
+    else:
+        _check_out(out, shape, X)
+    ks_matmul(a, b, c, d, K_values, X, out, batch, lay, dt)
     return out
 
 
 def chain(X, factors, layout="bsl", out=None, workspace=None):
-    """Y = X (K_1 ... K_L)^T; factors = [((a,b,c,d), K_values), ...] in product order."""
+    """Y = X (K_1 ... K_L)^T; factors = [((a,b,c,d), K_values), ...] in product
+    order (K_L is applied first).  Checks every factor's values, the input
+    width, `out` and the workspace size on the host before the call."""
     import torch
     lay = _code(layout, _LAYOUTS, "layout")
+    if len(factors) < 1:
+        raise ValueError("a chain needs at least one factor")
     _check_tensor(X, "X")
-    (a1, b1, c1, d1), _ = factors[0]
-    (aL, bL, cL, dL), _ = factors[-1]
-    N, M = aL * cL * dL, a1 * b1 * d1
-    batch = X.numel() // N
     dt = _dtype_of(X)
+    pats = [tuple(int(v) for v in p) for p, _ in factors]
+    for q, (p, kv) in enumerate(factors):
+        _check_values(kv, pats[q], X.dtype, X.device, "K_values of factor %d" % q)
+    for q in range(len(pats) - 1):
+        a0, b0, c0, d0 = pats[q]
+        a1, b1, c1, d1 = pats[q + 1]
+        if a0 * c0 * d0 != a1 * b1 * d1:
+            raise ValueError("factors %d and %d do not compose: a*c*d = %d, next a*b*d = %d"
+                             % (q, q + 1, a0 * c0 * d0, a1 * b1 * d1))
+    (a1, b1, c1, d1), (aL, bL, cL, dL) = pats[0], pats[-1]
+    N, M = aL * cL * dL, a1 * b1 * d1
+    batch = _check_batch(X, N, lay)
     ws_bytes = ks_chain_workspace_bytes(factors, batch, dt)
-    if workspace is None and ws_bytes > 0:
-        workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=X.device)
+    if workspace is None:
+        if ws_bytes > 0:
+            workspace = torch.empty(ws_bytes, dtype=torch.uint8, device=X.device)
+    else:
+        _check_tensor(workspace, "workspace")
+        if workspace.device != X.device:
+            raise ValueError("workspace is on %s, expected %s" % (workspace.device, X.device))
+    shape = (batch, M) if lay == BSF else (M, batch)
     if out is None:
-        out = torch.empty((batch, M) if lay == BSF else (M, batch), dtype=X.dtype, device=X.device)
+        out = torch.empty(shape, dtype=X.dtype, device=X.device)
+    else:
+        _check_out(out, shape, X)
     ws_avail = workspace.numel() * workspace.element_size() if workspace is not None else 0
     ks_chain(factors, X, out, batch, lay, dt, workspace, ws_avail)
     return out

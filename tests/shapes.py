@@ -18,3 +18,29 @@ DMA_ROW_GROUP_SHAPES = [(1, 128, 16, 16), (4, 128, 32, 4), (2, 128, 32, 8), (8, 
                         (4, 128, 16, 4), (2, 64, 64, 16), (4, 128, 16, 8), (4, 128, 64, 1), (8, 64, 32, 2),
                         (2, 48, 64, 1), (8, 128, 16, 2), (1, 16, 16, 4), (1, 16, 32, 4), (1, 64, 32, 8),
                         (1, 128, 32, 4), (1, 128, 16, 1), (2, 128, 16, 1)]
+
+
+def sweep_patterns():
+    """The benchmark's pattern sweep: a in {1,2,4,8}, b, c in
+    {16,32,48,64,96,128}, d in {1,2,4,8,16}, a*b*d <= 8192 and a*c*d <= 8192
+    (700 patterns)."""
+    return [(a, b, c, d) for a in (1, 2, 4, 8) for b in (16, 32, 48, 64, 96, 128) for c in (16, 32, 48, 64, 96, 128)
+            for d in (1, 2, 4, 8, 16) if a * b * d <= 8192 and a * c * d <= 8192]
+
+
+BUTTERFLY = [(2 ** (l - 1), 2, 2, 2 ** (10 - l)) for l in range(1, 11)]
+MONARCH = [(1, 32, 32, 32), (32, 32, 32, 1)]
+MLP = [(6, 64, 16, 8), (6, 16, 64, 8)]
+
+
+def bench_points():
+    """Every (pattern, batch, dtype, layout) single-factor call the benchmark
+    makes: the 5600 sweep points, then the tiny, butterfly, Monarch and
+    Transformer-MLP workloads (the chains run the same factors)."""
+    pts = [(p, batch, dtype, layout) for dtype in ("f32", "bf16") for batch in (4096, 25088)
+           for layout in ("bsf", "bsl") for p in sweep_patterns()]
+    pts += [((2, 4, 4, 2), 32, "f32", layout) for layout in ("bsf", "bsl")]
+    pts += [(p, 4096, "f32", layout) for p in BUTTERFLY for layout in ("bsf", "bsl")]
+    pts += [(p, 16384, dtype, layout) for p in MONARCH for dtype in ("f32", "bf16") for layout in ("bsf", "bsl")]
+    pts += [(p, 25088, dtype, layout) for p in MLP for dtype in ("f32", "bf16") for layout in ("bsf", "bsl")]
+    return pts

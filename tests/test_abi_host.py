@@ -100,3 +100,13 @@ def test_plan_describe_picks_expected_families():
     # large odd blocks fall back to the generic kernel
     assert "name=generic" in ks.ks_plan_describe(1, 17, 19, 3, 64, "bsf", "f32")
     assert ks.ks_plan_describe(1, 4, 4, 1, 0, "bsf", "f32") == "empty"
+
+
+def test_wrappers_reject_host_tensors():
+    """The tensor-level wrappers take device tensors only (there is no CPU
+    path); the check runs before the library is called."""
+    import torch
+    with pytest.raises(ValueError):
+        ks.matmul(torch.randn(16, 8), torch.randn(64), (2, 4, 4, 2), "bsl")
+    with pytest.raises(ValueError):
+        ks.chain(torch.randn(16, 8), [((2, 4, 4, 2), torch.randn(64))], "bsl")

@@ -9,8 +9,9 @@ fix, none of which re-types the oracle's own index formula.
   * special cases: a = d = 1 is a dense GEMM (Appendix B.1, Table 5 "Dense"
     row); b = c = 1 is a diagonal scaling; identity blocks give Y = X;
   * Figure 4 index sets (tests/golden/fig4_index_sets.json);
-  * two independent formulations written from Appendix A.1 (the batched-GEMM
-    reshape / bmm / reshape steps and the 4-D tensor contraction);
+  * two independent formulations: the permutation route of Section 2.1 with
+    perfect-shuffle matrices built from their definition in Appendix C, and
+    the 4-D tensor contraction of Appendix A.1;
   * chains equal the product of the dense factors (Appendix B.1, Table 5), and
     the dyadic butterfly chain with all blocks [[1,1],[1,-1]] is the
     Sylvester-Hadamard matrix (scipy.linalg.hadamard), the real analogue of the
@@ -141,14 +142,34 @@ def test_figure4_index_sets():
     assert sorted(seen_c) == list(range(a * c * d))
 
 
-def bmm_formulation(pattern, kv, x):
-    """Appendix A.1 batched-GEMM route: permute X, batched matmul with the
-    (ad, b, c) blocks, permute back (written from the described steps)."""
+def perfect_shuffle(p, q):
+    """The (p, q) perfect-shuffle permutation matrix of Appendix C: the rows of
+    the r x r identity (r = p*q) taken in the order of the index sets
+    R_0, R_1, ..., R_{q-1}, with R_i = {i + q*t : t < p}."""
+    r = p * q
+    order = [i + q * t for i in range(q) for t in range(p)]
+    return np.eye(r)[order, :]
+
+
+def permutation_formulation(pattern, kv, x):
+    """The permutation route of Section 2.1 (Algorithm 1) with the perfect
+    shuffles of Appendix C: K = L * BD * R^T, where BD is block-diagonal with
+    the a*d dense b x c blocks in (i*d + j) order and L, R are Kronecker
+    products of identities and perfect shuffles built from their definition.
+    Y = X K^T is then three dense products: permute the columns of X, multiply
+    by the block-diagonal matrix, permute back.
+
+    Which shuffle goes on which side: with the literal definition, taking the
+    (d, b) shuffle reads a vector laid out block-major (j*b + k) in the
+    interleaved order k*d + j of the rows of block (i, j), so the pair is
+    I_a (x) P_{d,b} on the left and I_a (x) P_{d,c} on the right (the
+    transposes of the (b, d) and (c, d) shuffles; any pair of permutations
+    that block-diagonalises K gives the same product)."""
     a, b, c, d = pattern
-    B = x.shape[0]
-    xp = x.reshape(B, a, c, d).transpose(0, 1, 3, 2).reshape(B, a * d, c).transpose(1, 0, 2)  # (ad, B, c)
-    yp = np.matmul(xp, np.transpose(kv, (0, 2, 1)))  # (ad, B, b)
-    return yp.transpose(1, 0, 2).reshape(B, a, d, b).transpose(0, 1, 3, 2).reshape(B, a * b * d)
+    L = np.kron(np.eye(a), perfect_shuffle(d, b))
+    R = np.kron(np.eye(a), perfect_shuffle(d, c))
+    BD = scipy.linalg.block_diag(*[np.asarray(kv[t], dtype=np.float64) for t in range(a * d)])
+    return ((x @ R) @ BD.T) @ L.T
 
 
 def contraction_formulation(pattern, kv, x):
@@ -164,7 +185,7 @@ def contraction_formulation(pattern, kv, x):
 def test_independent_formulations(pattern):
     kv, x = rand_case(pattern, 9, seed=13)
     y = oracle.matmul(pattern, kv, x, 9, "bsf")
-    np.testing.assert_allclose(y, bmm_formulation(pattern, kv, x), rtol=1e-12, atol=1e-12)
+    np.testing.assert_allclose(y, permutation_formulation(pattern, kv, x), rtol=1e-12, atol=1e-12)
     np.testing.assert_allclose(y, contraction_formulation(pattern, kv, x), rtol=1e-12, atol=1e-12)
 
 
@@ -266,3 +287,23 @@ def test_inputs_rounding_is_rne():
     back = inputs.to_f64(bits, "bf16")
     np.testing.assert_array_equal(back, [1.0, 1 + 2.0 ** -6, -2.5, 0.0])
     np.testing.assert_array_equal(inputs.to_f64(inputs.round_to(v, "f16"), "f16"), np.float16(v).astype(np.float64))
+
+
+def test_perfect_shuffle_definition():
+    # (2, 3): reshape 0..5 into a 2 x 3 matrix row-major and read it by columns.
+    P = perfect_shuffle(2, 3)
+    np.testing.assert_array_equal(P @ np.arange(6), [0, 3, 1, 4, 2, 5])
+    # a permutation matrix whose transpose is the (q, p) shuffle
+    np.testing.assert_array_equal(P @ P.T, np.eye(6))
+    np.testing.assert_array_equal(P.T, perfect_shuffle(3, 2))
+
+
+@pytest.mark.parametrize("pattern", [(2, 3, 2, 3), (1, 4, 8, 2), (3, 5, 2, 1), (2, 2, 3, 4)])
+def test_shuffles_block_diagonalise_the_support(pattern):
+    """Appendix C: the support I_a (x) 1_{b x c} (x) I_d is a permutation of
+    I_{ad} (x) 1_{b x c} (ad dense diagonal blocks)."""
+    a, b, c, d = pattern
+    L = np.kron(np.eye(a), perfect_shuffle(d, b))
+    R = np.kron(np.eye(a), perfect_shuffle(d, c))
+    S = np.kron(np.kron(np.eye(a), np.ones((b, c))), np.eye(d))
+    np.testing.assert_array_equal(L.T @ S @ R, np.kron(np.eye(a * d), np.ones((b, c))))
