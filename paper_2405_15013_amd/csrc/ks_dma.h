@@ -283,13 +283,11 @@ void ks_dma_kernel(Problem p, StagedTile t) {
 template <typename T, int V, bool STRIDED, int MT, int LP, int UD, int NT>
 hipError_t launch_dma_inst(const Problem& p, const StagedTile& t, hipStream_t s) {
   if (t.lds > 64 * 1024) {
-    static bool raised = false;  // opt in to more than 64 KB of dynamic LDS, once per instance
-    if (!raised) {
-      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ks_dma_kernel<T, V, STRIDED, MT, LP, UD, NT>),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, kDmaMaxLds);
-      if (e != hipSuccess) return e;
-      raised = true;
-    }
+    // Opt in to more than 64 KB of dynamic LDS once per instance (a function-
+    // local static: initialised exactly once even with concurrent callers).
+    static const hipError_t raised = hipFuncSetAttribute(reinterpret_cast<const void*>(&ks_dma_kernel<T, V, STRIDED, MT, LP, UD, NT>),
+                                                         hipFuncAttributeMaxDynamicSharedMemorySize, kDmaMaxLds);
+    if (raised != hipSuccess) return raised;
   }
   hipLaunchKernelGGL((ks_dma_kernel<T, V, STRIDED, MT, LP, UD, NT>), dim3(t.tiles), dim3(256), t.lds, s, p, t);
   return hipGetLastError();

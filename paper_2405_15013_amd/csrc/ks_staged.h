@@ -247,13 +247,11 @@ template <typename T, int LAYOUT, int V, bool STRIDED, int MT, int CPS>
 hipError_t launch_staged_inst(const Problem& p, const StagedTile& t, hipStream_t s) {
   if (t.lds > 64 * 1024) {
     // Opt in to more than 64 KB of dynamic LDS (once per instance).
-    static bool raised = false;
-    if (!raised) {
-      hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&ks_staged_kernel<T, LAYOUT, V, STRIDED, MT, CPS>),
-                                         hipFuncAttributeMaxDynamicSharedMemorySize, kStagedMaxLds);
-      if (e != hipSuccess) return e;
-      raised = true;
-    }
+    // Opt in to more than 64 KB of dynamic LDS once per instance (a function-
+    // local static: initialised exactly once even with concurrent callers).
+    static const hipError_t raised = hipFuncSetAttribute(reinterpret_cast<const void*>(&ks_staged_kernel<T, LAYOUT, V, STRIDED, MT, CPS>),
+                                                         hipFuncAttributeMaxDynamicSharedMemorySize, kStagedMaxLds);
+    if (raised != hipSuccess) return raised;
   }
   hipLaunchKernelGGL((ks_staged_kernel<T, LAYOUT, V, STRIDED, MT, CPS>), dim3(t.tiles), dim3(64 * t.W), t.lds, s, p,
                      t);
