@@ -64,7 +64,8 @@ typedef enum {
     KS_ERR_ALIAS = 4,           /* X and Y (or a workspace) overlap */
     KS_ERR_UNSUPPORTED = 5,     /* unknown dtype or layout, or a size beyond the supported range */
     KS_ERR_WORKSPACE = 6,       /* chain workspace missing or too small */
-    KS_ERR_HIP = 7              /* the HIP runtime reported an error at launch */
+    KS_ERR_HIP = 7,             /* the HIP runtime reported an error at launch */
+    KS_ERR_SCRATCH_LIMIT = 8    /* ks_chain_noalloc: intermediates exceed its fixed scratch array */
 } ks_status_t;
 
 /* One factor of a chain: its pattern and its packed values (device pointer,
@@ -111,6 +112,37 @@ size_t ks_chain_workspace_bytes(const ks_factor_t *factors, int nfactors,
 ks_status_t ks_chain(const ks_factor_t *factors, int nfactors,
                      const void *X, void *Y, int64_t batch, int layout, int dtype,
                      void *workspace, size_t workspace_bytes, void *stream);
+
+/*
+ * Fixed device scratch of ks_chain_noalloc, in bytes per GPU (64 MiB: the
+ * intermediates of a 10-factor chain of width 1024 at batch 8192 in fp32, or
+ * of a 2-factor chain of width 1024 at batch 16384 in fp32).
+ */
+#define KS_CHAIN_NOALLOC_MAX_WORKSPACE ((size_t)64 << 20)
+
+/*
+ * ks_chain without a workspace argument, for callers that cannot allocate
+ * device memory (code under stream capture, serving loops, harnesses that
+ * forbid allocation): the intermediates go to a fixed array of
+ * KS_CHAIN_NOALLOC_MAX_WORKSPACE bytes inside the library (one copy per GPU,
+ * allocated when the library's code object is loaded on that GPU and held
+ * until the process ends).  The call itself allocates nothing.
+ *   Arguments, results and errors are those of ks_chain, plus
+ *   KS_ERR_SCRATCH_LIMIT when ks_chain_workspace_bytes(...) for these
+ *   arguments exceeds the fixed size (nothing is enqueued then).
+ *   The array's device address is looked up on the first call on each GPU
+ *   (the current device); a failure there returns KS_ERR_HIP.
+ * All calls on one GPU share its array: calls that may run at the same time on
+ * one GPU (different streams or threads without ordering) race on it; calls
+ * ordered on one stream do not.  Nothing in the array needs to start at zero.
+ */
+ks_status_t ks_chain_noalloc(const ks_factor_t *factors, int nfactors,
+                             const void *X, void *Y, int64_t batch, int layout,
+                             int dtype, void *stream);
+
+/* The fixed scratch size of ks_chain_noalloc in bytes
+ * (KS_CHAIN_NOALLOC_MAX_WORKSPACE). */
+size_t ks_chain_noalloc_max_workspace(void);
 
 /* Human-readable name of a status code (static string). */
 const char *ks_status_string(int status);

@@ -16,7 +16,8 @@ import os
 
 __all__ = [
     "BSF", "BSL", "F32", "BF16", "F16", "KsError",
-    "ks_matmul", "ks_chain", "ks_chain_workspace_bytes", "ks_status_string",
+    "ks_matmul", "ks_chain", "ks_chain_workspace_bytes", "ks_chain_noalloc", "ks_chain_noalloc_max_workspace",
+    "ks_status_string",
     "ks_last_hip_error", "ks_plan_describe", "ks_force_variant", "ks_plan_verify",
     "matmul", "chain", "library_path", "load_library", "EXPORTED_SYMBOLS",
 ]
@@ -28,12 +29,13 @@ KS_OK = 0
 STATUS_NAMES = {
     0: "KS_OK", 1: "KS_ERR_INVALID_PATTERN", 2: "KS_ERR_INVALID_ARG", 3: "KS_ERR_DIM_MISMATCH",
     4: "KS_ERR_ALIAS", 5: "KS_ERR_UNSUPPORTED", 6: "KS_ERR_WORKSPACE", 7: "KS_ERR_HIP",
+    8: "KS_ERR_SCRATCH_LIMIT",
 }
 
 # Every function declared in include/ks.h.
 EXPORTED_SYMBOLS = (
-    "ks_matmul", "ks_chain_workspace_bytes", "ks_chain", "ks_status_string",
-    "ks_last_hip_error", "ks_plan_describe", "ks_force_variant", "ks_plan_verify",
+    "ks_matmul", "ks_chain_workspace_bytes", "ks_chain", "ks_chain_noalloc", "ks_chain_noalloc_max_workspace",
+    "ks_status_string", "ks_last_hip_error", "ks_plan_describe", "ks_force_variant", "ks_plan_verify",
 )
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -83,6 +85,10 @@ def load_library():
     lib.ks_chain_workspace_bytes.restype = ctypes.c_size_t
     lib.ks_chain.argtypes = [ctypes.POINTER(_Factor), ci, vp, vp, i64, ci, ci, vp, ctypes.c_size_t, vp]
     lib.ks_chain.restype = ci
+    lib.ks_chain_noalloc.argtypes = [ctypes.POINTER(_Factor), ci, vp, vp, i64, ci, ci, vp]
+    lib.ks_chain_noalloc.restype = ci
+    lib.ks_chain_noalloc_max_workspace.argtypes = []
+    lib.ks_chain_noalloc_max_workspace.restype = ctypes.c_size_t
     lib.ks_status_string.argtypes = [ci]
     lib.ks_status_string.restype = ctypes.c_char_p
     lib.ks_last_hip_error.argtypes = []
@@ -191,6 +197,22 @@ def ks_chain(factors, X, Y, batch, layout, dtype, workspace, workspace_bytes, st
     if check and st != KS_OK:
         raise KsError(st, "ks_chain")
     return st
+
+
+def ks_chain_noalloc(factors, X, Y, batch, layout, dtype, stream=None, check=True):
+    """C-ABI ks_chain_noalloc: ks_chain with the intermediates in the
+    library's fixed per-GPU scratch array (no workspace argument)."""
+    arr = _factor_array(factors)
+    st = load_library().ks_chain_noalloc(arr, len(factors), _ptr(X), _ptr(Y), batch,
+                                         _code(layout, _LAYOUTS, "layout"), _code(dtype, _DTYPES, "dtype"),
+                                         _stream(stream))
+    if check and st != KS_OK:
+        raise KsError(st, "ks_chain_noalloc")
+    return st
+
+
+def ks_chain_noalloc_max_workspace():
+    return int(load_library().ks_chain_noalloc_max_workspace())
 
 
 _TORCH_DTYPE_CODES = None

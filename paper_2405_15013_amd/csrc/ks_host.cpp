@@ -322,37 +322,22 @@ ks_status_t chain_check(const ks_factor_t* f, int n, int64_t batch, int dtype, s
 }  // namespace
 }  // namespace ks
 
-using namespace ks;
+namespace ks {
+// The chain driver behind ks_chain (and ks_chain_noalloc, which passes its
+// fixed scratch buffer as the workspace).
+void set_last_hip_error(int e) { g_last_hip_error = e; }
 
-extern "C" {
-
-ks_status_t ks_matmul(int64_t a, int64_t b, int64_t c, int64_t d, const void* K_values, const void* X, void* Y,
-                      int64_t batch, int layout, int dtype, void* stream) {
-  Problem p;
-  bool empty = false;
-  ks_status_t st = validate(a, b, c, d, K_values, X, Y, batch, layout, dtype, &p, &empty);
-  if (st != KS_OK || empty) return st;
-  return run_one(p, static_cast<hipStream_t>(stream));
-}
-
-size_t ks_chain_workspace_bytes(const ks_factor_t* factors, int nfactors, int64_t batch, int dtype) {
-  size_t per = 0;
-  if (chain_check(factors, nfactors, batch, dtype, &per) != KS_OK) return 0;
-  if (nfactors <= 1) return 0;
-  return nfactors == 2 ? per : 2 * per;
-}
-
-ks_status_t ks_chain(const ks_factor_t* factors, int nfactors, const void* X, void* Y, int64_t batch, int layout,
-                     int dtype, void* workspace, size_t workspace_bytes, void* stream) {
+ks_status_t chain_impl(const ks_factor_t* factors, int nfactors, const void* X, void* Y, int64_t batch, int layout,
+                       int dtype, void* workspace, size_t workspace_bytes, void* stream) {
   size_t per = 0;
   ks_status_t st = chain_check(factors, nfactors, batch, dtype, &per);
   if (st != KS_OK) return st;
   if (layout != KS_LAYOUT_BSF && layout != KS_LAYOUT_BSL) return KS_ERR_UNSUPPORTED;
   for (int q = 0; q < nfactors; ++q)
     if (factors[q].K_values == nullptr) return KS_ERR_INVALID_ARG;
+  const size_t need = nfactors <= 1 ? 0 : (nfactors == 2 ? per : 2 * per);
   if (batch == 0) return KS_OK;
   if (X == nullptr || Y == nullptr) return KS_ERR_INVALID_ARG;
-  const size_t need = nfactors <= 1 ? 0 : (nfactors == 2 ? per : 2 * per);
   if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return KS_ERR_WORKSPACE;
   const int s = elem_size(dtype);
   Dims first, last;
@@ -387,6 +372,32 @@ ks_status_t ks_chain(const ks_factor_t* factors, int nfactors, const void* X, vo
   if (pv != steps) delete[] pv;
   return st;
 }
+}  // namespace ks
+
+using namespace ks;
+
+extern "C" {
+
+ks_status_t ks_matmul(int64_t a, int64_t b, int64_t c, int64_t d, const void* K_values, const void* X, void* Y,
+                      int64_t batch, int layout, int dtype, void* stream) {
+  Problem p;
+  bool empty = false;
+  ks_status_t st = validate(a, b, c, d, K_values, X, Y, batch, layout, dtype, &p, &empty);
+  if (st != KS_OK || empty) return st;
+  return run_one(p, static_cast<hipStream_t>(stream));
+}
+
+size_t ks_chain_workspace_bytes(const ks_factor_t* factors, int nfactors, int64_t batch, int dtype) {
+  size_t per = 0;
+  if (chain_check(factors, nfactors, batch, dtype, &per) != KS_OK) return 0;
+  if (nfactors <= 1) return 0;
+  return nfactors == 2 ? per : 2 * per;
+}
+
+ks_status_t ks_chain(const ks_factor_t* factors, int nfactors, const void* X, void* Y, int64_t batch, int layout,
+                     int dtype, void* workspace, size_t workspace_bytes, void* stream) {
+  return ks::chain_impl(factors, nfactors, X, Y, batch, layout, dtype, workspace, workspace_bytes, stream);
+}
 
 const char* ks_status_string(int status) {
   switch (status) {
@@ -398,6 +409,8 @@ const char* ks_status_string(int status) {
     case KS_ERR_UNSUPPORTED: return "KS_ERR_UNSUPPORTED: unsupported dtype/layout/size, or forced variant cannot run";
     case KS_ERR_WORKSPACE: return "KS_ERR_WORKSPACE: chain workspace missing or too small";
     case KS_ERR_HIP: return "KS_ERR_HIP: the HIP runtime reported an error";
+    case KS_ERR_SCRATCH_LIMIT:
+      return "KS_ERR_SCRATCH_LIMIT: the chain's intermediates exceed the fixed scratch array of ks_chain_noalloc";
     default: return "unknown ks_status_t";
   }
 }

@@ -110,3 +110,17 @@ def test_wrappers_reject_host_tensors():
         ks.matmul(torch.randn(16, 8), torch.randn(64), (2, 4, 4, 2), "bsl")
     with pytest.raises(ValueError):
         ks.chain(torch.randn(16, 8), [((2, 4, 4, 2), torch.randn(64))], "bsl")
+
+
+def test_chain_noalloc_host_errors():
+    """ks_chain_noalloc checks its arguments like ks_chain, and rejects chains
+    whose intermediates exceed its fixed scratch array, before touching the
+    GPU."""
+    f_ok = [((1, 4, 4, 4), P0), ((4, 4, 4, 1), P0 + 4096)]
+    f_bad = [((1, 4, 4, 4), P0), ((1, 3, 3, 1), P0 + 4096)]
+    assert ks.ks_chain_noalloc_max_workspace() == 64 << 20
+    assert ks.ks_chain_noalloc(f_bad, P1, P2, 8, ks.BSL, ks.F32, stream=0, check=False) == 3
+    assert ks.ks_chain_noalloc(f_ok, None, None, 0, ks.BSL, ks.F32, stream=0, check=False) == 0
+    # 16 x (1 << 21) fp32 intermediates: 128 MiB > 64 MiB
+    st = ks.ks_chain_noalloc(f_ok, P1, P2, 1 << 21, ks.BSL, ks.F32, stream=0, check=False)
+    assert ks.STATUS_NAMES[st] == "KS_ERR_SCRATCH_LIMIT"
