@@ -39,6 +39,20 @@ typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
+// Wait for the last MFMAs before the epilogue reads their accumulators.
+// The compiler's hazard recognizer inserts the wait states it believes an
+// MFMA result needs before another instruction reads it, and no more; one
+// change that let the packed bf16 conversion read the result of a 16x16x16
+// bf16 MFMA at exactly that minimum distance gave wrong first conversions,
+// varying from run to run.  This adds 16 wait states (two 8-cycle s_nop)
+// between the MFMAs and the epilogue (scheduling barriers keep the code on
+// each side), at a cost of 16 cycles per wavefront.
+__device__ __forceinline__ void mfma_results_settle() {
+  __builtin_amdgcn_sched_barrier(0);
+  asm volatile("s_nop 7\n\ts_nop 7" ::: "memory");
+  __builtin_amdgcn_sched_barrier(0);
+}
+
 // Streaming (nontemporal) loads: X is read exactly once per launch.
 template <typename V>
 __device__ __forceinline__ V ld_stream(const V* p) { return __builtin_nontemporal_load(p); }

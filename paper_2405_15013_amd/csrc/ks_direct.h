@@ -144,6 +144,7 @@ template <typename T, int LAYOUT, int V, bool STRIDED, int MT>
 __device__ __forceinline__ void direct_store(const Problem& p, const DItem& it, int n, int g,
                                              const f32x4 (&acc)[MT][V]) {
   constexpr int S = sizeof(T);
+  mfma_results_settle();
   if (!direct_lane_valid(p, it, V, n)) return;
   constexpr int YPE = (LAYOUT == BSL || STRIDED) ? V : (4 * V * S < 16 ? 4 * V : 16 / S);
   constexpr int YNP = 4 * V / YPE;
@@ -245,6 +246,7 @@ __global__ __launch_bounds__(256) void ks_direct_kernel(Problem p, DirectTile t)
       cur.mma(acc);
       if (more) cur = nxt;
     }
+    mfma_results_settle();  // before the paths join (the join copies the accumulators)
   }
   if constexpr (S == 2) {
     if (c % CH) {  // c % 32 == 16: last 16 values of l with the 16x16x16 step
@@ -254,6 +256,7 @@ __global__ __launch_bounds__(256) void ks_direct_kernel(Problem p, DirectTile t)
       DChunk<T, LAYOUT, V, STRIDED, MT, 4> tail;
       tail.load(xl, lstride, qstride, kl, kmstride, kestride, c - 16, ntx);
       tail.mma(acc);
+      mfma_results_settle();
     }
   }
 

@@ -239,6 +239,7 @@ void ks_dma_kernel(Problem p, StagedTile t) {
   }
 
   // Structured epilogue: accumulators -> LDS output tile -> contiguous runs.
+  mfma_results_settle();
   __syncthreads();  // every wavefront is done with the stage buffers
   char* ycell0 = smem + dma_y_lds_lane(p, t, si, MT, S, n, g);
 #pragma unroll

@@ -106,7 +106,6 @@ bool plan_valu_bsf(const Problem& p, bool al16, Plan* pl) {
 }  // namespace
 bool plan_direct(const Problem& p, bool al16, Plan* pl);
 bool plan_staged(const Problem& p, bool al16, Plan* pl);
-bool plan_stream(const Problem& p, bool al16, Plan* pl);
 bool plan_dma(const Problem& p, bool al16, Plan* pl);
 namespace {
 
@@ -117,7 +116,6 @@ bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
     case V_VALU_BSF: return plan_valu_bsf(p, al16, pl);
     case V_DIRECT: return plan_direct(p, al16, pl);
     case V_STAGED: return plan_staged(p, al16, pl);
-    case V_STREAM: return plan_stream(p, al16, pl);
     case V_DMA: return plan_dma(p, al16, pl);
     default: return false;
   }
@@ -186,7 +184,6 @@ hipError_t launch(const Problem& p, const Plan& pl, hipStream_t s) {
     case V_VALU_BSF: return launch_valu_bsf(p, pl, s);
     case V_DIRECT: return launch_direct(p, pl, s);
     case V_STAGED: return launch_staged(p, pl, s);
-    case V_STREAM: return launch_stream(p, pl, s);
     case V_DMA: return launch_dma(p, pl, s);
     default: return hipErrorInvalidValue;
   }
@@ -262,10 +259,6 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
       snprintf(buf, sizeof buf, "ks_staged_kernel<%s,%d,%d,%s,%d,%d>", t, p.layout, pl.vec,
                pl.unroll ? "true" : "false", pl.waves_m, pl.cps);
       break;
-    case V_STREAM:
-      snprintf(buf, sizeof buf, "ks_stream_kernel<%s,%d,%d,%s,%d>", t, p.layout, pl.vec, pl.unroll ? "true" : "false",
-               pl.waves_m);
-      break;
     case V_DMA:
       // DMA instructions per wavefront per stage: 16*rs rows of lch*d*esize
       // bytes over four wavefronts of 64 16-byte lanes.
@@ -280,7 +273,7 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
 }
 
 std::string describe(const Problem& p, const Plan& pl) {
-  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "direct", "staged", "stream", "dma"};
+  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "direct", "staged", "?", "dma"};
   char buf[320];
   snprintf(buf, sizeof buf,
            "variant=%d name=%s vec=%d bt=%d jg=%d unroll=%d waves_m=%d waves_n=%d lds=%d grid=%u block=%u xcd=%d "

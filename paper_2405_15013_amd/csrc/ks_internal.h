@@ -17,7 +17,7 @@ enum Variant : int {
   V_VALU_BSF = 2,  // VALU, batch-size-first, small b and c
   V_DIRECT = 3,    // register-direct MFMA, one work item per wavefront, b and c multiples of 16
   V_STAGED = 4,    // LDS-staged MFMA, 4 work items per workgroup share coalesced X stages
-  V_STREAM = 5,    // register-direct MFMA, each wavefront streams a run of batch tiles
+  // 5: unused (a persistent streaming variant, measured slower and removed)
   V_DMA = 6,       // LDS-staged MFMA with X moved HBM -> LDS by DMA, three stage buffers (BSF, d >= 4)
   V_COUNT = 7
 };
@@ -63,7 +63,6 @@ hipError_t launch_valu_bsl(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_valu_bsf(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_direct(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_staged(const Problem& p, const Plan& pl, hipStream_t s);
-hipError_t launch_stream(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_dma(const Problem& p, const Plan& pl, hipStream_t s);
 
 }  // namespace ks

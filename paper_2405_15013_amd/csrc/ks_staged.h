@@ -195,6 +195,7 @@ __global__ __launch_bounds__(512) void ks_staged_kernel(Problem p, StagedTile t)
   } else {
     // Structured epilogue: accumulators -> LDS output tile -> contiguous runs.
     // (The loop's last barrier guarantees no wavefront still reads X stages.)
+    mfma_results_settle();
     const int r = 16 * si.rs + n;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)

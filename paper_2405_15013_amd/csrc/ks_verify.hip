@@ -16,14 +16,12 @@
 #include "ks_internal.h"
 #include "ks_direct_index.h"
 #include "ks_staged_index.h"
-#include "ks_stream_index.h"
 
 namespace ks {
 
 // Defined in ks_direct_plan.cpp and ks_staged_plan.cpp.
 DirectTile direct_tile(const Problem& p, const Plan& pl);
 StagedTile staged_tile_of(const Problem& p, const Plan& pl);
-StreamTile stream_tile_of(const Problem& p, const Plan& pl);
 
 // Defined in ks_host.cpp.
 bool plan_for_verify(int64_t a, int64_t b, int64_t c, int64_t d, int64_t batch, int layout, int dtype, Problem* p,
@@ -185,32 +183,6 @@ bool verify_direct(Checker& ck, const Plan& pl) {
       return ck.fail("fast item decode differs", item);
     if (!verify_item(ck, a1, strided, V, MT, S, chunks, nch)) return false;
   }
-  return ck.err.empty();
-}
-
-bool verify_stream(Checker& ck, const Plan& pl) {
-  const Problem& p = ck.p;
-  const StreamTile t = stream_tile_of(p, pl);
-  const int V = pl.vec, MT = pl.waves_m, S = p.dtype == F32 ? 4 : 2;
-  const bool strided = pl.unroll != 0;
-  if (t.kgroups * 16 * MT != p.b) return ck.fail("M-tiles do not cover b", p.b);
-  if (p.c % 16) return ck.fail("c not a multiple of 16", p.c);
-  if (t.nwaves < 1 || t.nwaves > t.tiles) return ck.fail("bad number of wavefronts", t.nwaves);
-  if (p.layout == BSF && (p.d % V || (!strided && V != p.d))) return ck.fail("bad j-vector", V);
-  if (p.layout == BSL && p.batch % V) return ck.fail("batch not a multiple of the vector width", p.batch);
-  int chunks[64][2], nch = 0;
-  if (p.c / 16 > 64) return ck.fail("c too large for the verifier", p.c);
-  for (int l0 = 0; l0 < p.c; l0 += 16) { chunks[nch][0] = l0; chunks[nch][1] = 4; ++nch; }
-  int next = 0;  // the shares must tile [0, tiles) in order
-  for (int w = 0; w < t.nwaves && ck.err.empty(); ++w) {
-    int first, count;
-    stream_share(t, w, &first, &count);
-    if (first != next || count < 0) return ck.fail("wavefront shares do not tile the tiles", w);
-    next = first + count;
-    for (int q = 0; q < count; ++q)
-      if (!verify_item(ck, stream_item(p, t, V, MT, first + q), strided, V, MT, S, chunks, nch)) return false;
-  }
-  if (next != t.tiles) return ck.fail("wavefront shares do not cover the tiles", next);
   return ck.err.empty();
 }
 
@@ -528,7 +500,6 @@ extern "C" ks_status_t ks_plan_verify(int64_t a, int64_t b, int64_t c, int64_t d
     case V_VALU_BSF: ok = verify_valu_bsf(ck, pl); break;
     case V_DIRECT: ok = verify_direct(ck, pl); break;
     case V_STAGED: ok = verify_staged(ck, pl); break;
-    case V_STREAM: ok = verify_stream(ck, pl); break;
     case V_DMA: ok = verify_dma(ck, pl); break;
     default: ck.fail("unknown variant", pl.variant);
   }

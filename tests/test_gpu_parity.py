@@ -15,7 +15,7 @@ from shapes import DMA_ROW_GROUP_SHAPES, DMA_SHAPES, MFMA_SHAPES
 
 pytestmark = pytest.mark.gpu
 
-VARIANTS = {"generic": 0, "valu_bsl": 1, "valu_bsf": 2, "direct": 3, "staged": 4, "stream": 5, "dma": 6}
+VARIANTS = {"generic": 0, "valu_bsl": 1, "valu_bsf": 2, "direct": 3, "staged": 4, "dma": 6}
 
 
 def run_gpu(pattern, x_logical, kv, batch, dtype, layout, variant=None, x_offset=0, y_offset=0):
@@ -233,16 +233,6 @@ def test_direct_forced(pattern, dtype, layout, batch):
     d > 4), c % 32 == 16 tails of the 16-bit path, and ragged batches (68: the
     16-bit batch-size-last path with 4 instead of 8 batch entries per lane)."""
     check(pattern, batch, dtype, layout, cfg=11, variant=VARIANTS["direct"], kdist="normal")
-
-
-@pytest.mark.parametrize("pattern", MFMA_SHAPES)
-@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
-@pytest.mark.parametrize("layout", ["bsf", "bsl"])
-@pytest.mark.parametrize("batch", [256, 72, 25088])
-def test_stream_forced(pattern, dtype, layout, batch):
-    """The streaming kernel: one tile per wavefront (small batches) and runs of
-    tiles per wavefront (full batch), every j-vector mode, ragged batches."""
-    check(pattern, batch, dtype, layout, cfg=13, variant=VARIANTS["stream"], kdist="normal")
 
 
 @pytest.mark.parametrize("pattern", [s for s in MFMA_SHAPES if s[3] <= 16])

@@ -1,0 +1,77 @@
+"""Static check of the compiled kernels (CPU only): no instruction reads an
+MFMA result from the vector registers within fewer than 16 wait states of
+the MFMA that writes it, on any control-flow path.
+
+Why: the compiler's hazard recognizer puts exactly the wait states it
+believes an MFMA result needs before the first read, and no more.  A kernel
+variant whose packed bf16 conversion (v_cvt_pk_bf16_f32) read the VGPR result
+of a 16x16x16 bf16 MFMA at that minimum distance gave wrong first
+conversions, varying from run to run, while the same kernels with the
+reads further away were exact.  The kernels therefore settle their MFMAs
+explicitly before the epilogue (ks_common.h, mfma_results_settle); this test
+keeps every kernel instance that way.  Results held in the accumulation
+registers (AGPRs) are moved out by v_accvgpr_read, whose wait states the
+recognizer supplies and which the full GPU parity suite exercises at that
+distance; they are checked only for being read by that instruction first.
+"""
+import concurrent.futures
+import os
+import subprocess
+import tempfile
+
+import pytest
+
+import isa_scan
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+CSRC = os.path.join(ROOT, "paper_2405_15013_amd", "csrc")
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+MIN_WAIT = 16
+
+
+def _device_asm(src, outdir):
+    out = os.path.join(outdir, os.path.basename(src) + ".s")
+    cmd = [HIPCC, "-O3", "-std=c++17", "--offload-arch=gfx950", "-Xclang", "-target-feature", "-Xclang",
+           "-packed-fp32-ops", "-I" + os.path.join(ROOT, "include"), "--cuda-device-only", "-S", src, "-o", out]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    assert r.returncode == 0, r.stderr[-2000:]
+    return out
+
+
+@pytest.fixture(scope="module")
+def kernel_asm():
+    if not os.path.exists(HIPCC):
+        pytest.skip("hipcc not available")
+    srcs = sorted(os.path.join(CSRC, f) for f in os.listdir(CSRC) if f.endswith(".hip"))
+    with tempfile.TemporaryDirectory() as d:
+        with concurrent.futures.ThreadPoolExecutor(max_workers=8) as ex:
+            paths = list(ex.map(lambda s: _device_asm(s, d), srcs))
+        yield {os.path.basename(p): isa_scan.functions(p) for p in paths}
+
+
+def test_mfma_results_are_read_late(kernel_asm):
+    bad, nmfma = [], 0
+    for f, fns in kernel_asm.items():
+        for fn, lines in fns.items():
+            for ws, op, reader, cls in isa_scan.mfma_result_reads(lines, cap=MIN_WAIT):
+                nmfma += 1
+                if reader is None:
+                    continue
+                if cls == "vgpr" and ws < MIN_WAIT:
+                    bad.append((f, fn, op, reader, ws))
+                if cls == "agpr" and ws < MIN_WAIT and not reader.startswith(("v_accvgpr_read", "v_accvgpr_mov")):
+                    bad.append((f, fn, op, reader, ws))
+    assert nmfma > 1000
+    assert not bad, bad[:10]
+
+
+def test_scanner_flags_a_read_at_the_minimum_distance():
+    """The scanner itself: an MFMA whose VGPR result is converted right after
+    the compiler's own wait states is reported at that distance."""
+    lines = ["v_mfma_f32_16x16x16_bf16 v[0:3], v[4:5], v[6:7], 0", "s_nop 7",
+             "v_cvt_pk_bf16_f32 v0, v0, v1", "s_endpgm"]
+    (ws, op, reader, cls), = isa_scan.mfma_result_reads(lines)
+    assert (ws, reader, cls) == (8, "v_cvt_pk_bf16_f32", "vgpr")
+    lines = ["v_mfma_f32_16x16x16_bf16 v[0:3], v[4:5], v[6:7], 0", "s_cbranch_scc1 .LBB0_2", "s_nop 7",
+             "s_nop 7", ".LBB0_2:", "v_cvt_pk_bf16_f32 v8, v2, v3", "s_endpgm"]
+    assert isa_scan.mfma_result_reads(lines)[0][0] == 1  # the branch skips the nops

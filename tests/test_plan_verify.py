@@ -77,7 +77,7 @@ def test_all_sweep_plans_staged(dtype, layout, batch, every):
 
 
 @pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
-@pytest.mark.parametrize("batch,every", [(72, 1), (1000, 3), (25088, 29)])
+@pytest.mark.parametrize("batch,every", [(72, 1), (1000, 7), (25088, 97)])
 def test_all_sweep_plans_dma(dtype, batch, every):
     """The LDS-DMA kernel (forced) on every batch-size-first sweep pattern:
     every DMA lane fills one unit of the stage from an in-bounds address, every
@@ -92,24 +92,6 @@ def test_all_sweep_plans_dma(dtype, batch, every):
                 bad.append((pattern, rep))
             else:
                 assert "name=dma" in ks.ks_plan_describe(*pattern, batch, "bsf", dtype)
-    finally:
-        ks.ks_force_variant(None)
-    assert not bad, bad[:5]
-
-
-@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
-@pytest.mark.parametrize("layout", ["bsf", "bsl"])
-@pytest.mark.parametrize("batch,every", [(72, 1), (25088, 17)])
-def test_all_sweep_plans_stream(dtype, layout, batch, every):
-    """The streaming kernel on the sweep patterns (forced), including full
-    batches where a wavefront walks several batch tiles."""
-    bad = []
-    ks.ks_force_variant(5)
-    try:
-        for pattern in sweep_patterns()[::every]:
-            st, rep = ks.ks_plan_verify(*pattern, batch, layout, dtype)
-            if st != 0:
-                bad.append((pattern, rep))
     finally:
         ks.ks_force_variant(None)
     assert not bad, bad[:5]
