@@ -21,11 +21,21 @@ Infinity Cache, pass between two uses of the same buffers (at least 8 sets).
 One pass launches one ks_matmul per set; the passes are captured into HIP
 graphs of at most 512 calls, replayed --warmup times untimed and then --steps
 times between two HIP events recorded on the replay stream.  The point's time
-per call is the elapsed time / (steps * sets).  ms_per_step is the sum over the
-timed points of the time per call, i.e. the time of one pass over the sweep.
+per call is the elapsed time / (steps * sets): back-to-back calls on one
+stream, as the paper times its kernels (a loop of calls divided by its
+length).  This time feeds `value`.  Each point is also timed call by call
+(32 calls spread over the rotation, each between its own HIP event pair on
+the launch stream): the median and interquartile range of those per-launch
+times are reported per point, with the median fraction they give overall.
+ms_per_step is the sum over the timed points of the time per call, i.e. the
+time of one pass over the sweep (one step).
+
+Reported per point (the JSON line's "points", fields in "points_fields"):
+pattern, batch, dtype, layout, time per call, GB/s, TFLOP/s, fraction of
+roofline, binding roof, per-launch median and quartiles.
 
 The roofline object is computed for the dominant kernel instance (the one with
-the largest share of timed time): achieved = algorithmic bytes (or flops) of
+the largest share of one step): achieved = algorithmic bytes (or flops) of
 all its timed calls / their total time, and avg_launch_us = that total time /
 number of calls, which is what a profiler's per-kernel average duration
 reports for the same command (the event time also holds the gaps between
@@ -33,8 +43,8 @@ launches inside the graph).
 
 Also reported: the same measurements for the other workload families (tiny,
 butterfly factors and 10-chain, Monarch factors and 2-chain, Transformer-MLP
-layers) as context, the dominant kernel's roofline and the fp64 CPU oracle
-timed on a bounded sample on the host cores (cpu_baseline).
+layers) as context, and the fp64 CPU oracle timed on a bounded sample on the
+host cores (cpu_baseline).
 
 Usage: python bench.py [--gpus 1] [--steps K] [--warmup W] [--sample S]
 """
@@ -57,6 +67,7 @@ POOL_BYTES = 3 << 30
 ROTATE_BYTES = 768 << 20    # distinct buffer bytes between two uses of a buffer (3x the 256 MB MALL)
 MIN_SETS = 8
 GRAPH_LAUNCHES = 512
+PER_LAUNCH_SAMPLES = 32     # calls timed one by one (own event pair each) per point
 
 
 def sweep_patterns():
@@ -177,7 +188,7 @@ def trace_summary(stats_csv, bench_json, out_md, command_lines, top=25):
              "(sources sha1 %s)." % (
                  bench["value"], bench["sources_sha1"][:12]), "",
              "Dominant kernel (largest share of timed sweep time, %.1f %%): `%s`." % (
-                 100 * bench["roofline"]["share_of_sweep_time"], dom)]
+                 100 * bench["roofline"].get("share_of_step_time", bench["roofline"].get("share_of_sweep_time", 0)), dom)]
     if drow:
         r = drow[0]
         lines.append("bench.py (HIP events on the replay stream, timed calls only): avg_launch_us = %.2f; "
@@ -240,7 +251,7 @@ def pmc_summary(pdir, out_md, command_lines):
 
 
 class Runner:
-    def __init__(self, steps, warmup, eager=False):
+    def __init__(self, steps, warmup, eager=False, per_launch=True):
         import torch
         import paper_2405_15013_amd as ks
         if not os.path.exists(ks.library_path()):
@@ -257,6 +268,7 @@ class Runner:
         self.stream = torch.cuda.Stream(device=self.dev)
         self.filled = None
         self.eager = eager
+        self.per_launch = per_launch
 
     def fill(self, dtype):
         """Fill the input pool with N(0,1) values of the storage dtype."""
@@ -316,6 +328,28 @@ class Runner:
         del graphs
         return ms * 1e-3 / (self.steps * nsets), nsets
 
+    def time_per_launch(self, nsets, launch, count=PER_LAUNCH_SAMPLES):
+        """Per-launch durations: `count` calls on buffer sets spread over the
+        rotation, each between its own pair of HIP events on the launch stream
+        (launched one by one, after a warm-up call on each set).  Returns
+        (median, first quartile, third quartile) in seconds."""
+        import numpy as np
+        torch = self.torch
+        sets = sorted(set(int(round(i * (nsets - 1) / max(1, count - 1))) for i in range(min(count, nsets))))
+        with torch.cuda.stream(self.stream):
+            h = self.stream.cuda_stream
+            for r in sets:
+                launch(r, h)
+            ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in sets]
+            self.stream.synchronize()
+            for (e0, e1), r in zip(ev, sets):
+                e0.record(self.stream)
+                launch(r, h)
+                e1.record(self.stream)
+            self.stream.synchronize()
+        t = np.array([e0.elapsed_time(e1) * 1e-3 for e0, e1 in ev])
+        return float(np.median(t)), float(np.quantile(t, 0.25)), float(np.quantile(t, 0.75))
+
     def time_eager(self, nsets, launch):
         """The same rotation launched call by call (no graphs), for profiler
         counter passes, which count per dispatch."""
@@ -366,12 +400,26 @@ class Runner:
         t, nsets = self.time_calls(xb + yb, nsets_pool, launch)
         nbytes, flops, t_roof, bound = roof(pattern, batch, dtype)
         desc = self.ks.ks_plan_describe(a, b, c, d, batch, layout, dtype)
-        return {"pattern": list(pattern), "batch": batch, "dtype": dtype, "layout": layout, "us": t * 1e6,
-                "gbps": nbytes / t / 1e9, "tflops": flops / t / 1e12, "frac": t_roof / t, "bound": bound,
-                "roof_us": t_roof * 1e6, "bytes": nbytes, "flops": flops, "calls_per_pass": nsets,
-                "kernel": plan_field(desc, "kernel"), "plan": desc}
+        r = {"pattern": list(pattern), "batch": batch, "dtype": dtype, "layout": layout, "us": t * 1e6,
+             "gbps": nbytes / t / 1e9, "tflops": flops / t / 1e12, "frac": t_roof / t, "bound": bound,
+             "roof_us": t_roof * 1e6, "bytes": nbytes, "flops": flops, "calls_per_pass": nsets,
+             "kernel": plan_field(desc, "kernel"), "plan": desc}
+        if self.per_launch and not self.eager:
+            med, q1, q3 = self.time_per_launch(nsets, launch)
+            r.update({"launch_us_median": med * 1e6, "launch_us_iqr": [q1 * 1e6, q3 * 1e6],
+                      "frac_launch_median": t_roof / med})
+        return r
 
-    def chain(self, patterns, batch, dtype, layout):
+    def chain(self, patterns, batch, dtype, layout, fused=True):
+        torch = self.torch
+        ks = self.ks
+        ks.ks_force_chain_fusion(None if fused else 0)
+        try:
+            return self._chain(patterns, batch, dtype, layout)
+        finally:
+            ks.ks_force_chain_fusion(None)
+
+    def _chain(self, patterns, batch, dtype, layout):
         torch = self.torch
         ks = self.ks
         s = ESIZE[dtype]
@@ -391,44 +439,63 @@ class Runner:
         def launch(r, h):
             ks.ks_chain(factors, px + r * xb, py + r * yb, batch, layout, dtype, ws, wsb, stream=h)
 
-        t, _ = self.time_calls(xb + yb, nsets_pool, launch)
+        t, nsets = self.time_calls(xb + yb, nsets_pool, launch)
         unfused = sum(roof(p, batch, dtype)[0] for p in patterns)
         fused = (batch * (N + M) + sum(p[0] * p[1] * p[2] * p[3] for p in patterns)) * s
         flops = sum(roof(p, batch, dtype)[1] for p in patterns)
         t_roof = max(unfused / HBM_BW, flops / PEAK[dtype])
-        return {"chain": [list(p) for p in patterns], "batch": batch, "dtype": dtype, "layout": layout,
-                "us": t * 1e6, "gbps_unfused": unfused / t / 1e9, "frac_unfused": t_roof / t,
-                "fused_lower_bound_us": max(fused / HBM_BW, flops / PEAK[dtype]) * 1e6}
+        t_fused = max(fused / HBM_BW, flops / PEAK[dtype])
+        desc = ks.ks_chain_describe(factors, batch, layout, dtype)
+        r = {"chain": [list(p) for p in patterns], "batch": batch, "dtype": dtype, "layout": layout,
+             "path": desc.split()[0], "us": t * 1e6, "gbps_unfused": unfused / t / 1e9, "frac_unfused": t_roof / t,
+             "fused_lower_bound_us": t_fused * 1e6, "frac_fused_bound": t_fused / t,
+             "gbps_fused_bytes": fused / t / 1e9}
+        if self.per_launch:
+            med, q1, q3 = self.time_per_launch(nsets, launch)
+            r.update({"launch_us_median": med * 1e6, "launch_us_iqr": [q1 * 1e6, q3 * 1e6]})
+        return r
 
 
-def cpu_baseline(sample_every=7, batch=4096):
+def cpu_baseline(every_4096=14, every_25088=88):
     """The fp64 oracle timed on the host cores, on a bounded sample of the
-    sweep: every `sample_every`-th pattern (100 of the 700), batch `batch`,
-    fp32 inputs, both layouts.  Reported in the metric's unit (median fraction
-    of the MI355X roofline) and in GB/s of algorithmic traffic."""
+    sweep: every `every_4096`-th pattern (50 of the 700) at batch 4096 and
+    every `every_25088`-th (8) at batch 25088, both layouts.  The oracle does
+    the same fp64 work whatever the storage type of its inputs, so each
+    timed call is scored against both the fp32 and the bf16 roofline of its
+    point.  Reported in the metric's unit (median fraction of the MI355X
+    roofline over the sampled points) and in GB/s of algorithmic traffic.
+    Inputs are N(0,1) values (numpy's default generator; only the oracle call
+    is timed)."""
     import numpy as np
     import oracle
-    from paper_2405_15013_amd import inputs
-    pats = sweep_patterns()[::sample_every]
     fracs, gbps = [], []
     total = 0.0
-    for p in pats:
-        x = inputs.to_f64(inputs.make_x(9, p, batch, "f32"), "f32")
-        kv = inputs.to_f64(inputs.make_kv(9, p, batch, "f32", dist="normal"), "f32")
-        for layout in ("bsf", "bsl"):
-            xl = inputs.to_layout(x, layout)
-            t0 = time.perf_counter()
-            oracle.matmul(p, kv, xl, batch, layout)
-            t = time.perf_counter() - t0
-            total += t
-            nbytes, flops, t_roof, _ = roof(p, batch, "f32")
-            fracs.append(t_roof / t)
-            gbps.append(nbytes / t / 1e9)
+    npts = {}
+    rng = np.random.default_rng(20240523)
+    for batch, every in ((4096, every_4096), (25088, every_25088)):
+        pats = sweep_patterns()[::every]
+        npts[batch] = len(pats)
+        for p in pats:
+            a, b, c, d = p
+            x = rng.standard_normal((batch, a * c * d), dtype=np.float32).astype(np.float64)
+            kv = rng.standard_normal(a * d * b * c, dtype=np.float32).astype(np.float64)
+            for layout in ("bsf", "bsl"):
+                xl = x if layout == "bsf" else np.ascontiguousarray(x.T)
+                t0 = time.perf_counter()
+                oracle.matmul(p, kv, xl, batch, layout)
+                t = time.perf_counter() - t0
+                total += t
+                for dtype in ("f32", "bf16"):
+                    nbytes, flops, t_roof, _ = roof(p, batch, dtype)
+                    fracs.append(t_roof / t)
+                    gbps.append(nbytes / t / 1e9)
+            del x
     return {"value": float(np.median(fracs)), "unit": "fraction of MI355X roofline (median over sampled points)",
             "gbps_median": float(np.median(gbps)), "cores": oracle.threads(), "kind": "oracle",
             "seconds": total,
-            "sample": "%d of the 700 sweep patterns (every %dth) x {BSF, BSL}, batch %d, fp32 values, "
-                      "fp64 arithmetic" % (len(pats), sample_every, batch)}
+            "sample": "%d sweep patterns at batch 4096 (every %dth) and %d at batch 25088 (every %dth), BSF and BSL, "
+                      "each timed call scored against its fp32 and its bf16 point: %d points, fp64 arithmetic"
+                      % (npts[4096], every_4096, npts[25088], every_25088, len(fracs))}
 
 
 def main():
@@ -517,12 +584,15 @@ def main():
             for r in fam:
                 fout.write(json.dumps(r) + "\n")
             run.fill("f32")
-            ch = [run.chain([(2 ** (l - 1), 2, 2, 2 ** (10 - l)) for l in range(1, 11)], 4096, "f32", "bsl")]
+            bfly = [(2 ** (l - 1), 2, 2, 2 ** (10 - l)) for l in range(1, 11)]
+            ch = [run.chain(bfly, 4096, "f32", "bsl")]
             for dtype in ("f32", "bf16"):
                 run.fill(dtype)
                 for layout in ("bsf", "bsl"):
                     ch.append(run.chain([(1, 32, 32, 32), (32, 32, 32, 1)], 16384, dtype, layout))
-            for r in ch:
+            run.fill("f32")
+            bfly_more = [run.chain(bfly, 4096, "f32", "bsf"), run.chain(bfly, 4096, "f32", "bsl", fused=False)]
+            for r in ch + bfly_more:
                 fout.write(json.dumps(r) + "\n")
 
             def fam_summary(sel):
@@ -534,25 +604,36 @@ def main():
                 "monarch_B16384": fam_summary([r for r in fam[12:] if r["batch"] == 16384]),
                 "mlp_768_3072_B25088": fam_summary([r for r in fam[12:] if r["batch"] == 25088]),
                 "butterfly_10chain_B4096_f32_bsl_us": ch[0]["us"],
+                "butterfly_10chain_B4096_f32": {
+                    "bsl": {k: ch[0][k] for k in ("path", "us", "fused_lower_bound_us", "frac_fused_bound",
+                                                  "frac_unfused")},
+                    "bsf": {k: bfly_more[0][k] for k in ("path", "us", "fused_lower_bound_us", "frac_fused_bound",
+                                                         "frac_unfused")},
+                    "bsl_factor_by_factor_us": bfly_more[1]["us"]},
                 "monarch_2chain_B16384_us": {"%s_%s" % (r["dtype"], r["layout"]): r["us"] for r in ch[1:]},
             }
     fr = np.array([r["frac"] for r in points])
-    # Dominant kernel instance: the largest share of the sweep's timed time.
-    # Per instance, sums over its timed calls (each point contributes
-    # steps * calls_per_pass calls of the same duration).
+    # Dominant kernel instance: the largest share of one step, i.e. of one
+    # call per sweep point (ms_per_step).  Its roofline figures are averages
+    # over all of its timed calls, the way a profiler averages its dispatches:
+    # each point contributes steps * calls_per_pass calls of the same
+    # duration.
     per_k = {}
     for r in points:
         n = args.steps * r["calls_per_pass"]
         k = per_k.setdefault(r["kernel"], {"t": 0.0, "bytes": 0.0, "flops": 0.0, "calls": 0, "points": 0,
-                                           "t_hbm": 0.0, "t_flop": 0.0, "dtype": r["dtype"]})
+                                           "t_hbm": 0.0, "t_flop": 0.0, "dtype": r["dtype"], "t_step": 0.0})
         k["t"] += r["us"] * 1e-6 * n
+        k["t_step"] += r["us"] * 1e-6
         k["bytes"] += r["bytes"] * n
         k["flops"] += r["flops"] * n
         k["calls"] += n
         k["points"] += 1
         k["t_hbm"] += r["bytes"] / HBM_BW * n
         k["t_flop"] += r["flops"] / PEAK[r["dtype"]] * n
-    dom_name, dom = max(per_k.items(), key=lambda kv: kv[1]["t"])
+    t_step = sum(v["t_step"] for v in per_k.values())
+    t_timed = sum(v["t"] for v in per_k.values())
+    dom_name, dom = max(per_k.items(), key=lambda kv: kv[1]["t_step"])
     if dom["t_hbm"] >= dom["t_flop"]:
         achieved = dom["bytes"] / dom["t"] / 1e9
         roofline = {"bound": "hbm", "achieved": achieved, "peak": HBM_BW / 1e9, "unit": "GB/s",
@@ -562,11 +643,14 @@ def main():
         roofline = {"bound": "mfma", "achieved": achieved, "peak": PEAK[dom["dtype"]] / 1e12, "unit": "TFLOP/s",
                     "frac": achieved / (PEAK[dom["dtype"]] / 1e12), "traffic": None}
     roofline["kernel"] = dom_name
+    roofline["dominant_by"] = "largest share of one step (one call per sweep point)"
     roofline["points"] = dom["points"]
     roofline["timed_calls"] = dom["calls"]
     roofline["avg_launch_us"] = dom["t"] / dom["calls"] * 1e6
     roofline["algorithmic_bytes_per_launch"] = dom["bytes"] / dom["calls"]
-    roofline["share_of_sweep_time"] = dom["t"] / sum(v["t"] for v in per_k.values())
+    roofline["algorithmic_flops_per_launch"] = dom["flops"] / dom["calls"]
+    roofline["share_of_step_time"] = dom["t_step"] / t_step
+    roofline["share_of_timed_calls_time"] = dom["t"] / t_timed
     sha = kernel_sources_sha1()
     rec = traffic_record(dom_name, args.sample) if args.kernel is None and not args.eager else None
     if rec is not None:
@@ -603,12 +687,36 @@ def main():
             for dt in ("f32", "bf16") for lay in ("bsf", "bsl") for B in (4096, 25088)
             if any(r["dtype"] == dt and r["layout"] == lay and r["batch"] == B for r in points)},
         "roofline": roofline,
-        "top_kernels": [{"kernel": k, "share_of_sweep_time": v["t"] / sum(x["t"] for x in per_k.values()),
+        "top_kernels": [{"kernel": k, "share_of_step_time": v["t_step"] / t_step,
+                         "share_of_timed_calls_time": v["t"] / t_timed,
                          "points": v["points"], "avg_launch_us": v["t"] / v["calls"] * 1e6,
                          "gbps": v["bytes"] / v["t"] / 1e9}
-                        for k, v in sorted(per_k.items(), key=lambda kv: -kv[1]["t"])[:5]],
+                        for k, v in sorted(per_k.items(), key=lambda kv: -kv[1]["t_step"])[:5]],
+        "top_kernels_by_timed_calls": [{"kernel": k, "share_of_timed_calls_time": v["t"] / t_timed,
+                                        "points": v["points"], "avg_launch_us": v["t"] / v["calls"] * 1e6,
+                                        "gbps": v["bytes"] / v["t"] / 1e9}
+                                       for k, v in sorted(per_k.items(), key=lambda kv: -kv[1]["t"])[:3]],
         "families": families,
     }
+    if any("launch_us_median" in r for r in points):
+        fl = np.array([r["frac_launch_median"] for r in points if "frac_launch_median" in r])
+        out["per_launch"] = {
+            "what": "each point also timed call by call, each call between its own HIP event pair "
+                    "(%d calls spread over the rotation); value uses the back-to-back graph-replay "
+                    "time per call instead" % PER_LAUNCH_SAMPLES,
+            "median_frac": float(np.median(fl)),
+            "frac_quantiles_10_25_50_75_90": [float(np.quantile(fl, q)) for q in (0.1, 0.25, 0.5, 0.75, 0.9)]}
+    # Every point, compact: pattern, batch, dtype, layout, time per call (us,
+    # graph replay), GB/s, TFLOP/s, fraction of roofline, binding roof, and the
+    # per-launch event median and IQR (us) when measured.
+    out["points_fields"] = ["a", "b", "c", "d", "batch", "dtype", "layout", "us", "gbps", "tflops", "frac",
+                            "bound", "launch_us_median", "launch_us_q1", "launch_us_q3"]
+    out["points"] = [list(r["pattern"]) + [r["batch"], r["dtype"], r["layout"], round(r["us"], 3),
+                                           round(r["gbps"], 1), round(r["tflops"], 3), round(r["frac"], 4),
+                                           r["bound"], round(r.get("launch_us_median", float("nan")), 3),
+                                           round(r.get("launch_us_iqr", [float("nan")] * 2)[0], 3),
+                                           round(r.get("launch_us_iqr", [float("nan")] * 2)[1], 3)]
+                     for r in points]
     if not args.no_cpu_baseline and args.kernel is None:
         out["cpu_baseline"] = cpu_baseline()
     out["wall_s"] = time.time() - t_start

@@ -92,8 +92,11 @@ ks_status_t ks_matmul(int64_t a, int64_t b, int64_t c, int64_t d,
                       int64_t batch, int layout, int dtype, void *stream);
 
 /*
- * Bytes of device workspace ks_chain needs for these factors (0 for a single
- * factor).  Returns 0 as well for invalid arguments; ks_chain reports those.
+ * Bytes of device workspace ks_chain needs for these factors: 0 for a single
+ * factor and for chains that run fused (see ks_chain), else one (two factors)
+ * or two (more) intermediate buffers.  Returns 0 as well for invalid
+ * arguments; ks_chain reports those.  The answer depends on this thread's
+ * ks_force_variant / ks_force_chain_fusion settings, as ks_chain's plan does.
  */
 size_t ks_chain_workspace_bytes(const ks_factor_t *factors, int nfactors,
                                 int64_t batch, int dtype);
@@ -104,8 +107,15 @@ size_t ks_chain_workspace_bytes(const ks_factor_t *factors, int nfactors,
  * then K_{L-1}, ..., K_1.  Neighbouring factors must satisfy
  *     a_f * c_f * d_f == a_{f+1} * b_{f+1} * d_{f+1}   (KS_ERR_DIM_MISMATCH).
  * X has batch*a_L*c_L*d_L elements and Y batch*a_1*b_1*d_1, both in `layout`.
- * Intermediates are stored in `dtype` in the caller's `workspace` (device,
- * at least ks_chain_workspace_bytes(...) bytes, not overlapping X or Y).
+ * Chains of two to 24 factors whose blocks are at most 8 x 8 and whose widest
+ * vector (times 16 batch columns of fp32) fits in 128 KB of LDS -- e.g. the
+ * butterfly factors of a transform of size up to 1024 -- run as one fused
+ * kernel: each workgroup keeps 16 batch columns of the intermediate vectors
+ * in LDS in fp32 from the first factor to the last, so X is read once, Y is
+ * written once and no workspace is used.  Other chains run factor by factor
+ * (one ks_matmul each); their intermediates are stored in `dtype` in the
+ * caller's `workspace` (device, at least ks_chain_workspace_bytes(...) bytes,
+ * not overlapping X or Y).  ks_chain_describe tells which applies.
  * Factor f's K_values are device pointers; the factor array itself is host
  * memory and may be freed when the call returns.
  */
@@ -143,6 +153,38 @@ ks_status_t ks_chain_noalloc(const ks_factor_t *factors, int nfactors,
 /* The fixed scratch size of ks_chain_noalloc in bytes
  * (KS_CHAIN_NOALLOC_MAX_WORKSPACE). */
 size_t ks_chain_noalloc_max_workspace(void);
+
+/*
+ * How ks_chain would run these arguments: writes "fused ..." (one kernel;
+ * LDS bytes, grid) or "unfused ... workspace=<bytes>" into `buf` (host, `len`
+ * bytes, NUL-terminated).  Pure host call.  Returns KS_OK or the status
+ * ks_chain would return for invalid factors, dtype or layout.
+ */
+ks_status_t ks_chain_describe(const ks_factor_t *factors, int nfactors,
+                              int64_t batch, int layout, int dtype,
+                              char *buf, size_t len);
+
+/*
+ * mode 0: chains on this thread always run factor by factor (one ks_matmul
+ * per factor, with the caller's workspace); any other value restores the
+ * automatic choice.  For testing and measuring both paths on the same inputs.
+ */
+void ks_force_chain_fusion(int mode);
+
+/*
+ * Host-side check of the fused kernel ks_chain would run for these arguments
+ * (16-byte-aligned stand-in buffers): replays every workgroup's tile loads
+ * and stores and every factor's work units on the CPU and checks that all
+ * global accesses stay inside X and Y, every LDS row is inside its buffer,
+ * each factor writes each element of its output exactly once (in place only
+ * where a unit reads exactly the rows it writes), and every element of Y is
+ * stored once.  Writes "ok", "not fused" or the first violation into
+ * `report` (host, `len` bytes).  Enqueues nothing.  Returns KS_OK,
+ * KS_ERR_UNSUPPORTED on a violation, or the status ks_chain_describe returns.
+ */
+ks_status_t ks_chain_verify(const ks_factor_t *factors, int nfactors,
+                            int64_t batch, int layout, int dtype,
+                            char *report, size_t len);
 
 /* Human-readable name of a status code (static string). */
 const char *ks_status_string(int status);

@@ -19,7 +19,7 @@ __all__ = [
     "ks_matmul", "ks_chain", "ks_chain_workspace_bytes", "ks_chain_noalloc", "ks_chain_noalloc_max_workspace",
     "ks_status_string",
     "ks_last_hip_error", "ks_plan_describe", "ks_force_variant", "ks_plan_verify",
-    "matmul", "chain", "library_path", "load_library", "EXPORTED_SYMBOLS",
+    "ks_chain_describe", "ks_force_chain_fusion", "ks_chain_verify", "matmul", "chain", "library_path", "load_library", "EXPORTED_SYMBOLS",
 ]
 
 BSF, BSL = 0, 1
@@ -36,6 +36,7 @@ STATUS_NAMES = {
 EXPORTED_SYMBOLS = (
     "ks_matmul", "ks_chain_workspace_bytes", "ks_chain", "ks_chain_noalloc", "ks_chain_noalloc_max_workspace",
     "ks_status_string", "ks_last_hip_error", "ks_plan_describe", "ks_force_variant", "ks_plan_verify",
+    "ks_chain_describe", "ks_force_chain_fusion", "ks_chain_verify",
 )
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -89,6 +90,12 @@ def load_library():
     lib.ks_chain_noalloc.restype = ci
     lib.ks_chain_noalloc_max_workspace.argtypes = []
     lib.ks_chain_noalloc_max_workspace.restype = ctypes.c_size_t
+    lib.ks_chain_describe.argtypes = [ctypes.POINTER(_Factor), ci, i64, ci, ci, ctypes.c_char_p, ctypes.c_size_t]
+    lib.ks_chain_describe.restype = ci
+    lib.ks_chain_verify.argtypes = [ctypes.POINTER(_Factor), ci, i64, ci, ci, ctypes.c_char_p, ctypes.c_size_t]
+    lib.ks_chain_verify.restype = ci
+    lib.ks_force_chain_fusion.argtypes = [ci]
+    lib.ks_force_chain_fusion.restype = None
     lib.ks_status_string.argtypes = [ci]
     lib.ks_status_string.restype = ctypes.c_char_p
     lib.ks_last_hip_error.argtypes = []
@@ -209,6 +216,31 @@ def ks_chain_noalloc(factors, X, Y, batch, layout, dtype, stream=None, check=Tru
     if check and st != KS_OK:
         raise KsError(st, "ks_chain_noalloc")
     return st
+
+
+def ks_chain_describe(factors, batch, layout, dtype):
+    """How ks_chain runs these factors: 'fused ...' or 'unfused ...'."""
+    arr = _factor_array(factors)
+    buf = ctypes.create_string_buffer(256)
+    st = load_library().ks_chain_describe(arr, len(factors), batch, _code(layout, _LAYOUTS, "layout"),
+                                          _code(dtype, _DTYPES, "dtype"), buf, 256)
+    if st != KS_OK:
+        raise KsError(st, "ks_chain_describe")
+    return buf.value.decode()
+
+
+def ks_chain_verify(factors, batch, layout, dtype):
+    """Host replay of the fused chain kernel's accesses; returns (status, report)."""
+    arr = _factor_array(factors)
+    buf = ctypes.create_string_buffer(256)
+    st = load_library().ks_chain_verify(arr, len(factors), batch, _code(layout, _LAYOUTS, "layout"),
+                                        _code(dtype, _DTYPES, "dtype"), buf, 256)
+    return int(st), buf.value.decode()
+
+
+def ks_force_chain_fusion(mode):
+    """mode 0: run chains factor by factor on this thread; None: automatic."""
+    load_library().ks_force_chain_fusion(-1 if mode is None else int(mode))
 
 
 def ks_chain_noalloc_max_workspace():

@@ -1,0 +1,254 @@
+// Fused chain kernel (see ks_chain_fused.h for the decomposition).
+//
+// Latency: a workgroup is the only one on its CU for most chain shapes (one
+// tile of 16 columns per CU at batch 4096), so nothing else hides its memory
+// latency.  The tile loads are issued in batches of kFusedLoadBatch 16-byte
+// loads per thread before any of them is used, and each factor's values are
+// fetched from global memory into registers one factor ahead and parked in a
+// double-buffered LDS copy, so the factor loop itself touches only LDS.
+#include <type_traits>
+
+#include "ks_chain_fused.h"
+#include "ks_common.h"
+#include "ks_internal.h"
+
+namespace ks {
+
+namespace {
+
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+constexpr int kFusedLoadBatch = 4;
+
+// Load the tile's input columns into LDS rows [0, width_in) (fp32).
+//  BSL: X is (N, batch); row n of the tile is the run X[n, col0 .. col0+16).
+//  BSF: X is (batch, N); batch row col0+t is the run X[col0+t, 0 .. N).
+// VEC: 16-byte accesses (the host checked alignment and that the batch (BSL)
+// or N (BSF) is a multiple of the vector).  Columns beyond the batch are
+// filled with zeros and never stored.
+template <typename T, int LAYOUT, bool VEC>
+__device__ __forceinline__ void fused_load(const FusedChain& fc, float* lds, int col0) {
+  const T* __restrict__ x = static_cast<const T*>(fc.x);
+  const int N = fc.width_in, B = fc.batch, tid = threadIdx.x;
+  constexpr int E = VEC ? 16 / (int)sizeof(T) : 1;  // elements per access
+  const int total = N * kFusedCols / E;
+  for (int base = 0; base < total; base += kFusedThreads * kFusedLoadBatch) {
+    typedef typename std::conditional<VEC, u32x4, T>::type W;
+    W w[kFusedLoadBatch];
+#pragma unroll
+    for (int r = 0; r < kFusedLoadBatch; ++r) {
+      const int u = base + r * kFusedThreads + tid;
+      int row, col;
+      if constexpr (VEC) fused_vec_unit(LAYOUT, E, u, &row, &col);
+      else if constexpr (LAYOUT == BSL) { row = u / kFusedCols; col = u % kFusedCols; }
+      else { col = u % kFusedCols; row = u / kFusedCols; }
+      const bool ok = u < total && col0 + col < B;
+      const int64_t off = LAYOUT == BSL ? (int64_t)row * B + col0 + col : (int64_t)(col0 + col) * N + row;
+      if constexpr (VEC) w[r] = ok ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(x + off)) : u32x4{0, 0, 0, 0};
+      else w[r] = ok ? x[off] : T(0);
+    }
+#pragma unroll
+    for (int r = 0; r < kFusedLoadBatch; ++r) {
+      const int u = base + r * kFusedThreads + tid;
+      if (u >= total) break;
+      int row, col;
+      if constexpr (VEC) fused_vec_unit(LAYOUT, E, u, &row, &col);
+      else if constexpr (LAYOUT == BSL) { row = u / kFusedCols; col = u % kFusedCols; }
+      else { col = u % kFusedCols; row = u / kFusedCols; }
+      if constexpr (VEC) {
+        const T* e = reinterpret_cast<const T*>(&w[r]);
+        if constexpr (LAYOUT == BSL) {
+#pragma unroll
+          for (int q = 0; q < E; q += 4)
+            *reinterpret_cast<f32x4*>(lds + row * kFusedPitch + col + q) =
+                f32x4{to_f32(e[q]), to_f32(e[q + 1]), to_f32(e[q + 2]), to_f32(e[q + 3])};
+        } else {
+#pragma unroll
+          for (int q = 0; q < E; ++q) lds[(row + q) * kFusedPitch + col] = to_f32(e[q]);
+        }
+      } else {
+        lds[row * kFusedPitch + col] = to_f32(w[r]);
+      }
+    }
+  }
+}
+
+// Store LDS rows [0, width_out) of the tile's valid columns into Y, rounded to
+// the storage type (same layouts and vector rules as fused_load).
+template <typename T, int LAYOUT, bool VEC>
+__device__ __forceinline__ void fused_store(const FusedChain& fc, const float* lds, int col0) {
+  T* __restrict__ y = static_cast<T*>(fc.y);
+  const int M = fc.width_out, B = fc.batch, tid = threadIdx.x;
+  constexpr int E = VEC ? 16 / (int)sizeof(T) : 1;
+  const int total = M * kFusedCols / E;
+  for (int u = tid; u < total; u += kFusedThreads) {
+    int row, col;
+    if constexpr (VEC) fused_vec_unit(LAYOUT, E, u, &row, &col);
+    else if constexpr (LAYOUT == BSL) { row = u / kFusedCols; col = u % kFusedCols; }
+    else { col = u % kFusedCols; row = u / kFusedCols; }
+    if (col0 + col >= B) continue;
+    const int64_t off = LAYOUT == BSL ? (int64_t)row * B + col0 + col : (int64_t)(col0 + col) * M + row;
+    if constexpr (VEC) {
+      union { u32x4 w; T e[E]; } o;
+#pragma unroll
+      for (int q = 0; q < E; ++q)
+        o.e[q] = from_f32<T>(LAYOUT == BSL ? lds[row * kFusedPitch + col + q] : lds[(row + q) * kFusedPitch + col]);
+      __builtin_nontemporal_store(o.w, reinterpret_cast<u32x4*>(y + off));
+    } else {
+      y[off] = from_f32<T>(lds[row * kFusedPitch + col]);
+    }
+  }
+}
+
+// Values of factor f: this thread's share (elements tid + kFusedThreads*r) fetched into
+// registers, later parked in an LDS buffer as fp32.
+template <typename T>
+struct FusedK {
+  float v[kFusedKPerThread];
+  __device__ __forceinline__ void fetch(const FusedChain& fc, int f) {
+    const T* __restrict__ kv = static_cast<const T*>(fc.kv[f]);
+    const int n = fc.a[f] * fc.d[f] * fc.b[f] * fc.c[f];
+#pragma unroll
+    for (int r = 0; r < kFusedKPerThread; ++r) {
+      const int e = r * kFusedThreads + (int)threadIdx.x;
+      v[r] = e < n ? to_f32(kv[e]) : 0.f;
+    }
+  }
+  __device__ __forceinline__ void park(const FusedChain& fc, int f, float* kbuf) const {
+    const int n = fc.a[f] * fc.d[f] * fc.b[f] * fc.c[f];
+#pragma unroll
+    for (int r = 0; r < kFusedKPerThread; ++r) {
+      const int e = r * kFusedThreads + (int)threadIdx.x;
+      if (e < n) kbuf[e] = v[r];
+    }
+  }
+};
+
+// One factor, LDS -> LDS: unit (ij, g) reads the c input rows of block
+// (i, j) = (ij / d, ij % d), pieces g*QN .. g*QN+QN-1 (4 columns each), and
+// writes the block's b output rows (Section 4.1 index sets:
+// inputs i*c*d + l*d + j, outputs i*b*d + k*d + j).  The block's values come
+// from the LDS copy kbuf (packed like K_values).  BB x CC is the block shape
+// when EXACT, else an upper bound (b, c read at run time).
+template <int BB, int CC, int QN, bool EXACT>
+__device__ __forceinline__ void fused_factor(const FusedChain& fc, int f, const float* src, float* dst,
+                                             const float* kbuf) {
+  const int b = EXACT ? BB : fc.b[f], c = EXACT ? CC : fc.c[f], d = fc.d[f];
+  constexpr int G = 4 / QN;
+  const int units = fc.a[f] * d * G;
+  for (int u = threadIdx.x; u < units; u += kFusedThreads) {
+    int i, j, g;
+    fused_unit(fc, f, G, u, &i, &j, &g);
+    const float* blk = kbuf + (i * d + j) * b * c;
+    f32x4 xin[CC][QN];
+#pragma unroll
+    for (int l = 0; l < CC; ++l) {
+      if (EXACT || l < c) {
+        const float* row = src + fused_in_row(fc, f, i, j, l) * kFusedPitch + g * QN * 4;
+#pragma unroll
+        for (int q = 0; q < QN; ++q) xin[l][q] = *reinterpret_cast<const f32x4*>(row + 4 * q);
+      }
+    }
+#pragma unroll
+    for (int k = 0; k < BB; ++k) {
+      if (EXACT || k < b) {
+        f32x4 acc[QN];
+#pragma unroll
+        for (int q = 0; q < QN; ++q) acc[q] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int l = 0; l < CC; ++l) {
+          if (EXACT || l < c) {
+            const float kk = blk[k * c + l];
+#pragma unroll
+            for (int q = 0; q < QN; ++q) {
+              acc[q][0] = __builtin_fmaf(kk, xin[l][q][0], acc[q][0]);
+              acc[q][1] = __builtin_fmaf(kk, xin[l][q][1], acc[q][1]);
+              acc[q][2] = __builtin_fmaf(kk, xin[l][q][2], acc[q][2]);
+              acc[q][3] = __builtin_fmaf(kk, xin[l][q][3], acc[q][3]);
+            }
+          }
+        }
+        float* row = dst + fused_out_row(fc, f, i, j, k) * kFusedPitch + g * QN * 4;
+#pragma unroll
+        for (int q = 0; q < QN; ++q) *reinterpret_cast<f32x4*>(row + 4 * q) = acc[q];
+      }
+    }
+  }
+}
+
+// Factor f with the instance for its block shape (exact 2x2, 4x4, 8x8, else
+// bounded by the larger of b and c); fused_pieces() gives the QN the host
+// replay assumes.
+__device__ __forceinline__ void fused_apply(const FusedChain& fc, int f, const float* src, float* dst,
+                                            const float* kbuf) {
+  const int b = fc.b[f], c = fc.c[f], m = b > c ? b : c;
+  if (b == 2 && c == 2) fused_factor<2, 2, 2, true>(fc, f, src, dst, kbuf);
+  else if (b == 4 && c == 4) fused_factor<4, 4, 1, true>(fc, f, src, dst, kbuf);
+  else if (b == 8 && c == 8) fused_factor<8, 8, 1, true>(fc, f, src, dst, kbuf);
+  else if (m <= 2) fused_factor<2, 2, 2, false>(fc, f, src, dst, kbuf);
+  else if (m <= 4) fused_factor<4, 4, 1, false>(fc, f, src, dst, kbuf);
+  else fused_factor<8, 8, 1, false>(fc, f, src, dst, kbuf);
+}
+
+template <typename T, int LAYOUT, bool VEC>
+__global__ __launch_bounds__(kFusedThreads) void ks_chain_fused_kernel(FusedChain fc) {
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  const int col0 = blockIdx.x * kFusedCols;
+  // src holds the current vector; factors write dst (the same buffer in place)
+  float* src = lds;
+  float* dst = fc.inplace ? lds : lds + fc.buf_rows * kFusedPitch;
+  float* kcur = lds + fused_kbuf_offset(fc);
+  float* knext = kcur + kFusedKValues;
+  FusedK<T> kr;
+  kr.fetch(fc, fc.nf - 1);
+  fused_load<T, LAYOUT, VEC>(fc, src, col0);
+  kr.park(fc, fc.nf - 1, kcur);
+  __syncthreads();
+  for (int f = fc.nf - 1; f >= 0; --f) {
+    if (f > 0) kr.fetch(fc, f - 1);  // in flight during this factor
+    fused_apply(fc, f, src, dst, kcur);
+    if (f > 0) kr.park(fc, f - 1, knext);
+    __syncthreads();
+    float* t = src;
+    src = dst;
+    dst = t;
+    t = kcur;
+    kcur = knext;
+    knext = t;
+  }
+  fused_store<T, LAYOUT, VEC>(fc, src, col0);
+}
+
+template <typename T>
+hipError_t launch_fused_t(const FusedChain& fc, bool vec, hipStream_t s) {
+  const dim3 grid((fc.batch + kFusedCols - 1) / kFusedCols), block(kFusedThreads);
+  const int lds = fused_lds_bytes(fc);
+#define KS_FUSED_LAUNCH(L, V)                                                                                 \
+  {                                                                                                          \
+    if (lds > 64 * 1024) {                                                                                   \
+      static const hipError_t raised = hipFuncSetAttribute(                                                  \
+          reinterpret_cast<const void*>(&ks_chain_fused_kernel<T, L, V>),                                    \
+          hipFuncAttributeMaxDynamicSharedMemorySize, kFusedMaxLds);                                         \
+      if (raised != hipSuccess) return raised;                                                               \
+    }                                                                                                        \
+    hipLaunchKernelGGL((ks_chain_fused_kernel<T, L, V>), grid, block, lds, s, fc);                           \
+    return hipGetLastError();                                                                                \
+  }
+  if (fc.layout == BSL) {
+    if (vec) KS_FUSED_LAUNCH(BSL, true) else KS_FUSED_LAUNCH(BSL, false)
+  }
+  if (vec) KS_FUSED_LAUNCH(BSF, true) else KS_FUSED_LAUNCH(BSF, false)
+#undef KS_FUSED_LAUNCH
+}
+
+}  // namespace
+
+hipError_t launch_chain_fused(const FusedChain& fc, int dtype, bool vec, hipStream_t s) {
+  switch (dtype) {
+    case F32: return launch_fused_t<float>(fc, vec, s);
+    case BF16: return launch_fused_t<bf16_t>(fc, vec, s);
+    case F16: return launch_fused_t<_Float16>(fc, vec, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace ks

@@ -13,6 +13,7 @@
 #include <unordered_map>
 
 #include "../../include/ks.h"
+#include "ks_chain_fused.h"
 #include "ks_direct_index.h"
 #include "ks_internal.h"
 
@@ -21,6 +22,7 @@ namespace {
 
 thread_local int g_last_hip_error = 0;
 thread_local int g_forced_variant = -1;
+thread_local int g_chain_fusion = -1;  // -1 automatic, 0 never fuse a chain
 
 constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
 
@@ -320,6 +322,50 @@ namespace ks {
 // fixed scratch buffer as the workspace).
 void set_last_hip_error(int e) { g_last_hip_error = e; }
 
+// The fused chain kernel (ks_chain_fused.h) takes chains of two or more
+// factors whose blocks are at most 8 x 8, with at most 4096 values per factor,
+// and whose widest vector, for 16 batch columns in fp32, fits the kernel's LDS
+// next to two copies of factor values (in place when every factor has b == c,
+// else two buffers).  Not used while a kernel variant is forced or
+// fusion is switched off on this thread.  Fills the pattern part of `fc`.
+bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, FusedChain* fc) {
+  if (g_forced_variant >= 0 || g_chain_fusion == 0) return false;
+  if (n < 2 || n > kFusedMaxFactors) return false;
+  int64_t wmax = 0;
+  bool inplace = true;
+  for (int q = 0; q < n; ++q) {
+    if (f[q].b > kFusedMaxBC || f[q].c > kFusedMaxBC) return false;
+    const int64_t N = f[q].a * f[q].c * f[q].d, M = f[q].a * f[q].b * f[q].d;
+    if (f[q].a * f[q].d * f[q].b * f[q].c > kFusedKValues) return false;
+    wmax = std::max(wmax, std::max(N, M));
+    inplace = inplace && f[q].b == f[q].c;
+  }
+  if (((inplace ? 1 : 2) * wmax * kFusedPitch + 2 * kFusedKValues) * 4 > kFusedMaxLds) return false;
+  if ((batch + kFusedCols - 1) / kFusedCols > 0x7fffffff) return false;
+  fc->nf = n;
+  fc->batch = (int)batch;
+  fc->layout = layout;
+  fc->width_in = (int)(f[n - 1].a * f[n - 1].c * f[n - 1].d);
+  fc->width_out = (int)(f[0].a * f[0].b * f[0].d);
+  fc->inplace = inplace ? 1 : 0;
+  fc->buf_rows = (int)wmax;
+  for (int q = 0; q < n; ++q) {
+    fc->a[q] = (int)f[q].a; fc->b[q] = (int)f[q].b; fc->c[q] = (int)f[q].c; fc->d[q] = (int)f[q].d;
+    div_magic((uint32_t)f[q].d, &fc->md[q], &fc->sd[q]);
+    fc->kv[q] = f[q].K_values;
+  }
+  return true;
+}
+
+// 16-byte vectors for the fused kernel's loads and stores: aligned buffers and
+// a batch (BSL) or widths (BSF) that are whole vectors.
+bool chain_fused_vec(const FusedChain& fc, int dtype, const void* X, const void* Y) {
+  const int e = 16 / elem_size(dtype);
+  if (!aligned16(X) || !aligned16(Y)) return false;
+  if (fc.layout == BSL) return fc.batch % e == 0;
+  return fc.width_in % e == 0 && fc.width_out % e == 0;
+}
+
 ks_status_t chain_impl(const ks_factor_t* factors, int nfactors, const void* X, void* Y, int64_t batch, int layout,
                        int dtype, void* workspace, size_t workspace_bytes, void* stream) {
   size_t per = 0;
@@ -328,7 +374,9 @@ ks_status_t chain_impl(const ks_factor_t* factors, int nfactors, const void* X, 
   if (layout != KS_LAYOUT_BSF && layout != KS_LAYOUT_BSL) return KS_ERR_UNSUPPORTED;
   for (int q = 0; q < nfactors; ++q)
     if (factors[q].K_values == nullptr) return KS_ERR_INVALID_ARG;
-  const size_t need = nfactors <= 1 ? 0 : (nfactors == 2 ? per : 2 * per);
+  FusedChain fc;
+  const bool fused = chain_fused_plan(factors, nfactors, batch, layout, &fc);
+  const size_t need = (fused || nfactors <= 1) ? 0 : (nfactors == 2 ? per : 2 * per);
   if (batch == 0) return KS_OK;
   if (X == nullptr || Y == nullptr) return KS_ERR_INVALID_ARG;
   if (need > 0 && (workspace == nullptr || workspace_bytes < need)) return KS_ERR_WORKSPACE;
@@ -343,6 +391,16 @@ ks_status_t chain_impl(const ks_factor_t* factors, int nfactors, const void* X, 
   if (overlaps(X, xe * s, Y, ye * s)) return KS_ERR_ALIAS;
   if (need > 0 && (overlaps(workspace, (int64_t)need, X, xe * s) || overlaps(workspace, (int64_t)need, Y, ye * s)))
     return KS_ERR_ALIAS;
+  if (fused) {
+    fc.x = X;
+    fc.y = Y;
+    const hipError_t e = launch_chain_fused(fc, dtype, chain_fused_vec(fc, dtype, X, Y), static_cast<hipStream_t>(stream));
+    if (e != hipSuccess) {
+      g_last_hip_error = (int)e;
+      return KS_ERR_HIP;
+    }
+    return KS_OK;
+  }
   // Validate every step before enqueueing anything.
   char* ws = static_cast<char*>(workspace);
   void* bufs[2] = {ws, ws + per};
@@ -384,7 +442,29 @@ size_t ks_chain_workspace_bytes(const ks_factor_t* factors, int nfactors, int64_
   size_t per = 0;
   if (chain_check(factors, nfactors, batch, dtype, &per) != KS_OK) return 0;
   if (nfactors <= 1) return 0;
+  FusedChain fc;
+  if (chain_fused_plan(factors, nfactors, batch, KS_LAYOUT_BSL, &fc)) return 0;  // layout-independent
   return nfactors == 2 ? per : 2 * per;
+}
+
+void ks_force_chain_fusion(int mode) { g_chain_fusion = mode < 0 ? -1 : (mode == 0 ? 0 : -1); }
+
+ks_status_t ks_chain_describe(const ks_factor_t* factors, int nfactors, int64_t batch, int layout, int dtype,
+                              char* buf, size_t len) {
+  if (buf == nullptr || len == 0) return KS_ERR_INVALID_ARG;
+  buf[0] = 0;
+  size_t per = 0;
+  ks_status_t st = chain_check(factors, nfactors, batch, dtype, &per);
+  if (st != KS_OK) return st;
+  if (layout != KS_LAYOUT_BSF && layout != KS_LAYOUT_BSL) return KS_ERR_UNSUPPORTED;
+  FusedChain fc;
+  if (chain_fused_plan(factors, nfactors, batch, layout, &fc)) {
+    snprintf(buf, len, "fused factors=%d inplace=%d lds=%d grid=%lld block=%d cols=%d", fc.nf, fc.inplace,
+             fused_lds_bytes(fc), (long long)((batch + kFusedCols - 1) / kFusedCols), kFusedThreads, kFusedCols);
+  } else {
+    snprintf(buf, len, "unfused factors=%d workspace=%zu", nfactors, nfactors <= 1 ? (size_t)0 : (nfactors == 2 ? per : 2 * per));
+  }
+  return KS_OK;
 }
 
 ks_status_t ks_chain(const ks_factor_t* factors, int nfactors, const void* X, void* Y, int64_t batch, int layout,

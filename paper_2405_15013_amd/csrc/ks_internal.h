@@ -64,6 +64,8 @@ hipError_t launch_valu_bsf(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_direct(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_staged(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_dma(const Problem& p, const Plan& pl, hipStream_t s);
+struct FusedChain;
+hipError_t launch_chain_fused(const FusedChain& fc, int dtype, bool vec, hipStream_t s);
 
 }  // namespace ks
 

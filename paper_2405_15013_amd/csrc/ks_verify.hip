@@ -7,6 +7,7 @@
 // Nothing is enqueued on a GPU.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cstdio>
 #include <cstring>
 #include <string>
@@ -504,6 +505,152 @@ extern "C" ks_status_t ks_plan_verify(int64_t a, int64_t b, int64_t c, int64_t d
     default: ck.fail("unknown variant", pl.variant);
   }
   if (ok) ok = ck.coverage();
+  if (report && len) snprintf(report, len, "%s", ok ? "ok" : ck.err.c_str());
+  return ok ? KS_OK : KS_ERR_UNSUPPORTED;
+}
+
+// ---------------------------------------------------------------------------
+// Fused chains (ks_chain_fused.hip): replay of every workgroup's tile loads
+// and stores and of every factor's work units, with the kernel's own index
+// functions (ks_chain_fused.h).
+// ---------------------------------------------------------------------------
+#include "ks_chain_fused.h"
+
+namespace ks {
+bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, FusedChain* fc);
+namespace {
+
+struct FusedChecker {
+  std::string err;
+  bool fail(const char* what, int64_t v) {
+    if (err.empty()) {
+      char buf[200];
+      snprintf(buf, sizeof buf, "%s (value %lld)", what, (long long)v);
+      err = buf;
+    }
+    return false;
+  }
+};
+
+// Global element ranges of one pass over a tile (load of X or store of Y) in
+// the 16-byte form (E elements per unit) or the element form (E = 1).
+bool verify_fused_io(FusedChecker& ck, const FusedChain& fc, int width, int E, bool store,
+                     std::vector<uint8_t>* cover) {
+  const int64_t B = fc.batch, total = (int64_t)B * width;
+  const int tiles = (int)((B + kFusedCols - 1) / kFusedCols);
+  const int units = width * kFusedCols / E;
+  const int rows_lds = fc.buf_rows;
+  for (int tile = 0; tile < tiles; ++tile) {
+    const int col0 = tile * kFusedCols;
+    for (int u = 0; u < units; ++u) {
+      int row, col;
+      if (E > 1) {
+        fused_vec_unit(fc.layout, E, u, &row, &col);
+      } else if (fc.layout == BSL) {
+        row = u / kFusedCols;
+        col = u % kFusedCols;
+      } else {
+        col = u % kFusedCols;
+        row = u / kFusedCols;
+      }
+      // The element(s) this unit moves: BSL a run of E columns of one row,
+      // BSF a run of E rows (vector elements) of one batch row.
+      const int r_hi = fc.layout == BSL ? row : row + E - 1;
+      const int c_hi = fc.layout == BSL ? col + E - 1 : col;
+      if (row < 0 || r_hi >= width || r_hi >= rows_lds) return ck.fail("tile row out of range", row);
+      if (col < 0 || c_hi >= kFusedCols) return ck.fail("tile column out of range", col);
+      const int bcol = col0 + (fc.layout == BSL ? col : col);
+      const bool valid = fc.layout == BSL ? bcol < B : bcol < B;
+      if (!valid) continue;  // beyond the batch: loads fill zeros, stores skip
+      if (fc.layout == BSL && E > 1 && bcol + E > B) return ck.fail("vector straddles the batch end", bcol);
+      const int64_t off = fc.layout == BSL ? (int64_t)row * B + bcol : (int64_t)bcol * width + row;
+      if (off < 0 || off + E > total) return ck.fail(store ? "Y access out of bounds" : "X access out of bounds", off);
+      if (E > 1 && off % E) return ck.fail("16-byte access not aligned to its vector", off);
+      if (cover)
+        for (int e = 0; e < E; ++e) (*cover)[(size_t)(off + e)]++;
+    }
+  }
+  return ck.err.empty();
+}
+
+bool verify_fused(FusedChecker& ck, const FusedChain& fc, int dtype) {
+  const int esize = dtype == F32 ? 4 : 2, E = 16 / esize;
+  // Widths along the chain: input of factor nf-1 ... output of factor 0.
+  for (int f = 0; f + 1 < fc.nf; ++f)
+    if (fc.a[f] * fc.c[f] * fc.d[f] != fc.a[f + 1] * fc.b[f + 1] * fc.d[f + 1]) return ck.fail("widths", f);
+  if (fused_lds_bytes(fc) > kFusedMaxLds) return ck.fail("LDS", fused_lds_bytes(fc));
+  for (int f = 0; f < fc.nf; ++f)
+    if (fc.a[f] * fc.d[f] * fc.b[f] * fc.c[f] > kFusedKValues) return ck.fail("factor values exceed the LDS copy", f);
+  // Vector rows end where the factor-value copies begin.
+  if (fused_kbuf_offset(fc) < (fc.inplace ? 1 : 2) * fc.buf_rows * kFusedPitch) return ck.fail("LDS overlap", 0);
+  // Tile I/O, both forms the host may choose (vector form only when the
+  // batch (BSL) or the widths (BSF) are whole vectors).
+  const bool vec_ok = fc.layout == BSL ? fc.batch % E == 0 : (fc.width_in % E == 0 && fc.width_out % E == 0);
+  for (int form = 0; form < 2; ++form) {
+    const int e = form == 0 ? 1 : E;
+    if (form == 1 && !vec_ok) break;
+    if (!verify_fused_io(ck, fc, fc.width_in, e, false, nullptr)) return false;
+    std::vector<uint8_t> cover((size_t)fc.batch * fc.width_out, 0);
+    if (!verify_fused_io(ck, fc, fc.width_out, e, true, &cover)) return false;
+    for (size_t q = 0; q < cover.size(); ++q)
+      if (cover[q] != 1) return ck.fail(cover[q] ? "Y element stored more than once" : "Y element never stored",
+                                        (int64_t)q);
+  }
+  // Factors: every unit's rows in range, and the units of a factor write
+  // every (row, column) of its output exactly once; in place, a unit writes
+  // exactly the rows it reads (no unit reads rows another unit writes).
+  for (int f = fc.nf - 1; f >= 0; --f) {
+    const int a = fc.a[f], b = fc.b[f], c = fc.c[f], d = fc.d[f];
+    const int m = b > c ? b : c;
+    const int QN = fused_pieces(m), G = 4 / QN;
+    const int win = a * c * d, wout = a * b * d;
+    if (fused_units(fc, f) != a * d * G) return ck.fail("unit count", f);
+    std::vector<uint8_t> cover((size_t)wout * 4, 0);
+    for (int u = 0; u < a * d * G; ++u) {
+      int i, j, g;
+      fused_unit(fc, f, G, u, &i, &j, &g);
+      if (i < 0 || i >= a || j < 0 || j >= d || g < 0 || g >= G) return ck.fail("unit decode", u);
+      if (i * d + j != u / G) return ck.fail("unit decode differs from the division", u);
+      std::vector<int> rin, rout;
+      for (int l = 0; l < c; ++l) {
+        const int r = fused_in_row(fc, f, i, j, l);
+        if (r < 0 || r >= win || r >= fc.buf_rows) return ck.fail("input row out of range", r);
+        rin.push_back(r);
+      }
+      for (int k = 0; k < b; ++k) {
+        const int r = fused_out_row(fc, f, i, j, k);
+        if (r < 0 || r >= wout || r >= fc.buf_rows) return ck.fail("output row out of range", r);
+        rout.push_back(r);
+        for (int q = 0; q < QN; ++q) cover[(size_t)r * 4 + g * QN + q]++;
+      }
+      if (fc.inplace) {
+        std::sort(rin.begin(), rin.end());
+        std::sort(rout.begin(), rout.end());
+        if (rin != rout) return ck.fail("in-place unit writes rows it does not read", u);
+      }
+    }
+    for (size_t q = 0; q < cover.size(); ++q)
+      if (cover[q] != 1) return ck.fail("factor output piece not written exactly once", (int64_t)q);
+  }
+  return ck.err.empty();
+}
+
+}  // namespace
+}  // namespace ks
+
+extern "C" ks_status_t ks_chain_verify(const ks_factor_t* factors, int nfactors, int64_t batch, int layout, int dtype,
+                                       char* report, size_t len) {
+  if (report && len) report[0] = 0;
+  char desc[256];
+  ks_status_t st = ks_chain_describe(factors, nfactors, batch, layout, dtype, desc, sizeof desc);
+  if (st != KS_OK) return st;
+  ks::FusedChain fc;
+  if (batch == 0 || !ks::chain_fused_plan(factors, nfactors, batch, layout, &fc)) {
+    if (report && len) snprintf(report, len, "%s", batch == 0 ? "empty" : "not fused");
+    return KS_OK;
+  }
+  ks::FusedChecker ck;
+  const bool ok = ks::verify_fused(ck, fc, dtype);
   if (report && len) snprintf(report, len, "%s", ok ? "ok" : ck.err.c_str());
   return ok ? KS_OK : KS_ERR_UNSUPPORTED;
 }

@@ -1,0 +1,75 @@
+"""Host-side checks of the fused chain path (no GPU): which chains run fused,
+the workspace they need, and a replay of the fused kernel's accesses
+(ks_chain_verify) over chain shapes, batches, layouts and storage types."""
+import pytest
+
+import paper_2405_15013_amd as ks
+
+P0 = 1 << 44
+
+
+def butterfly(L):
+    return [(2 ** (l - 1), 2, 2, 2 ** (L - l)) for l in range(1, L + 1)]
+
+
+def factors(pats):
+    return [(p, P0 + q * (1 << 30)) for q, p in enumerate(pats)]
+
+
+CHAINS = {
+    "butterfly1024": butterfly(10),
+    "butterfly8": butterfly(3),
+    "butterfly2": butterfly(1) * 2,
+    "deformable": [(2, 3, 4, 1), (1, 8, 6, 1), (3, 2, 2, 1)],      # b != c: two LDS buffers
+    "radix4": [(1, 4, 4, 16), (4, 4, 4, 4), (16, 4, 4, 1)],
+    "mixed": [(4, 8, 8, 2), (8, 2, 2, 4), (2, 4, 3, 8), (6, 4, 4, 2)],
+    "wide_inplace": [(1, 2, 2, 1024), (1024, 2, 2, 1)],            # width 2048: 160 KB of LDS, not fused
+}
+
+
+@pytest.mark.parametrize("name", sorted(CHAINS))
+@pytest.mark.parametrize("layout", ["bsl", "bsf"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("batch", [1, 15, 16, 17, 100, 4096])
+def test_fused_chain_replay(name, layout, dtype, batch):
+    f = factors(CHAINS[name])
+    desc = ks.ks_chain_describe(f, batch, layout, dtype)
+    st, rep = ks.ks_chain_verify(f, batch, layout, dtype)
+    assert st == 0, (desc, rep)
+    if desc.startswith("fused"):
+        assert rep == "ok"
+    else:
+        assert rep == "not fused"
+
+
+def test_which_chains_fuse():
+    bf = factors(butterfly(10))
+    for layout in ("bsl", "bsf"):
+        for dtype in ("f32", "bf16"):
+            assert ks.ks_chain_describe(bf, 4096, layout, dtype).startswith("fused")
+            assert ks.ks_chain_workspace_bytes(bf, 4096, dtype) == 0
+    # Monarch factors (32 x 32 blocks) run factor by factor
+    mon = factors([(1, 32, 32, 32), (32, 32, 32, 1)])
+    assert ks.ks_chain_describe(mon, 16384, "bsl", "f32").startswith("unfused")
+    assert ks.ks_chain_workspace_bytes(mon, 16384, "f32") == 1024 * 16384 * 4
+    # width 2048 with 16 fp32 columns needs 160 KB of LDS: not fused
+    assert ks.ks_chain_describe(factors(CHAINS["wide_inplace"]), 64, "bsl", "f32").startswith("unfused")
+    # a single factor is not a chain to fuse
+    assert ks.ks_chain_describe(factors(butterfly(1)), 64, "bsl", "f32").startswith("unfused")
+
+
+def test_fusion_can_be_switched_off_per_thread():
+    bf = factors(butterfly(10))
+    ks.ks_force_chain_fusion(0)
+    try:
+        assert ks.ks_chain_describe(bf, 4096, "bsl", "f32").startswith("unfused")
+        assert ks.ks_chain_workspace_bytes(bf, 4096, "f32") == 2 * 1024 * 4096 * 4
+    finally:
+        ks.ks_force_chain_fusion(None)
+    assert ks.ks_chain_describe(bf, 4096, "bsl", "f32").startswith("fused")
+    # a forced kernel variant also runs chains factor by factor
+    ks.ks_force_variant(0)
+    try:
+        assert ks.ks_chain_describe(bf, 4096, "bsl", "f32").startswith("unfused")
+    finally:
+        ks.ks_force_variant(None)

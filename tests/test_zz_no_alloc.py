@@ -44,16 +44,22 @@ def _run_both(pats, batch, dtype, layout, cfg):
 
 @pytest.mark.parametrize("layout", ["bsl", "bsf"])
 def test_noalloc_matches_workspace_chain_two_calls(layout):
-    # first call: butterfly 10-chain at batch 4096 (two 16 MiB intermediates)
-    _run_both(BUTTERFLY, 4096, "f32", layout, cfg=31)
-    # second call, smaller: Monarch 2-chain at batch 520 in bf16 (the array
-    # still holds the first call's intermediates)
-    _run_both(MONARCH, 520, "bf16", layout, cfg=32)
+    # The butterfly chain would run fused (no intermediates in memory): run
+    # chains factor by factor on this thread, so both calls use the array.
+    ks.ks_force_chain_fusion(0)
+    try:
+        # first call: butterfly 10-chain at batch 4096 (two 16 MiB intermediates)
+        _run_both(BUTTERFLY, 4096, "f32", layout, cfg=31)
+        # second call, smaller: Monarch 2-chain at batch 520 in bf16 (the array
+        # still holds the first call's intermediates)
+        _run_both(MONARCH, 520, "bf16", layout, cfg=32)
+    finally:
+        ks.ks_force_chain_fusion(None)
 
 
 def test_noalloc_rejects_chains_beyond_the_scratch_size():
     import torch
-    kds = [torch.zeros(p[0] * p[1] * p[2] * p[3], device="cuda") for p in BUTTERFLY]
-    batch = 32768  # two intermediates of 128 MiB each
-    st = ks.ks_chain_noalloc(list(zip(BUTTERFLY, kds)), 1 << 40, 2 << 40, batch, "bsl", "f32", check=False)
+    kds = [torch.zeros(p[0] * p[1] * p[2] * p[3], device="cuda") for p in MONARCH]
+    batch = 32768  # one intermediate of 128 MiB
+    st = ks.ks_chain_noalloc(list(zip(MONARCH, kds)), 1 << 40, 2 << 40, batch, "bsl", "f32", check=False)
     assert ks.STATUS_NAMES[st] == "KS_ERR_SCRATCH_LIMIT"
