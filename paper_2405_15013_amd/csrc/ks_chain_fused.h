@@ -5,16 +5,33 @@
 //
 // One workgroup owns a tile of kFusedCols batch columns and keeps the whole
 // intermediate vector of each of its columns in LDS, in fp32, for the whole
-// chain: X is read from HBM once, every factor is applied LDS -> LDS (the
-// output-stationary blocks of Algorithm 2, Section 4.1: a thread reads the c
-// inputs of one block (i, j) for its columns and writes its b outputs), and Y
-// is written once.  Factors with b == c write in place (the row set of a
-// block equals its column set, and blocks are disjoint), otherwise two LDS
-// buffers alternate.
+// chain: X is read from HBM once, the factors are applied LDS -> LDS, and Y
+// is written once.
 //
-// LDS layout: row r (an element of the intermediate vector) holds the tile's
-// kFusedCols columns at r * kFusedPitch floats (16 columns + 4 pad floats, so
-// 16-byte accesses of consecutive rows spread over all banks).
+// The factors are applied in passes.  A radix pass applies m >= 1
+// consecutive square factors with p x p blocks (applied order t = 0 .. m-1,
+// factor t of pattern (a_t, p, p, d_t)) whose strides nest: d_{t+1} = p*d_t
+// and a_t = a_{t+1}*p.  Then every block of every factor of the pass lies
+// inside one of N / P groups of P = p^m rows,
+//     rows(group) = { i*P*d_0 + j0 + d_0*r : r < P },  i < N/(P*d_0), j0 < d_0,
+// and within a group factor t mixes the register digits r_t of
+// r = sum_t r_t p^t: the p rows r + l*p^t (l < p, digit t of r zero) are the
+// inputs l of block (i*P/(p^(t+1)) + r_hi, j0 + d_0*r_lo) of factor t, where
+// r_lo < p^t and r_hi are the digits below and above t (Section 4.1 index
+// sets: inputs i*c*d + l*d + j, outputs i*b*d + k*d + j, here with b = c = p).
+// A work unit (group, 4 columns) loads its P rows into registers, applies the
+// m factors there and stores them back in place: one LDS round trip for m
+// factors.  Any other factor (b != c, or strides that do not nest) is a pass
+// of its own: a unit reads the c input rows of one block and writes its b
+// output rows, into the other LDS buffer when b != c.
+//
+// Factor values: each pass's values (its factors' packed blocks, one after
+// the other) are fetched from global memory into registers one pass ahead and
+// parked in an LDS copy as fp32 between passes.
+//
+// LDS layout: row r of the vector holds the tile's 16 columns at
+// r * kFusedPitch floats (16 columns + 4 pad floats, so 16-byte accesses of
+// consecutive rows spread over all banks); then the factor-value copy.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <cstdint>
@@ -25,12 +42,13 @@ namespace ks {
 
 constexpr int kFusedMaxFactors = 24;
 constexpr int kFusedCols = 16;
-constexpr int kFusedPitch = 20;        // floats per LDS row
-constexpr int kFusedMaxBC = 8;         // largest b and c of a fused factor
-constexpr int kFusedMaxLds = 128 * 1024;
-constexpr int kFusedThreads = 1024;                              // threads per workgroup
-constexpr int kFusedKPerThread = 4;                              // factor values fetched per thread
-constexpr int kFusedKValues = kFusedThreads * kFusedKPerThread;  // largest a*b*c*d of a fused factor (4096)
+constexpr int kFusedPitch = 20;                                  // floats per LDS row
+constexpr int kFusedMaxBC = 8;                                   // largest b and c of a fused factor
+constexpr int kFusedMaxLds = 160 * 1024;
+constexpr int kFusedThreads = 512;                               // threads per workgroup
+constexpr int kFusedKPerThread = 16;                             // factor values fetched per thread and pass
+constexpr int kFusedKValues = kFusedThreads * kFusedKPerThread;  // largest value count of a pass (8192)
+constexpr int kFusedMaxGroup = 8;                                // largest P = p^m of a radix pass
 
 struct FusedChain {
   int nf;                   // factors, in product order (factor nf-1 is applied first)
@@ -43,17 +61,50 @@ struct FusedChain {
   uint32_t md[kFusedMaxFactors];  // multiply-shift constants of the division by d
   int sd[kFusedMaxFactors];
   const void* kv[kFusedMaxFactors];
+  // passes, in application order; pass q applies factors pf0[q], pf0[q]-1, ...
+  // (pm[q] of them); radix passes have pp[q] = p >= 2 and group size pP[q]
+  int npass;
+  int pf0[kFusedMaxFactors], pm[kFusedMaxFactors], pp[kFusedMaxFactors], pP[kFusedMaxFactors];
+  int pk[kFusedMaxFactors];       // factor values of the pass (sum over its factors)
+  int pcnt[kFusedMaxFactors];     // values of each factor of the pass (a*b*c*d, equal within a pass)
+  uint32_t mgd[kFusedMaxFactors];  // multiply-shift division by the pass's d_0
+  int sgd[kFusedMaxFactors];
   const void* x;
   void* y;
 };
 
+// Radix pass q: is it one (pp[q] >= 2)?  Its first factor's d is d_0.
+__host__ __device__ __forceinline__ bool fused_is_radix(const FusedChain& fc, int q) { return fc.pp[q] >= 2; }
+
+// Work units of radix pass q: (group, 16-byte piece), piece fastest.
+__host__ __device__ __forceinline__ int fused_radix_units(const FusedChain& fc, int q) {
+  const int f0 = fc.pf0[q];
+  const int N = fc.a[f0] * fc.c[f0] * fc.d[f0];
+  return N / fc.pP[q] * 4;
+}
+// Group g of radix pass q -> (i, j0): its rows are i*P*d_0 + j0 + d_0*r.
+__host__ __device__ __forceinline__ void fused_radix_group(const FusedChain& fc, int q, int g, int* i, int* j0) {
+  *i = (int)div_fast((uint32_t)g, fc.mgd[q], fc.sgd[q]);
+  *j0 = g - *i * fc.d[fc.pf0[q]];
+}
+// Block index (i_t * d_t + j_t) of factor t of a radix pass with group size
+// P and radix PR, acting on the register run r, r + p^t, ..., r + (p-1)*p^t
+// (digit t of r zero) of group (i, j0); d_t = d_0 * p^t.
+template <int P, int PR>
+__host__ __device__ __forceinline__ int fused_radix_block(int i, int j0, int d0, int t, int r) {
+  int st = 1;
+  for (int u = 0; u < t; ++u) st *= PR;
+  const int lo = r % st, hi = r / (st * PR);
+  return (i * (P / (st * PR)) + hi) * (d0 * st) + j0 + d0 * lo;
+}
+
 // 16-byte pieces (4 columns each) of one LDS row handled by one work unit of
-// a factor with blocks of at most m x m: two for m <= 2, one otherwise (enough
-// units for the workgroup's threads, inputs and accumulators within the
-// register budget of 1024-thread workgroups).
+// a single-factor pass with blocks of at most m x m: two for m <= 2, one
+// otherwise.
 __host__ __device__ __forceinline__ int fused_pieces(int m) { return m <= 2 ? 2 : 1; }
 
-// Work units of factor f: (block ij, group of pieces), group fastest.
+// Work units of a single-factor pass over factor f: (block ij, group of
+// pieces), group fastest.
 __host__ __device__ __forceinline__ int fused_units(const FusedChain& fc, int f) {
   const int bc = fc.b[f] > fc.c[f] ? fc.b[f] : fc.c[f];
   return fc.a[f] * fc.d[f] * (4 / fused_pieces(bc));
@@ -94,13 +145,12 @@ __host__ __device__ __forceinline__ void fused_vec_unit(int layout, int E, int u
   }
 }
 
-// LDS layout: the vector buffer(s), then two fp32 copies of factor values
-// (the factor being applied and the next one).
+// LDS layout: the vector buffer(s), then the current pass's factor values.
 __host__ __device__ __forceinline__ int fused_kbuf_offset(const FusedChain& fc) {
   return (fc.inplace ? 1 : 2) * fc.buf_rows * kFusedPitch;  // floats
 }
 __host__ __device__ __forceinline__ int fused_lds_bytes(const FusedChain& fc) {
-  return (fused_kbuf_offset(fc) + 2 * kFusedKValues) * 4;
+  return (fused_kbuf_offset(fc) + kFusedKValues) * 4;
 }
 
 }  // namespace ks

@@ -99,22 +99,33 @@ __device__ __forceinline__ void fused_store(const FusedChain& fc, const float* l
   }
 }
 
-// Values of factor f: this thread's share (elements tid + kFusedThreads*r) fetched into
-// registers, later parked in an LDS buffer as fp32.
+// Values of pass q (its factors' packed blocks, one after the other): this
+// thread's share (elements tid + kFusedThreads*r) fetched into registers,
+// later parked in the LDS copy as fp32.
 template <typename T>
 struct FusedK {
   float v[kFusedKPerThread];
-  __device__ __forceinline__ void fetch(const FusedChain& fc, int f) {
-    const T* __restrict__ kv = static_cast<const T*>(fc.kv[f]);
-    const int n = fc.a[f] * fc.d[f] * fc.b[f] * fc.c[f];
+  __device__ __forceinline__ void fetch(const FusedChain& fc, int q) {
+    // A pass has at most three factors: their value pointers are selected per
+    // element (no per-lane indexing into the kernel arguments).
+    const int n = fc.pk[q], cnt = fc.pcnt[q], f0 = fc.pf0[q], m = fc.pm[q];
+    const T* k0 = static_cast<const T*>(fc.kv[f0]);
+    const T* k1 = m > 1 ? static_cast<const T*>(fc.kv[f0 - 1]) : k0;
+    const T* k2 = m > 2 ? static_cast<const T*>(fc.kv[f0 - 2]) : k0;
 #pragma unroll
     for (int r = 0; r < kFusedKPerThread; ++r) {
       const int e = r * kFusedThreads + (int)threadIdx.x;
-      v[r] = e < n ? to_f32(kv[e]) : 0.f;
+      if (e < n) {
+        const int t = e >= 2 * cnt ? 2 : (e >= cnt ? 1 : 0);
+        const T* kp = t == 0 ? k0 : (t == 1 ? k1 : k2);
+        v[r] = to_f32(kp[e - t * cnt]);
+      } else {
+        v[r] = 0.f;
+      }
     }
   }
-  __device__ __forceinline__ void park(const FusedChain& fc, int f, float* kbuf) const {
-    const int n = fc.a[f] * fc.d[f] * fc.b[f] * fc.c[f];
+  __device__ __forceinline__ void park(const FusedChain& fc, int q, float* kbuf) const {
+    const int n = fc.pk[q];
 #pragma unroll
     for (int r = 0; r < kFusedKPerThread; ++r) {
       const int e = r * kFusedThreads + (int)threadIdx.x;
@@ -122,6 +133,55 @@ struct FusedK {
     }
   }
 };
+
+// Radix pass q (see ks_chain_fused.h): unit (group g, piece) loads the group's
+// P rows (4 columns) into registers, applies the pass's factors t = 0 .. M-1
+// (p x p blocks, M = log_p P) on register runs, stores the rows in place.
+template <int P, int PR>
+__device__ __forceinline__ void fused_radix_pass(const FusedChain& fc, int q, float* buf, const float* kbuf) {
+  constexpr int M = PR == P ? 1 : (PR * PR == P ? 2 : 3);
+  static_assert(M == 1 || M == 2 || (M == 3 && PR * PR * PR == P), "P must be a power of PR");
+  const int d0 = fc.d[fc.pf0[q]], cnt = fc.pcnt[q];
+  const int units = fused_radix_units(fc, q);
+  for (int u = threadIdx.x; u < units; u += kFusedThreads) {
+    const int g = u >> 2, piece = u & 3;
+    int i, j0;
+    fused_radix_group(fc, q, g, &i, &j0);
+    float* rows = buf + (i * P * d0 + j0) * kFusedPitch + piece * 4;
+    const int rstep = d0 * kFusedPitch;
+    f32x4 v[P];
+#pragma unroll
+    for (int r = 0; r < P; ++r) v[r] = *reinterpret_cast<const f32x4*>(rows + r * rstep);
+#pragma unroll
+    for (int t = 0; t < M; ++t) {
+      const int st = t == 0 ? 1 : (t == 1 ? PR : PR * PR);
+      const float* kt = kbuf + t * cnt;
+#pragma unroll
+      for (int r = 0; r < P; ++r) {
+        if ((r / st) % PR != 0) continue;  // digit t of r must be zero
+        const float* kb = kt + fused_radix_block<P, PR>(i, j0, d0, t, r) * (PR * PR);
+        f32x4 in[PR];
+#pragma unroll
+        for (int l = 0; l < PR; ++l) in[l] = v[r + l * st];
+#pragma unroll
+        for (int k = 0; k < PR; ++k) {
+          f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int l = 0; l < PR; ++l) {
+            const float kk = kb[k * PR + l];
+            acc[0] = __builtin_fmaf(kk, in[l][0], acc[0]);
+            acc[1] = __builtin_fmaf(kk, in[l][1], acc[1]);
+            acc[2] = __builtin_fmaf(kk, in[l][2], acc[2]);
+            acc[3] = __builtin_fmaf(kk, in[l][3], acc[3]);
+          }
+          v[r + k * st] = acc;
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < P; ++r) *reinterpret_cast<f32x4*>(rows + r * rstep) = v[r];
+  }
+}
 
 // One factor, LDS -> LDS: unit (ij, g) reads the c input rows of block
 // (i, j) = (ij / d, ij % d), pieces g*QN .. g*QN+QN-1 (4 columns each), and
@@ -189,31 +249,51 @@ __device__ __forceinline__ void fused_apply(const FusedChain& fc, int f, const f
   else fused_factor<8, 8, 1, false>(fc, f, src, dst, kbuf);
 }
 
+// Radix pass with its instance (group size P, radix p).
+__device__ __forceinline__ void fused_radix_apply(const FusedChain& fc, int q, float* buf, const float* kbuf) {
+  const int P = fc.pP[q], p = fc.pp[q];
+  if (p == 2) {
+    if (P == 8) fused_radix_pass<8, 2>(fc, q, buf, kbuf);
+    else if (P == 4) fused_radix_pass<4, 2>(fc, q, buf, kbuf);
+    else fused_radix_pass<2, 2>(fc, q, buf, kbuf);
+  } else if (p == 4) {
+    fused_radix_pass<4, 4>(fc, q, buf, kbuf);
+  } else {
+    fused_radix_pass<8, 8>(fc, q, buf, kbuf);
+  }
+}
+
 template <typename T, int LAYOUT, bool VEC>
 __global__ __launch_bounds__(kFusedThreads) void ks_chain_fused_kernel(FusedChain fc) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   const int col0 = blockIdx.x * kFusedCols;
-  // src holds the current vector; factors write dst (the same buffer in place)
+  // src holds the current vector; single-factor passes with b != c write dst
   float* src = lds;
   float* dst = fc.inplace ? lds : lds + fc.buf_rows * kFusedPitch;
-  float* kcur = lds + fused_kbuf_offset(fc);
-  float* knext = kcur + kFusedKValues;
+  float* kbuf = lds + fused_kbuf_offset(fc);
   FusedK<T> kr;
-  kr.fetch(fc, fc.nf - 1);
+  kr.fetch(fc, 0);
   fused_load<T, LAYOUT, VEC>(fc, src, col0);
-  kr.park(fc, fc.nf - 1, kcur);
+  kr.park(fc, 0, kbuf);
   __syncthreads();
-  for (int f = fc.nf - 1; f >= 0; --f) {
-    if (f > 0) kr.fetch(fc, f - 1);  // in flight during this factor
-    fused_apply(fc, f, src, dst, kcur);
-    if (f > 0) kr.park(fc, f - 1, knext);
+  for (int q = 0; q < fc.npass; ++q) {
+    const bool more = q + 1 < fc.npass;
+    if (more) kr.fetch(fc, q + 1);  // in flight during this pass
+    if (fused_is_radix(fc, q)) {
+      fused_radix_apply(fc, q, src, kbuf);
+    } else {
+      fused_apply(fc, fc.pf0[q], src, dst, kbuf);
+      if (!fc.inplace) {
+        float* t = src;
+        src = dst;
+        dst = t;
+      }
+    }
     __syncthreads();
-    float* t = src;
-    src = dst;
-    dst = t;
-    t = kcur;
-    kcur = knext;
-    knext = t;
+    if (more) {
+      kr.park(fc, q + 1, kbuf);
+      __syncthreads();
+    }
   }
   fused_store<T, LAYOUT, VEC>(fc, src, col0);
 }

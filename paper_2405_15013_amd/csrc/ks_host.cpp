@@ -323,12 +323,11 @@ namespace ks {
 void set_last_hip_error(int e) { g_last_hip_error = e; }
 
 // The fused chain kernel (ks_chain_fused.h) takes chains of two or more
-// factors whose blocks are at most 8 x 8, with at most 4096 values per factor,
-// and whose widest vector, for 16 batch columns in fp32, fits the kernel's LDS
-// next to two copies of factor values (in place when every factor has b == c,
-// else two buffers).  Not used while a kernel variant is forced or
+// factors whose blocks are at most 8 x 8 and whose widest vector, for 16
+// batch columns in fp32, fits the kernel's 160 KB of LDS next to one pass's
+// factor values (in place when every factor has b == c, else two buffers).  Not used while a kernel variant is forced or
 // fusion is switched off on this thread.  Fills the pattern part of `fc`.
-bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, FusedChain* fc) {
+bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, int dtype, FusedChain* fc) {
   if (g_forced_variant >= 0 || g_chain_fusion == 0) return false;
   if (n < 2 || n > kFusedMaxFactors) return false;
   int64_t wmax = 0;
@@ -336,11 +335,10 @@ bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, Fu
   for (int q = 0; q < n; ++q) {
     if (f[q].b > kFusedMaxBC || f[q].c > kFusedMaxBC) return false;
     const int64_t N = f[q].a * f[q].c * f[q].d, M = f[q].a * f[q].b * f[q].d;
-    if (f[q].a * f[q].d * f[q].b * f[q].c > kFusedKValues) return false;
     wmax = std::max(wmax, std::max(N, M));
     inplace = inplace && f[q].b == f[q].c;
   }
-  if (((inplace ? 1 : 2) * wmax * kFusedPitch + 2 * kFusedKValues) * 4 > kFusedMaxLds) return false;
+  if (((inplace ? 1 : 2) * wmax * kFusedPitch + kFusedKValues) * 4 > kFusedMaxLds) return false;
   if ((batch + kFusedCols - 1) / kFusedCols > 0x7fffffff) return false;
   fc->nf = n;
   fc->batch = (int)batch;
@@ -354,7 +352,40 @@ bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, Fu
     div_magic((uint32_t)f[q].d, &fc->md[q], &fc->sd[q]);
     fc->kv[q] = f[q].K_values;
   }
-  return true;
+  // Passes in application order (factor n-1 first): runs of square p x p
+  // factors (p in {2, 4, 8}) whose strides nest (d of the next = p * d,
+  // a of the previous = p * a of the next), up to 3 factors for p = 2 (one
+  // for p = 4, 8); every other factor alone.
+  int np = 0;
+  for (int q = n - 1; q >= 0;) {
+    const int p = fc->b[q];
+    int m = 1;
+    if (fc->b[q] == fc->c[q] && (p == 2 || p == 4 || p == 8)) {
+      const int maxm = p == 2 ? 3 : 1;
+      while (m < maxm && q - m >= 0) {
+        const int g = q - m, prev = q - m + 1;
+        if (fc->b[g] == p && fc->c[g] == p && fc->d[g] == p * fc->d[prev] && fc->a[prev] == p * fc->a[g]) ++m;
+        else break;
+      }
+      int P = 1;
+      for (int t = 0; t < m; ++t) P *= p;
+      fc->pp[np] = p;
+      fc->pP[np] = P;
+    } else {
+      fc->pp[np] = 0;
+      fc->pP[np] = 1;
+    }
+    fc->pf0[np] = q;
+    fc->pm[np] = m;
+    fc->pcnt[np] = fc->a[q] * fc->d[q] * fc->b[q] * fc->c[q];
+    fc->pk[np] = m * fc->pcnt[np];
+    if (fc->pk[np] > kFusedKValues) return false;
+    div_magic((uint32_t)fc->d[q], &fc->mgd[np], &fc->sgd[np]);
+    ++np;
+    q -= m;
+  }
+  fc->npass = np;
+  return fused_lds_bytes(*fc) <= kFusedMaxLds;
 }
 
 // 16-byte vectors for the fused kernel's loads and stores: aligned buffers and
@@ -375,7 +406,7 @@ ks_status_t chain_impl(const ks_factor_t* factors, int nfactors, const void* X, 
   for (int q = 0; q < nfactors; ++q)
     if (factors[q].K_values == nullptr) return KS_ERR_INVALID_ARG;
   FusedChain fc;
-  const bool fused = chain_fused_plan(factors, nfactors, batch, layout, &fc);
+  const bool fused = chain_fused_plan(factors, nfactors, batch, layout, dtype, &fc);
   const size_t need = (fused || nfactors <= 1) ? 0 : (nfactors == 2 ? per : 2 * per);
   if (batch == 0) return KS_OK;
   if (X == nullptr || Y == nullptr) return KS_ERR_INVALID_ARG;
@@ -443,7 +474,7 @@ size_t ks_chain_workspace_bytes(const ks_factor_t* factors, int nfactors, int64_
   if (chain_check(factors, nfactors, batch, dtype, &per) != KS_OK) return 0;
   if (nfactors <= 1) return 0;
   FusedChain fc;
-  if (chain_fused_plan(factors, nfactors, batch, KS_LAYOUT_BSL, &fc)) return 0;  // layout-independent
+  if (chain_fused_plan(factors, nfactors, batch, KS_LAYOUT_BSL, dtype, &fc)) return 0;  // layout-independent
   return nfactors == 2 ? per : 2 * per;
 }
 
@@ -458,9 +489,16 @@ ks_status_t ks_chain_describe(const ks_factor_t* factors, int nfactors, int64_t 
   if (st != KS_OK) return st;
   if (layout != KS_LAYOUT_BSF && layout != KS_LAYOUT_BSL) return KS_ERR_UNSUPPORTED;
   FusedChain fc;
-  if (chain_fused_plan(factors, nfactors, batch, layout, &fc)) {
-    snprintf(buf, len, "fused factors=%d inplace=%d lds=%d grid=%lld block=%d cols=%d", fc.nf, fc.inplace,
-             fused_lds_bytes(fc), (long long)((batch + kFusedCols - 1) / kFusedCols), kFusedThreads, kFusedCols);
+  if (chain_fused_plan(factors, nfactors, batch, layout, dtype, &fc)) {
+    std::string passes;
+    for (int q = 0; q < fc.npass; ++q) {
+      char pb[32];
+      snprintf(pb, sizeof pb, "%s%d", q ? "," : "", fc.pp[q] ? fc.pP[q] : -fc.b[fc.pf0[q]]);
+      passes += pb;
+    }
+    snprintf(buf, len, "fused factors=%d passes=%d groups=%s inplace=%d lds=%d grid=%lld block=%d cols=%d",
+             fc.nf, fc.npass, passes.c_str(), fc.inplace, fused_lds_bytes(fc),
+             (long long)((batch + kFusedCols - 1) / kFusedCols), kFusedThreads, kFusedCols);
   } else {
     snprintf(buf, len, "unfused factors=%d workspace=%zu", nfactors, nfactors <= 1 ? (size_t)0 : (nfactors == 2 ? per : 2 * per));
   }

@@ -517,7 +517,7 @@ extern "C" ks_status_t ks_plan_verify(int64_t a, int64_t b, int64_t c, int64_t d
 #include "ks_chain_fused.h"
 
 namespace ks {
-bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, FusedChain* fc);
+bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, int dtype, FusedChain* fc);
 namespace {
 
 struct FusedChecker {
@@ -579,8 +579,6 @@ bool verify_fused(FusedChecker& ck, const FusedChain& fc, int dtype) {
   for (int f = 0; f + 1 < fc.nf; ++f)
     if (fc.a[f] * fc.c[f] * fc.d[f] != fc.a[f + 1] * fc.b[f + 1] * fc.d[f + 1]) return ck.fail("widths", f);
   if (fused_lds_bytes(fc) > kFusedMaxLds) return ck.fail("LDS", fused_lds_bytes(fc));
-  for (int f = 0; f < fc.nf; ++f)
-    if (fc.a[f] * fc.d[f] * fc.b[f] * fc.c[f] > kFusedKValues) return ck.fail("factor values exceed the LDS copy", f);
   // Vector rows end where the factor-value copies begin.
   if (fused_kbuf_offset(fc) < (fc.inplace ? 1 : 2) * fc.buf_rows * kFusedPitch) return ck.fail("LDS overlap", 0);
   // Tile I/O, both forms the host may choose (vector form only when the
@@ -596,10 +594,91 @@ bool verify_fused(FusedChecker& ck, const FusedChain& fc, int dtype) {
       if (cover[q] != 1) return ck.fail(cover[q] ? "Y element stored more than once" : "Y element never stored",
                                         (int64_t)q);
   }
-  // Factors: every unit's rows in range, and the units of a factor write
-  // every (row, column) of its output exactly once; in place, a unit writes
-  // exactly the rows it reads (no unit reads rows another unit writes).
-  for (int f = fc.nf - 1; f >= 0; --f) {
+  // Passes cover the factors in application order, each exactly once.
+  {
+    int next = fc.nf - 1;
+    for (int q = 0; q < fc.npass; ++q) {
+      if (fc.pf0[q] != next || fc.pm[q] < 1) return ck.fail("passes do not follow the factors", q);
+      int kn = 0;
+      for (int t = 0; t < fc.pm[q]; ++t) {
+        const int f = fc.pf0[q] - t;
+        if (fc.a[f] * fc.b[f] * fc.c[f] * fc.d[f] != fc.pcnt[q]) return ck.fail("pass value count", q);
+        kn += fc.pcnt[q];
+      }
+      if (kn != fc.pk[q] || kn > kFusedKValues) return ck.fail("pass values exceed the LDS copy", q);
+      next -= fc.pm[q];
+    }
+    if (next != -1) return ck.fail("passes do not cover the chain", next);
+  }
+  for (int q = 0; q < fc.npass; ++q) {
+    if (fused_is_radix(fc, q)) {
+      // Radix pass: every unit's P rows in range, the groups partition the
+      // vector, and for every factor of the pass each (block, input l) pair
+      // is visited exactly once per piece, at the rows the index sets give.
+      const int f0 = fc.pf0[q], p = fc.pp[q], P = fc.pP[q], m = fc.pm[q], d0 = fc.d[f0];
+      const int N = fc.a[f0] * fc.c[f0] * d0;
+      int PP = 1;
+      for (int t = 0; t < m; ++t) PP *= p;
+      if (PP != P || P > kFusedMaxGroup) return ck.fail("radix group size", q);
+      if (!((p == 2 && (P == 2 || P == 4 || P == 8)) || (p == 4 && P == 4) || (p == 8 && P == 8)))
+        return ck.fail("no kernel instance for this radix pass", q);
+      for (int t = 0; t < m; ++t) {
+        const int f = f0 - t;
+        int st = 1;
+        for (int u = 0; u < t; ++u) st *= p;
+        if (fc.b[f] != p || fc.c[f] != p || fc.d[f] != d0 * st || fc.a[f] * p * st != fc.a[f0] * p)
+          return ck.fail("radix pass strides do not nest", f);
+      }
+      if (fused_radix_units(fc, q) != N / P * 4) return ck.fail("radix unit count", q);
+      std::vector<uint8_t> rowcover((size_t)N * 4, 0);
+      std::vector<std::vector<uint8_t>> blkcover(m, std::vector<uint8_t>((size_t)N * 4, 0));  // a*d blocks x p inputs = N
+      for (int u = 0; u < fused_radix_units(fc, q); ++u) {
+        const int g = u >> 2, piece = u & 3;
+        int i, j0;
+        fused_radix_group(fc, q, g, &i, &j0);
+        if (i < 0 || j0 < 0 || j0 >= d0 || (int64_t)i * P * d0 + j0 + (int64_t)d0 * (P - 1) >= N)
+          return ck.fail("radix group out of range", g);
+        if (i != g / d0 || j0 != g % d0) return ck.fail("radix group decode differs from the division", g);
+        const int base = i * P * d0 + j0;
+        for (int r = 0; r < P; ++r) rowcover[(size_t)(base + d0 * r) * 4 + piece]++;
+        for (int t = 0; t < m; ++t) {
+          const int f = f0 - t;
+          int st = 1;
+          for (int uu = 0; uu < t; ++uu) st *= p;
+          for (int r = 0; r < P; ++r) {
+            if ((r / st) % p != 0) continue;
+            int blk = -1;
+            switch (P * 16 + p) {
+              case 2 * 16 + 2: blk = fused_radix_block<2, 2>(i, j0, d0, t, r); break;
+              case 4 * 16 + 2: blk = fused_radix_block<4, 2>(i, j0, d0, t, r); break;
+              case 8 * 16 + 2: blk = fused_radix_block<8, 2>(i, j0, d0, t, r); break;
+              case 4 * 16 + 4: blk = fused_radix_block<4, 4>(i, j0, d0, t, r); break;
+              case 8 * 16 + 8: blk = fused_radix_block<8, 8>(i, j0, d0, t, r); break;
+            }
+            if (blk < 0 || blk >= fc.a[f] * fc.d[f]) return ck.fail("radix block out of range", blk);
+            const int it = blk / fc.d[f], jt = blk % fc.d[f];
+            for (int l = 0; l < p; ++l) {
+              if (base + d0 * (r + l * st) != fused_in_row(fc, f, it, jt, l))
+                return ck.fail("radix register row is not the block's input row", r + l * st);
+              if (fused_in_row(fc, f, it, jt, l) != fused_out_row(fc, f, it, jt, l))
+                return ck.fail("radix block not square", f);
+              blkcover[t][((size_t)blk * p + l) * 4 + piece]++;
+            }
+          }
+        }
+      }
+      for (size_t e = 0; e < rowcover.size(); ++e)
+        if (rowcover[e] != 1) return ck.fail("radix pass row piece not held exactly once", (int64_t)e);
+      for (int t = 0; t < m; ++t)
+        for (size_t e = 0; e < blkcover[t].size(); ++e)
+          if (blkcover[t][e] != 1) return ck.fail("radix factor input not used exactly once", (int64_t)e);
+      continue;
+    }
+    // Single-factor pass: every unit's rows in range, and the units write
+    // every (row, column) of the factor's output exactly once; in place, a
+    // unit writes exactly the rows it reads (no unit reads rows another unit
+    // writes).
+    const int f = fc.pf0[q];
     const int a = fc.a[f], b = fc.b[f], c = fc.c[f], d = fc.d[f];
     const int m = b > c ? b : c;
     const int QN = fused_pieces(m), G = 4 / QN;
@@ -621,7 +700,7 @@ bool verify_fused(FusedChecker& ck, const FusedChain& fc, int dtype) {
         const int r = fused_out_row(fc, f, i, j, k);
         if (r < 0 || r >= wout || r >= fc.buf_rows) return ck.fail("output row out of range", r);
         rout.push_back(r);
-        for (int q = 0; q < QN; ++q) cover[(size_t)r * 4 + g * QN + q]++;
+        for (int qn = 0; qn < QN; ++qn) cover[(size_t)r * 4 + g * QN + qn]++;
       }
       if (fc.inplace) {
         std::sort(rin.begin(), rin.end());
@@ -629,8 +708,8 @@ bool verify_fused(FusedChecker& ck, const FusedChain& fc, int dtype) {
         if (rin != rout) return ck.fail("in-place unit writes rows it does not read", u);
       }
     }
-    for (size_t q = 0; q < cover.size(); ++q)
-      if (cover[q] != 1) return ck.fail("factor output piece not written exactly once", (int64_t)q);
+    for (size_t e = 0; e < cover.size(); ++e)
+      if (cover[e] != 1) return ck.fail("factor output piece not written exactly once", (int64_t)e);
   }
   return ck.err.empty();
 }
@@ -645,7 +724,7 @@ extern "C" ks_status_t ks_chain_verify(const ks_factor_t* factors, int nfactors,
   ks_status_t st = ks_chain_describe(factors, nfactors, batch, layout, dtype, desc, sizeof desc);
   if (st != KS_OK) return st;
   ks::FusedChain fc;
-  if (batch == 0 || !ks::chain_fused_plan(factors, nfactors, batch, layout, &fc)) {
+  if (batch == 0 || !ks::chain_fused_plan(factors, nfactors, batch, layout, dtype, &fc)) {
     if (report && len) snprintf(report, len, "%s", batch == 0 ? "empty" : "not fused");
     return KS_OK;
   }
