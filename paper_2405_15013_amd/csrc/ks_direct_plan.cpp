@@ -7,6 +7,7 @@
 // wavefronts read the same X tile) against registers and parallelism.
 #include "ks_direct_index.h"
 #include "ks_internal.h"
+#include "ks_masked_index.h"
 
 namespace ks {
 
@@ -16,6 +17,9 @@ hipError_t launch_direct_bf16(const Problem& p, const DirectTile& t, int V, bool
                               hipStream_t s);
 hipError_t launch_direct_f16(const Problem& p, const DirectTile& t, int V, bool strided, int mt, unsigned grid,
                              hipStream_t s);
+hipError_t launch_masked_f32(const Problem& p, const MaskedTile& t, int V, unsigned grid, hipStream_t s);
+hipError_t launch_masked_bf16(const Problem& p, const MaskedTile& t, int V, unsigned grid, hipStream_t s);
+hipError_t launch_masked_f16(const Problem& p, const MaskedTile& t, int V, unsigned grid, hipStream_t s);
 
 // Largest MT instantiated for (storage size, layout, V); keep in sync with
 // direct_mt_max() in ks_direct.h.
@@ -88,6 +92,58 @@ bool plan_direct(const Problem& p, bool al16, Plan* pl) {
   pl->grid = (unsigned)grid;
   pl->xcd_remap = 0;
   return true;
+}
+
+// Masked register-direct kernel (ks_masked.h): blocks larger than the VALU
+// kernels take (b or c > 16) that the other MFMA kernels cannot run.  The
+// access width V is the widest the layout, the batch (BSL) or d (BSF) and the
+// buffers' alignment allow (up to 16 bytes along the batch in BSL, up to 4
+// consecutive j in BSF), 8-byte pieces only for 16-bit BSL.
+int masked_vec(const Problem& p) {
+  const int s = p.dtype == F32 ? 4 : 2;
+  const int vmax = p.layout == BSL ? 16 / s : 4;
+  int V = vmax;
+  for (; V > 1; V /= 2) {
+    if (p.layout == BSL && p.batch % V) continue;
+    if (p.layout == BSF && p.d % V) continue;
+    if (V * s >= 8 && p.align % (V * s)) continue;  // vector accesses need their alignment
+    // 8-byte pieces measured slower than element pieces here except for
+    // 16-bit batch-size-last runs (e.g. fp32 BSF (6,64,16,8) at batch 25088:
+    // 2.0 ms with 8-byte pieces, 0.68 ms with 4-byte ones)
+    if (V * s == 8 && !(p.layout == BSL && s == 2)) continue;
+    break;
+  }
+  return V;
+}
+
+bool plan_masked(const Problem& p, Plan* pl) {
+  if (p.b <= 16 && p.c <= 16 && (p.b % 16 || p.c % 16)) return false;  // the VALU kernels' blocks
+  const int V = masked_vec(p);
+  const MaskedTile t = masked_tile(p, V);
+  const int64_t items = (int64_t)t.nbt * p.a * t.jgroups * t.kgroups;
+  if (items > 0x7fffffff - 3) return false;
+  pl->variant = V_MASKED;
+  pl->vec = V;
+  pl->unroll = 0;
+  pl->waves_m = 1;
+  pl->waves_n = t.kgroups;
+  pl->bt = p.layout == BSL ? 16 * V : 16;
+  pl->jg = p.layout == BSL ? 1 : V;
+  pl->lds_bytes = 0;
+  pl->block = 256;
+  pl->grid = (unsigned)((items + 3) / 4);
+  pl->xcd_remap = 0;
+  return true;
+}
+
+hipError_t launch_masked(const Problem& p, const Plan& pl, hipStream_t s) {
+  const MaskedTile t = masked_tile(p, pl.vec);
+  switch (p.dtype) {
+    case F32: return launch_masked_f32(p, t, pl.vec, pl.grid, s);
+    case BF16: return launch_masked_bf16(p, t, pl.vec, pl.grid, s);
+    case F16: return launch_masked_f16(p, t, pl.vec, pl.grid, s);
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_direct(const Problem& p, const Plan& pl, hipStream_t s) {

@@ -109,6 +109,7 @@ bool plan_valu_bsf(const Problem& p, bool al16, Plan* pl) {
 bool plan_direct(const Problem& p, bool al16, Plan* pl);
 bool plan_staged(const Problem& p, bool al16, Plan* pl);
 bool plan_dma(const Problem& p, bool al16, Plan* pl);
+bool plan_masked(const Problem& p, Plan* pl);
 namespace {
 
 bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
@@ -119,6 +120,7 @@ bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
     case V_DIRECT: return plan_direct(p, al16, pl);
     case V_STAGED: return plan_staged(p, al16, pl);
     case V_DMA: return plan_dma(p, al16, pl);
+    case V_MASKED: return plan_masked(p, pl);
     default: return false;
   }
 }
@@ -126,8 +128,10 @@ bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
 // Automatic choice: MFMA block GEMM when b and c make each (i, j) block a real
 // dense contraction (batch-size-first through LDS: DMA-fed for d <= 16,
 // register-staged beyond; register-direct for batch-size-last and small
-// batch-size-first problems); VALU kernels for small blocks; the generic
-// kernel for whatever is left.
+// batch-size-first problems); VALU kernels for small blocks; the masked
+// register-direct kernel for larger blocks the others cannot take (b or c not
+// a multiple of 16, odd batches, unaligned buffers); the generic kernel only
+// when forced.
 bool plan_auto(const Problem& p, bool al16, Plan* pl) {
   // Batch-size-first with d <= 2: the DMA kernel from 8 MB of X + Y up
   // (measured: below that the register-direct items' shorter latency wins).
@@ -137,21 +141,22 @@ bool plan_auto(const Problem& p, bool al16, Plan* pl) {
   if (plan_direct(p, al16, pl)) return true;
   if (p.layout == BSL && plan_valu_bsl(p, al16, pl)) return true;
   if (p.layout == BSF && plan_valu_bsf(p, al16, pl)) return true;
+  if (plan_masked(p, pl)) return true;
   return plan_generic(p, pl);
 }
 
 struct PlanKey {
   int64_t a, b, c, d, batch;
-  int layout, dtype, al16, forced;
+  int layout, dtype, al16, align, forced;
   bool operator==(const PlanKey& o) const {
     return a == o.a && b == o.b && c == o.c && d == o.d && batch == o.batch && layout == o.layout &&
-           dtype == o.dtype && al16 == o.al16 && forced == o.forced;
+           dtype == o.dtype && al16 == o.al16 && align == o.align && forced == o.forced;
   }
 };
 struct PlanKeyHash {
   size_t operator()(const PlanKey& k) const {
     uint64_t h = 1469598103934665603ull;
-    const int64_t v[9] = {k.a, k.b, k.c, k.d, k.batch, k.layout, k.dtype, k.al16, k.forced};
+    const int64_t v[10] = {k.a, k.b, k.c, k.d, k.batch, k.layout, k.dtype, k.al16, k.align, k.forced};
     for (int64_t x : v) { h ^= (uint64_t)x; h *= 1099511628211ull; }
     return (size_t)h;
   }
@@ -163,7 +168,7 @@ std::unordered_map<PlanKey, Plan, PlanKeyHash>* g_plans = nullptr;
 // Returns false when a forced variant cannot run the problem.
 bool get_plan(const Problem& p, bool al16, Plan* out) {
   const int forced = g_forced_variant;
-  PlanKey key{p.a, p.b, p.c, p.d, p.batch, p.layout, p.dtype, al16 ? 1 : 0, forced};
+  PlanKey key{p.a, p.b, p.c, p.d, p.batch, p.layout, p.dtype, al16 ? 1 : 0, p.align, forced};
   {
     std::lock_guard<std::mutex> lk(g_plan_mu);
     if (!g_plans) g_plans = new std::unordered_map<PlanKey, Plan, PlanKeyHash>();
@@ -187,6 +192,7 @@ hipError_t launch(const Problem& p, const Plan& pl, hipStream_t s) {
     case V_DIRECT: return launch_direct(p, pl, s);
     case V_STAGED: return launch_staged(p, pl, s);
     case V_DMA: return launch_dma(p, pl, s);
+    case V_MASKED: return launch_masked(p, pl, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -215,6 +221,8 @@ ks_status_t validate(int64_t a, int64_t b, int64_t c, int64_t d, const void* kv,
   p->N = (int)dm.N; p->M = (int)dm.M;
   p->layout = layout; p->dtype = dtype;
   p->kv = kv; p->x = x; p->y = y;
+  const uintptr_t bits = reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(y) | 16;
+  p->align = (int)(bits & (~bits + 1));  // lowest set bit: 1, 2, 4, 8 or 16
   return KS_OK;
 }
 
@@ -267,6 +275,7 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
       snprintf(buf, sizeof buf, "ks_dma_kernel<%s,%d,%s,%d,%d,%d,%d>", t, pl.vec, pl.unroll ? "true" : "false",
                pl.waves_m, pl.cps, (int)(pl.rs * pl.nt * pl.lch * p.d * (p.dtype == F32 ? 4 : 2) / 256), pl.nt);
       break;
+    case V_MASKED: snprintf(buf, sizeof buf, "ks_masked_kernel<%s,%d,%d>", t, p.layout, pl.vec); break;
     default: snprintf(buf, sizeof buf, "?");
   }
   std::string r(buf);
@@ -275,7 +284,7 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
 }
 
 std::string describe(const Problem& p, const Plan& pl) {
-  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "direct", "staged", "?", "dma"};
+  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "direct", "staged", "?", "dma", "masked"};
   char buf[320];
   snprintf(buf, sizeof buf,
            "variant=%d name=%s vec=%d bt=%d jg=%d unroll=%d waves_m=%d waves_n=%d lds=%d grid=%u block=%u xcd=%d "

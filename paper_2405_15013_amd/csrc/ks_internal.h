@@ -19,7 +19,8 @@ enum Variant : int {
   V_STAGED = 4,    // LDS-staged MFMA, 4 work items per workgroup share coalesced X stages
   // 5: unused (a persistent streaming variant, measured slower and removed)
   V_DMA = 6,       // LDS-staged MFMA with X moved HBM -> LDS by DMA, three stage buffers (BSF, d >= 4)
-  V_COUNT = 7
+  V_MASKED = 7,    // register-direct MFMA with zero-padded tiles and narrow accesses (any b, c, batch, alignment)
+  V_COUNT = 8
 };
 
 // Problem description shared by all kernels.  Sizes fit in int32 (checked by
@@ -33,6 +34,7 @@ struct Problem {
   const void* kv;
   const void* x;
   void* y;
+  int align;     // largest power of two (<= 16) dividing the byte addresses of x and y
 };
 
 // Launch description produced by the planner.
@@ -64,6 +66,7 @@ hipError_t launch_valu_bsf(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_direct(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_staged(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_dma(const Problem& p, const Plan& pl, hipStream_t s);
+hipError_t launch_masked(const Problem& p, const Plan& pl, hipStream_t s);
 struct FusedChain;
 hipError_t launch_chain_fused(const FusedChain& fc, int dtype, bool vec, hipStream_t s);
 

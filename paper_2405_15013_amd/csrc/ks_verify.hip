@@ -16,6 +16,7 @@
 #include "../../include/ks.h"
 #include "ks_internal.h"
 #include "ks_direct_index.h"
+#include "ks_masked_index.h"
 #include "ks_staged_index.h"
 
 namespace ks {
@@ -158,6 +159,85 @@ bool verify_item(Checker& ck, const DItem& it, bool strided, int V, int MT, int 
         if ((off * S) % (ype * S)) return ck.fail("Y piece not aligned to its size", off);
         ck.write_y(off, ype);
       }
+  return ck.err.empty();
+}
+
+// Masked kernel with access width V: every X piece is the V elements of
+// value l the product needs (or zero padding), K elements inside the block,
+// every Y element of the batch written exactly once, vector accesses aligned.
+bool verify_masked_v(Checker& ck, int V) {
+  const Problem& p = ck.p;
+  const int S = p.dtype == F32 ? 4 : 2, LP = masked_lp(S), CH = 4 * LP;
+  const MaskedTile t = masked_tile(p, V);
+  if (t.kgroups * 16 < p.b || t.nchunks * CH < p.c) return ck.fail("masked tiles do not cover the block", V);
+  if (p.layout == BSL && p.batch % V) return ck.fail("batch not a multiple of the access width", V);
+  if (p.layout == BSF && p.d % V) return ck.fail("d not a multiple of the access width", V);
+  const int VK = p.layout == BSL ? 1 : V;
+  for (int item = 0; item < t.items && ck.err.empty(); ++item) {
+    const MItem it = masked_item(p, t, V, item);
+    if (it.i < 0 || it.i >= p.a) return ck.fail("item i out of range", item);
+    for (int lane = 0; lane < 64; ++lane) {
+      const int n = lane & 15, g = lane >> 4;
+      for (int ch = 0; ch < t.nchunks; ++ch)
+        for (int q = 0; q < LP; ++q) {
+          const int l = ch * CH + LP * g + q;
+          const int64_t off = masked_x_off(p, it, V, l, n);
+          if (off >= 0) {
+            if (V * S >= 8 && (off * S) % (V * S)) return ck.fail("X vector not aligned to its size", off);
+            ck.read_x(off, V);
+            for (int e = 0; e < V; ++e) {
+              DItem di;
+              di.i = it.i; di.j0 = it.j0; di.k0 = it.k0; di.beta0 = it.beta0;
+              // the same element the register-direct kernels' definition gives
+              // for (l, column e): BSL batch beta0 + V*n + e, BSF j0 + e
+              const int64_t want = p.layout == BSL
+                  ? ((int64_t)it.i * p.c * p.d + (int64_t)l * p.d + it.j0) * p.batch + it.beta0 + V * n + e
+                  : (int64_t)(it.beta0 + n) * p.N + (int64_t)it.i * p.c * p.d + (int64_t)l * p.d + it.j0 + e;
+              (void)di;
+              if (off + e != want) return ck.fail("masked operand element is not the X value needed", off + e);
+            }
+          } else if (l < p.c && masked_col_valid(p, it, V, n)) {
+            return ck.fail("needed X piece treated as padding", l);
+          }
+          if (t.kvec && q == 0)
+            for (int e = 0; e < VK; ++e) {
+              const int64_t ko = masked_k_off(p, it, e, n, l);
+              if (ko >= 0) {
+                if ((ko * S) % 16) return ck.fail("K operand vector not 16-byte aligned", ko);
+                ck.read_k(ko, LP);
+              }
+            }
+          for (int e = 0; e < VK; ++e) {
+            const int64_t ko = masked_k_off(p, it, e, n, l);
+            if (ko >= 0) {
+              ck.read_k(ko, 1);
+              if (ko != (((int64_t)it.i * p.d + it.j0 + e) * p.b + it.k0 + n) * p.c + l)
+                return ck.fail("masked K element is not the block value needed", ko);
+            } else if (it.k0 + n < p.b && l < p.c) {
+              return ck.fail("needed K value treated as padding", l);
+            }
+          }
+        }
+      for (int r = 0; r < 4; ++r) {
+        const int64_t off = masked_y_off(p, it, V, n, g, r);
+        if (off < 0) continue;
+        if (V * S >= 8 && (off * S) % (V * S)) return ck.fail("Y vector not aligned to its size", off);
+        ck.write_y(off, V);
+      }
+    }
+  }
+  return ck.err.empty();
+}
+
+// The planned access width, then every narrower one the planner would pick
+// for less aligned buffers (each with its own coverage check).
+bool verify_masked(Checker& ck, const Plan& pl) {
+  if (!verify_masked_v(ck, pl.vec)) return false;
+  for (int V = pl.vec / 2; V >= 1; V /= 2) {
+    if (!ck.coverage()) return false;
+    std::fill(ck.cover.begin(), ck.cover.end(), 0);
+    if (!verify_masked_v(ck, V)) return false;
+  }
   return ck.err.empty();
 }
 
@@ -502,6 +582,7 @@ extern "C" ks_status_t ks_plan_verify(int64_t a, int64_t b, int64_t c, int64_t d
     case V_DIRECT: ok = verify_direct(ck, pl); break;
     case V_STAGED: ok = verify_staged(ck, pl); break;
     case V_DMA: ok = verify_dma(ck, pl); break;
+    case V_MASKED: ok = verify_masked(ck, pl); break;
     default: ck.fail("unknown variant", pl.variant);
   }
   if (ok) ok = ck.coverage();

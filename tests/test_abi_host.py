@@ -71,7 +71,16 @@ def test_alias_detected():
     assert ks.ks_matmul(2, 4, 4, 2, P0, P1, P0 + 4, 32, ks.BSL, ks.F32, stream=0, check=False) == 4
 
 
-def test_chain_errors():
+@pytest.fixture
+def factor_by_factor():
+    """Chains below run factor by factor (no fused kernel), so their
+    workspace checks apply; every call is rejected before any launch."""
+    ks.ks_force_chain_fusion(0)
+    yield
+    ks.ks_force_chain_fusion(None)
+
+
+def test_chain_errors(factor_by_factor):
     f_ok = [((1, 4, 4, 4), P0), ((4, 4, 4, 1), P0 + 4096)]
     f_bad = [((1, 4, 4, 4), P0), ((1, 3, 3, 1), P0 + 4096)]
     assert ks.ks_chain_workspace_bytes(f_bad, 8, ks.F32) == 0
@@ -97,8 +106,8 @@ def test_plan_describe_picks_expected_families():
     # butterfly factor, batch-size-last -> VALU streaming kernel
     assert "name=valu_bsl" in ks.ks_plan_describe(4, 2, 2, 128, 4096, "bsl", "f32")
     assert "name=valu_bsf" in ks.ks_plan_describe(4, 2, 2, 128, 4096, "bsf", "f32")
-    # large odd blocks fall back to the generic kernel
-    assert "name=generic" in ks.ks_plan_describe(1, 17, 19, 3, 64, "bsf", "f32")
+    # large odd blocks run on the masked MFMA kernel (zero-padded tiles)
+    assert "name=masked" in ks.ks_plan_describe(1, 17, 19, 3, 64, "bsf", "f32")
     assert ks.ks_plan_describe(1, 4, 4, 1, 0, "bsf", "f32") == "empty"
 
 
@@ -112,7 +121,7 @@ def test_wrappers_reject_host_tensors():
         ks.chain(torch.randn(16, 8), [((2, 4, 4, 2), torch.randn(64))], "bsl")
 
 
-def test_chain_noalloc_host_errors():
+def test_chain_noalloc_host_errors(factor_by_factor):
     """ks_chain_noalloc checks its arguments like ks_chain, and rejects chains
     whose intermediates exceed its fixed scratch array, before touching the
     GPU."""

@@ -322,3 +322,30 @@ def test_wrappers_reject_mismatched_tensors():
         ks.chain(x, [f[0], ((4, 4, 3, 1), torch.randn(48, device=dev))], "bsl")  # X width 12 != 16
     with pytest.raises(ValueError):
         ks.chain(x, [((1, 4, 4, 2), torch.randn(32, device=dev)), f[1]], "bsl")  # 8 != 16
+
+
+MASKED_CASES = [((1, 64, 64, 1), 25087, "bsl"), ((1, 24, 24, 8), 4096, "bsl"), ((1, 24, 24, 8), 4096, "bsf"),
+                ((6, 64, 16, 8), 25087, "bsl"), ((6, 64, 16, 8), 25090, "bsl"), ((1, 100, 36, 2), 1001, "bsf"),
+                ((3, 20, 40, 1), 37, "bsl"), ((4, 16, 17, 2), 130, "bsf"), ((1, 33, 16, 5), 1001, "bsl")]
+
+
+@pytest.mark.parametrize("case_", MASKED_CASES, ids=[str(c) for c in MASKED_CASES])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+def test_masked_kernel(case_, dtype):
+    """The masked MFMA kernel (zero-padded tiles, narrow accesses): b or c not
+    a multiple of 16, batch-size-last batches that are not a multiple of the
+    vector; the whole output against the oracle."""
+    pattern, batch, layout = case_
+    desc = ks.ks_plan_describe(*pattern, batch, layout, dtype)
+    assert "name=masked" in desc, desc
+    check(pattern, batch, dtype, layout, cfg=17, kdist="normal")
+
+
+@pytest.mark.parametrize("pattern", [(1, 32, 32, 4), (6, 64, 16, 8), (1, 24, 24, 8)])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("offsets", [(1, 3), (2, 2), (4, 0)])
+def test_offset_buffers_run_masked(pattern, layout, dtype, offsets):
+    """Buffers shifted off 16-byte alignment by 1, 2 or 4 elements: the masked
+    kernel at the access width their alignment allows."""
+    check(pattern, 256, dtype, layout, cfg=18, x_offset=offsets[0], y_offset=offsets[1], kdist="normal")

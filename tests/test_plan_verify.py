@@ -143,3 +143,23 @@ def test_dma_row_group_plans_covered():
             for batch in (4096, 4000):
                 st, rep = ks.ks_plan_verify(*p, batch, "bsf", dt)
                 assert st == 0, (p, dt, batch, rep)
+
+
+ODD = [(1, 24, 24, 8), (1, 17, 33, 3), (2, 48, 80, 2), (6, 64, 16, 8), (1, 64, 64, 1), (3, 20, 40, 1), (1, 100, 36, 2),
+       (4, 16, 17, 2), (1, 33, 16, 5)]
+
+
+@pytest.mark.parametrize("pattern", ODD)
+@pytest.mark.parametrize("batch", [1, 37, 1001, 4096, 25087])
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+def test_no_generic_plan_for_large_blocks(pattern, batch, layout, dtype):
+    """Blocks with b or c above 16 always get an MFMA kernel (the masked one
+    when b or c is not a multiple of 16 or the batch is not a multiple of the
+    vector), whose host replay passes at every access width the planner may
+    pick for less aligned buffers."""
+    desc = ks.ks_plan_describe(*pattern, batch, layout, dtype)
+    assert "name=generic" not in desc, desc
+    if batch <= 4096:
+        st, rep = ks.ks_plan_verify(*pattern, batch, layout, dtype)
+        assert st == 0, (desc, rep)
