@@ -68,6 +68,12 @@ typedef enum {
     KS_ERR_SCRATCH_LIMIT = 8    /* ks_chain_noalloc: intermediates exceed its fixed scratch array */
 } ks_status_t;
 
+/* Output activation of ks_matmul_bias_act. */
+typedef enum {
+    KS_ACT_NONE = 0,
+    KS_ACT_GELU = 1 /* exact GELU: x * Phi(x) = 0.5 x (1 + erf(x / sqrt 2)) */
+} ks_act_t;
+
 /* One factor of a chain: its pattern and its packed values (device pointer,
  * layout as K_values above). */
 typedef struct {
@@ -90,6 +96,23 @@ typedef struct {
 ks_status_t ks_matmul(int64_t a, int64_t b, int64_t c, int64_t d,
                       const void *K_values, const void *X, void *Y,
                       int64_t batch, int layout, int dtype, void *stream);
+
+/*
+ * Y = act(X K^T + bias): ks_matmul with the bias and activation of a
+ * Transformer MLP layer applied in the kernels' epilogue, in fp32 before the
+ * rounding to the storage type (paper appendix, ViT-S/16 submodule table:
+ * "Linear + bias" rows and the feed-forward block Linear + GELU).
+ *   bias  device, a*b*d elements of `dtype`, one per output feature m (the
+ *         column of Y in BSF, its row in BSL), added to every batch entry;
+ *         NULL for no bias.  Must not overlap Y (KS_ERR_ALIAS).
+ *   act   KS_ACT_NONE or KS_ACT_GELU (other values: KS_ERR_UNSUPPORTED).
+ * Every other argument, the result layout and the errors are ks_matmul's;
+ * ks_matmul(...) is ks_matmul_bias_act(..., NULL, KS_ACT_NONE, ...).
+ */
+ks_status_t ks_matmul_bias_act(int64_t a, int64_t b, int64_t c, int64_t d,
+                               const void *K_values, const void *bias, int act,
+                               const void *X, void *Y, int64_t batch,
+                               int layout, int dtype, void *stream);
 
 /*
  * Bytes of device workspace ks_chain needs for these factors: 0 for a single

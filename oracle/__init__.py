@@ -13,7 +13,8 @@ sets, Section 2.2 layouts, Appendix B.1 Table 5 chain order).
 Parity status: every function here is pinned by ``tests/test_oracle_pins.py``
 (brute-force dense products built with numpy's ``kron``, the dense-GEMM and
 diagonal special cases, the Sylvester-Hadamard closed form for butterfly
-chains, the adjoint identity, and the Figure 4 index sets).
+chains, the adjoint identity, the Figure 4 index sets, and for the bias/GELU
+epilogue the normal CDF of scipy.stats at sample points).
 """
 import ctypes
 import os
@@ -34,7 +35,7 @@ def build(force=False):
     """Compile ks_oracle.c into libks_oracle.so next to it (gcc, OpenMP)."""
     if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
         tmp = _LIB + ".tmp%d" % os.getpid()
-        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", _SRC, "-o", tmp])
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", _SRC, "-o", tmp, "-lm"])
         os.replace(tmp, _LIB)
     return _LIB
 
@@ -53,6 +54,8 @@ def _load():
         lib.kso_dense.restype = ctypes.c_int
         lib.kso_chain.argtypes = [ctypes.c_int, p, p, p, p, i64, ctypes.c_int, ctypes.c_int]
         lib.kso_chain.restype = ctypes.c_int
+        lib.kso_bias_act.argtypes = [p, p, i64, i64, ctypes.c_int, ctypes.c_int]
+        lib.kso_bias_act.restype = ctypes.c_int
         lib.kso_max_threads.argtypes = []
         lib.kso_max_threads.restype = ctypes.c_int
         _lib = lib
@@ -140,3 +143,20 @@ def chain(patterns, kvs, x, batch, layout, nthreads=0):
     if rc != 0:
         raise ValueError("kso_chain rejected its arguments (%d)" % rc)
     return y
+
+
+def bias_act(y, bias, layout, act):
+    """act(Y + bias) elementwise per output feature m (bias: M values or
+    None; act: None/"none" or "gelu"), returning a new fp64 array in the same
+    layout as y ((batch, M) for BSF, (M, batch) for BSL)."""
+    lay = _layout_code(layout)
+    out = np.array(y, dtype=np.float64, copy=True, order="C")
+    M = out.shape[1] if lay == BSF else out.shape[0]
+    batch = out.shape[0] if lay == BSF else out.shape[1]
+    b = None if bias is None else _f64(bias)
+    assert b is None or b.size == M
+    a = {None: 0, "none": 0, "gelu": 1}[act]
+    rc = _load().kso_bias_act(_ptr(out), None if b is None else _ptr(b), M, batch, lay, a)
+    if rc != 0:
+        raise ValueError("kso_bias_act rejected its arguments (%d)" % rc)
+    return out

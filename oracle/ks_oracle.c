@@ -37,6 +37,7 @@
  * Build: a plain C compiler with OpenMP, e.g.
  *   gcc -O2 -fopenmp -fPIC -shared ks_oracle.c -o libks_oracle.so
  */
+#include <math.h>
 #include <stddef.h>
 #include <stdint.h>
 #include <stdlib.h>
@@ -212,4 +213,30 @@ int kso_chain(int nfactors, const int64_t *pat, const double *const *Kvs,
     free(cur);
     free(nxt);
     return rc;
+}
+
+/*
+ * Output epilogue of a Transformer MLP layer built from a KS factor (paper
+ * appendix, ViT-S/16 submodule table: "Linear + bias" rows, and the
+ * feed-forward block Linear + GELU): in place on Y (batch x M in `layout`),
+ *     Y[beta, m] = act(Y[beta, m] + bias[m]),
+ * with bias NULL for no bias, act 0 for none and 1 for the exact GELU
+ * x * Phi(x) = 0.5 * x * (1 + erf(x / sqrt(2))).  fp64.
+ */
+int kso_bias_act(double *Y, const double *bias, int64_t M, int64_t batch, int layout, int act)
+{
+    if (M < 1 || batch < 0 || (act != 0 && act != 1))
+        return -1;
+    if (layout != KSO_BSF && layout != KSO_BSL)
+        return -1;
+    for (int64_t beta = 0; beta < batch; ++beta) {
+        for (int64_t m = 0; m < M; ++m) {
+            double *y = &Y[kso_index(layout, beta, m, batch, M)];
+            double v = *y + (bias ? bias[m] : 0.0);
+            if (act == 1)
+                v = 0.5 * v * (1.0 + erf(v / sqrt(2.0)));
+            *y = v;
+        }
+    }
+    return 0;
 }

@@ -19,11 +19,13 @@ __all__ = [
     "ks_matmul", "ks_chain", "ks_chain_workspace_bytes", "ks_chain_noalloc", "ks_chain_noalloc_max_workspace",
     "ks_status_string",
     "ks_last_hip_error", "ks_plan_describe", "ks_force_variant", "ks_plan_verify",
-    "ks_chain_describe", "ks_force_chain_fusion", "ks_chain_verify", "matmul", "chain", "library_path", "load_library", "EXPORTED_SYMBOLS",
+    "ks_chain_describe", "ks_force_chain_fusion", "ks_chain_verify", "ks_matmul_bias_act",
+    "ACT_NONE", "ACT_GELU", "matmul", "chain", "library_path", "load_library", "EXPORTED_SYMBOLS",
 ]
 
 BSF, BSL = 0, 1
 F32, BF16, F16 = 0, 1, 2
+ACT_NONE, ACT_GELU = 0, 1
 
 KS_OK = 0
 STATUS_NAMES = {
@@ -36,7 +38,7 @@ STATUS_NAMES = {
 EXPORTED_SYMBOLS = (
     "ks_matmul", "ks_chain_workspace_bytes", "ks_chain", "ks_chain_noalloc", "ks_chain_noalloc_max_workspace",
     "ks_status_string", "ks_last_hip_error", "ks_plan_describe", "ks_force_variant", "ks_plan_verify",
-    "ks_chain_describe", "ks_force_chain_fusion", "ks_chain_verify",
+    "ks_chain_describe", "ks_force_chain_fusion", "ks_chain_verify", "ks_matmul_bias_act",
 )
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -82,6 +84,8 @@ def load_library():
     i64, vp, ci = ctypes.c_int64, ctypes.c_void_p, ctypes.c_int
     lib.ks_matmul.argtypes = [i64, i64, i64, i64, vp, vp, vp, i64, ci, ci, vp]
     lib.ks_matmul.restype = ci
+    lib.ks_matmul_bias_act.argtypes = [i64, i64, i64, i64, vp, vp, ci, vp, vp, i64, ci, ci, vp]
+    lib.ks_matmul_bias_act.restype = ci
     lib.ks_chain_workspace_bytes.argtypes = [ctypes.POINTER(_Factor), ci, i64, ci]
     lib.ks_chain_workspace_bytes.restype = ctypes.c_size_t
     lib.ks_chain.argtypes = [ctypes.POINTER(_Factor), ci, vp, vp, i64, ci, ci, vp, ctypes.c_size_t, vp]
@@ -178,6 +182,20 @@ def ks_matmul(a, b, c, d, K_values, X, Y, batch, layout, dtype, stream=None, che
                                   _stream(stream))
     if check and st != KS_OK:
         raise KsError(st, "ks_matmul")
+    return st
+
+
+_ACTS = {"none": ACT_NONE, "gelu": ACT_GELU}
+
+
+def ks_matmul_bias_act(a, b, c, d, K_values, bias, act, X, Y, batch, layout, dtype, stream=None, check=True):
+    """C-ABI ks_matmul_bias_act: Y = act(X K^T + bias) (bias may be None)."""
+    st = load_library().ks_matmul_bias_act(a, b, c, d, _ptr(K_values), _ptr(bias),
+                                           _code(act if act is not None else "none", _ACTS, "activation"),
+                                           _ptr(X), _ptr(Y), batch, _code(layout, _LAYOUTS, "layout"),
+                                           _code(dtype, _DTYPES, "dtype"), _stream(stream))
+    if check and st != KS_OK:
+        raise KsError(st, "ks_matmul_bias_act")
     return st
 
 
@@ -308,11 +326,12 @@ def _check_out(out, shape, X):
         raise ValueError("out has shape %s, expected %s" % (tuple(out.shape), tuple(shape)))
 
 
-def matmul(X, K_values, pattern, layout="bsl", out=None):
-    """Allocate Y (unless `out` is given) and run ks_matmul.  X is
-    (batch, a*c*d) for BSF or (a*c*d, batch) for BSL; K_values is (a*d, b, c)
-    or flat; all three share one dtype and device.  Every argument is checked
-    on the host before the call (the C ABI sees only pointers)."""
+def matmul(X, K_values, pattern, layout="bsl", out=None, bias=None, act=None):
+    """Allocate Y (unless `out` is given) and run ks_matmul, or
+    ks_matmul_bias_act when `bias` (a*b*d values) or `act` ("gelu") is given.
+    X is (batch, a*c*d) for BSF or (a*c*d, batch) for BSL; K_values is
+    (a*d, b, c) or flat; all share one dtype and device.  Every argument is
+    checked on the host before the call (the C ABI sees only pointers)."""
     import torch
     a, b, c, d = (int(v) for v in pattern)
     lay = _code(layout, _LAYOUTS, "layout")
@@ -326,7 +345,16 @@ def matmul(X, K_values, pattern, layout="bsl", out=None):
         out = torch.empty(shape, dtype=X.dtype, device=X.device)
     else:
         _check_out(out, shape, X)
-    ks_matmul(a, b, c, d, K_values, X, out, batch, lay, dt)
+    if bias is None and act is None:
+        ks_matmul(a, b, c, d, K_values, X, out, batch, lay, dt)
+        return out
+    if bias is not None:
+        _check_tensor(bias, "bias")
+        if bias.dtype != X.dtype or bias.device != X.device:
+            raise TypeError("bias must have X's dtype and device")
+        if bias.numel() != M:
+            raise ValueError("bias has %d elements, the output has a*b*d = %d features" % (bias.numel(), M))
+    ks_matmul_bias_act(a, b, c, d, K_values, bias, act, X, out, batch, lay, dt)
     return out
 
 

@@ -25,6 +25,7 @@
 #pragma once
 #include "ks_common.h"
 #include "ks_direct_index.h"
+#include "ks_epilogue.h"
 #include "ks_internal.h"
 
 namespace ks {
@@ -142,10 +143,28 @@ __device__ __forceinline__ void direct_mma(const uint32_t* xw, const uint32_t (&
 // pieces of YPE contiguous elements (ks_direct_index.h, direct_y_off).
 template <typename T, int LAYOUT, int V, bool STRIDED, int MT>
 __device__ __forceinline__ void direct_store(const Problem& p, const DItem& it, int n, int g,
-                                             const f32x4 (&acc)[MT][V]) {
+                                             const f32x4 (&acc_in)[MT][V]) {
   constexpr int S = sizeof(T);
   mfma_results_settle();
   if (!direct_lane_valid(p, it, V, n)) return;
+  f32x4 acc[MT][V];
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+    for (int e = 0; e < V; ++e) acc[mt][e] = acc_in[mt][e];
+  if (epilogue_on(p)) {
+    // output feature of accumulator (mt, e, r): row k = k0 + 16 mt + 4 g + r
+    // of block (i, j), j = j0 (+ e in BSF)
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int e = 0; e < V; ++e)
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const int k = it.k0 + 16 * mt + 4 * g + r, j = it.j0 + (LAYOUT == BSF ? e : 0);
+          acc[mt][e][r] = epilogue_apply<T>(p, acc[mt][e][r], it.i * p.b * p.d + k * p.d + j);
+        }
+  }
   constexpr int YPE = (LAYOUT == BSL || STRIDED) ? V : (4 * V * S < 16 ? 4 * V : 16 / S);
   constexpr int YNP = 4 * V / YPE;
   constexpr int YPB = YPE * S;

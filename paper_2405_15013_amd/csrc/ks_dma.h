@@ -240,6 +240,21 @@ void ks_dma_kernel(Problem p, StagedTile t) {
 
   // Structured epilogue: accumulators -> LDS output tile -> contiguous runs.
   mfma_results_settle();
+  if (epilogue_on(p)) {
+    // output feature of accumulator (u, mt, e, r4): row k = k0 + 16 mt + 4 g + r4
+    // of block (i, j0 + e)
+#pragma unroll
+    for (int u = 0; u < NT; ++u)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4) {
+            const int k = it.k0 + 16 * mt + 4 * g + r4;
+            acc[u][mt][e][r4] = epilogue_apply<T>(p, acc[u][mt][e][r4], st.i * p.b * p.d + k * p.d + it.j0 + e);
+          }
+  }
   __syncthreads();  // every wavefront is done with the stage buffers
   char* ycell0 = smem + dma_y_lds_lane(p, t, si, MT, S, n, g);
 #pragma unroll

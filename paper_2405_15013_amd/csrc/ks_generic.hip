@@ -5,6 +5,7 @@
 // over l < c (paper, Section 4.1, row/col index sets of Algorithm 2).  It is the
 // fallback for patterns the tiled kernels do not cover (e.g. b or c not a
 // multiple of 16 and too large for the VALU kernels); correctness over speed.
+#include "ks_epilogue.h"
 #include "ks_internal.h"
 #include "ks_common.h"
 
@@ -36,6 +37,7 @@ __global__ __launch_bounds__(256) void ks_generic_kernel(Problem p) {
       const int64_t step = (int64_t)p.d * p.batch;
       for (int l = 0; l < p.c; ++l) acc += to_f32(blk[l]) * to_f32(xc[l * step]);
     }
+    if (epilogue_on(p)) acc = epilogue_apply<T>(p, acc, (int)m);
     y[idx] = from_f32<T>(acc);
   }
 }

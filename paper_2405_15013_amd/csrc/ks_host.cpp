@@ -223,6 +223,8 @@ ks_status_t validate(int64_t a, int64_t b, int64_t c, int64_t d, const void* kv,
   p->kv = kv; p->x = x; p->y = y;
   const uintptr_t bits = reinterpret_cast<uintptr_t>(x) | reinterpret_cast<uintptr_t>(y) | 16;
   p->align = (int)(bits & (~bits + 1));  // lowest set bit: 1, 2, 4, 8 or 16
+  p->bias = nullptr;
+  p->act = 0;
   return KS_OK;
 }
 
@@ -475,6 +477,21 @@ ks_status_t ks_matmul(int64_t a, int64_t b, int64_t c, int64_t d, const void* K_
   bool empty = false;
   ks_status_t st = validate(a, b, c, d, K_values, X, Y, batch, layout, dtype, &p, &empty);
   if (st != KS_OK || empty) return st;
+  return run_one(p, static_cast<hipStream_t>(stream));
+}
+
+ks_status_t ks_matmul_bias_act(int64_t a, int64_t b, int64_t c, int64_t d, const void* K_values, const void* bias,
+                               int act, const void* X, void* Y, int64_t batch, int layout, int dtype, void* stream) {
+  Problem p;
+  bool empty = false;
+  ks_status_t st = validate(a, b, c, d, K_values, X, Y, batch, layout, dtype, &p, &empty);
+  if (st != KS_OK) return st;
+  if (act != KS_ACT_NONE && act != KS_ACT_GELU) return KS_ERR_UNSUPPORTED;
+  if (empty) return KS_OK;
+  if (bias != nullptr && overlaps(bias, (int64_t)p.M * elem_size(dtype), Y, (int64_t)p.batch * p.M * elem_size(dtype)))
+    return KS_ERR_ALIAS;
+  p.bias = bias;
+  p.act = act;
   return run_one(p, static_cast<hipStream_t>(stream));
 }
 

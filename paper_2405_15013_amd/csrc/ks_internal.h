@@ -35,6 +35,8 @@ struct Problem {
   const void* x;
   void* y;
   int align;     // largest power of two (<= 16) dividing the byte addresses of x and y
+  const void* bias;  // epilogue (ks_epilogue.h): per-output-feature bias (M values) or null
+  int act;           // epilogue activation: 0 none, 1 GELU
 };
 
 // Launch description produced by the planner.

@@ -129,8 +129,13 @@ __global__ __launch_bounds__(256) void ks_masked_kernel(Problem p, MaskedTile t)
     const int64_t off = masked_y_off(p, it, V, n, g, r);
     if (off < 0) continue;
     T v[V];
+    const int k = it.k0 + 4 * g + r;
 #pragma unroll
-    for (int e = 0; e < V; ++e) v[e] = from_f32<T>(acc[0][e][r]);
+    for (int e = 0; e < V; ++e) {
+      float y = acc[0][e][r];
+      if (epilogue_on(p)) y = epilogue_apply<T>(p, y, it.i * p.b * p.d + k * p.d + it.j0 + (LAYOUT == BSF ? e : 0));
+      v[e] = from_f32<T>(y);
+    }
     masked_store<T, V>(static_cast<T*>(p.y) + off, v);
   }
 }

@@ -196,6 +196,17 @@ __global__ __launch_bounds__(512) void ks_staged_kernel(Problem p, StagedTile t)
     // Structured epilogue: accumulators -> LDS output tile -> contiguous runs.
     // (The loop's last barrier guarantees no wavefront still reads X stages.)
     mfma_results_settle();
+    if (epilogue_on(p)) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4) {
+            const int k = it.k0 + 16 * mt + 4 * g + r4;
+            acc[mt][e][r4] = epilogue_apply<T>(p, acc[mt][e][r4], it.i * p.b * p.d + k * p.d + it.j0 + e);
+          }
+    }
     const int r = 16 * si.rs + n;
 #pragma unroll
     for (int mt = 0; mt < MT; ++mt)

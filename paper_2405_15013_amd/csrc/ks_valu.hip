@@ -7,6 +7,7 @@
 // once.  With blocks this small the work is a pure stream (2*b*c flops per
 // (b + c) elements moved), so the kernels are built for coalesced 16-byte
 // nontemporal loads and stores, not for arithmetic.
+#include "ks_epilogue.h"
 #include "ks_internal.h"
 #include "ks_common.h"
 
@@ -89,6 +90,10 @@ __global__ __launch_bounds__(256) void ks_valu_bsl_kernel(Problem p) {
           for (int e = 0; e < VEC; ++e) acc[e] = __builtin_fmaf(to_f32(blk[k * c + l]), xv[u][l][e], acc[e]);
         }
       }
+      if (epilogue_on(p)) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] = epilogue_apply<T>(p, acc[e], (int)yrow0 + k * d);
+      }
       store_vec<T, VEC>(y + yrow0 * batch + k * ystep + (size_t)v * VEC, acc);
     }
   }
@@ -136,6 +141,10 @@ __global__ __launch_bounds__(256) void ks_valu_bsf_kernel(Problem p) {
 #pragma unroll
         for (int e = 0; e < V; ++e) acc[e] = __builtin_fmaf(to_f32(blk[(size_t)e * b * c + k * c + l]), xv[l][e], acc[e]);
       }
+    }
+    if (epilogue_on(p)) {
+#pragma unroll
+      for (int e = 0; e < V; ++e) acc[e] = epilogue_apply<T>(p, acc[e], i * b * d + k * d + j0 + e);
     }
     store_vec<T, V>(ys + (size_t)k * d, acc);
   }

@@ -349,3 +349,54 @@ def test_offset_buffers_run_masked(pattern, layout, dtype, offsets):
     """Buffers shifted off 16-byte alignment by 1, 2 or 4 elements: the masked
     kernel at the access width their alignment allows."""
     check(pattern, 256, dtype, layout, cfg=18, x_offset=offsets[0], y_offset=offsets[1], kdist="normal")
+
+
+# --- bias + GELU epilogue (ks_matmul_bias_act) --------------------------------
+
+EPI_CASES = [("generic", (2, 4, 4, 2), "bsl", 40), ("valu_bsl", (2, 4, 4, 2), "bsl", 64),
+             ("valu_bsf", (4, 2, 2, 8), "bsf", 50), ("direct", (6, 64, 16, 8), "bsl", 256),
+             ("direct", (2, 48, 80, 2), "bsf", 72), ("staged", (1, 32, 32, 32), "bsf", 100),
+             ("dma", (6, 64, 16, 8), "bsf", 1000), ("dma", (4, 48, 96, 4), "bsf", 72),
+             ("masked", (1, 24, 24, 8), "bsl", 100), ("masked", (1, 100, 36, 2), "bsf", 37),
+             (None, (6, 64, 16, 8), "bsl", 25088), (None, (6, 16, 64, 8), "bsf", 25088)]
+VARIANTS["masked"] = 7
+
+
+@pytest.mark.parametrize("case_", EPI_CASES, ids=["%s-%s-%s-%d" % c for c in EPI_CASES])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("epi", ["bias", "bias_gelu", "gelu"])
+def test_bias_gelu_epilogue(case_, dtype, epi):
+    """Y = act(X K^T + bias) from every kernel family's epilogue against the
+    oracle's matmul followed by its bias/GELU step."""
+    import torch
+    variant, pattern, layout, batch = case_
+    a, b, c, d = pattern
+    M = a * b * d
+    x, kv, x64, kv64 = case(19, pattern, batch, dtype, "normal", "normal")
+    bias = inputs.round_to(np.random.default_rng(M + batch).standard_normal(M), dtype) if epi != "gelu" else None
+    act = "gelu" if "gelu" in epi else None
+    xd = to_device(inputs.to_layout(x, layout), dtype)
+    kd = to_device(kv, dtype)
+    bd = to_device(bias, dtype) if bias is not None else None
+    yd = nan_tensor((batch * M,), dtype)
+    ks.ks_force_variant(None if variant is None else VARIANTS[variant])
+    try:
+        desc = ks.ks_plan_describe(a, b, c, d, batch, layout, dtype)
+        ks.ks_matmul_bias_act(a, b, c, d, kd, bd, act, xd, yd, batch, layout, dtype)
+    finally:
+        ks.ks_force_variant(None)
+    torch.cuda.synchronize()
+    y = inputs.from_layout(from_device(yd, dtype).reshape((batch, M) if layout == "bsf" else (M, batch)), layout)
+    y64 = oracle.bias_act(oracle.matmul(pattern, kv64, x64, batch, "bsf"),
+                          None if bias is None else inputs.to_f64(bias, dtype), "bsf", act)
+    err = rel_err(y, y64)
+    assert err <= TOL[dtype], "%s %s: rel err %.3e [%s]" % (case_, epi, err, desc)
+
+
+def test_bias_act_rejects_bad_arguments():
+    import torch
+    kd = torch.ones(64, device="cuda")
+    x = torch.ones(16, 8, device="cuda")
+    y = torch.empty(16, 8, device="cuda")
+    assert ks.ks_matmul_bias_act(2, 4, 4, 2, kd, None, 2, x, y, 8, "bsl", "f32", check=False) == 5  # unknown act
+    assert ks.ks_matmul_bias_act(2, 4, 4, 2, kd, y, 0, x, y, 8, "bsl", "f32", check=False) == 4     # bias aliases Y

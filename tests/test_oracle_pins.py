@@ -307,3 +307,31 @@ def test_shuffles_block_diagonalise_the_support(pattern):
     R = np.kron(np.eye(a), perfect_shuffle(d, c))
     S = np.kron(np.kron(np.eye(a), np.ones((b, c))), np.eye(d))
     np.testing.assert_array_equal(L.T @ S @ R, np.kron(np.eye(a * d), np.ones((b, c))))
+
+
+def test_gelu_is_x_times_normal_cdf():
+    """The epilogue's GELU is x * Phi(x), Phi the standard normal CDF
+    (scipy.stats.norm.cdf), at sample points including 0, +-1 and the tails."""
+    import scipy.stats
+    x = np.array([[-6.0, -2.5, -1.0, -0.3, 0.0, 0.3, 1.0, 2.5, 6.0]])
+    got = oracle.bias_act(x, None, "bsf", "gelu")
+    # absolute tolerance: 1 + erf(x / sqrt 2) cancels for large negative x
+    np.testing.assert_allclose(got, x * scipy.stats.norm.cdf(x), rtol=1e-13, atol=1e-14)
+    assert got[0, 4] == 0.0 and abs(got[0, 6] - 0.8413447460685429) < 1e-15
+
+
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+def test_bias_is_added_per_output_feature(layout):
+    """Bias m is added to column m of the (batch, M) result in either layout;
+    with all-zero blocks the layer's output is act(bias) for every row."""
+    pattern = (2, 3, 4, 2)
+    kv, x = rand_case(pattern, 5, seed=41)
+    M = 2 * 3 * 2
+    bias = np.random.default_rng(3).standard_normal(M)
+    y = inputs.from_layout(oracle.matmul(pattern, kv, inputs.to_layout(x, layout), 5, layout), layout)
+    yb = oracle.bias_act(inputs.to_layout(y, layout), bias, layout, None)
+    np.testing.assert_array_equal(inputs.from_layout(yb, layout), y + bias[None, :])
+    import scipy.stats
+    y0 = oracle.matmul(pattern, np.zeros_like(kv), inputs.to_layout(x, layout), 5, layout)
+    yg = inputs.from_layout(oracle.bias_act(y0, bias, layout, "gelu"), layout)
+    np.testing.assert_allclose(yg, np.broadcast_to(bias * scipy.stats.norm.cdf(bias), (5, M)), rtol=1e-14)
