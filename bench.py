@@ -61,8 +61,9 @@ if ROOT not in sys.path:
 
 METRIC = "KS matmul achieved GB/s & TFLOP/s, fraction of roofline (median over patterns)"
 HBM_BW = 8.0e12
-PEAK = {"f32": 157.3e12, "bf16": 2516.6e12, "f16": 2516.6e12}
-ESIZE = {"f32": 4, "bf16": 2, "f16": 2}
+PEAK = {"f32": 157.3e12, "bf16": 2516.6e12, "f16": 2516.6e12, "fp8": 5033.2e12}
+ESIZE = {"f32": 4, "bf16": 2, "f16": 2, "fp8": 1}     # bytes per element of X and K
+YSIZE = {"f32": 4, "bf16": 2, "f16": 2, "fp8": 2}     # bytes per element of Y (fp8 inputs give bf16 outputs)
 POOL_BYTES = 3 << 30
 ROTATE_BYTES = 768 << 20    # distinct buffer bytes between two uses of a buffer (3x the 256 MB MALL)
 MIN_SETS = 8
@@ -84,7 +85,7 @@ def sweep_patterns():
 def roof(pattern, batch, dtype):
     a, b, c, d = pattern
     nnz = a * b * c * d
-    nbytes = (batch * a * c * d + batch * a * b * d + nnz) * ESIZE[dtype]
+    nbytes = (batch * a * c * d + nnz) * ESIZE[dtype] + batch * a * b * d * YSIZE[dtype]
     flops = 2.0 * batch * nnz
     t_hbm = nbytes / HBM_BW
     t_flop = flops / PEAK[dtype]
@@ -275,13 +276,20 @@ class Runner:
         torch = self.torch
         if self.filled == dtype:
             return
-        tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
-        view = self.pool_x.view(tdt)
         g = torch.Generator(device=self.dev)
         g.manual_seed(20240523)
         chunk = 1 << 26
-        for s in range(0, view.numel(), chunk):
-            view[s:s + chunk].normal_(generator=g)
+        if dtype == "fp8":  # N(0,1) drawn in bf16, rounded to E4M3
+            view = self.pool_x.view(torch.float8_e4m3fn)
+            for s in range(0, view.numel(), chunk):
+                n = min(chunk, view.numel() - s)
+                view[s:s + n] = torch.randn(n, device=self.dev, generator=g, dtype=torch.bfloat16).to(
+                    torch.float8_e4m3fn)
+        else:
+            tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
+            view = self.pool_x.view(tdt)
+            for s in range(0, view.numel(), chunk):
+                view[s:s + chunk].normal_(generator=g)
         torch.cuda.synchronize()
         self.filled = dtype
 
@@ -370,24 +378,31 @@ class Runner:
             e1.synchronize()
         return e0.elapsed_time(e1) * 1e-3 / (self.steps * nsets)
 
-    def point(self, pattern, batch, dtype, layout, only_kernel=None):
+    def point(self, pattern, batch, dtype, layout, only_kernel=None, epilogue=False):
         torch = self.torch
         a, b, c, d = pattern
         s = ESIZE[dtype]
         N, M = a * c * d, a * b * d
         xb = (batch * N * s + 255) // 256 * 256
-        yb = (batch * M * s + 255) // 256 * 256
-        tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16}[dtype]
+        yb = (batch * M * YSIZE[dtype] + 255) // 256 * 256
+        tdt = {"f32": torch.float32, "bf16": torch.bfloat16, "f16": torch.float16,
+               "fp8": torch.float8_e4m3fn}[dtype]
         kv = torch.randn(a * d * b * c, device=self.dev).to(tdt)
         px, py = self.pool_x.data_ptr(), self.pool_y.data_ptr()
         lay = 0 if layout == "bsf" else 1
-        dt = {"f32": 0, "bf16": 1, "f16": 2}[dtype]
+        dt = {"f32": 0, "bf16": 1, "f16": 2, "fp8": 3}[dtype]
         kp = kv.data_ptr()
         nsets_pool = max(1, POOL_BYTES // max(xb, yb))
         lib = self.lib
 
+        bias = torch.randn(M, device=self.dev).to(torch.bfloat16 if dtype == "fp8" else tdt) if epilogue else None
+
         def launch(r, h):
-            st = lib.ks_matmul(a, b, c, d, kp, px + r * xb, py + r * yb, batch, lay, dt, h)
+            if epilogue:  # Y = GELU(X K^T + bias)
+                st = lib.ks_matmul_bias_act(a, b, c, d, kp, bias.data_ptr(), 1, px + r * xb, py + r * yb, batch,
+                                            lay, dt, h)
+            else:
+                st = lib.ks_matmul(a, b, c, d, kp, px + r * xb, py + r * yb, batch, lay, dt, h)
             if st != 0:
                 raise RuntimeError("ks_matmul failed: %s" % self.ks.ks_status_string(st))
 
@@ -401,6 +416,7 @@ class Runner:
         nbytes, flops, t_roof, bound = roof(pattern, batch, dtype)
         desc = self.ks.ks_plan_describe(a, b, c, d, batch, layout, dtype)
         r = {"pattern": list(pattern), "batch": batch, "dtype": dtype, "layout": layout, "us": t * 1e6,
+             "epilogue": "bias+gelu" if epilogue else None,
              "gbps": nbytes / t / 1e9, "tflops": flops / t / 1e12, "frac": t_roof / t, "bound": bound,
              "roof_us": t_roof * 1e6, "bytes": nbytes, "flops": flops, "calls_per_pass": nsets,
              "kernel": plan_field(desc, "kernel"), "plan": desc}
@@ -583,6 +599,23 @@ def main():
                         fam.append(run.point(p, 25088, dtype, layout))
             for r in fam:
                 fout.write(json.dumps(r) + "\n")
+            # FP8 (E4M3 inputs, bf16 outputs): the MLP layers and every 7th
+            # sweep pattern at both batches and layouts
+            run.fill("fp8")
+            fp8 = [run.point(p, 25088, "fp8", layout) for p in ((6, 64, 16, 8), (6, 16, 64, 8))
+                   for layout in ("bsf", "bsl")]
+            fp8_sweep = [run.point(p, batch, "fp8", layout) for batch in (4096, 25088) for layout in ("bsf", "bsl")
+                         for p in sweep_patterns()[::7]]
+            for r in fp8 + fp8_sweep:
+                fout.write(json.dumps(r) + "\n")
+            # bias + GELU epilogue on the MLP up-projection (768 -> 3072)
+            epi = []
+            for dtype in ("f32", "bf16"):
+                run.fill(dtype)
+                for layout in ("bsf", "bsl"):
+                    epi.append(run.point((6, 64, 16, 8), 25088, dtype, layout, epilogue=True))
+            for r in epi:
+                fout.write(json.dumps(r) + "\n")
             run.fill("f32")
             bfly = [(2 ** (l - 1), 2, 2, 2 ** (10 - l)) for l in range(1, 11)]
             ch = [run.chain(bfly, 4096, "f32", "bsl")]
@@ -611,6 +644,15 @@ def main():
                                                          "frac_unfused")},
                     "bsl_factor_by_factor_us": bfly_more[1]["us"]},
                 "monarch_2chain_B16384_us": {"%s_%s" % (r["dtype"], r["layout"]): r["us"] for r in ch[1:]},
+                "fp8_mlp_B25088": {"%s_%s" % (tuple(r["pattern"]), r["layout"]): {
+                    "us": r["us"], "gbps": r["gbps"], "frac": r["frac"]} for r in fp8},
+                "fp8_sweep_every7th": {"points": len(fp8_sweep),
+                                       "median_frac": float(np.median([r["frac"] for r in fp8_sweep])),
+                                       "median_gbps": float(np.median([r["gbps"] for r in fp8_sweep]))},
+                "mlp_up_bias_gelu_B25088": {"%s_%s" % (r["dtype"], r["layout"]): {
+                    "us": r["us"], "frac": r["frac"], "us_without_epilogue": next(
+                        q["us"] for q in fam[12:] if q["batch"] == 25088 and tuple(q["pattern"]) == (6, 64, 16, 8)
+                        and q["dtype"] == r["dtype"] and q["layout"] == r["layout"])} for r in epi},
             }
     fr = np.array([r["frac"] for r in points])
     # Dominant kernel instance: the largest share of one step, i.e. of one

@@ -20,9 +20,11 @@
  *   KS_LAYOUT_BSF  batch-size-first: X is (batch, N), Y is (batch, M);
  *   KS_LAYOUT_BSL  batch-size-last:  X is (N, batch), Y is (M, batch).
  *
- * Types: X, K_values and Y share one storage type (fp32, bf16 or fp16);
- * products are accumulated in fp32 and the result is rounded to the storage
- * type with round-to-nearest-even.
+ * Types: X, K_values and Y share one storage type (fp32, bf16 or fp16), or,
+ * for KS_FP8_E4M3, X and K_values are FP8 E4M3 and Y is bf16; products are
+ * accumulated in fp32 and the result is rounded to Y's type with
+ * round-to-nearest-even (the paper's conclusion names lower precision as its
+ * kernel's open limitation).
  *
  * Ownership: every pointer argument except `pattern` arrays and factor lists is
  * a device pointer owned by the caller; the library allocates no device memory.
@@ -51,9 +53,12 @@ typedef enum {
 } ks_layout_t;
 
 typedef enum {
-    KS_F32 = 0,  /* IEEE binary32 */
-    KS_BF16 = 1, /* bfloat16 */
-    KS_F16 = 2   /* IEEE binary16 */
+    KS_F32 = 0,     /* IEEE binary32 */
+    KS_BF16 = 1,    /* bfloat16 */
+    KS_F16 = 2,     /* IEEE binary16 */
+    KS_FP8_E4M3 = 3 /* X and K_values in OCP FP8 E4M3 ("E4M3FN": bias 7, no
+                       infinities, max 448); Y (and a bias) in bfloat16.
+                       Single factors only (ks_chain: KS_ERR_UNSUPPORTED). */
 } ks_dtype_t;
 
 typedef enum {

@@ -15,7 +15,7 @@ import ctypes
 import os
 
 __all__ = [
-    "BSF", "BSL", "F32", "BF16", "F16", "KsError",
+    "BSF", "BSL", "F32", "BF16", "F16", "FP8", "KsError",
     "ks_matmul", "ks_chain", "ks_chain_workspace_bytes", "ks_chain_noalloc", "ks_chain_noalloc_max_workspace",
     "ks_status_string",
     "ks_last_hip_error", "ks_plan_describe", "ks_force_variant", "ks_plan_verify",
@@ -24,7 +24,7 @@ __all__ = [
 ]
 
 BSF, BSL = 0, 1
-F32, BF16, F16 = 0, 1, 2
+F32, BF16, F16, FP8 = 0, 1, 2, 3
 ACT_NONE, ACT_GELU = 0, 1
 
 KS_OK = 0
@@ -125,7 +125,7 @@ def _code(v, table, what):
 
 _LAYOUTS = {"bsf": BSF, "bsl": BSL}
 _DTYPES = {"f32": F32, "fp32": F32, "float32": F32, "bf16": BF16, "bfloat16": BF16, "f16": F16, "fp16": F16,
-           "float16": F16}
+           "float16": F16, "fp8": FP8, "e4m3": FP8, "float8_e4m3fn": FP8}
 
 
 def _ptr(t):
@@ -272,7 +272,8 @@ def _dtype_of(t):
     global _TORCH_DTYPE_CODES
     import torch
     if _TORCH_DTYPE_CODES is None:
-        _TORCH_DTYPE_CODES = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16}
+        _TORCH_DTYPE_CODES = {torch.float32: F32, torch.bfloat16: BF16, torch.float16: F16,
+                              torch.float8_e4m3fn: FP8}
     if t.dtype not in _TORCH_DTYPE_CODES:
         raise TypeError("unsupported dtype %s" % t.dtype)
     return _TORCH_DTYPE_CODES[t.dtype]
@@ -313,12 +314,14 @@ def _check_batch(X, N, lay):
     return batch
 
 
-def _check_out(out, shape, X):
-    """A caller-supplied output: contiguous, of X's dtype and device, with
-    exactly batch*M elements (the library writes all of them)."""
+def _check_out(out, shape, X, dtype=None):
+    """A caller-supplied output: contiguous, of the output dtype (X's unless
+    given) and X's device, with exactly batch*M elements (the library writes
+    all of them)."""
     _check_tensor(out, "out")
-    if out.dtype != X.dtype:
-        raise TypeError("out has dtype %s, expected %s" % (out.dtype, X.dtype))
+    dtype = X.dtype if dtype is None else dtype
+    if out.dtype != dtype:
+        raise TypeError("out has dtype %s, expected %s" % (out.dtype, dtype))
     if out.device != X.device:
         raise ValueError("out is on %s, expected %s" % (out.device, X.device))
     n = shape[0] * shape[1]
@@ -341,17 +344,18 @@ def matmul(X, K_values, pattern, layout="bsl", out=None, bias=None, act=None):
     N, M = a * c * d, a * b * d
     batch = _check_batch(X, N, lay)
     shape = (batch, M) if lay == BSF else (M, batch)
+    ydtype = torch.bfloat16 if dt == FP8 else X.dtype  # FP8 inputs give bf16 outputs
     if out is None:
-        out = torch.empty(shape, dtype=X.dtype, device=X.device)
+        out = torch.empty(shape, dtype=ydtype, device=X.device)
     else:
-        _check_out(out, shape, X)
+        _check_out(out, shape, X, ydtype)
     if bias is None and act is None:
         ks_matmul(a, b, c, d, K_values, X, out, batch, lay, dt)
         return out
     if bias is not None:
         _check_tensor(bias, "bias")
-        if bias.dtype != X.dtype or bias.device != X.device:
-            raise TypeError("bias must have X's dtype and device")
+        if bias.dtype != ydtype or bias.device != X.device:
+            raise TypeError("bias must have the output's dtype (%s) and X's device" % ydtype)
         if bias.numel() != M:
             raise ValueError("bias has %d elements, the output has a*b*d = %d features" % (bias.numel(), M))
     ks_matmul_bias_act(a, b, c, d, K_values, bias, act, X, out, batch, lay, dt)

@@ -1,0 +1,185 @@
+// FP8 (OCP E4M3) register-direct MFMA kernel: X and K_values hold 8-bit E4M3
+// codes, products accumulate in fp32 on v_mfma_f32_16x16x32_fp8_fp8 (8
+// values of l per lane and operand), Y is written in bfloat16 (the paper's
+// conclusion names low precision as the open limitation of its kernel; its
+// half-precision results are in the appendix).
+//
+// Work decomposition, padding and index arithmetic are the masked kernel's
+// (ks_masked_index.h): one wavefront per item, 16 x 16 tiles padded with
+// zeros, accesses of V consecutive elements (V bytes of X, 2V bytes of Y).
+#include "ks_direct.h"
+#include "ks_epilogue.h"
+#include "ks_masked_index.h"
+
+namespace ks {
+
+namespace {
+
+// N consecutive bytes (N-byte aligned when N is 2, 4, 8 or 16).
+template <int N>
+__device__ __forceinline__ void fp8_load(const uint8_t* p, uint8_t (&v)[N]) {
+  if constexpr (N == 16) {
+    const u32x4 w = *reinterpret_cast<const u32x4*>(p);
+    __builtin_memcpy(v, &w, 16);
+  } else if constexpr (N == 8) {
+    const u32x2 w = *reinterpret_cast<const u32x2*>(p);
+    __builtin_memcpy(v, &w, 8);
+  } else if constexpr (N == 4) {
+    const uint32_t w = *reinterpret_cast<const uint32_t*>(p);
+    __builtin_memcpy(v, &w, 4);
+  } else if constexpr (N == 2) {
+    const uint16_t w = *reinterpret_cast<const uint16_t*>(p);
+    __builtin_memcpy(v, &w, 2);
+  } else {
+    v[0] = p[0];
+  }
+}
+
+template <int LAYOUT, int V>
+__global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
+  constexpr int LP = 8;       // values of l per lane and MFMA
+  constexpr int CH = 4 * LP;  // values of l per chunk
+  constexpr int VK = LAYOUT == BSL ? 1 : V;
+  const int lane = threadIdx.x & 63;
+  const int item = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  if (item >= t.items) return;  // wave-uniform
+  const int n = lane & 15, g = lane >> 4;
+  const MItem it = masked_item(p, t, V, item);
+  const uint8_t* __restrict__ x = static_cast<const uint8_t*>(p.x);
+  const uint8_t* __restrict__ kv = static_cast<const uint8_t*>(p.kv);
+
+  f32x4 acc[V];
+#pragma unroll
+  for (int e = 0; e < V; ++e) acc[e] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int ch = 0; ch < t.nchunks; ++ch) {
+    const int l0 = ch * CH + LP * g;
+    uint8_t xs[LP][V];
+    uint8_t ks[VK][LP];
+#pragma unroll
+    for (int q = 0; q < LP; ++q) {
+      const int64_t off = masked_x_off(p, it, V, l0 + q, n);
+      if (off >= 0) {
+        fp8_load<V>(x + off, xs[q]);
+      } else {
+#pragma unroll
+        for (int e = 0; e < V; ++e) xs[q][e] = 0;
+      }
+    }
+#pragma unroll
+    for (int e = 0; e < VK; ++e) {
+      if (t.kvec) {  // the lane's 8 values of l are one aligned 8-byte run of row k
+        const int64_t ko = masked_k_off(p, it, e, n, l0);
+        if (ko >= 0) {
+          fp8_load<LP>(kv + ko, ks[e]);
+        } else {
+#pragma unroll
+          for (int q = 0; q < LP; ++q) ks[e][q] = 0;
+        }
+      } else {
+#pragma unroll
+        for (int q = 0; q < LP; ++q) {
+          const int64_t ko = masked_k_off(p, it, e, n, l0 + q);
+          ks[e][q] = ko >= 0 ? kv[ko] : 0;
+        }
+      }
+    }
+    // operands: 8 codes per lane, value l0 + q in byte q
+    uint64_t kw[VK];
+#pragma unroll
+    for (int e = 0; e < VK; ++e) {
+      uint64_t w = 0;
+#pragma unroll
+      for (int q = 0; q < LP; ++q) w |= (uint64_t)ks[e][q] << (8 * q);
+      kw[e] = w;
+    }
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      uint64_t xw = 0;
+#pragma unroll
+      for (int q = 0; q < LP; ++q) xw |= (uint64_t)xs[q][e] << (8 * q);
+      acc[e] = __builtin_amdgcn_mfma_f32_16x16x32_fp8_fp8((long)kw[LAYOUT == BSL ? 0 : e], (long)xw, acc[e], 0, 0, 0);
+    }
+  }
+  mfma_results_settle();
+  // outputs k = k0 + 4g + r in bfloat16
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int64_t off = masked_y_off(p, it, V, n, g, r);
+    if (off < 0) continue;
+    const int k = it.k0 + 4 * g + r;
+    uint16_t v[V];
+#pragma unroll
+    for (int e = 0; e < V; ++e) {
+      float y = acc[e][r];
+      if (epilogue_on(p))
+        y = epilogue_apply<bf16_t>(p, y, it.i * p.b * p.d + k * p.d + it.j0 + (LAYOUT == BSF ? e : 0));
+      v[e] = from_f32<bf16_t>(y);
+    }
+    bf16_t* yo = static_cast<bf16_t*>(p.y) + off;
+    if constexpr (V == 8) {
+      u32x4 w;
+      __builtin_memcpy(&w, v, 16);
+      __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(yo));
+    } else if constexpr (V == 4) {
+      u32x2 w;
+      __builtin_memcpy(&w, v, 8);
+      __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(yo));
+    } else {
+#pragma unroll
+      for (int e = 0; e < V; ++e) yo[e] = v[e];
+    }
+  }
+}
+
+}  // namespace
+
+// Access width V (elements): BSL up to 8 along the batch, BSF up to 4
+// consecutive j, as the batch / d and the buffers' alignment allow (X pieces
+// of V bytes, Y pieces of 2V bytes).
+int fp8_vec(const Problem& p) {
+  int V = p.layout == BSL ? 8 : 4;
+  for (; V > 1; V /= 2) {
+    if (p.layout == BSL && p.batch % V) continue;
+    if (p.layout == BSF && p.d % V) continue;
+    if (p.align % (2 * V)) continue;
+    break;
+  }
+  return V;
+}
+
+bool plan_fp8(const Problem& p, Plan* pl) {
+  if (p.dtype != FP8) return false;
+  const int V = fp8_vec(p);
+  const MaskedTile t = masked_tile(p, V);
+  const int64_t items = (int64_t)t.nbt * p.a * t.jgroups * t.kgroups;
+  if (items > 0x7fffffff - 3) return false;
+  pl->variant = V_FP8;
+  pl->vec = V;
+  pl->unroll = 0;
+  pl->waves_m = 1;
+  pl->waves_n = t.kgroups;
+  pl->bt = p.layout == BSL ? 16 * V : 16;
+  pl->jg = p.layout == BSL ? 1 : V;
+  pl->lds_bytes = 0;
+  pl->block = 256;
+  pl->grid = (unsigned)((items + 3) / 4);
+  pl->xcd_remap = 0;
+  return true;
+}
+
+hipError_t launch_fp8(const Problem& p, const Plan& pl, hipStream_t s) {
+  const MaskedTile t = masked_tile(p, pl.vec);
+  const dim3 g(pl.grid), b(256);
+#define KS_FP8(L, VV)                                                        \
+  if (p.layout == L && pl.vec == VV) {                                       \
+    hipLaunchKernelGGL((ks_fp8_kernel<L, VV>), g, b, 0, s, p, t);           \
+    return hipGetLastError();                                                \
+  }
+  KS_FP8(BSL, 1) KS_FP8(BSL, 2) KS_FP8(BSL, 4) KS_FP8(BSL, 8)
+  KS_FP8(BSF, 1) KS_FP8(BSF, 2) KS_FP8(BSF, 4)
+#undef KS_FP8
+  return hipErrorInvalidValue;
+}
+
+}  // namespace ks

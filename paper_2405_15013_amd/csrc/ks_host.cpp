@@ -26,7 +26,11 @@ thread_local int g_chain_fusion = -1;  // -1 automatic, 0 never fuse a chain
 
 constexpr int64_t kMaxElems = (int64_t(1) << 31) - 1;
 
+// Bytes per element of X and K_values (in) and of Y and bias (out): FP8
+// inputs (E4M3) produce bfloat16 outputs.
 int elem_size(int dtype) { return dtype == F32 ? 4 : 2; }
+int in_size(int dtype) { return dtype == FP8 ? 1 : elem_size(dtype); }
+int out_size(int dtype) { return dtype == FP8 ? 2 : elem_size(dtype); }
 
 bool mul_ok(int64_t x, int64_t y, int64_t* out) { return !__builtin_mul_overflow(x, y, out); }
 
@@ -110,6 +114,7 @@ bool plan_direct(const Problem& p, bool al16, Plan* pl);
 bool plan_staged(const Problem& p, bool al16, Plan* pl);
 bool plan_dma(const Problem& p, bool al16, Plan* pl);
 bool plan_masked(const Problem& p, Plan* pl);
+bool plan_fp8(const Problem& p, Plan* pl);
 namespace {
 
 bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
@@ -121,6 +126,7 @@ bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
     case V_STAGED: return plan_staged(p, al16, pl);
     case V_DMA: return plan_dma(p, al16, pl);
     case V_MASKED: return plan_masked(p, pl);
+    case V_FP8: return plan_fp8(p, pl);
     default: return false;
   }
 }
@@ -133,6 +139,7 @@ bool plan_variant(int v, const Problem& p, bool al16, Plan* pl) {
 // a multiple of 16, odd batches, unaligned buffers); the generic kernel only
 // when forced.
 bool plan_auto(const Problem& p, bool al16, Plan* pl) {
+  if (p.dtype == FP8) return plan_fp8(p, pl);  // the only FP8 kernel
   // Batch-size-first with d <= 2: the DMA kernel from 8 MB of X + Y up
   // (measured: below that the register-direct items' shorter latency wins).
   const int64_t xy_bytes = (int64_t)p.batch * (p.N + p.M) * (p.dtype == F32 ? 4 : 2);
@@ -176,7 +183,8 @@ bool get_plan(const Problem& p, bool al16, Plan* out) {
     if (it != g_plans->end()) { *out = it->second; return true; }
   }
   Plan pl;
-  bool ok = forced >= 0 ? plan_variant(forced, p, al16, &pl) : plan_auto(p, al16, &pl);
+  bool ok = forced >= 0 ? ((p.dtype == FP8) == (forced == V_FP8) && plan_variant(forced, p, al16, &pl))
+                        : plan_auto(p, al16, &pl);
   if (!ok) return false;
   std::lock_guard<std::mutex> lk(g_plan_mu);
   (*g_plans)[key] = pl;
@@ -193,6 +201,7 @@ hipError_t launch(const Problem& p, const Plan& pl, hipStream_t s) {
     case V_STAGED: return launch_staged(p, pl, s);
     case V_DMA: return launch_dma(p, pl, s);
     case V_MASKED: return launch_masked(p, pl, s);
+    case V_FP8: return launch_fp8(p, pl, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -204,7 +213,7 @@ ks_status_t validate(int64_t a, int64_t b, int64_t c, int64_t d, const void* kv,
   ks_status_t st = check_pattern(a, b, c, d, &dm);
   if (st != KS_OK) return st;
   if (layout != KS_LAYOUT_BSF && layout != KS_LAYOUT_BSL) return KS_ERR_UNSUPPORTED;
-  if (dtype != KS_F32 && dtype != KS_BF16 && dtype != KS_F16) return KS_ERR_UNSUPPORTED;
+  if (dtype != KS_F32 && dtype != KS_BF16 && dtype != KS_F16 && dtype != KS_FP8_E4M3) return KS_ERR_UNSUPPORTED;
   if (batch < 0) return KS_ERR_INVALID_ARG;
   if (kv == nullptr) return KS_ERR_INVALID_ARG;
   *empty = (batch == 0);
@@ -213,9 +222,9 @@ ks_status_t validate(int64_t a, int64_t b, int64_t c, int64_t d, const void* kv,
   int64_t xe, ye;
   if (!mul_ok(batch, dm.N, &xe) || !mul_ok(batch, dm.M, &ye)) return KS_ERR_UNSUPPORTED;
   if (xe > kMaxElems || ye > kMaxElems || dm.nnz > kMaxElems || batch > kMaxElems) return KS_ERR_UNSUPPORTED;
-  const int s = elem_size(dtype);
-  if (overlaps(x, xe * s, y, ye * s)) return KS_ERR_ALIAS;
-  if (overlaps(kv, dm.nnz * s, y, ye * s)) return KS_ERR_ALIAS;
+  const int si = in_size(dtype), so = out_size(dtype);
+  if (overlaps(x, xe * si, y, ye * so)) return KS_ERR_ALIAS;
+  if (overlaps(kv, dm.nnz * si, y, ye * so)) return KS_ERR_ALIAS;
   p->a = (int)a; p->b = (int)b; p->c = (int)c; p->d = (int)d;
   p->batch = (int)batch;
   p->N = (int)dm.N; p->M = (int)dm.M;
@@ -245,7 +254,7 @@ ks_status_t run_one(const Problem& p, hipStream_t s) {
 // symbol without namespace, spaces or parameter list (profiler summaries are
 // matched against it).
 std::string kernel_name(const Problem& p, const Plan& pl) {
-  static const char* tnames[] = {"float", "unsigned short", "_Float16"};
+  static const char* tnames[] = {"float", "unsigned short", "_Float16", "unsigned char"};
   const char* t = tnames[p.dtype];
   const int m = p.b > p.c ? p.b : p.c;
   const int mx = m <= 2 ? 2 : (m <= 4 ? 4 : (m <= 8 ? 8 : 16));
@@ -278,6 +287,7 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
                pl.waves_m, pl.cps, (int)(pl.rs * pl.nt * pl.lch * p.d * (p.dtype == F32 ? 4 : 2) / 256), pl.nt);
       break;
     case V_MASKED: snprintf(buf, sizeof buf, "ks_masked_kernel<%s,%d,%d>", t, p.layout, pl.vec); break;
+    case V_FP8: snprintf(buf, sizeof buf, "ks_fp8_kernel<%d,%d>", p.layout, pl.vec); break;
     default: snprintf(buf, sizeof buf, "?");
   }
   std::string r(buf);
@@ -286,7 +296,7 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
 }
 
 std::string describe(const Problem& p, const Plan& pl) {
-  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "direct", "staged", "?", "dma", "masked"};
+  static const char* names[] = {"generic", "valu_bsl", "valu_bsf", "direct", "staged", "?", "dma", "masked", "fp8"};
   char buf[320];
   snprintf(buf, sizeof buf,
            "variant=%d name=%s vec=%d bt=%d jg=%d unroll=%d waves_m=%d waves_n=%d lds=%d grid=%u block=%u xcd=%d "
@@ -304,6 +314,8 @@ size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
 // or 0 if the arguments are invalid.
 ks_status_t chain_check(const ks_factor_t* f, int n, int64_t batch, int dtype, size_t* per_buf) {
   if (f == nullptr || n < 1) return KS_ERR_INVALID_ARG;
+  // (FP8 chains are not supported: a factor's bf16 output is not the next
+  // factor's FP8 input.)
   if (dtype != KS_F32 && dtype != KS_BF16 && dtype != KS_F16) return KS_ERR_UNSUPPORTED;
   if (batch < 0) return KS_ERR_INVALID_ARG;
   int64_t widest = 0;
@@ -488,7 +500,7 @@ ks_status_t ks_matmul_bias_act(int64_t a, int64_t b, int64_t c, int64_t d, const
   if (st != KS_OK) return st;
   if (act != KS_ACT_NONE && act != KS_ACT_GELU) return KS_ERR_UNSUPPORTED;
   if (empty) return KS_OK;
-  if (bias != nullptr && overlaps(bias, (int64_t)p.M * elem_size(dtype), Y, (int64_t)p.batch * p.M * elem_size(dtype)))
+  if (bias != nullptr && overlaps(bias, (int64_t)p.M * out_size(dtype), Y, (int64_t)p.batch * p.M * out_size(dtype)))
     return KS_ERR_ALIAS;
   p.bias = bias;
   p.act = act;

@@ -7,7 +7,7 @@
 namespace ks {
 
 enum Layout : int { BSF = 0, BSL = 1 };
-enum Dtype : int { F32 = 0, BF16 = 1, F16 = 2 };
+enum Dtype : int { F32 = 0, BF16 = 1, F16 = 2, FP8 = 3 };  // FP8: X, K in E4M3, Y in bf16
 
 // Kernel variants (the numbering is the "variant=" field of ks_plan_describe
 // and the argument of ks_force_variant).
@@ -20,7 +20,8 @@ enum Variant : int {
   // 5: unused (a persistent streaming variant, measured slower and removed)
   V_DMA = 6,       // LDS-staged MFMA with X moved HBM -> LDS by DMA, three stage buffers (BSF, d >= 4)
   V_MASKED = 7,    // register-direct MFMA with zero-padded tiles and narrow accesses (any b, c, batch, alignment)
-  V_COUNT = 8
+  V_FP8 = 8,       // FP8 (E4M3) inputs, bf16 output: the masked decomposition on fp8 MFMAs
+  V_COUNT = 9
 };
 
 // Problem description shared by all kernels.  Sizes fit in int32 (checked by
@@ -69,6 +70,7 @@ hipError_t launch_direct(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_staged(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_dma(const Problem& p, const Plan& pl, hipStream_t s);
 hipError_t launch_masked(const Problem& p, const Plan& pl, hipStream_t s);
+hipError_t launch_fp8(const Problem& p, const Plan& pl, hipStream_t s);
 struct FusedChain;
 hipError_t launch_chain_fused(const FusedChain& fc, int dtype, bool vec, hipStream_t s);
 

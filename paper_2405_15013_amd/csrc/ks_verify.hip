@@ -167,7 +167,14 @@ bool verify_item(Checker& ck, const DItem& it, bool strided, int V, int MT, int 
 // every Y element of the batch written exactly once, vector accesses aligned.
 bool verify_masked_v(Checker& ck, int V) {
   const Problem& p = ck.p;
+  const bool fp8 = p.dtype == FP8;
   const int S = p.dtype == F32 ? 4 : 2, LP = masked_lp(S), CH = 4 * LP;
+  // bytes of an X piece / Y piece when it is one vector access (0: element
+  // accesses): the masked kernel moves V*S >= 8 bytes as vectors, the FP8
+  // kernel V >= 2 bytes of X and 2V >= 8 bytes of Y
+  const int xvec = fp8 ? (V >= 2 ? V : 0) : (V * S >= 8 ? V * S : 0);
+  const int yvec = fp8 ? (2 * V >= 8 ? 2 * V : 0) : (V * S >= 8 ? V * S : 0);
+  const int xs = fp8 ? 1 : S, ys = fp8 ? 2 : S;
   const MaskedTile t = masked_tile(p, V);
   if (t.kgroups * 16 < p.b || t.nchunks * CH < p.c) return ck.fail("masked tiles do not cover the block", V);
   if (p.layout == BSL && p.batch % V) return ck.fail("batch not a multiple of the access width", V);
@@ -183,7 +190,7 @@ bool verify_masked_v(Checker& ck, int V) {
           const int l = ch * CH + LP * g + q;
           const int64_t off = masked_x_off(p, it, V, l, n);
           if (off >= 0) {
-            if (V * S >= 8 && (off * S) % (V * S)) return ck.fail("X vector not aligned to its size", off);
+            if (xvec && (off * xs) % xvec) return ck.fail("X vector not aligned to its size", off);
             ck.read_x(off, V);
             for (int e = 0; e < V; ++e) {
               DItem di;
@@ -203,7 +210,7 @@ bool verify_masked_v(Checker& ck, int V) {
             for (int e = 0; e < VK; ++e) {
               const int64_t ko = masked_k_off(p, it, e, n, l);
               if (ko >= 0) {
-                if ((ko * S) % 16) return ck.fail("K operand vector not 16-byte aligned", ko);
+                if ((ko * xs) % (LP * xs)) return ck.fail("K operand vector not aligned to its size", ko);
                 ck.read_k(ko, LP);
               }
             }
@@ -221,7 +228,7 @@ bool verify_masked_v(Checker& ck, int V) {
       for (int r = 0; r < 4; ++r) {
         const int64_t off = masked_y_off(p, it, V, n, g, r);
         if (off < 0) continue;
-        if (V * S >= 8 && (off * S) % (V * S)) return ck.fail("Y vector not aligned to its size", off);
+        if (yvec && (off * ys) % yvec) return ck.fail("Y vector not aligned to its size", off);
         ck.write_y(off, V);
       }
     }
@@ -583,6 +590,7 @@ extern "C" ks_status_t ks_plan_verify(int64_t a, int64_t b, int64_t c, int64_t d
     case V_STAGED: ok = verify_staged(ck, pl); break;
     case V_DMA: ok = verify_dma(ck, pl); break;
     case V_MASKED: ok = verify_masked(ck, pl); break;
+    case V_FP8: ok = verify_masked(ck, pl); break;
     default: ck.fail("unknown variant", pl.variant);
   }
   if (ok) ok = ck.coverage();

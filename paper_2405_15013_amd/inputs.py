@@ -7,8 +7,9 @@ consume what it returns, so both sides always see the same values.
 Distributions follow the paper's benchmark set-up (Appendix E.1): inputs X are
 i.i.d. N(0, 1) and the nonzeros of K are i.i.d. uniform on [-1/sqrt(c), 1/sqrt(c)].
 Values are drawn in float64 and rounded to the storage dtype with
-round-to-nearest-even (float64 -> float32 -> bfloat16/float16), so the
-rounded values are exactly representable in every wider format.
+round-to-nearest-even (float64 -> float32 -> bfloat16/float16; float64 ->
+FP8 E4M3 with saturation at +-448), so the rounded values are exactly
+representable in every wider format.
 
 Streams: numpy PCG64 seeded with SeedSequence([BASE_SEED, cfg, a, b, c, d,
 batch, tensor]); tensor 0 is X and tensor 1 + f is the packed values of
@@ -18,7 +19,43 @@ import numpy as np
 
 BASE_SEED = 20240523
 
-DTYPES = ("f32", "bf16", "f16")
+DTYPES = ("f32", "bf16", "f16", "fp8")
+
+
+def _e4m3_table():
+    """The 256 values of the OCP FP8 E4M3 ("E4M3FN") encoding: sign, 4-bit
+    exponent with bias 7, 3-bit mantissa, subnormals at exponent 0, no
+    infinities, NaN at codes 0x7F and 0xFF; largest finite value 448."""
+    vals = np.empty(256, dtype=np.float64)
+    for code in range(256):
+        s, e, m = code >> 7, (code >> 3) & 15, code & 7
+        if e == 15 and m == 7:
+            v = np.nan
+        elif e == 0:
+            v = m * 2.0 ** -9
+        else:
+            v = (1 + m / 8.0) * 2.0 ** (e - 7)
+        vals[code] = -v if s else v
+    return vals
+
+
+E4M3_VALUES = _e4m3_table()
+E4M3_MAX = 448.0
+
+
+def e4m3_from_f64(x64):
+    """Round to the nearest E4M3 value (ties to the even code), saturating to
+    +-448; returns the 8-bit codes as uint8.  NaN inputs give code 0x7F."""
+    x = np.asarray(x64, dtype=np.float64)
+    pos = E4M3_VALUES[:127]  # codes 0 .. 126: 0, then increasing positive values
+    a = np.minimum(np.abs(x), E4M3_MAX)
+    hi = np.clip(np.searchsorted(pos, a, side="left"), 0, 126)
+    lo = np.clip(hi - 1, 0, 126)
+    dlo, dhi = a - pos[lo], pos[hi] - a
+    pick_hi = (dhi < dlo) | ((dhi == dlo) & (hi % 2 == 0))
+    code = np.where(pick_hi, hi, lo).astype(np.uint8)
+    code = np.where(np.signbit(x) & (code != 0), code | 0x80, code).astype(np.uint8)
+    return np.where(np.isnan(x), np.uint8(0x7F), code).astype(np.uint8)
 
 
 def generator(cfg, pattern, batch, tensor):
@@ -51,6 +88,8 @@ def round_to(x64, dtype):
         return bf16_bits_from_f32(x32)
     if dtype == "f16":
         return x32.astype(np.float16)
+    if dtype == "fp8":
+        return e4m3_from_f64(x64)
     raise ValueError("unknown dtype %r" % (dtype,))
 
 
@@ -58,6 +97,8 @@ def to_f64(arr, dtype):
     """Storage array -> exact float64 values."""
     if dtype == "bf16":
         return f32_from_bf16_bits(arr).astype(np.float64)
+    if dtype == "fp8":
+        return E4M3_VALUES[np.asarray(arr, dtype=np.uint8)]
     return np.asarray(arr).astype(np.float64)
 
 

@@ -10,7 +10,7 @@ from paper_2405_15013_amd import inputs
 # Normwise tolerance max|Y - Y64| / max|Y64| against the fp64 oracle: fp32
 # storage with fp32 accumulation, and 16-bit storage with fp32 accumulation
 # (one final rounding to a 2^-8 / 2^-11 ulp format dominates).
-TOL = {"f32": 1e-5, "bf16": 1e-2, "f16": 1e-2}
+TOL = {"f32": 1e-5, "bf16": 1e-2, "f16": 1e-2, "fp8": 1e-2}  # fp8: E4M3 inputs, bf16 output
 
 
 def torch_dtype(dtype):
@@ -23,6 +23,8 @@ def to_device(arr, dtype, device="cuda"):
     a = np.ascontiguousarray(arr)
     if dtype == "bf16":
         return torch.from_numpy(a.view(np.int16)).to(device).view(torch.bfloat16)
+    if dtype == "fp8":
+        return torch.from_numpy(a.view(np.uint8)).to(device).view(torch.float8_e4m3fn)
     return torch.from_numpy(a).to(device)
 
 

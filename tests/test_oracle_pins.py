@@ -335,3 +335,23 @@ def test_bias_is_added_per_output_feature(layout):
     y0 = oracle.matmul(pattern, np.zeros_like(kv), inputs.to_layout(x, layout), 5, layout)
     yg = inputs.from_layout(oracle.bias_act(y0, bias, layout, "gelu"), layout)
     np.testing.assert_allclose(yg, np.broadcast_to(bias * scipy.stats.norm.cdf(bias), (5, M)), rtol=1e-14)
+
+
+def test_e4m3_encoding():
+    """FP8 E4M3 (OCP) input rounding: the code table's landmarks, ties to even,
+    saturation, and agreement with PyTorch's float8_e4m3fn conversion."""
+    v = inputs.E4M3_VALUES
+    assert v[0x00] == 0.0 and v[0x01] == 2.0 ** -9 and v[0x08] == 2.0 ** -6 and v[0x38] == 1.0
+    assert v[0x7E] == 448.0 and np.isnan(v[0x7F]) and v[0xB8] == -1.0
+    pos = v[:127]
+    assert np.all(np.diff(pos) > 0)
+    # ties: halfway between 1 (code 0x38, even) and 1.125 (0x39) -> 1; between 1.125 and 1.25 (0x3A) -> 1.25
+    # below half the smallest subnormal 2^-9 -> 0; above it -> 2^-9
+    got = inputs.to_f64(inputs.round_to(np.array([1.0625, 1.1875, 1000.0, -1000.0, -0.0, 3e-4, 1.5e-3]), "fp8"),
+                        "fp8")
+    np.testing.assert_array_equal(got, [1.0, 1.25, 448.0, -448.0, 0.0, 0.0, 2.0 ** -9])
+    import torch
+    x = np.random.default_rng(5).standard_normal(20000) * 10
+    x = x[np.abs(x) <= 448]
+    ref = torch.from_numpy(x).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    np.testing.assert_array_equal(inputs.round_to(x, "fp8"), ref)
