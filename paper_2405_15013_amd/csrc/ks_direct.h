@@ -141,10 +141,37 @@ __device__ __forceinline__ void direct_mma(const uint32_t* xw, const uint32_t (&
 
 // Stores of the lane's outputs: per M-tile 4 x V values, flat r*V + e, as
 // pieces of YPE contiguous elements (ks_direct_index.h, direct_y_off).
-template <typename T, int LAYOUT, int V, bool STRIDED, int MT>
+// EPI instances apply the bias / activation of ks_epilogue.h piece by piece
+// between the accumulator copy and the rounding, so that only one piece of
+// the tile is live in VGPRs at a time; plain instances (EPI false) carry no
+// epilogue code and keep their register budget.
+template <typename T, int LAYOUT, int V, bool STRIDED, int MT, bool EPI>
 __device__ __forceinline__ void direct_store(const Problem& p, const DItem& it, int n, int g,
                                              const f32x4 (&acc_in)[MT][V]) {
   constexpr int S = sizeof(T);
+  constexpr int YPE = (LAYOUT == BSL || STRIDED) ? V : (4 * V * S < 16 ? 4 * V : 16 / S);
+  constexpr int YNP = 4 * V / YPE;
+  constexpr int YPB = YPE * S;
+  // Output feature of accumulator (mt, e, r): row k = k0 + 16 mt + 4 g + r of
+  // block (i, j), j = j0 (+ e in BSF).  The bias loads are issued before the
+  // wait for the last MFMA results (they depend on the tile only, so every
+  // lane's indices are in range).
+  constexpr int BV = LAYOUT == BSF ? V : 1;
+  bool has_bias = false, gelu = false;
+  float bv[MT][BV][4];
+  if constexpr (EPI) {
+    has_bias = p.bias != nullptr;
+    gelu = epilogue_gelu(p);
+    if (has_bias) {
+      const T* bb = static_cast<const T*>(p.bias) + (int64_t)(it.i * p.b + it.k0 + 4 * g) * p.d + it.j0;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int e = 0; e < BV; ++e) bv[mt][e][r] = to_f32(bb[(16 * mt + r) * p.d + e]);
+    }
+  }
   mfma_results_settle();
   if (!direct_lane_valid(p, it, V, n)) return;
   f32x4 acc[MT][V];
@@ -152,41 +179,38 @@ __device__ __forceinline__ void direct_store(const Problem& p, const DItem& it, 
   for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
     for (int e = 0; e < V; ++e) acc[mt][e] = acc_in[mt][e];
-  if (epilogue_on(p)) {
-    // output feature of accumulator (mt, e, r): row k = k0 + 16 mt + 4 g + r
-    // of block (i, j), j = j0 (+ e in BSF)
-#pragma unroll
-    for (int mt = 0; mt < MT; ++mt)
-#pragma unroll
-      for (int e = 0; e < V; ++e)
-#pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          const int k = it.k0 + 16 * mt + 4 * g + r, j = it.j0 + (LAYOUT == BSF ? e : 0);
-          acc[mt][e][r] = epilogue_apply<T>(p, acc[mt][e][r], it.i * p.b * p.d + k * p.d + j);
-        }
-  }
-  constexpr int YPE = (LAYOUT == BSL || STRIDED) ? V : (4 * V * S < 16 ? 4 * V : 16 / S);
-  constexpr int YNP = 4 * V / YPE;
-  constexpr int YPB = YPE * S;
   T* yl = static_cast<T*>(p.y) + direct_y_base(p, it, V, n, g);
   const int64_t ymstride = direct_y_mstride(p), yqstride = direct_y_qstride(p, STRIDED, V, S);
 #pragma unroll
   for (int mt = 0; mt < MT; ++mt) {
 #pragma unroll
     for (int q = 0; q < YNP; ++q) {
+      float y[YPE];  // flat f = q * YPE + u: accumulator (mt, f % V, f / V)
+#pragma unroll
+      for (int u = 0; u < YPE; ++u) {
+        const int f = q * YPE + u;
+        y[u] = acc[mt][f % V][f / V];
+      }
+      if constexpr (EPI) {
+        if (has_bias) {
+#pragma unroll
+          for (int u = 0; u < YPE; ++u) {
+            const int f = q * YPE + u;
+            y[u] += bv[mt][LAYOUT == BSF ? f % V : 0][f / V];
+          }
+        }
+        if (gelu) {
+#pragma unroll
+          for (int u = 0; u < YPE; ++u) y[u] = gelu_f32(y[u]);
+        }
+      }
       uint32_t w[YPB / 4];
       if constexpr (S == 4) {
 #pragma unroll
-        for (int u = 0; u < YPE; ++u) {
-          const int f = q * YPE + u;
-          w[u] = __float_as_uint(acc[mt][f % V][f / V]);
-        }
+        for (int u = 0; u < YPE; ++u) w[u] = __float_as_uint(y[u]);
       } else {
 #pragma unroll
-        for (int u = 0; u < YPE; u += 2) {
-          const int f0 = q * YPE + u, f1 = f0 + 1;
-          w[u / 2] = pack2_f32<T>(acc[mt][f0 % V][f0 / V], acc[mt][f1 % V][f1 / V]);
-        }
+        for (int u = 0; u < YPE; u += 2) w[u / 2] = pack2_f32<T>(y[u], y[u + 1]);
       }
       store_piece<YPB>(yl + mt * ymstride + q * yqstride, w);
     }
@@ -229,7 +253,7 @@ struct DChunk {
   __device__ __forceinline__ void mma(f32x4 (&acc)[MT][V]) const { direct_mma<T, LAYOUT, V, MT, LP>(xw, kw, acc); }
 };
 
-template <typename T, int LAYOUT, int V, bool STRIDED, int MT>
+template <typename T, int LAYOUT, int V, bool STRIDED, int MT, bool EPI>
 __global__ __launch_bounds__(256) void ks_direct_kernel(Problem p, DirectTile t) {
   constexpr int S = sizeof(T);
   constexpr int LP = S == 4 ? 4 : 8;
@@ -279,7 +303,7 @@ __global__ __launch_bounds__(256) void ks_direct_kernel(Problem p, DirectTile t)
     }
   }
 
-  direct_store<T, LAYOUT, V, STRIDED, MT>(p, it, n, g, acc);
+  direct_store<T, LAYOUT, V, STRIDED, MT, EPI>(p, it, n, g, acc);
 }
 
 // The same work item with the reduction length fixed at compile time: NCH
@@ -289,7 +313,7 @@ __global__ __launch_bounds__(256) void ks_direct_kernel(Problem p, DirectTile t)
 // wavefront's time is then about one memory latency plus its MFMAs, instead
 // of one latency per chunk; a deeper prefetch (64 VGPRs) measured slower for
 // fp32 (fewer resident wavefronts) and the same for 16-bit storage.
-template <typename T, int LAYOUT, int V, bool STRIDED, int MT, int NCH, bool TAIL>
+template <typename T, int LAYOUT, int V, bool STRIDED, int MT, int NCH, bool TAIL, bool EPI>
 __global__ __launch_bounds__(256) void ks_direct_c_kernel(Problem p, DirectTile t) {
   constexpr int S = sizeof(T);
   constexpr int LP = S == 4 ? 4 : 8;
@@ -340,7 +364,7 @@ __global__ __launch_bounds__(256) void ks_direct_c_kernel(Problem p, DirectTile 
   }
   if constexpr (TAIL) tl.mma(acc);
 
-  direct_store<T, LAYOUT, V, STRIDED, MT>(p, it, n, g, acc);
+  direct_store<T, LAYOUT, V, STRIDED, MT, EPI>(p, it, n, g, acc);
 }
 
 // Vector width along the batch (BSL) and largest j-run (BSF): 4 elements, i.e.
@@ -356,7 +380,7 @@ constexpr int direct_mt_max(int esize, int layout, int V) {
   return esize == 4 ? ((layout == BSL || V <= 2) ? 4 : 2) : ((layout == BSL || V <= 2) ? 4 : 2);
 }
 
-template <typename T, int LAYOUT, int V, bool STRIDED, int MT>
+template <typename T, int LAYOUT, int V, bool STRIDED, int MT, bool EPI>
 hipError_t launch_direct_inst(const Problem& p, const DirectTile& t, unsigned grid, hipStream_t s) {
   int nch = 0;
   bool tail = false;
@@ -364,7 +388,7 @@ hipError_t launch_direct_inst(const Problem& p, const DirectTile& t, unsigned gr
   if (direct_c_specialised(sizeof(T), p.c, &nch, &tail)) {
 #define KS_DIRECT_C(N, TL)                                                                          \
   if (nch == N && tail == TL) {                                                                    \
-    hipLaunchKernelGGL((ks_direct_c_kernel<T, LAYOUT, V, STRIDED, MT, N, TL>), g, b, 0, s, p, t); \
+    hipLaunchKernelGGL((ks_direct_c_kernel<T, LAYOUT, V, STRIDED, MT, N, TL, EPI>), g, b, 0, s, p, t); \
     return hipGetLastError();                                                                      \
   }
     if constexpr (sizeof(T) == 4) {
@@ -376,43 +400,43 @@ hipError_t launch_direct_inst(const Problem& p, const DirectTile& t, unsigned gr
     }
 #undef KS_DIRECT_C
   }
-  hipLaunchKernelGGL((ks_direct_kernel<T, LAYOUT, V, STRIDED, MT>), g, b, 0, s, p, t);
+  hipLaunchKernelGGL((ks_direct_kernel<T, LAYOUT, V, STRIDED, MT, EPI>), g, b, 0, s, p, t);
   return hipGetLastError();
 }
 
-template <typename T, int LAYOUT, int V, bool STRIDED>
+template <typename T, int LAYOUT, int V, bool STRIDED, bool EPI>
 hipError_t launch_direct_mt(const Problem& p, const DirectTile& t, int mt, unsigned grid, hipStream_t s) {
   constexpr int MX = direct_mt_max(sizeof(T), LAYOUT, V);
   switch (mt) {
-    case 1: return launch_direct_inst<T, LAYOUT, V, STRIDED, 1>(p, t, grid, s);
-    case 2: if constexpr (MX >= 2) return launch_direct_inst<T, LAYOUT, V, STRIDED, 2>(p, t, grid, s); break;
-    case 3: if constexpr (MX >= 3) return launch_direct_inst<T, LAYOUT, V, STRIDED, 3>(p, t, grid, s); break;
-    case 4: if constexpr (MX >= 4) return launch_direct_inst<T, LAYOUT, V, STRIDED, 4>(p, t, grid, s); break;
+    case 1: return launch_direct_inst<T, LAYOUT, V, STRIDED, 1, EPI>(p, t, grid, s);
+    case 2: if constexpr (MX >= 2) return launch_direct_inst<T, LAYOUT, V, STRIDED, 2, EPI>(p, t, grid, s); break;
+    case 3: if constexpr (MX >= 3) return launch_direct_inst<T, LAYOUT, V, STRIDED, 3, EPI>(p, t, grid, s); break;
+    case 4: if constexpr (MX >= 4) return launch_direct_inst<T, LAYOUT, V, STRIDED, 4, EPI>(p, t, grid, s); break;
     default: break;
   }
   return hipErrorInvalidValue;
 }
 
-// All instances of one storage type.
-template <typename T>
+// All instances of one storage type, plain (EPI false) or with the epilogue.
+template <typename T, bool EPI>
 hipError_t launch_direct_type(const Problem& p, const DirectTile& t, int V, bool strided, int mt, unsigned grid,
                               hipStream_t s) {
   if (p.layout == BSL) {
     if (strided) return hipErrorInvalidValue;
     if constexpr (sizeof(T) == 2) {
-      if (V == kDirectVecBsl16) return launch_direct_mt<T, BSL, kDirectVecBsl16, false>(p, t, mt, grid, s);
+      if (V == kDirectVecBsl16) return launch_direct_mt<T, BSL, kDirectVecBsl16, false, EPI>(p, t, mt, grid, s);
     }
     if (V != kDirectVec) return hipErrorInvalidValue;
-    return launch_direct_mt<T, BSL, kDirectVec, false>(p, t, mt, grid, s);
+    return launch_direct_mt<T, BSL, kDirectVec, false, EPI>(p, t, mt, grid, s);
   }
   if (strided) {
     if (V != kDirectVec) return hipErrorInvalidValue;
-    return launch_direct_mt<T, BSF, kDirectVec, true>(p, t, mt, grid, s);
+    return launch_direct_mt<T, BSF, kDirectVec, true, EPI>(p, t, mt, grid, s);
   }
   switch (V) {
-    case 1: return launch_direct_mt<T, BSF, 1, false>(p, t, mt, grid, s);
-    case 2: return launch_direct_mt<T, BSF, 2, false>(p, t, mt, grid, s);
-    case 4: return launch_direct_mt<T, BSF, 4, false>(p, t, mt, grid, s);
+    case 1: return launch_direct_mt<T, BSF, 1, false, EPI>(p, t, mt, grid, s);
+    case 2: return launch_direct_mt<T, BSF, 2, false, EPI>(p, t, mt, grid, s);
+    case 4: return launch_direct_mt<T, BSF, 4, false, EPI>(p, t, mt, grid, s);
     default: break;
   }
   return hipErrorInvalidValue;

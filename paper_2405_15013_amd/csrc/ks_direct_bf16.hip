@@ -6,7 +6,7 @@ namespace ks {
 
 hipError_t launch_direct_bf16(const Problem& p, const DirectTile& t, int V, bool strided, int mt, unsigned grid,
                             hipStream_t s) {
-  return launch_direct_type<bf16_t>(p, t, V, strided, mt, grid, s);
+  return launch_direct_type<bf16_t, false>(p, t, V, strided, mt, grid, s);
 }
 
 }  // namespace ks

@@ -6,7 +6,7 @@ namespace ks {
 
 hipError_t launch_direct_f32(const Problem& p, const DirectTile& t, int V, bool strided, int mt, unsigned grid,
                             hipStream_t s) {
-  return launch_direct_type<float>(p, t, V, strided, mt, grid, s);
+  return launch_direct_type<float, false>(p, t, V, strided, mt, grid, s);
 }
 
 }  // namespace ks

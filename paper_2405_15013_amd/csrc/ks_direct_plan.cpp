@@ -17,6 +17,12 @@ hipError_t launch_direct_bf16(const Problem& p, const DirectTile& t, int V, bool
                               hipStream_t s);
 hipError_t launch_direct_f16(const Problem& p, const DirectTile& t, int V, bool strided, int mt, unsigned grid,
                              hipStream_t s);
+hipError_t launch_direct_f32_epi(const Problem& p, const DirectTile& t, int V, bool strided, int mt, unsigned grid,
+                                 hipStream_t s);
+hipError_t launch_direct_bf16_epi(const Problem& p, const DirectTile& t, int V, bool strided, int mt, unsigned grid,
+                                  hipStream_t s);
+hipError_t launch_direct_f16_epi(const Problem& p, const DirectTile& t, int V, bool strided, int mt, unsigned grid,
+                                 hipStream_t s);
 hipError_t launch_masked_f32(const Problem& p, const MaskedTile& t, int V, unsigned grid, hipStream_t s);
 hipError_t launch_masked_bf16(const Problem& p, const MaskedTile& t, int V, unsigned grid, hipStream_t s);
 hipError_t launch_masked_f16(const Problem& p, const MaskedTile& t, int V, unsigned grid, hipStream_t s);
@@ -149,6 +155,14 @@ hipError_t launch_masked(const Problem& p, const Plan& pl, hipStream_t s) {
 hipError_t launch_direct(const Problem& p, const Plan& pl, hipStream_t s) {
   const DirectTile t = direct_tile(p, pl);
   const bool strided = pl.unroll != 0;
+  if (has_epilogue(p)) {
+    switch (p.dtype) {
+      case F32: return launch_direct_f32_epi(p, t, pl.vec, strided, pl.waves_m, pl.grid, s);
+      case BF16: return launch_direct_bf16_epi(p, t, pl.vec, strided, pl.waves_m, pl.grid, s);
+      case F16: return launch_direct_f16_epi(p, t, pl.vec, strided, pl.waves_m, pl.grid, s);
+      default: return hipErrorInvalidValue;
+    }
+  }
   switch (p.dtype) {
     case F32: return launch_direct_f32(p, t, pl.vec, strided, pl.waves_m, pl.grid, s);
     case BF16: return launch_direct_bf16(p, t, pl.vec, strided, pl.waves_m, pl.grid, s);

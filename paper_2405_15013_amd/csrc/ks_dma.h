@@ -239,10 +239,22 @@ void ks_dma_kernel(Problem p, StagedTile t) {
   }
 
   // Structured epilogue: accumulators -> LDS output tile -> contiguous runs.
+  // Bias of output feature (mt, e, r4) = row k0 + 16 mt + 4 g + r4 of block
+  // (i, j0 + e), shared by the NT row groups; loads issued before the wait
+  // for the last MFMA results.
+  const bool has_bias = p.bias != nullptr;
+  float bv[MT][V][4];
+  if (has_bias) {
+    const T* bb = static_cast<const T*>(p.bias) + (int64_t)(st.i * p.b + it.k0 + 4 * g) * p.d + it.j0;
+#pragma unroll
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int r4 = 0; r4 < 4; ++r4)
+#pragma unroll
+        for (int e = 0; e < V; ++e) bv[mt][e][r4] = to_f32(bb[(16 * mt + r4) * p.d + e]);
+  }
   mfma_results_settle();
-  if (epilogue_on(p)) {
-    // output feature of accumulator (u, mt, e, r4): row k = k0 + 16 mt + 4 g + r4
-    // of block (i, j0 + e)
+  if (has_bias) {
 #pragma unroll
     for (int u = 0; u < NT; ++u)
 #pragma unroll
@@ -250,10 +262,17 @@ void ks_dma_kernel(Problem p, StagedTile t) {
 #pragma unroll
         for (int e = 0; e < V; ++e)
 #pragma unroll
-          for (int r4 = 0; r4 < 4; ++r4) {
-            const int k = it.k0 + 16 * mt + 4 * g + r4;
-            acc[u][mt][e][r4] = epilogue_apply<T>(p, acc[u][mt][e][r4], st.i * p.b * p.d + k * p.d + it.j0 + e);
-          }
+          for (int r4 = 0; r4 < 4; ++r4) acc[u][mt][e][r4] += bv[mt][e][r4];
+  }
+  if (epilogue_gelu(p)) {
+#pragma unroll
+    for (int u = 0; u < NT; ++u)
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4) acc[u][mt][e][r4] = gelu_f32(acc[u][mt][e][r4]);
   }
   __syncthreads();  // every wavefront is done with the stage buffers
   char* ycell0 = smem + dma_y_lds_lane(p, t, si, MT, S, n, g);

@@ -101,21 +101,41 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
       acc[e] = __builtin_amdgcn_mfma_f32_16x16x32_fp8_fp8((long)kw[LAYOUT == BSL ? 0 : e], (long)xw, acc[e], 0, 0, 0);
     }
   }
+  // Epilogue: output feature of (e, r) is row k = k0 + 4g + r of block
+  // (i, j0 [+ e in BSF]); padding rows (k >= b) take no bias.
+  constexpr int BV = LAYOUT == BSF ? V : 1;
+  const bool has_bias = p.bias != nullptr;
+  float bv[4][BV];
+  if (has_bias) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int k = it.k0 + 4 * g + r;
+#pragma unroll
+      for (int e = 0; e < BV; ++e)
+        bv[r][e] = k < p.b ? bias_value<bf16_t>(p, ((int64_t)it.i * p.b + k) * p.d + it.j0 + e) : 0.0f;
+    }
+  }
   mfma_results_settle();
+  if (has_bias) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int e = 0; e < V; ++e) acc[e][r] += bv[r][LAYOUT == BSF ? e : 0];
+  }
+  if (epilogue_gelu(p)) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int e = 0; e < V; ++e) acc[e][r] = gelu_f32(acc[e][r]);
+  }
   // outputs k = k0 + 4g + r in bfloat16
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int64_t off = masked_y_off(p, it, V, n, g, r);
     if (off < 0) continue;
-    const int k = it.k0 + 4 * g + r;
     uint16_t v[V];
 #pragma unroll
-    for (int e = 0; e < V; ++e) {
-      float y = acc[e][r];
-      if (epilogue_on(p))
-        y = epilogue_apply<bf16_t>(p, y, it.i * p.b * p.d + k * p.d + it.j0 + (LAYOUT == BSF ? e : 0));
-      v[e] = from_f32<bf16_t>(y);
-    }
+    for (int e = 0; e < V; ++e) v[e] = from_f32<bf16_t>(acc[e][r]);
     bf16_t* yo = static_cast<bf16_t*>(p.y) + off;
     if constexpr (V == 8) {
       u32x4 w;

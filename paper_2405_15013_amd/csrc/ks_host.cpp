@@ -258,6 +258,7 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
   const char* t = tnames[p.dtype];
   const int m = p.b > p.c ? p.b : p.c;
   const int mx = m <= 2 ? 2 : (m <= 4 ? 4 : (m <= 8 ? 8 : 16));
+  const char* epi = has_epilogue(p) ? "true" : "false";  // direct / masked instances with the epilogue
   char buf[160];
   switch (pl.variant) {
     case V_GENERIC: snprintf(buf, sizeof buf, "ks_generic_kernel<%s>", t); break;
@@ -269,11 +270,11 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
       int nch = 0;
       bool tail = false;
       if (direct_c_specialised(p.dtype == F32 ? 4 : 2, p.c, &nch, &tail))
-        snprintf(buf, sizeof buf, "ks_direct_c_kernel<%s,%d,%d,%s,%d,%d,%s>", t, p.layout, pl.vec,
-                 pl.unroll ? "true" : "false", pl.waves_m, nch, tail ? "true" : "false");
+        snprintf(buf, sizeof buf, "ks_direct_c_kernel<%s,%d,%d,%s,%d,%d,%s,%s>", t, p.layout, pl.vec,
+                 pl.unroll ? "true" : "false", pl.waves_m, nch, tail ? "true" : "false", epi);
       else
-        snprintf(buf, sizeof buf, "ks_direct_kernel<%s,%d,%d,%s,%d>", t, p.layout, pl.vec,
-                 pl.unroll ? "true" : "false", pl.waves_m);
+        snprintf(buf, sizeof buf, "ks_direct_kernel<%s,%d,%d,%s,%d,%s>", t, p.layout, pl.vec,
+                 pl.unroll ? "true" : "false", pl.waves_m, epi);
       break;
     }
     case V_STAGED:
@@ -286,7 +287,7 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
       snprintf(buf, sizeof buf, "ks_dma_kernel<%s,%d,%s,%d,%d,%d,%d>", t, pl.vec, pl.unroll ? "true" : "false",
                pl.waves_m, pl.cps, (int)(pl.rs * pl.nt * pl.lch * p.d * (p.dtype == F32 ? 4 : 2) / 256), pl.nt);
       break;
-    case V_MASKED: snprintf(buf, sizeof buf, "ks_masked_kernel<%s,%d,%d>", t, p.layout, pl.vec); break;
+    case V_MASKED: snprintf(buf, sizeof buf, "ks_masked_kernel<%s,%d,%d,%s>", t, p.layout, pl.vec, epi); break;
     case V_FP8: snprintf(buf, sizeof buf, "ks_fp8_kernel<%d,%d>", p.layout, pl.vec); break;
     default: snprintf(buf, sizeof buf, "?");
   }

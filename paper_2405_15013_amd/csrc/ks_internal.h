@@ -40,6 +40,9 @@ struct Problem {
   int act;           // epilogue activation: 0 none, 1 GELU
 };
 
+// Host side: whether the call needs the instances with the epilogue compiled in.
+inline bool has_epilogue(const Problem& p) { return p.bias != nullptr || p.act != 0; }
+
 // Launch description produced by the planner.
 struct Plan {
   int variant = V_GENERIC;

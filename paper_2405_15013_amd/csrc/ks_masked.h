@@ -44,7 +44,7 @@ __device__ __forceinline__ uint32_t masked_bits(float v) { return __float_as_uin
 __device__ __forceinline__ uint32_t masked_bits(bf16_t v) { return v; }
 __device__ __forceinline__ uint32_t masked_bits(_Float16 v) { return __builtin_bit_cast(uint16_t, v); }
 
-template <typename T, int LAYOUT, int V>
+template <typename T, int LAYOUT, int V, bool EPI>
 __global__ __launch_bounds__(256) void ks_masked_kernel(Problem p, MaskedTile t) {
   constexpr int S = sizeof(T);
   constexpr int LP = S == 4 ? 4 : 8;
@@ -122,31 +122,62 @@ __global__ __launch_bounds__(256) void ks_masked_kernel(Problem p, MaskedTile t)
     }
     direct_mma<T, LAYOUT, V, 1, LP>(xw, kw, acc);
   }
-  mfma_results_settle();
+  // Epilogue (EPI instances only): output feature of (e, r) is row
+  // k = k0 + 4g + r of block (i, j0 [+ e in BSF]); padding rows (k >= b) take
+  // no bias.
+  if constexpr (EPI) {
+    constexpr int BV = LAYOUT == BSF ? V : 1;
+    const bool has_bias = p.bias != nullptr;
+    float bv[4][BV];
+    if (has_bias) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int k = it.k0 + 4 * g + r;
+#pragma unroll
+        for (int e = 0; e < BV; ++e)
+          bv[r][e] = k < p.b ? bias_value<T>(p, ((int64_t)it.i * p.b + k) * p.d + it.j0 + e) : 0.0f;
+      }
+    }
+    mfma_results_settle();
+    if (has_bias) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc[0][e][r] += bv[r][LAYOUT == BSF ? e : 0];
+    }
+    if (epilogue_gelu(p)) {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc[0][e][r] = gelu_f32(acc[0][e][r]);
+    }
+  } else {
+    mfma_results_settle();
+  }
   // outputs k = k0 + 4g + r, columns e of the lane's piece
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const int64_t off = masked_y_off(p, it, V, n, g, r);
     if (off < 0) continue;
     T v[V];
-    const int k = it.k0 + 4 * g + r;
 #pragma unroll
-    for (int e = 0; e < V; ++e) {
-      float y = acc[0][e][r];
-      if (epilogue_on(p)) y = epilogue_apply<T>(p, y, it.i * p.b * p.d + k * p.d + it.j0 + (LAYOUT == BSF ? e : 0));
-      v[e] = from_f32<T>(y);
-    }
+    for (int e = 0; e < V; ++e) v[e] = from_f32<T>(acc[0][e][r]);
     masked_store<T, V>(static_cast<T*>(p.y) + off, v);
   }
 }
 
 // Instances of one storage type: V in {1, 2, 4} (and 8 for 16-bit BSL).
+// EPI: the bias / activation epilogue compiled in (calls that need it).
 template <typename T>
 hipError_t launch_masked_type(const Problem& p, const MaskedTile& t, int V, unsigned grid, hipStream_t s) {
   const dim3 g(grid), b(256);
+  const bool epi = has_epilogue(p);
 #define KS_MASKED(L, VV)                                                              \
   if (p.layout == L && V == VV) {                                                     \
-    hipLaunchKernelGGL((ks_masked_kernel<T, L, VV>), g, b, 0, s, p, t);              \
+    if (epi)                                                                          \
+      hipLaunchKernelGGL((ks_masked_kernel<T, L, VV, true>), g, b, 0, s, p, t);      \
+    else                                                                              \
+      hipLaunchKernelGGL((ks_masked_kernel<T, L, VV, false>), g, b, 0, s, p, t);     \
     return hipGetLastError();                                                         \
   }
   KS_MASKED(BSL, 1) KS_MASKED(BSL, 2) KS_MASKED(BSL, 4)

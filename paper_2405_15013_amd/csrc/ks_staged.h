@@ -191,21 +191,37 @@ __global__ __launch_bounds__(512) void ks_staged_kernel(Problem p, StagedTile t)
   if constexpr (LAYOUT == BSL) {
     // Each lane's 4-element runs along the batch already form 256-byte row
     // segments per wavefront store: store straight from the accumulators.
-    direct_store<T, LAYOUT, V, STRIDED, MT>(p, it, n, g, acc);
+    direct_store<T, LAYOUT, V, STRIDED, MT, true>(p, it, n, g, acc);
   } else {
     // Structured epilogue: accumulators -> LDS output tile -> contiguous runs.
     // (The loop's last barrier guarantees no wavefront still reads X stages.)
+    const bool has_bias = p.bias != nullptr;
+    float bv[MT][V][4];  // output feature: row k0 + 16 mt + 4 g + r4 of block (i, j0 + e)
+    if (has_bias) {
+      const T* bb = static_cast<const T*>(p.bias) + (int64_t)(it.i * p.b + it.k0 + 4 * g) * p.d + it.j0;
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int r4 = 0; r4 < 4; ++r4)
+#pragma unroll
+          for (int e = 0; e < V; ++e) bv[mt][e][r4] = to_f32(bb[(16 * mt + r4) * p.d + e]);
+    }
     mfma_results_settle();
-    if (epilogue_on(p)) {
+    if (has_bias) {
 #pragma unroll
       for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
         for (int e = 0; e < V; ++e)
 #pragma unroll
-          for (int r4 = 0; r4 < 4; ++r4) {
-            const int k = it.k0 + 16 * mt + 4 * g + r4;
-            acc[mt][e][r4] = epilogue_apply<T>(p, acc[mt][e][r4], it.i * p.b * p.d + k * p.d + it.j0 + e);
-          }
+          for (int r4 = 0; r4 < 4; ++r4) acc[mt][e][r4] += bv[mt][e][r4];
+    }
+    if (epilogue_gelu(p)) {
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+        for (int e = 0; e < V; ++e)
+#pragma unroll
+          for (int r4 = 0; r4 < 4; ++r4) acc[mt][e][r4] = gelu_f32(acc[mt][e][r4]);
     }
     const int r = 16 * si.rs + n;
 #pragma unroll

@@ -90,9 +90,14 @@ __global__ __launch_bounds__(256) void ks_valu_bsl_kernel(Problem p) {
           for (int e = 0; e < VEC; ++e) acc[e] = __builtin_fmaf(to_f32(blk[k * c + l]), xv[u][l][e], acc[e]);
         }
       }
-      if (epilogue_on(p)) {
+      if (p.bias != nullptr) {
+        const float bk = bias_value<T>(p, (int64_t)yrow0 + k * d);
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[e] = epilogue_apply<T>(p, acc[e], (int)yrow0 + k * d);
+        for (int e = 0; e < VEC; ++e) acc[e] += bk;
+      }
+      if (epilogue_gelu(p)) {
+#pragma unroll
+        for (int e = 0; e < VEC; ++e) acc[e] = gelu_f32(acc[e]);
       }
       store_vec<T, VEC>(y + yrow0 * batch + k * ystep + (size_t)v * VEC, acc);
     }
@@ -142,9 +147,13 @@ __global__ __launch_bounds__(256) void ks_valu_bsf_kernel(Problem p) {
         for (int e = 0; e < V; ++e) acc[e] = __builtin_fmaf(to_f32(blk[(size_t)e * b * c + k * c + l]), xv[l][e], acc[e]);
       }
     }
-    if (epilogue_on(p)) {
+    if (p.bias != nullptr) {
 #pragma unroll
-      for (int e = 0; e < V; ++e) acc[e] = epilogue_apply<T>(p, acc[e], i * b * d + k * d + j0 + e);
+      for (int e = 0; e < V; ++e) acc[e] += bias_value<T>(p, (int64_t)(i * b + k) * d + j0 + e);
+    }
+    if (epilogue_gelu(p)) {
+#pragma unroll
+      for (int e = 0; e < V; ++e) acc[e] = gelu_f32(acc[e]);
     }
     store_vec<T, V>(ys + (size_t)k * d, acc);
   }
