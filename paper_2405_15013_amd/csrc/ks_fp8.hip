@@ -140,11 +140,13 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
     if constexpr (V == 8) {
       u32x4 w;
       __builtin_memcpy(&w, v, 16);
-      __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(yo));
+      if constexpr (LAYOUT == BSL) __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(yo));
+      else *reinterpret_cast<u32x4*>(yo) = w;
     } else if constexpr (V == 4) {
       u32x2 w;
       __builtin_memcpy(&w, v, 8);
-      __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(yo));
+      if constexpr (LAYOUT == BSL) __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(yo));
+      else *reinterpret_cast<u32x2*>(yo) = w;
     } else {
 #pragma unroll
       for (int e = 0; e < V; ++e) yo[e] = v[e];
@@ -154,11 +156,13 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
 
 }  // namespace
 
-// Access width V (elements): BSL up to 8 along the batch, BSF up to 4
-// consecutive j, as the batch / d and the buffers' alignment allow (X pieces
-// of V bytes, Y pieces of 2V bytes).
+// Access width V (elements): up to 8 along the batch (BSL) or consecutive j
+// (BSF), as the batch / d and the buffers' alignment allow (X pieces of V
+// bytes, Y pieces of 2V bytes).  In BSF with V = d = 8 a lane's X operand is
+// one contiguous 64-byte run of its batch row (8 values of l x 8 j) and its 4
+// output rows one contiguous 64-byte run of Y.
 int fp8_vec(const Problem& p) {
-  int V = p.layout == BSL ? 8 : 4;
+  int V = 8;
   for (; V > 1; V /= 2) {
     if (p.layout == BSL && p.batch % V) continue;
     if (p.layout == BSF && p.d % V) continue;
@@ -197,7 +201,7 @@ hipError_t launch_fp8(const Problem& p, const Plan& pl, hipStream_t s) {
     return hipGetLastError();                                                \
   }
   KS_FP8(BSL, 1) KS_FP8(BSL, 2) KS_FP8(BSL, 4) KS_FP8(BSL, 8)
-  KS_FP8(BSF, 1) KS_FP8(BSF, 2) KS_FP8(BSF, 4)
+  KS_FP8(BSF, 1) KS_FP8(BSF, 2) KS_FP8(BSF, 4) KS_FP8(BSF, 8)
 #undef KS_FP8
   return hipErrorInvalidValue;
 }

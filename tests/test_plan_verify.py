@@ -163,3 +163,19 @@ def test_no_generic_plan_for_large_blocks(pattern, batch, layout, dtype):
     if batch <= 4096:
         st, rep = ks.ks_plan_verify(*pattern, batch, layout, dtype)
         assert st == 0, (desc, rep)
+
+
+@pytest.mark.parametrize("layout", ["bsf", "bsl"])
+@pytest.mark.parametrize("batch", [4096, 1001])
+def test_fp8_sweep_plans(layout, batch):
+    """Host replay of the FP8 kernel's plan (access width up to 8 in both
+    layouts) over every sweep pattern: coverage, padding, alignment."""
+    for pattern in sweep_patterns()[::15] + [(6, 64, 16, 8), (6, 16, 64, 8), (1, 17, 33, 3), (4, 48, 32, 16)]:
+        st, rep = ks.ks_plan_verify(*pattern, batch, layout, "fp8")
+        assert st == 0, "%s B=%d %s: %s" % (pattern, batch, layout, rep)
+        assert "name=fp8" in ks.ks_plan_describe(*pattern, batch, layout, "fp8")
+
+
+def test_fp8_bsf_uses_full_rows_when_d_is_8():
+    desc = ks.ks_plan_describe(6, 64, 16, 8, 25088, "bsf", "fp8")
+    assert "vec=8" in desc, desc
