@@ -26,8 +26,9 @@
 // output rows, into the other LDS buffer when b != c.
 //
 // Factor values: each pass's values (its factors' packed blocks, one after
-// the other) are fetched from global memory into registers one pass ahead and
-// parked in an LDS copy as fp32 between passes.
+// the other) are fetched from global memory into registers one pass ahead
+// (runs of 4 consecutive values per load when the buffers allow) and parked
+// in an LDS copy as fp32 between passes.
 //
 // LDS layout: row r of the vector holds the tile's 16 columns at
 // r * kFusedPitch floats (16 columns + 4 pad floats, so 16-byte accesses of
@@ -57,6 +58,8 @@ struct FusedChain {
   int width_in, width_out;  // a*c*d of factor nf-1, a*b*d of factor 0
   int inplace;              // every factor has b == c: one LDS buffer
   int buf_rows;             // rows of one LDS buffer (the widest vector)
+  int kvec;                 // factor values fetched 4 at a time: every factor's count is a multiple
+                            // of 4 and its values are aligned to 4 elements (set at launch)
   int a[kFusedMaxFactors], b[kFusedMaxFactors], c[kFusedMaxFactors], d[kFusedMaxFactors];
   uint32_t md[kFusedMaxFactors];  // multiply-shift constants of the division by d
   int sd[kFusedMaxFactors];

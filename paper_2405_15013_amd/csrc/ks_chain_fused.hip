@@ -3,9 +3,10 @@
 // Latency: a workgroup is the only one on its CU for most chain shapes (one
 // tile of 16 columns per CU at batch 4096), so nothing else hides its memory
 // latency.  The tile loads are issued in batches of kFusedLoadBatch 16-byte
-// loads per thread before any of them is used, and each factor's values are
-// fetched from global memory into registers one factor ahead and parked in a
-// double-buffered LDS copy, so the factor loop itself touches only LDS.
+// loads per thread before any of them is used (one batch for a 64 KB tile of
+// fp32 or a 32 KB tile of 16-bit values), and each pass's values are
+// fetched from global memory into registers one pass ahead and parked in the
+// LDS copy after the pass, so the pass loop itself touches only LDS.
 #include <type_traits>
 
 #include "ks_chain_fused.h"
@@ -17,7 +18,7 @@ namespace ks {
 namespace {
 
 typedef float f32x4 __attribute__((ext_vector_type(4)));
-constexpr int kFusedLoadBatch = 4;
+constexpr int kFusedLoadBatch = 8;
 
 // Load the tile's input columns into LDS rows [0, width_in) (fp32).
 //  BSL: X is (N, batch); row n of the tile is the run X[n, col0 .. col0+16).
@@ -100,11 +101,15 @@ __device__ __forceinline__ void fused_store(const FusedChain& fc, const float* l
 }
 
 // Values of pass q (its factors' packed blocks, one after the other): this
-// thread's share (elements tid + kFusedThreads*r) fetched into registers,
-// later parked in the LDS copy as fp32.
+// thread's share fetched into registers in the storage type (so that no
+// conversion waits for the loads), converted and parked in the LDS copy after
+// the pass.  Scalar form: elements tid + kFusedThreads*r.  Vector form
+// (fc.kvec): runs of 4 elements 4*(tid + kFusedThreads*r) .. +3, one 16- or
+// 8-byte load and one 16-byte LDS write each (no run crosses a factor, whose
+// counts are multiples of 4).
 template <typename T>
 struct FusedK {
-  float v[kFusedKPerThread];
+  T v[kFusedKPerThread];
   __device__ __forceinline__ void fetch(const FusedChain& fc, int q) {
     // A pass has at most three factors: their value pointers are selected per
     // element (no per-lane indexing into the kernel arguments).
@@ -112,24 +117,46 @@ struct FusedK {
     const T* k0 = static_cast<const T*>(fc.kv[f0]);
     const T* k1 = m > 1 ? static_cast<const T*>(fc.kv[f0 - 1]) : k0;
     const T* k2 = m > 2 ? static_cast<const T*>(fc.kv[f0 - 2]) : k0;
+    if (fc.kvec) {
+      typedef typename std::conditional<sizeof(T) == 4, u32x4, u32x2>::type W;
+#pragma unroll
+      for (int r = 0; r < kFusedKPerThread / 4; ++r) {
+        const int e = 4 * (r * kFusedThreads + (int)threadIdx.x);
+        if (e < n) {
+          const int t = e >= 2 * cnt ? 2 : (e >= cnt ? 1 : 0);
+          const T* kp = t == 0 ? k0 : (t == 1 ? k1 : k2);
+          const W w = *reinterpret_cast<const W*>(kp + (e - t * cnt));
+          __builtin_memcpy(&v[4 * r], &w, sizeof(W));
+        }
+      }
+      return;
+    }
 #pragma unroll
     for (int r = 0; r < kFusedKPerThread; ++r) {
       const int e = r * kFusedThreads + (int)threadIdx.x;
       if (e < n) {
         const int t = e >= 2 * cnt ? 2 : (e >= cnt ? 1 : 0);
         const T* kp = t == 0 ? k0 : (t == 1 ? k1 : k2);
-        v[r] = to_f32(kp[e - t * cnt]);
-      } else {
-        v[r] = 0.f;
+        v[r] = kp[e - t * cnt];
       }
     }
   }
   __device__ __forceinline__ void park(const FusedChain& fc, int q, float* kbuf) const {
     const int n = fc.pk[q];
+    if (fc.kvec) {
+#pragma unroll
+      for (int r = 0; r < kFusedKPerThread / 4; ++r) {
+        const int e = 4 * (r * kFusedThreads + (int)threadIdx.x);
+        if (e < n)
+          *reinterpret_cast<f32x4*>(kbuf + e) =
+              f32x4{to_f32(v[4 * r]), to_f32(v[4 * r + 1]), to_f32(v[4 * r + 2]), to_f32(v[4 * r + 3])};
+      }
+      return;
+    }
 #pragma unroll
     for (int r = 0; r < kFusedKPerThread; ++r) {
       const int e = r * kFusedThreads + (int)threadIdx.x;
-      if (e < n) kbuf[e] = v[r];
+      if (e < n) kbuf[e] = to_f32(v[r]);
     }
   }
 };

@@ -371,6 +371,7 @@ bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, in
   fc->width_out = (int)(f[0].a * f[0].b * f[0].d);
   fc->inplace = inplace ? 1 : 0;
   fc->buf_rows = (int)wmax;
+  fc->kvec = 0;  // set at launch (chain_fused_kvec)
   for (int q = 0; q < n; ++q) {
     fc->a[q] = (int)f[q].a; fc->b[q] = (int)f[q].b; fc->c[q] = (int)f[q].c; fc->d[q] = (int)f[q].d;
     div_magic((uint32_t)f[q].d, &fc->md[q], &fc->sd[q]);
@@ -421,6 +422,17 @@ bool chain_fused_vec(const FusedChain& fc, int dtype, const void* X, const void*
   return fc.width_in % e == 0 && fc.width_out % e == 0;
 }
 
+// Runs of 4 factor values per load: every pass's per-factor count is a
+// multiple of 4 and every factor's values are aligned to 4 elements.
+bool chain_fused_kvec(const FusedChain& fc, int dtype) {
+  const uintptr_t al = 4 * (uintptr_t)elem_size(dtype);
+  for (int q = 0; q < fc.nf; ++q)
+    if (reinterpret_cast<uintptr_t>(fc.kv[q]) % al) return false;
+  for (int q = 0; q < fc.npass; ++q)
+    if (fc.pcnt[q] % 4) return false;
+  return true;
+}
+
 ks_status_t chain_impl(const ks_factor_t* factors, int nfactors, const void* X, void* Y, int64_t batch, int layout,
                        int dtype, void* workspace, size_t workspace_bytes, void* stream) {
   size_t per = 0;
@@ -449,6 +461,7 @@ ks_status_t chain_impl(const ks_factor_t* factors, int nfactors, const void* X, 
   if (fused) {
     fc.x = X;
     fc.y = Y;
+    fc.kvec = chain_fused_kvec(fc, dtype) ? 1 : 0;
     const hipError_t e = launch_chain_fused(fc, dtype, chain_fused_vec(fc, dtype, X, Y), static_cast<hipStream_t>(stream));
     if (e != hipSuccess) {
       g_last_hip_error = (int)e;
