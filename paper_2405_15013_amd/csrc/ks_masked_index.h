@@ -29,7 +29,7 @@ struct MaskedTile {
   int nbt;       // batch tiles (16*V entries in BSL, 16 rows in BSF)
   int items;     // nbt * a * jgroups * kgroups
   int nchunks;   // ceil(c / CH), CH = 4 * LP values of l per chunk
-  int kvec;      // K read as 16-byte operands (c a multiple of CH, K_values 16-byte aligned)
+  int kvec;      // K read as LP-element operands (c a multiple of LP, K_values aligned to them)
 };
 
 struct MItem {
@@ -47,9 +47,12 @@ KS_MHD MaskedTile masked_tile(const Problem& p, int V) {
   const int span = p.layout == BSL ? 16 * V : 16;
   t.nbt = (p.batch + span - 1) / span;
   t.items = t.nbt * p.a * t.jgroups * t.kgroups;
-  const int ch = 4 * masked_lp(p.dtype == F32 ? 4 : 2);
+  const int lp = masked_lp(p.dtype == F32 ? 4 : 2), ch = 4 * lp;
   t.nchunks = (p.c + ch - 1) / ch;
-  t.kvec = (p.c % ch == 0 && (reinterpret_cast<uintptr_t>(p.kv) & 15) == 0) ? 1 : 0;
+  // A lane's LP values of l (from a multiple of LP) are one vector of its K
+  // row when c is a multiple of LP: wholly inside the row or wholly padding.
+  const int esize = p.dtype == F32 ? 4 : (p.dtype == FP8 ? 1 : 2);
+  t.kvec = (p.c % lp == 0 && (reinterpret_cast<uintptr_t>(p.kv) % (uintptr_t)(lp * esize)) == 0) ? 1 : 0;
   return t;
 }
 
