@@ -35,6 +35,26 @@ __device__ __forceinline__ void fp8_load(const uint8_t* p, uint8_t (&v)[N]) {
   }
 }
 
+// 4 x 4 transpose of 16-byte pieces across the four 16-lane rows of a
+// wavefront: on entry register r of lane row g holds piece M[g][r], on exit
+// it holds M[r][g] (for each lane column n).  Two v_permlane16_swap (rows 1
+// and 3 of the first operand exchanged with rows 0 and 2 of the second), then
+// two v_permlane32_swap (rows 2-3 of the first with rows 0-1 of the second),
+// per dword.
+__device__ __forceinline__ void fp8_rows_transpose(u32x4 (&m)[4]) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    auto s01 = __builtin_amdgcn_permlane16_swap(m[0][w], m[1][w], false, false);
+    auto s23 = __builtin_amdgcn_permlane16_swap(m[2][w], m[3][w], false, false);
+    auto s02 = __builtin_amdgcn_permlane32_swap(s01[0], s23[0], false, false);
+    auto s13 = __builtin_amdgcn_permlane32_swap(s01[1], s23[1], false, false);
+    m[0][w] = s02[0];
+    m[1][w] = s13[0];
+    m[2][w] = s02[1];
+    m[3][w] = s13[1];
+  }
+}
+
 template <int LAYOUT, int V>
 __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
   constexpr int LP = 8;       // values of l per lane and MFMA
@@ -45,6 +65,9 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
   if (item >= t.items) return;  // wave-uniform
   const int n = lane & 15, g = lane >> 4;
   const MItem it = masked_item(p, t, V, item);
+  // Batch-size-first with d = 8 (= V), c a multiple of 8 and 16-byte aligned
+  // buffers: X and Y move as whole 64-byte row runs (fp8_rows_transpose).
+  const bool rows8 = LAYOUT == BSF && V == 8 && p.d == 8 && p.c % 8 == 0 && p.align >= 16;
   const uint8_t* __restrict__ x = static_cast<const uint8_t*>(p.x);
   const uint8_t* __restrict__ kv = static_cast<const uint8_t*>(p.kv);
 
@@ -56,14 +79,33 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
     const int l0 = ch * CH + LP * g;
     uint8_t xs[LP][V];
     uint8_t ks[VK][LP];
+    if (rows8) {
+      // Rows of d = 8: a lane's operand (8 values of l x 8 j) is the 64-byte
+      // run of its batch row from l0*8.  Load x of the wavefront reads, for
+      // lane row g, piece g of lane row x's run (four lanes cover one run),
+      // then the pieces move to their lanes.
+      u32x4 m[4];
+      const bool col = masked_col_valid(p, it, V, n);
 #pragma unroll
-    for (int q = 0; q < LP; ++q) {
-      const int64_t off = masked_x_off(p, it, V, l0 + q, n);
-      if (off >= 0) {
-        fp8_load<V>(x + off, xs[q]);
-      } else {
+      for (int xr = 0; xr < 4; ++xr) {
+        const int lx = ch * CH + LP * xr;
+        m[xr] = u32x4{0, 0, 0, 0};
+        if (col && lx < p.c)
+          m[xr] = *reinterpret_cast<const u32x4*>(x + (int64_t)(it.beta0 + n) * p.N +
+                                                  ((int64_t)it.i * p.c + lx) * 8 + 16 * g);
+      }
+      fp8_rows_transpose(m);
+      __builtin_memcpy(xs, m, 64);
+    } else {
 #pragma unroll
-        for (int e = 0; e < V; ++e) xs[q][e] = 0;
+      for (int q = 0; q < LP; ++q) {
+        const int64_t off = masked_x_off(p, it, V, l0 + q, n);
+        if (off >= 0) {
+          fp8_load<V>(x + off, xs[q]);
+        } else {
+#pragma unroll
+          for (int e = 0; e < V; ++e) xs[q][e] = 0;
+        }
       }
     }
 #pragma unroll
@@ -127,6 +169,28 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
     for (int r = 0; r < 4; ++r)
 #pragma unroll
       for (int e = 0; e < V; ++e) acc[e][r] = gelu_f32(acc[e][r]);
+  }
+  if (rows8) {
+    // Lane row g's outputs k = k0 + 4g + r (r = 0..3, 8 j each) are one
+    // 64-byte run of its batch row; after the transpose, store x writes piece
+    // g of lane row x's run, so four lanes write 64 contiguous bytes.
+    u32x4 m[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      uint16_t v[8];
+#pragma unroll
+      for (int e = 0; e < 8; ++e) v[e] = from_f32<bf16_t>(acc[e][r]);
+      __builtin_memcpy(&m[r], v, 16);
+    }
+    fp8_rows_transpose(m);
+    if (!masked_col_valid(p, it, V, n)) return;
+    bf16_t* yrow = static_cast<bf16_t*>(p.y) + (int64_t)(it.beta0 + n) * p.M + (int64_t)it.i * p.b * 8;
+#pragma unroll
+    for (int xr = 0; xr < 4; ++xr) {
+      const int k = it.k0 + 4 * xr + g;
+      if (k < p.b) *reinterpret_cast<u32x4*>(yrow + (int64_t)k * 8) = m[xr];
+    }
+    return;
   }
   // outputs k = k0 + 4g + r in bfloat16
 #pragma unroll

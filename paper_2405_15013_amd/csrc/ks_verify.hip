@@ -180,15 +180,39 @@ bool verify_masked_v(Checker& ck, int V) {
   if (p.layout == BSL && p.batch % V) return ck.fail("batch not a multiple of the access width", V);
   if (p.layout == BSF && p.d % V) return ck.fail("d not a multiple of the access width", V);
   const int VK = p.layout == BSL ? 1 : V;
+  // FP8 batch-size-first rows of d = 8: X and Y move as 64-byte row runs,
+  // lane row g taking piece g of lane row x's run (x = 0..3).
+  const bool rows8 = fp8 && p.layout == BSF && V == 8 && p.d == 8 && p.c % 8 == 0 && p.align >= 16;
   for (int item = 0; item < t.items && ck.err.empty(); ++item) {
     const MItem it = masked_item(p, t, V, item);
     if (it.i < 0 || it.i >= p.a) return ck.fail("item i out of range", item);
     for (int lane = 0; lane < 64; ++lane) {
       const int n = lane & 15, g = lane >> 4;
+      if (rows8 && masked_col_valid(p, it, V, n)) {
+        for (int ch = 0; ch < t.nchunks; ++ch)
+          for (int x = 0; x < 4; ++x) {
+            const int lx = ch * CH + LP * x;
+            if (lx >= p.c) continue;
+            const int64_t off = (int64_t)(it.beta0 + n) * p.N + ((int64_t)it.i * p.c + lx) * 8 + 16 * g;
+            if (off % 16) return ck.fail("row-run X piece not 16-byte aligned", off);
+            ck.read_x(off, 16);
+            for (int h = 0; h < 2; ++h)
+              if (masked_x_off(p, it, V, lx + 2 * g + h, n) != off + 8 * h)
+                return ck.fail("row-run X piece is not the values of its lane row", off);
+          }
+        for (int x = 0; x < 4; ++x) {
+          const int k = it.k0 + 4 * x + g;
+          if (k >= p.b) continue;
+          const int64_t off = (int64_t)(it.beta0 + n) * p.M + ((int64_t)it.i * p.b + k) * 8;
+          if (off != masked_y_off(p, it, V, n, x, g)) return ck.fail("row-run Y piece is not its output", off);
+          if ((off * 2) % 16) return ck.fail("row-run Y piece not 16-byte aligned", off);
+          ck.write_y(off, 8);
+        }
+      }
       for (int ch = 0; ch < t.nchunks; ++ch)
         for (int q = 0; q < LP; ++q) {
           const int l = ch * CH + LP * g + q;
-          const int64_t off = masked_x_off(p, it, V, l, n);
+          const int64_t off = rows8 ? -1 : masked_x_off(p, it, V, l, n);
           if (off >= 0) {
             if (xvec && (off * xs) % xvec) return ck.fail("X vector not aligned to its size", off);
             ck.read_x(off, V);
@@ -203,7 +227,7 @@ bool verify_masked_v(Checker& ck, int V) {
               (void)di;
               if (off + e != want) return ck.fail("masked operand element is not the X value needed", off + e);
             }
-          } else if (l < p.c && masked_col_valid(p, it, V, n)) {
+          } else if (!rows8 && l < p.c && masked_col_valid(p, it, V, n)) {
             return ck.fail("needed X piece treated as padding", l);
           }
           if (t.kvec && q == 0)
@@ -225,7 +249,7 @@ bool verify_masked_v(Checker& ck, int V) {
             }
           }
         }
-      for (int r = 0; r < 4; ++r) {
+      for (int r = 0; r < 4 && !rows8; ++r) {
         const int64_t off = masked_y_off(p, it, V, n, g, r);
         if (off < 0) continue;
         if (yvec && (off * ys) % yvec) return ck.fail("Y vector not aligned to its size", off);
