@@ -167,6 +167,115 @@ def copy_calibration(nbytes=64 << 20, pairs=8, reps=20):
     print(json.dumps({"copy_calibration_bytes": nbytes, "dispatches": reps}), flush=True)
 
 
+COPY_FLOOR_MB = (0.5, 1, 2, 4, 8, 16, 32, 64, 128, 256)
+
+
+def copy_floor(run):
+    """Time a plain device copy (torch copy_, read n bytes and write n bytes)
+    with the sweep's own protocol (buffer rotation >= 768 MB, HIP graphs, time
+    per call): the fraction of the HBM roof that moving the same bytes reaches
+    under that protocol, per size (the per-launch cost included)."""
+    import torch
+    xs = run.pool_x.view(torch.float32)
+    ys = run.pool_y.view(torch.float32)
+    rows = []
+    for mb in COPY_FLOOR_MB:
+        n = (int(mb * 2**20) // 2 // 4 + 63) // 64 * 64  # elements per side: mb MB moved in total
+        nb = n * 4
+        sets = max(1, min(xs.numel(), ys.numel()) // n)
+
+        def launch(r, h, n=n):
+            ys[r * n:(r + 1) * n].copy_(xs[r * n:(r + 1) * n])
+
+        t, _ = run.time_calls(2 * nb, sets, launch)
+        rows.append({"bytes": 2 * nb, "us": t * 1e6, "frac": 2 * nb / HBM_BW / t})
+    return rows
+
+
+def copy_floor_frac(rows, nbytes):
+    """The copy floor's fraction at `nbytes` moved (log-linear in bytes between
+    the measured sizes, the largest size's rate beyond them)."""
+    pts = sorted((r["bytes"], r["us"]) for r in rows)
+    if nbytes >= pts[-1][0]:
+        us = pts[-1][1] * nbytes / pts[-1][0]
+    elif nbytes <= pts[0][0]:
+        us = pts[0][1]
+    else:
+        for (b0, u0), (b1, u1) in zip(pts, pts[1:]):
+            if b0 <= nbytes <= b1:
+                w = math.log(nbytes / b0) / math.log(b1 / b0)
+                us = u0 + w * (u1 - u0)
+                break
+    return nbytes / HBM_BW / (us * 1e-6)
+
+
+def points_summary(points_jsonl, out_md, command_lines, floor_json=None, lowest=50):
+    """Per-class tables of a bench run's per-point records: for every (dtype,
+    layout, batch) a b x c matrix of the median fraction of roofline over the
+    sweep patterns with that (b, c), the class median beside the copy floor's
+    (same bytes, same protocol; when `floor_json` holds a --copy-floor run),
+    and the `lowest` points with the smallest fraction."""
+    import statistics
+    pts = [json.loads(l) for l in open(points_jsonl) if l.strip()]
+    sweep = set(sweep_patterns())
+    pts = [p for p in pts if p.get("epilogue") is None and p["dtype"] in ("f32", "bf16")
+           and p["batch"] in (4096, 25088) and "frac" in p and tuple(p["pattern"]) in sweep]
+    seen, uniq = set(), []
+    for p in pts:  # one record per sweep point (the families repeat some)
+        key = (tuple(p["pattern"]), p["batch"], p["dtype"], p["layout"])
+        if key not in seen:
+            seen.add(key)
+            uniq.append(p)
+    pts = uniq
+    floor = json.load(open(floor_json))["copy_floor"] if floor_json else None
+    bs = sorted({p["pattern"][1] for p in pts})
+    cs = sorted({p["pattern"][2] for p in pts})
+    lines = ["# Sweep points by class: median fraction of roofline", "",
+             "Command (from the repository root):", "", "```"] + command_lines + ["```", "",
+             "%d sweep points.  Fraction = roof time / time per call (graph replay over a >= 768 MB "
+             "rotation, the number that feeds the bench's value)." % len(pts), ""]
+    if floor:
+        lines += ["Copy floor (plain device copy of the same number of bytes, same protocol): "
+                  + ", ".join("%.3g MB %.3f" % (r["bytes"] / 1e6, r["frac"]) for r in floor) + ".", ""]
+    lines += ["| class | points | median fraction | median copy-floor fraction | median GB/s |",
+              "|---|---:|---:|---:|---:|"]
+    classes = [(dt, lay, bt) for dt in ("f32", "bf16") for lay in ("bsf", "bsl") for bt in (4096, 25088)]
+    for dt, lay, bt in classes:
+        c = [p for p in pts if (p["dtype"], p["layout"], p["batch"]) == (dt, lay, bt)]
+        if not c:
+            continue
+        cf = statistics.median(copy_floor_frac(floor, p["bytes"]) for p in c) if floor else float("nan")
+        lines.append("| %s %s B=%d | %d | %.3f | %.3f | %.0f |" % (
+            dt, lay.upper(), bt, len(c), statistics.median(p["frac"] for p in c), cf,
+            statistics.median(p["gbps"] for p in c)))
+    lines.append("")
+    for dt, lay, bt in classes:
+        c = [p for p in pts if (p["dtype"], p["layout"], p["batch"]) == (dt, lay, bt)]
+        if not c:
+            continue
+        lines += ["%s %s B=%d: median fraction by b (rows) and c (columns)" % (dt, lay.upper(), bt), "",
+                  "| b \\ c | " + " | ".join(str(x) for x in cs) + " |", "|---" * (len(cs) + 1) + "|"]
+        for b in bs:
+            cells = []
+            for cc in cs:
+                v = [p["frac"] for p in c if p["pattern"][1] == b and p["pattern"][2] == cc]
+                cells.append("%.2f" % statistics.median(v) if v else "")
+            lines.append("| %d | " % b + " | ".join(cells) + " |")
+        lines.append("")
+    low = sorted(pts, key=lambda p: p["frac"])[:lowest]
+    lines += ["The %d points with the smallest fraction:" % lowest, "",
+              "| pattern (a,b,c,d) | B | dtype | layout | us | GB/s | fraction | bound | kernel |",
+              "|---|---:|---|---|---:|---:|---:|---|---|"]
+    for p in low:
+        lines.append("| %s | %d | %s | %s | %.2f | %.0f | %.3f | %s | `%s` |" % (
+            tuple(p["pattern"]), p["batch"], p["dtype"], p["layout"].upper(), p["us"], p["gbps"], p["frac"],
+            p["bound"], p["kernel"]))
+    lines.append("")
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
+
+
 def trace_summary(stats_csv, bench_json, out_md, command_lines, top=25):
     """Write the kernel-trace summary (rocprofv3 --kernel-trace --stats) of a
     bench run, with the dominant kernel's profiler average beside the
@@ -536,6 +645,12 @@ def main():
                     help="summarise counter passes in DIR into OUT_MD (no GPU)")
     ap.add_argument("--trace-summary", nargs=3, metavar=("STATS_CSV", "BENCH_JSON", "OUT_MD"),
                     help="summarise a rocprofv3 kernel_stats.csv of a bench run into OUT_MD (no GPU)")
+    ap.add_argument("--copy-floor", default=None, metavar="OUT_JSON",
+                    help="only time a plain device copy at 0.5-256 MB with the sweep's protocol, into OUT_JSON")
+    ap.add_argument("--points-summary", nargs=2, metavar=("POINTS_JSONL", "OUT_MD"),
+                    help="summarise a --points-out file by class into OUT_MD (no GPU)")
+    ap.add_argument("--copy-floor-in", default=None, metavar="FLOOR_JSON",
+                    help="a --copy-floor result for --points-summary")
     ap.add_argument("--pmc-command", action="append", default=[],
                     help="command line recorded in the --pmc-summary / --trace-summary output (repeatable)")
     args = ap.parse_args()
@@ -544,6 +659,9 @@ def main():
         return
     if args.trace_summary:
         trace_summary(*args.trace_summary, args.pmc_command)
+        return
+    if args.points_summary:
+        points_summary(args.points_summary[0], args.points_summary[1], args.pmc_command, args.copy_floor_in)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the KS matmul path shards over the batch with no "
@@ -554,6 +672,12 @@ def main():
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     if args.copy_calibration:
         copy_calibration()
+        return
+    if args.copy_floor:
+        rows = copy_floor(Runner(args.steps, args.warmup, per_launch=False))
+        with open(args.copy_floor, "w") as fh:
+            json.dump({"copy_floor": rows}, fh)
+        print(json.dumps({"copy_floor": rows}), flush=True)
         return
     t_start = time.time()
     run = Runner(args.steps, args.warmup, eager=args.eager)

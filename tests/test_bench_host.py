@@ -118,3 +118,34 @@ def test_plan_kernel_names_are_library_symbols():
     missing = sorted(n for n in seen if n not in syms)
     assert not missing, missing[:5]
     assert any(n.startswith("ks_dma_kernel<") for n in seen) and any(n.startswith("ks_direct_c_kernel<") for n in seen)
+
+
+def test_copy_floor_frac_interpolates_in_log_bytes():
+    rows = [{"bytes": 1 << 20, "us": 2.0}, {"bytes": 4 << 20, "us": 4.0}]
+    # at the measured sizes: bytes / 8 TB/s / time
+    assert abs(bench.copy_floor_frac(rows, 1 << 20) - (1 << 20) / 8e12 / 2e-6) < 1e-12
+    # halfway in log(bytes) between 1 and 4 MiB: time halfway, 3 us
+    assert abs(bench.copy_floor_frac(rows, 2 << 20) - (2 << 20) / 8e12 / 3e-6) < 1e-12
+    # beyond the largest size: the largest size's rate
+    assert abs(bench.copy_floor_frac(rows, 8 << 20) - bench.copy_floor_frac(rows, 4 << 20)) < 1e-12
+
+
+def test_points_summary_tables(tmp_path):
+    pats = bench.sweep_patterns()
+    recs = []
+    for i, p in enumerate(pats[:40]):
+        for dtype in ("f32", "bf16"):
+            recs.append({"pattern": list(p), "batch": 4096, "dtype": dtype, "layout": "bsl", "us": 5.0,
+                         "epilogue": None, "gbps": 1000.0 + i, "frac": 0.01 * (i + 1), "bound": "hbm",
+                         "bytes": 1 << 20, "kernel": "k%d" % i})
+    recs.append(dict(recs[0], pattern=[2, 2, 2, 512]))  # a family point: not a sweep pattern
+    pts = tmp_path / "points.jsonl"
+    pts.write_text("\n".join(json.dumps(r) for r in recs) + "\n")
+    floor = tmp_path / "floor.json"
+    floor.write_text(json.dumps({"copy_floor": [{"bytes": 1 << 20, "us": 2.0, "frac": 0.06}]}))
+    out = tmp_path / "summary.md"
+    bench.points_summary(str(pts), str(out), ["cmd"], str(floor), lowest=5)
+    text = out.read_text()
+    assert "| f32 BSL B=4096 | 40 |" in text and "| bf16 BSL B=4096 | 40 |" in text
+    assert "(2, 2, 2, 512)" not in text
+    assert text.count("`k0`") == 2 and "0.010" in text  # the lowest point of each dtype listed
