@@ -65,9 +65,13 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
   if (item >= t.items) return;  // wave-uniform
   const int n = lane & 15, g = lane >> 4;
   const MItem it = masked_item(p, t, V, item);
-  // Batch-size-first with d = 8 (= V), c a multiple of 8 and 16-byte aligned
-  // buffers: X and Y move as whole 64-byte row runs (fp8_rows_transpose).
-  const bool rows8 = LAYOUT == BSF && V == 8 && p.d == 8 && p.c % 8 == 0 && p.align >= 16;
+  // Batch-size-first with V = d, c a multiple of 8 and 16-byte aligned
+  // buffers: a lane's X operand (8 values of l x d j) is one run of 8d bytes
+  // of its batch row, and (b a multiple of 4) its outputs k0 + 4g .. + 3 one
+  // run of 4d bf16.  d = 8: 64-byte runs, four lanes per run
+  // (fp8_rows_transpose); d = 1, 2, 4: each lane moves its own run.
+  const bool runs = LAYOUT == BSF && V == p.d && p.c % 8 == 0 && p.align >= 16;
+  const bool rows8 = runs && V == 8;
   const uint8_t* __restrict__ x = static_cast<const uint8_t*>(p.x);
   const uint8_t* __restrict__ kv = static_cast<const uint8_t*>(p.kv);
 
@@ -95,7 +99,22 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
                                                   ((int64_t)it.i * p.c + lx) * 8 + 16 * g);
       }
       fp8_rows_transpose(m);
-      __builtin_memcpy(xs, m, 64);
+      if constexpr (V == 8) __builtin_memcpy(xs, m, 64);
+    } else if (V <= 4 && runs) {
+      if constexpr (V <= 4) {
+        // the run of values l0 .. l0 + 7 (8V bytes: 8, 16 or two 16-byte loads)
+        constexpr int NB = LP * V < 16 ? LP * V : 16;
+        const int64_t off = masked_x_off(p, it, V, l0, n);
+        if (off >= 0) {
+          fp8_load<NB>(x + off, reinterpret_cast<uint8_t(&)[NB]>(xs[0][0]));
+          if constexpr (LP * V == 32) fp8_load<16>(x + off + 16, reinterpret_cast<uint8_t(&)[16]>(xs[LP / 2][0]));
+        } else {
+#pragma unroll
+          for (int q = 0; q < LP; ++q)
+#pragma unroll
+            for (int e = 0; e < V; ++e) xs[q][e] = 0;
+        }
+      }
     } else {
 #pragma unroll
       for (int q = 0; q < LP; ++q) {
@@ -179,7 +198,7 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
     for (int r = 0; r < 4; ++r) {
       uint16_t v[8];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = from_f32<bf16_t>(acc[e][r]);
+      for (int e = 0; e < 8; ++e) v[e] = from_f32<bf16_t>(acc[e < V ? e : 0][r]);  // V == 8 here
       __builtin_memcpy(&m[r], v, 16);
     }
     fp8_rows_transpose(m);
@@ -189,6 +208,30 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
     for (int xr = 0; xr < 4; ++xr) {
       const int k = it.k0 + 4 * xr + g;
       if (k < p.b) *reinterpret_cast<u32x4*>(yrow + (int64_t)k * 8) = m[xr];
+    }
+    return;
+  }
+  if (V <= 4 && runs && p.b % 4 == 0) {
+    // outputs k0 + 4g .. k0 + 4g + 3 (all j): one run of 4V bf16
+    const int64_t off = masked_y_off(p, it, V, n, g, 0);
+    if (off < 0) return;
+    uint16_t v[4 * V];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int e = 0; e < V; ++e) v[r * V + e] = from_f32<bf16_t>(acc[e][r]);
+    bf16_t* yo = static_cast<bf16_t*>(p.y) + off;
+    if constexpr (V == 1) {
+      u32x2 w;
+      __builtin_memcpy(&w, v, 8);
+      *reinterpret_cast<u32x2*>(yo) = w;
+    } else if constexpr (V <= 4) {
+#pragma unroll
+      for (int h = 0; h < 4 * V / 8; ++h) {
+        u32x4 w;
+        __builtin_memcpy(&w, v + 8 * h, 16);
+        *reinterpret_cast<u32x4*>(yo + 8 * h) = w;
+      }
     }
     return;
   }

@@ -180,9 +180,13 @@ bool verify_masked_v(Checker& ck, int V) {
   if (p.layout == BSL && p.batch % V) return ck.fail("batch not a multiple of the access width", V);
   if (p.layout == BSF && p.d % V) return ck.fail("d not a multiple of the access width", V);
   const int VK = p.layout == BSL ? 1 : V;
-  // FP8 batch-size-first rows of d = 8: X and Y move as 64-byte row runs,
-  // lane row g taking piece g of lane row x's run (x = 0..3).
-  const bool rows8 = fp8 && p.layout == BSF && V == 8 && p.d == 8 && p.c % 8 == 0 && p.align >= 16;
+  // FP8 batch-size-first with V = d: a lane's X operand is one run of 8V
+  // bytes from value l0 and (b a multiple of 4) its outputs one run of 4V
+  // bf16; for d = 8 the runs are 64 bytes and lane row g takes piece g of
+  // lane row x's run (x = 0..3).
+  const bool runs = fp8 && p.layout == BSF && V == p.d && p.c % 8 == 0 && p.align >= 16;
+  const bool rows8 = runs && V == 8;
+  const bool yruns = runs && V <= 4 && p.b % 4 == 0;
   for (int item = 0; item < t.items && ck.err.empty(); ++item) {
     const MItem it = masked_item(p, t, V, item);
     if (it.i < 0 || it.i >= p.a) return ck.fail("item i out of range", item);
@@ -209,10 +213,33 @@ bool verify_masked_v(Checker& ck, int V) {
           ck.write_y(off, 8);
         }
       }
+      if (runs && !rows8 && masked_col_valid(p, it, V, n))
+        for (int ch = 0; ch < t.nchunks; ++ch) {
+          const int l0 = ch * CH + LP * g;
+          const int64_t off = masked_x_off(p, it, V, l0, n);
+          if (l0 >= p.c) continue;
+          if (off < 0) return ck.fail("X run treated as padding", l0);
+          const int nb = LP * V < 16 ? LP * V : 16;
+          for (int h = 0; h < LP * V / nb; ++h)
+            if ((off + h * nb) % nb) return ck.fail("X run piece not aligned to its size", off + h * nb);
+          ck.read_x(off, LP * V);
+          for (int q = 0; q < LP; ++q)
+            if (masked_x_off(p, it, V, l0 + q, n) != off + q * V) return ck.fail("X run is not the values of the lane", l0 + q);
+        }
+      if (yruns && masked_col_valid(p, it, V, n)) {
+        const int64_t off = masked_y_off(p, it, V, n, g, 0);
+        if (off >= 0) {
+          const int nb = V == 1 ? 8 : 16;  // bytes per store
+          if ((off * 2) % nb) return ck.fail("Y run not aligned to its stores", off);
+          for (int r = 0; r < 4; ++r)
+            if (masked_y_off(p, it, V, n, g, r) != off + r * V) return ck.fail("Y run is not the lane's outputs", off);
+          ck.write_y(off, 4 * V);
+        }
+      }
       for (int ch = 0; ch < t.nchunks; ++ch)
         for (int q = 0; q < LP; ++q) {
           const int l = ch * CH + LP * g + q;
-          const int64_t off = rows8 ? -1 : masked_x_off(p, it, V, l, n);
+          const int64_t off = runs ? -1 : masked_x_off(p, it, V, l, n);
           if (off >= 0) {
             if (xvec && (off * xs) % xvec) return ck.fail("X vector not aligned to its size", off);
             ck.read_x(off, V);
@@ -227,7 +254,7 @@ bool verify_masked_v(Checker& ck, int V) {
               (void)di;
               if (off + e != want) return ck.fail("masked operand element is not the X value needed", off + e);
             }
-          } else if (!rows8 && l < p.c && masked_col_valid(p, it, V, n)) {
+          } else if (!runs && l < p.c && masked_col_valid(p, it, V, n)) {
             return ck.fail("needed X piece treated as padding", l);
           }
           if (t.kvec && q == 0)
@@ -249,7 +276,7 @@ bool verify_masked_v(Checker& ck, int V) {
             }
           }
         }
-      for (int r = 0; r < 4 && !rows8; ++r) {
+      for (int r = 0; r < 4 && !rows8 && !yruns; ++r) {
         const int64_t off = masked_y_off(p, it, V, n, g, r);
         if (off < 0) continue;
         if (yvec && (off * ys) % yvec) return ck.fail("Y vector not aligned to its size", off);

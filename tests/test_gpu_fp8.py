@@ -38,7 +38,8 @@ def run_fp8(pattern, batch, layout, cfg=51, bias=False, act=None, x_offset=0, y_
 
 SHAPES = [(1, 64, 64, 1), (6, 64, 16, 8), (6, 16, 64, 8), (1, 32, 32, 32), (32, 32, 32, 1), (2, 128, 128, 4),
           (8, 16, 96, 2), (4, 48, 32, 16), (1, 24, 24, 8), (1, 17, 33, 3),
-          (2, 17, 24, 8), (3, 48, 8, 8)]  # d = 8 row runs with padded k rows / c = 8
+          (2, 17, 24, 8), (3, 48, 8, 8),  # d = 8 row runs with padded k rows / c = 8
+          (2, 20, 8, 4), (3, 18, 16, 2)]  # per-lane runs: padded k rows (b = 20), b not a multiple of 4
 
 
 @pytest.mark.parametrize("pattern", SHAPES)
