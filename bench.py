@@ -96,17 +96,60 @@ def plan_field(desc, key):
     return dict(kv.split("=", 1) for kv in desc.split())[key]
 
 
-def kernel_sources_sha1():
+# Translation units that build each kernel family (csrc/ file name prefix of
+# the .hip files; the .cpp files that plan its launches, which decide the
+# tiles and which calls run it, count too, as does ks_host.cpp).
+KERNEL_FAMILY_SOURCES = {
+    "ks_dma_kernel": "ks_dma_", "ks_direct_c_kernel": "ks_direct_", "ks_direct_kernel": "ks_direct_",
+    "ks_staged_kernel": "ks_staged_", "ks_masked_kernel": "ks_masked_", "ks_fp8_kernel": "ks_fp8",
+    "ks_valu_bsl_kernel": "ks_valu", "ks_valu_bsf_kernel": "ks_valu", "ks_generic_kernel": "ks_generic",
+    "ks_chain_fused_kernel": "ks_chain_fused",
+}
+KERNEL_FAMILY_PLANNERS = {"ks_dma_": "ks_staged_plan.cpp", "ks_staged_": "ks_staged_plan.cpp",
+                          "ks_direct_": "ks_direct_plan.cpp", "ks_masked_": "ks_direct_plan.cpp"}
+
+
+def _include_closure(paths):
+    """The files and every header they include with #include "..." (resolved
+    in csrc/ or include/), transitively."""
+    import re
+    dirs = [os.path.join(ROOT, "paper_2405_15013_amd", "csrc"), os.path.join(ROOT, "include")]
+    seen, todo = set(), list(paths)
+    while todo:
+        p = todo.pop()
+        if p in seen:
+            continue
+        seen.add(p)
+        with open(p) as fh:
+            for m in re.finditer(r'^#include "([^"]+)"', fh.read(), re.M):
+                for d in dirs:
+                    q = os.path.normpath(os.path.join(d, m.group(1)))
+                    if os.path.exists(q):
+                        todo.append(q)
+                        break
+    return sorted(seen)
+
+
+def kernel_sources_sha1(kernel=None):
     """Hash of the sources the kernels are built from (and their build
     script): a traffic record taken from profiler counters is used only while
-    this hash is unchanged."""
+    this hash is unchanged.  With `kernel` (an instance name), only that
+    kernel family's translation units and the headers they include."""
     import hashlib
     h = hashlib.sha1()
     csrc = os.path.join(ROOT, "paper_2405_15013_amd", "csrc")
-    names = sorted(f for f in os.listdir(csrc) if f.endswith((".h", ".hip", ".cpp")) and f != "ks_verify.hip")
-    for f in names + ["../build.py"]:
-        with open(os.path.join(csrc, f), "rb") as fh:
-            h.update(f.encode() + b"\0" + fh.read())
+    if kernel is None:
+        files = [os.path.join(csrc, f) for f in sorted(os.listdir(csrc))
+                 if f.endswith((".h", ".hip", ".cpp")) and f != "ks_verify.hip"]
+    else:
+        prefix = KERNEL_FAMILY_SOURCES[kernel.split("<")[0]]
+        files = _include_closure([os.path.join(csrc, f) for f in sorted(os.listdir(csrc))
+                                  if f.startswith(prefix) and f.endswith(".hip")])
+        files += [os.path.join(csrc, f) for f in sorted({KERNEL_FAMILY_PLANNERS.get(prefix, "ks_host.cpp"),
+                                                          "ks_host.cpp"})]
+    for p in files + [os.path.join(csrc, "..", "build.py")]:
+        with open(p, "rb") as fh:
+            h.update(os.path.basename(p).encode() + b"\0" + fh.read())
     return h.hexdigest()
 
 
@@ -120,7 +163,10 @@ def traffic_record(kernel, sample_every):
     pdir = os.path.join(ROOT, "profiles")
     if not os.path.isdir(pdir):
         return None
-    sha = kernel_sources_sha1()
+    try:
+        sha = kernel_sources_sha1(kernel)
+    except KeyError:
+        return None
     for f in sorted(os.listdir(pdir)):
         if not f.endswith(".md"):
             continue
@@ -237,17 +283,24 @@ def points_summary(points_jsonl, out_md, command_lines, floor_json=None, lowest=
     if floor:
         lines += ["Copy floor (plain device copy of the same number of bytes, same protocol): "
                   + ", ".join("%.3g MB %.3f" % (r["bytes"] / 1e6, r["frac"]) for r in floor) + ".", ""]
-    lines += ["| class | points | median fraction | median copy-floor fraction | median GB/s |",
-              "|---|---:|---:|---:|---:|"]
+    lines += ["| class | points | median fraction | median copy-floor fraction | median fraction / copy floor | median GB/s |",
+              "|---|---:|---:|---:|---:|---:|"]
     classes = [(dt, lay, bt) for dt in ("f32", "bf16") for lay in ("bsf", "bsl") for bt in (4096, 25088)]
     for dt, lay, bt in classes:
         c = [p for p in pts if (p["dtype"], p["layout"], p["batch"]) == (dt, lay, bt)]
         if not c:
             continue
         cf = statistics.median(copy_floor_frac(floor, p["bytes"]) for p in c) if floor else float("nan")
-        lines.append("| %s %s B=%d | %d | %.3f | %.3f | %.0f |" % (
-            dt, lay.upper(), bt, len(c), statistics.median(p["frac"] for p in c), cf,
+        rel = statistics.median(p["frac"] / copy_floor_frac(floor, p["bytes"]) for p in c) if floor else float("nan")
+        lines.append("| %s %s B=%d | %d | %.3f | %.3f | %.2f | %.0f |" % (
+            dt, lay.upper(), bt, len(c), statistics.median(p["frac"] for p in c), cf, rel,
             statistics.median(p["gbps"] for p in c)))
+    if floor:
+        lines.append("| all | %d | %.3f | %.3f | %.2f | %.0f |" % (
+            len(pts), statistics.median(p["frac"] for p in pts),
+            statistics.median(copy_floor_frac(floor, p["bytes"]) for p in pts),
+            statistics.median(p["frac"] / copy_floor_frac(floor, p["bytes"]) for p in pts),
+            statistics.median(p["gbps"] for p in pts)))
     lines.append("")
     for dt, lay, bt in classes:
         c = [p for p in pts if (p["dtype"], p["layout"], p["batch"]) == (dt, lay, bt)]
@@ -306,7 +359,7 @@ def trace_summary(stats_csv, bench_json, out_md, command_lines, top=25):
                          bench["roofline"]["avg_launch_us"], float(r["AverageNs"]) / 1e3, r["Calls"]))
     lines += ["", "| Kernel | Calls | Total ms | Avg us | % |", "|---|---:|---:|---:|---:|"]
     for r in rows[:top]:
-        name = r["Name"].replace("void ", "").split("(")[0]
+        name = r["Name"].replace("void ", "").replace("(anonymous namespace)::", "").split("(")[0]
         lines.append("| `%s` | %s | %.1f | %.2f | %.2f |" % (name, r["Calls"], float(r["TotalDurationNs"]) / 1e6,
                                                           float(r["AverageNs"]) / 1e3, float(r["Percentage"])))
     lines.append("")
@@ -336,7 +389,7 @@ def pmc_summary(pdir, out_md, command_lines):
     fetch = float(np.mean(list(kf.values()))) * 1024.0 * f_scale
     write = float(np.mean(list(kw.values()))) * 1024.0 * w_scale
     alg = bench["roofline"]["algorithmic_bytes_per_launch"]
-    rec = {"kernel": kernel, "sources_sha1": bench["sources_sha1"], "sample_every": bench["config"]["sample_every"],
+    rec = {"kernel": kernel, "sources_sha1": kernel_sources_sha1(kernel), "sample_every": bench["config"]["sample_every"],
            "dispatches": [len(kf), len(kw)], "timed_calls": bench["roofline"]["timed_calls"],
            "fetch_scale": f_scale, "write_scale": w_scale,
            "fetch_bytes_per_launch": fetch, "write_bytes_per_launch": write,

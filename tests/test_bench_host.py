@@ -79,7 +79,7 @@ def test_traffic_record_needs_current_sources(tmp_path, monkeypatch):
     k = "ks_x_kernel<float>"
     pdir = tmp_path / "profiles"
     pdir.mkdir()
-    rec = {"kernel": k, "sources_sha1": bench.kernel_sources_sha1(), "sample_every": 1,
+    rec = {"kernel": k, "sources_sha1": bench.kernel_sources_sha1("ks_dma_kernel<float>"), "sample_every": 1,
            "traffic_bytes_per_launch": 123.0}
     (pdir / "a.md").write_text("# x\n" + bench.TRAFFIC_TAG + json.dumps(rec) + "\n")
     stale = dict(rec, kernel="ks_y_kernel<float>", sources_sha1="0" * 40)
@@ -87,7 +87,7 @@ def test_traffic_record_needs_current_sources(tmp_path, monkeypatch):
     # The records are read from ROOT/profiles; the hash stays the real tree's.
     sha = rec["sources_sha1"]
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
-    monkeypatch.setattr(bench, "kernel_sources_sha1", lambda: sha)
+    monkeypatch.setattr(bench, "kernel_sources_sha1", lambda kernel=None: sha)
     assert bench.traffic_record(k, 1)["traffic_bytes_per_launch"] == 123.0
     assert bench.traffic_record(k, 2) is None
     assert bench.traffic_record("ks_y_kernel<float>", 1) is None
@@ -149,3 +149,15 @@ def test_points_summary_tables(tmp_path):
     assert "| f32 BSL B=4096 | 40 |" in text and "| bf16 BSL B=4096 | 40 |" in text
     assert "(2, 2, 2, 512)" not in text
     assert text.count("`k0`") == 2 and "0.010" in text  # the lowest point of each dtype listed
+
+
+def test_kernel_family_hash_covers_its_sources_only():
+    """The traffic record of a kernel family is keyed on the sources that build
+    it (its translation units, their headers, its planners): another family's
+    source does not change it, a shared header does."""
+    dma = bench.kernel_sources_sha1("ks_dma_kernel<float,4,true,1,4,4,2>")
+    assert dma == bench.kernel_sources_sha1("ks_dma_kernel<unsignedshort,1,false,1,8,2,4>")
+    assert dma != bench.kernel_sources_sha1("ks_fp8_kernel<0,8>")
+    files = [os.path.basename(p) for p in bench._include_closure(
+        [os.path.join(bench.ROOT, "paper_2405_15013_amd", "csrc", "ks_dma_f32_v1.hip")])]
+    assert "ks_dma.h" in files and "ks_direct.h" in files and "ks_fp8.hip" not in files
