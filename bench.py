@@ -329,6 +329,56 @@ def points_summary(points_jsonl, out_md, command_lines, floor_json=None, lowest=
     print("\n".join(lines))
 
 
+MFMA_COUNTERS = ("SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_WAIT_INST_ANY", "SQ_VALU_MFMA_BUSY_CYCLES", "SQ_INSTS_MFMA",
+                 "GRBM_GUI_ACTIVE")
+
+
+def mfma_summary(csv_paths, out_md, command_lines):
+    """MFMA utilisation of kernel instances from one counter pass each
+    (rocprofv3 --pmc with MFMA_COUNTERS over `bench.py --kernel NAME --eager`):
+    counters summed over the instance's dispatches, kernel time from their
+    start and end timestamps, matrix-pipe busy fraction over the chip's 1024
+    SIMDs at 2.4 GHz, and the fraction of wavefront cycles spent waiting."""
+    import csv
+    cols = []
+    for path in csv_paths:
+        tot, spans, kname = {}, {}, None
+        with open(path) as fh:
+            for r in csv.DictReader(fh):
+                if not r["Kernel_Name"].replace(" ", "").replace("void", "").startswith("ks::"):
+                    continue
+                kname = r["Kernel_Name"].replace("void ", "").replace(" ", "").split("(")[0]
+                tot[r["Counter_Name"]] = tot.get(r["Counter_Name"], 0.0) + float(r["Counter_Value"])
+                spans[r["Dispatch_Id"]] = (int(r["Start_Timestamp"]), int(r["End_Timestamp"]))
+        t = sum(e - b for b, e in spans.values()) * 1e-9
+        busy = tot.get("SQ_VALU_MFMA_BUSY_CYCLES", 0.0)
+        cols.append({"kernel": kname, "dispatches": len(spans), "time_s": t, "mfma": tot.get("SQ_INSTS_MFMA", 0.0),
+                     "busy": busy, "busy_frac": busy / (1024 * t * 2.4e9) if t else float("nan"),
+                     "wait_frac": tot.get("SQ_WAIT_INST_ANY", 0.0) / max(1.0, tot.get("SQ_WAVE_CYCLES", 0.0)),
+                     "waves": tot.get("SQ_WAVES", 0.0)})
+    lines = ["# MFMA utilisation of the fp32 MFMA-bound instances over their sweep points", "",
+             "Command (one counter pass per instance, from the repository root; the sweep points of the instance "
+             "launched call by call):", "", "```"] + command_lines + ["```", "",
+             "| | " + " | ".join("`%s`" % c["kernel"] for c in cols) + " |", "|---" + "|---:" * len(cols) + "|",
+             "| dispatches | " + " | ".join("%d" % c["dispatches"] for c in cols) + " |",
+             "| kernel time (sum) | " + " | ".join("%.2f ms" % (c["time_s"] * 1e3) for c in cols) + " |",
+             "| SQ_INSTS_MFMA | " + " | ".join("%.4g" % c["mfma"] for c in cols) + " |",
+             "| SQ_VALU_MFMA_BUSY_CYCLES | " + " | ".join("%.4g" % c["busy"] for c in cols) + " |",
+             "| busy cycles per MFMA | " + " | ".join("%.1f" % (c["busy"] / max(1.0, c["mfma"])) for c in cols) + " |",
+             "| MFMA busy / (1024 SIMDs x kernel time x 2.4 GHz) | " + " | ".join(
+                 "%.2f" % c["busy_frac"] for c in cols) + " |",
+             "| SQ_WAIT_INST_ANY / SQ_WAVE_CYCLES | " + " | ".join("%.2f" % c["wait_frac"] for c in cols) + " |",
+             "| SQ_WAVES | " + " | ".join("%.4g" % c["waves"] for c in cols) + " |", "",
+             "Reading: the fp32 matrix pipes are busy %.0f-%.0f %% of these kernels' time (one 16x16x4 fp32 MFMA "
+             "keeps a pipe busy 32 cycles) while the resident wavefronts wait on outstanding operations %.0f-%.0f %% "
+             "of their cycles: these points are bound by latency inside the kernel, not by MFMA throughput." % (
+                 100 * min(c["busy_frac"] for c in cols), 100 * max(c["busy_frac"] for c in cols),
+                 100 * min(c["wait_frac"] for c in cols), 100 * max(c["wait_frac"] for c in cols)), ""]
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines))
+    print("\n".join(lines))
+
+
 def trace_summary(stats_csv, bench_json, out_md, command_lines, top=25):
     """Write the kernel-trace summary (rocprofv3 --kernel-trace --stats) of a
     bench run, with the dominant kernel's profiler average beside the
@@ -702,6 +752,8 @@ def main():
                     help="only time a plain device copy at 0.5-256 MB with the sweep's protocol, into OUT_JSON")
     ap.add_argument("--points-summary", nargs=2, metavar=("POINTS_JSONL", "OUT_MD"),
                     help="summarise a --points-out file by class into OUT_MD (no GPU)")
+    ap.add_argument("--mfma-summary", nargs="+", metavar="CSV_THEN_OUT_MD",
+                    help="summarise MFMA counter passes (counter_collection.csv files, then OUT_MD; no GPU)")
     ap.add_argument("--copy-floor-in", default=None, metavar="FLOOR_JSON",
                     help="a --copy-floor result for --points-summary")
     ap.add_argument("--pmc-command", action="append", default=[],
@@ -712,6 +764,9 @@ def main():
         return
     if args.trace_summary:
         trace_summary(*args.trace_summary, args.pmc_command)
+        return
+    if args.mfma_summary:
+        mfma_summary(args.mfma_summary[:-1], args.mfma_summary[-1], args.pmc_command)
         return
     if args.points_summary:
         points_summary(args.points_summary[0], args.points_summary[1], args.pmc_command, args.copy_floor_in)
