@@ -55,11 +55,24 @@ __device__ __forceinline__ void fp8_rows_transpose(u32x4 (&m)[4]) {
   }
 }
 
-template <int LAYOUT, int V>
+// One chunk (32 values of l) of a wavefront's operands as loaded, before any
+// use of the data, so that the next chunk's loads are in flight while this
+// one is multiplied: X as 16 dwords (the lane's 8 values of l x V, or for
+// 64-byte row runs the pieces still in their loading lanes), K as MT x VK
+// runs of 8 values of l (2 dwords each).
+template <int V, int MT, int VK>
+struct Fp8Chunk {
+  static constexpr int XW = 2 * V;  // dwords of the lane's X operand
+  uint32_t xw[XW < 16 ? 16 : XW];
+  uint32_t kw[MT][VK][2];
+};
+
+template <int LAYOUT, int V, int MT>
 __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
   constexpr int LP = 8;       // values of l per lane and MFMA
   constexpr int CH = 4 * LP;  // values of l per chunk
   constexpr int VK = LAYOUT == BSL ? 1 : V;
+  using Chunk = Fp8Chunk<V, MT, VK>;
   const int lane = threadIdx.x & 63;
   const int item = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   if (item >= t.items) return;  // wave-uniform
@@ -67,55 +80,52 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
   const MItem it = masked_item(p, t, V, item);
   // Batch-size-first with V = d, c a multiple of 8 and 16-byte aligned
   // buffers: a lane's X operand (8 values of l x d j) is one run of 8d bytes
-  // of its batch row, and (b a multiple of 4) its outputs k0 + 4g .. + 3 one
-  // run of 4d bf16.  d = 8: 64-byte runs, four lanes per run
+  // of its batch row, and (b a multiple of 4) its outputs k0 + 4g .. + 3 of
+  // each M-tile one run of 4d bf16.  d = 8: 64-byte runs, four lanes per run
   // (fp8_rows_transpose); d = 1, 2, 4: each lane moves its own run.
   const bool runs = LAYOUT == BSF && V == p.d && p.c % 8 == 0 && p.align >= 16;
   const bool rows8 = runs && V == 8;
+  const bool col = masked_col_valid(p, it, V, n);
   const uint8_t* __restrict__ x = static_cast<const uint8_t*>(p.x);
   const uint8_t* __restrict__ kv = static_cast<const uint8_t*>(p.kv);
 
-  f32x4 acc[V];
-#pragma unroll
-  for (int e = 0; e < V; ++e) acc[e] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  for (int ch = 0; ch < t.nchunks; ++ch) {
+  // Issue the loads of chunk ch (no use of the loaded data).
+  auto load = [&](int ch, Chunk& cb) {
     const int l0 = ch * CH + LP * g;
-    uint8_t xs[LP][V];
-    uint8_t ks[VK][LP];
     if (rows8) {
-      // Rows of d = 8: a lane's operand (8 values of l x 8 j) is the 64-byte
-      // run of its batch row from l0*8.  Load x of the wavefront reads, for
-      // lane row g, piece g of lane row x's run (four lanes cover one run),
-      // then the pieces move to their lanes.
-      u32x4 m[4];
-      const bool col = masked_col_valid(p, it, V, n);
+      // load xr: piece g of lane row xr's 64-byte run (values from ch*CH + 8xr)
 #pragma unroll
       for (int xr = 0; xr < 4; ++xr) {
         const int lx = ch * CH + LP * xr;
-        m[xr] = u32x4{0, 0, 0, 0};
+        u32x4 w = u32x4{0, 0, 0, 0};
         if (col && lx < p.c)
-          m[xr] = *reinterpret_cast<const u32x4*>(x + (int64_t)(it.beta0 + n) * p.N +
-                                                  ((int64_t)it.i * p.c + lx) * 8 + 16 * g);
+          w = *reinterpret_cast<const u32x4*>(x + (int64_t)(it.beta0 + n) * p.N + ((int64_t)it.i * p.c + lx) * 8 + 16 * g);
+#pragma unroll
+        for (int w2 = 0; w2 < 4; ++w2) cb.xw[4 * xr + w2] = w[w2];
       }
-      fp8_rows_transpose(m);
-      if constexpr (V == 8) __builtin_memcpy(xs, m, 64);
     } else if (V <= 4 && runs) {
       if constexpr (V <= 4) {
-        // the run of values l0 .. l0 + 7 (8V bytes: 8, 16 or two 16-byte loads)
-        constexpr int NB = LP * V < 16 ? LP * V : 16;
+        // the run of values l0 .. l0 + 7 (8V bytes: one or two vectors)
         const int64_t off = masked_x_off(p, it, V, l0, n);
+#pragma unroll
+        for (int w2 = 0; w2 < 2 * V; ++w2) cb.xw[w2] = 0;
         if (off >= 0) {
-          fp8_load<NB>(x + off, reinterpret_cast<uint8_t(&)[NB]>(xs[0][0]));
-          if constexpr (LP * V == 32) fp8_load<16>(x + off + 16, reinterpret_cast<uint8_t(&)[16]>(xs[LP / 2][0]));
-        } else {
+          if constexpr (V == 1) {
+            const u32x2 w = *reinterpret_cast<const u32x2*>(x + off);
+            cb.xw[0] = w[0];
+            cb.xw[1] = w[1];
+          } else {
 #pragma unroll
-          for (int q = 0; q < LP; ++q)
+            for (int h = 0; h < V / 2; ++h) {
+              const u32x4 w = *reinterpret_cast<const u32x4*>(x + off + 16 * h);
 #pragma unroll
-            for (int e = 0; e < V; ++e) xs[q][e] = 0;
+              for (int w2 = 0; w2 < 4; ++w2) cb.xw[4 * h + w2] = w[w2];
+            }
+          }
         }
       }
     } else {
+      uint8_t xs[LP][V];
 #pragma unroll
       for (int q = 0; q < LP; ++q) {
         const int64_t off = masked_x_off(p, it, V, l0 + q, n);
@@ -126,137 +136,183 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
           for (int e = 0; e < V; ++e) xs[q][e] = 0;
         }
       }
+      __builtin_memcpy(cb.xw, xs, LP * V);
     }
 #pragma unroll
-    for (int e = 0; e < VK; ++e) {
-      if (t.kvec) {  // the lane's 8 values of l are one aligned 8-byte run of row k
-        const int64_t ko = masked_k_off(p, it, e, n, l0);
-        if (ko >= 0) {
-          fp8_load<LP>(kv + ko, ks[e]);
+    for (int mt = 0; mt < MT; ++mt)
+#pragma unroll
+      for (int e = 0; e < VK; ++e) {
+        // the lane's 8 values of l of K row k0 + 16 mt + n of block (i, j0 + e)
+        const int64_t ko = masked_k_off(p, it, e, 16 * mt + n, l0);
+        if (t.kvec) {  // one aligned 8-byte run (c a multiple of 8)
+          u32x2 w = u32x2{0, 0};
+          if (ko >= 0) w = *reinterpret_cast<const u32x2*>(kv + ko);
+          cb.kw[mt][e][0] = w[0];
+          cb.kw[mt][e][1] = w[1];
         } else {
+          uint8_t ks[LP];
 #pragma unroll
-          for (int q = 0; q < LP; ++q) ks[e][q] = 0;
-        }
-      } else {
-#pragma unroll
-        for (int q = 0; q < LP; ++q) {
-          const int64_t ko = masked_k_off(p, it, e, n, l0 + q);
-          ks[e][q] = ko >= 0 ? kv[ko] : 0;
+          for (int q = 0; q < LP; ++q) {
+            const int64_t kq = masked_k_off(p, it, e, 16 * mt + n, l0 + q);
+            ks[q] = kq >= 0 ? kv[kq] : 0;
+          }
+          __builtin_memcpy(cb.kw[mt][e], ks, LP);
         }
       }
-    }
-    // operands: 8 codes per lane, value l0 + q in byte q
-    uint64_t kw[VK];
+  };
+
+  // The MFMAs of one chunk: B operand of chain e = the lane's 8 values of l
+  // at j (BSF) or batch entry (BSL) e, byte q = value l0 + q.
+  f32x4 acc[MT][V];
 #pragma unroll
-    for (int e = 0; e < VK; ++e) {
-      uint64_t w = 0;
+  for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int q = 0; q < LP; ++q) w |= (uint64_t)ks[e][q] << (8 * q);
-      kw[e] = w;
+    for (int e = 0; e < V; ++e) acc[mt][e] = f32x4{0.f, 0.f, 0.f, 0.f};
+  auto mma = [&](Chunk& cb) {
+    uint8_t xs[LP][V];
+    if (rows8) {
+      if constexpr (V == 8) {
+        u32x4 m[4];
+#pragma unroll
+        for (int xr = 0; xr < 4; ++xr) m[xr] = u32x4{cb.xw[4 * xr], cb.xw[4 * xr + 1], cb.xw[4 * xr + 2], cb.xw[4 * xr + 3]};
+        fp8_rows_transpose(m);
+        __builtin_memcpy(xs, m, 64);
+      }
+    } else {
+      __builtin_memcpy(xs, cb.xw, LP * V);
     }
 #pragma unroll
     for (int e = 0; e < V; ++e) {
       uint64_t xw = 0;
 #pragma unroll
       for (int q = 0; q < LP; ++q) xw |= (uint64_t)xs[q][e] << (8 * q);
-      acc[e] = __builtin_amdgcn_mfma_f32_16x16x32_fp8_fp8((long)kw[LAYOUT == BSL ? 0 : e], (long)xw, acc[e], 0, 0, 0);
+#pragma unroll
+      for (int mt = 0; mt < MT; ++mt) {
+        const uint64_t kw = (uint64_t)cb.kw[mt][LAYOUT == BSL ? 0 : e][0] | ((uint64_t)cb.kw[mt][LAYOUT == BSL ? 0 : e][1] << 32);
+        acc[mt][e] = __builtin_amdgcn_mfma_f32_16x16x32_fp8_fp8((long)kw, (long)xw, acc[mt][e], 0, 0, 0);
+      }
     }
+  };
+
+  for (int ch = 0; ch < t.nchunks; ++ch) {
+    Chunk cur;
+    load(ch, cur);
+    mma(cur);
   }
-  // Epilogue: output feature of (e, r) is row k = k0 + 4g + r of block
-  // (i, j0 [+ e in BSF]); padding rows (k >= b) take no bias.
+
+  // Epilogue: output feature of (mt, e, r) is row k = k0 + 16 mt + 4g + r of
+  // block (i, j0 [+ e in BSF]); padding rows (k >= b) take no bias.
   constexpr int BV = LAYOUT == BSF ? V : 1;
   const bool has_bias = p.bias != nullptr;
-  float bv[4][BV];
+  float bv[MT][4][BV];
   if (has_bias) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int k = it.k0 + 4 * g + r;
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int e = 0; e < BV; ++e)
-        bv[r][e] = k < p.b ? bias_value<bf16_t>(p, ((int64_t)it.i * p.b + k) * p.d + it.j0 + e) : 0.0f;
-    }
+      for (int r = 0; r < 4; ++r) {
+        const int k = it.k0 + 16 * mt + 4 * g + r;
+#pragma unroll
+        for (int e = 0; e < BV; ++e)
+          bv[mt][r][e] = k < p.b ? bias_value<bf16_t>(p, ((int64_t)it.i * p.b + k) * p.d + it.j0 + e) : 0.0f;
+      }
   }
   mfma_results_settle();
   if (has_bias) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int e = 0; e < V; ++e) acc[e][r] += bv[r][LAYOUT == BSF ? e : 0];
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc[mt][e][r] += bv[mt][r][LAYOUT == BSF ? e : 0];
   }
   if (epilogue_gelu(p)) {
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+    for (int mt = 0; mt < MT; ++mt)
 #pragma unroll
-      for (int e = 0; e < V; ++e) acc[e][r] = gelu_f32(acc[e][r]);
+      for (int r = 0; r < 4; ++r)
+#pragma unroll
+        for (int e = 0; e < V; ++e) acc[mt][e][r] = gelu_f32(acc[mt][e][r]);
   }
-  if (rows8) {
-    // Lane row g's outputs k = k0 + 4g + r (r = 0..3, 8 j each) are one
-    // 64-byte run of its batch row; after the transpose, store x writes piece
-    // g of lane row x's run, so four lanes write 64 contiguous bytes.
-    u32x4 m[4];
+
+#pragma unroll
+  for (int mt = 0; mt < MT; ++mt) {
+    MItem im = it;  // the M-tile's output rows k0 + 16 mt ..
+    im.k0 += 16 * mt;
+    if (rows8) {
+      if constexpr (V == 8) {
+        // Lane row g's outputs k = k0 + 4g + r (r = 0..3, 8 j each) are one
+        // 64-byte run of its batch row; after the transpose, store xr writes
+        // piece g of lane row xr's run, so four lanes write 64 contiguous bytes.
+        u32x4 m[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          uint16_t v[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) v[e] = from_f32<bf16_t>(acc[mt][e][r]);
+          __builtin_memcpy(&m[r], v, 16);
+        }
+        fp8_rows_transpose(m);
+        if (col) {
+          bf16_t* yrow = static_cast<bf16_t*>(p.y) + (int64_t)(im.beta0 + n) * p.M + (int64_t)im.i * p.b * 8;
+#pragma unroll
+          for (int xr = 0; xr < 4; ++xr) {
+            const int k = im.k0 + 4 * xr + g;
+            if (k < p.b) *reinterpret_cast<u32x4*>(yrow + (int64_t)k * 8) = m[xr];
+          }
+        }
+      }
+      continue;
+    }
+    if (V <= 4 && runs && p.b % 4 == 0) {
+      if constexpr (V <= 4) {
+        // outputs k0 + 4g .. k0 + 4g + 3 (all j): one run of 4V bf16
+        const int64_t off = masked_y_off(p, im, V, n, g, 0);
+        if (off >= 0) {
+          uint16_t v[4 * V];
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+#pragma unroll
+            for (int e = 0; e < V; ++e) v[r * V + e] = from_f32<bf16_t>(acc[mt][e][r]);
+          bf16_t* yo = static_cast<bf16_t*>(p.y) + off;
+          if constexpr (V == 1) {
+            u32x2 w;
+            __builtin_memcpy(&w, v, 8);
+            *reinterpret_cast<u32x2*>(yo) = w;
+          } else {
+#pragma unroll
+            for (int h = 0; h < 4 * V / 8; ++h) {
+              u32x4 w;
+              __builtin_memcpy(&w, v + 8 * h, 16);
+              *reinterpret_cast<u32x4*>(yo + 8 * h) = w;
+            }
+          }
+        }
+      }
+      continue;
+    }
+    // outputs k = k0 + 4g + r in bfloat16
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
-      uint16_t v[8];
+      const int64_t off = masked_y_off(p, im, V, n, g, r);
+      if (off < 0) continue;
+      uint16_t v[V];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) v[e] = from_f32<bf16_t>(acc[e < V ? e : 0][r]);  // V == 8 here
-      __builtin_memcpy(&m[r], v, 16);
-    }
-    fp8_rows_transpose(m);
-    if (!masked_col_valid(p, it, V, n)) return;
-    bf16_t* yrow = static_cast<bf16_t*>(p.y) + (int64_t)(it.beta0 + n) * p.M + (int64_t)it.i * p.b * 8;
-#pragma unroll
-    for (int xr = 0; xr < 4; ++xr) {
-      const int k = it.k0 + 4 * xr + g;
-      if (k < p.b) *reinterpret_cast<u32x4*>(yrow + (int64_t)k * 8) = m[xr];
-    }
-    return;
-  }
-  if (V <= 4 && runs && p.b % 4 == 0) {
-    // outputs k0 + 4g .. k0 + 4g + 3 (all j): one run of 4V bf16
-    const int64_t off = masked_y_off(p, it, V, n, g, 0);
-    if (off < 0) return;
-    uint16_t v[4 * V];
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int e = 0; e < V; ++e) v[r * V + e] = from_f32<bf16_t>(acc[e][r]);
-    bf16_t* yo = static_cast<bf16_t*>(p.y) + off;
-    if constexpr (V == 1) {
-      u32x2 w;
-      __builtin_memcpy(&w, v, 8);
-      *reinterpret_cast<u32x2*>(yo) = w;
-    } else if constexpr (V <= 4) {
-#pragma unroll
-      for (int h = 0; h < 4 * V / 8; ++h) {
+      for (int e = 0; e < V; ++e) v[e] = from_f32<bf16_t>(acc[mt][e][r]);
+      bf16_t* yo = static_cast<bf16_t*>(p.y) + off;
+      if constexpr (V == 8) {
         u32x4 w;
-        __builtin_memcpy(&w, v + 8 * h, 16);
-        *reinterpret_cast<u32x4*>(yo + 8 * h) = w;
+        __builtin_memcpy(&w, v, 16);
+        if constexpr (LAYOUT == BSL) __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(yo));
+        else *reinterpret_cast<u32x4*>(yo) = w;
+      } else if constexpr (V == 4) {
+        u32x2 w;
+        __builtin_memcpy(&w, v, 8);
+        if constexpr (LAYOUT == BSL) __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(yo));
+        else *reinterpret_cast<u32x2*>(yo) = w;
+      } else {
+#pragma unroll
+        for (int e = 0; e < V; ++e) yo[e] = v[e];
       }
-    }
-    return;
-  }
-  // outputs k = k0 + 4g + r in bfloat16
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int64_t off = masked_y_off(p, it, V, n, g, r);
-    if (off < 0) continue;
-    uint16_t v[V];
-#pragma unroll
-    for (int e = 0; e < V; ++e) v[e] = from_f32<bf16_t>(acc[e][r]);
-    bf16_t* yo = static_cast<bf16_t*>(p.y) + off;
-    if constexpr (V == 8) {
-      u32x4 w;
-      __builtin_memcpy(&w, v, 16);
-      if constexpr (LAYOUT == BSL) __builtin_nontemporal_store(w, reinterpret_cast<u32x4*>(yo));
-      else *reinterpret_cast<u32x4*>(yo) = w;
-    } else if constexpr (V == 4) {
-      u32x2 w;
-      __builtin_memcpy(&w, v, 8);
-      if constexpr (LAYOUT == BSL) __builtin_nontemporal_store(w, reinterpret_cast<u32x2*>(yo));
-      else *reinterpret_cast<u32x2*>(yo) = w;
-    } else {
-#pragma unroll
-      for (int e = 0; e < V; ++e) yo[e] = v[e];
     }
   }
 }
@@ -279,16 +335,32 @@ int fp8_vec(const Problem& p) {
   return V;
 }
 
+// M-tiles per wavefront: the largest MT in {4, 2, 1} (2 at most for access
+// widths of 4 or 8, whose accumulators and operands would otherwise leave one
+// wavefront per SIMD) that divides the 16-row tiles of b and leaves at least
+// 768 wavefronts; more M-tiles read each X operand once for more output rows.
+int fp8_mt(const Problem& p, int V) {
+  const int mtmax = V >= 4 ? 2 : 4;
+  const int tiles = (p.b + 15) / 16;
+  for (int mt = mtmax; mt > 1; mt /= 2) {
+    if (tiles % mt) continue;
+    const MaskedTile t = masked_tile(p, V, mt);
+    if ((int64_t)t.nbt * p.a * t.jgroups * t.kgroups >= 768) return mt;
+  }
+  return 1;
+}
+
 bool plan_fp8(const Problem& p, Plan* pl) {
   if (p.dtype != FP8) return false;
   const int V = fp8_vec(p);
-  const MaskedTile t = masked_tile(p, V);
+  const int MT = fp8_mt(p, V);
+  const MaskedTile t = masked_tile(p, V, MT);
   const int64_t items = (int64_t)t.nbt * p.a * t.jgroups * t.kgroups;
   if (items > 0x7fffffff - 3) return false;
   pl->variant = V_FP8;
   pl->vec = V;
   pl->unroll = 0;
-  pl->waves_m = 1;
+  pl->waves_m = MT;
   pl->waves_n = t.kgroups;
   pl->bt = p.layout == BSL ? 16 * V : 16;
   pl->jg = p.layout == BSL ? 1 : V;
@@ -300,15 +372,19 @@ bool plan_fp8(const Problem& p, Plan* pl) {
 }
 
 hipError_t launch_fp8(const Problem& p, const Plan& pl, hipStream_t s) {
-  const MaskedTile t = masked_tile(p, pl.vec);
+  const MaskedTile t = masked_tile(p, pl.vec, pl.waves_m);
   const dim3 g(pl.grid), b(256);
-#define KS_FP8(L, VV)                                                        \
-  if (p.layout == L && pl.vec == VV) {                                       \
-    hipLaunchKernelGGL((ks_fp8_kernel<L, VV>), g, b, 0, s, p, t);           \
+#define KS_FP8(L, VV, M)                                                     \
+  if (p.layout == L && pl.vec == VV && pl.waves_m == M) {                    \
+    hipLaunchKernelGGL((ks_fp8_kernel<L, VV, M>), g, b, 0, s, p, t);        \
     return hipGetLastError();                                                \
   }
-  KS_FP8(BSL, 1) KS_FP8(BSL, 2) KS_FP8(BSL, 4) KS_FP8(BSL, 8)
-  KS_FP8(BSF, 1) KS_FP8(BSF, 2) KS_FP8(BSF, 4) KS_FP8(BSF, 8)
+  KS_FP8(BSL, 1, 1) KS_FP8(BSL, 2, 1) KS_FP8(BSL, 4, 1) KS_FP8(BSL, 8, 1)
+  KS_FP8(BSL, 1, 2) KS_FP8(BSL, 2, 2) KS_FP8(BSL, 4, 2) KS_FP8(BSL, 8, 2)
+  KS_FP8(BSL, 1, 4) KS_FP8(BSL, 2, 4)
+  KS_FP8(BSF, 1, 1) KS_FP8(BSF, 2, 1) KS_FP8(BSF, 4, 1) KS_FP8(BSF, 8, 1)
+  KS_FP8(BSF, 1, 2) KS_FP8(BSF, 2, 2) KS_FP8(BSF, 4, 2) KS_FP8(BSF, 8, 2)
+  KS_FP8(BSF, 1, 4) KS_FP8(BSF, 2, 4)
 #undef KS_FP8
   return hipErrorInvalidValue;
 }

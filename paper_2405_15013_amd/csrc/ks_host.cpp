@@ -288,7 +288,7 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
                pl.waves_m, pl.cps, (int)(pl.rs * pl.nt * pl.lch * p.d * (p.dtype == F32 ? 4 : 2) / 256), pl.nt);
       break;
     case V_MASKED: snprintf(buf, sizeof buf, "ks_masked_kernel<%s,%d,%d,%s>", t, p.layout, pl.vec, epi); break;
-    case V_FP8: snprintf(buf, sizeof buf, "ks_fp8_kernel<%d,%d>", p.layout, pl.vec); break;
+    case V_FP8: snprintf(buf, sizeof buf, "ks_fp8_kernel<%d,%d,%d>", p.layout, pl.vec, pl.waves_m); break;
     default: snprintf(buf, sizeof buf, "?");
   }
   std::string r(buf);

@@ -24,7 +24,8 @@
 namespace ks {
 
 struct MaskedTile {
-  int kgroups;   // ceil(b / 16)
+  int mt;        // 16-row output tiles per wavefront (1; the FP8 kernel also 2 or 4)
+  int kgroups;   // ceil(b / (16 * mt))
   int jgroups;   // BSL: d; BSF: d / V
   int nbt;       // batch tiles (16*V entries in BSL, 16 rows in BSF)
   int items;     // nbt * a * jgroups * kgroups
@@ -40,9 +41,10 @@ struct MItem {
 // FP8, 16x16x32 MFMAs).
 KS_MHD int masked_lp(int esize) { return esize == 4 ? 4 : 8; }
 
-KS_MHD MaskedTile masked_tile(const Problem& p, int V) {
+KS_MHD MaskedTile masked_tile(const Problem& p, int V, int mt = 1) {
   MaskedTile t;
-  t.kgroups = (p.b + 15) / 16;
+  t.mt = mt;
+  t.kgroups = (p.b + 16 * mt - 1) / (16 * mt);
   t.jgroups = p.layout == BSL ? p.d : p.d / V;
   const int span = p.layout == BSL ? 16 * V : 16;
   t.nbt = (p.batch + span - 1) / span;
@@ -67,7 +69,7 @@ KS_MHD MItem masked_item(const Problem& p, const MaskedTile& t, int V, int item)
   rest /= t.nbt;
   const int jg = rest % t.jgroups;
   it.i = rest / t.jgroups;
-  it.k0 = 16 * kg;
+  it.k0 = 16 * t.mt * kg;
   if (p.layout == BSL) {
     it.j0 = jg;
     it.beta0 = bt * 16 * V;

@@ -165,7 +165,7 @@ bool verify_item(Checker& ck, const DItem& it, bool strided, int V, int MT, int 
 // Masked kernel with access width V: every X piece is the V elements of
 // value l the product needs (or zero padding), K elements inside the block,
 // every Y element of the batch written exactly once, vector accesses aligned.
-bool verify_masked_v(Checker& ck, int V) {
+bool verify_masked_v(Checker& ck, int V, int MT) {
   const Problem& p = ck.p;
   const bool fp8 = p.dtype == FP8;
   const int S = p.dtype == F32 ? 4 : 2, LP = masked_lp(S), CH = 4 * LP;
@@ -175,8 +175,8 @@ bool verify_masked_v(Checker& ck, int V) {
   const int xvec = fp8 ? (V >= 2 ? V : 0) : (V * S >= 8 ? V * S : 0);
   const int yvec = fp8 ? (2 * V >= 8 ? 2 * V : 0) : (V * S >= 8 ? V * S : 0);
   const int xs = fp8 ? 1 : S, ys = fp8 ? 2 : S;
-  const MaskedTile t = masked_tile(p, V);
-  if (t.kgroups * 16 < p.b || t.nchunks * CH < p.c) return ck.fail("masked tiles do not cover the block", V);
+  const MaskedTile t = masked_tile(p, V, MT);
+  if (t.kgroups * 16 * MT < p.b || t.nchunks * CH < p.c) return ck.fail("masked tiles do not cover the block", V);
   if (p.layout == BSL && p.batch % V) return ck.fail("batch not a multiple of the access width", V);
   if (p.layout == BSF && p.d % V) return ck.fail("d not a multiple of the access width", V);
   const int VK = p.layout == BSL ? 1 : V;
@@ -204,14 +204,17 @@ bool verify_masked_v(Checker& ck, int V) {
               if (masked_x_off(p, it, V, lx + 2 * g + h, n) != off + 8 * h)
                 return ck.fail("row-run X piece is not the values of its lane row", off);
           }
-        for (int x = 0; x < 4; ++x) {
-          const int k = it.k0 + 4 * x + g;
-          if (k >= p.b) continue;
-          const int64_t off = (int64_t)(it.beta0 + n) * p.M + ((int64_t)it.i * p.b + k) * 8;
-          if (off != masked_y_off(p, it, V, n, x, g)) return ck.fail("row-run Y piece is not its output", off);
-          if ((off * 2) % 16) return ck.fail("row-run Y piece not 16-byte aligned", off);
-          ck.write_y(off, 8);
-        }
+        for (int mt = 0; mt < MT; ++mt)
+          for (int x = 0; x < 4; ++x) {
+            MItem im = it;
+            im.k0 += 16 * mt;
+            const int k = im.k0 + 4 * x + g;
+            if (k >= p.b) continue;
+            const int64_t off = (int64_t)(im.beta0 + n) * p.M + ((int64_t)im.i * p.b + k) * 8;
+            if (off != masked_y_off(p, im, V, n, x, g)) return ck.fail("row-run Y piece is not its output", off);
+            if ((off * 2) % 16) return ck.fail("row-run Y piece not 16-byte aligned", off);
+            ck.write_y(off, 8);
+          }
       }
       if (runs && !rows8 && masked_col_valid(p, it, V, n))
         for (int ch = 0; ch < t.nchunks; ++ch) {
@@ -226,16 +229,19 @@ bool verify_masked_v(Checker& ck, int V) {
           for (int q = 0; q < LP; ++q)
             if (masked_x_off(p, it, V, l0 + q, n) != off + q * V) return ck.fail("X run is not the values of the lane", l0 + q);
         }
-      if (yruns && masked_col_valid(p, it, V, n)) {
-        const int64_t off = masked_y_off(p, it, V, n, g, 0);
-        if (off >= 0) {
-          const int nb = V == 1 ? 8 : 16;  // bytes per store
-          if ((off * 2) % nb) return ck.fail("Y run not aligned to its stores", off);
-          for (int r = 0; r < 4; ++r)
-            if (masked_y_off(p, it, V, n, g, r) != off + r * V) return ck.fail("Y run is not the lane's outputs", off);
-          ck.write_y(off, 4 * V);
+      if (yruns && masked_col_valid(p, it, V, n))
+        for (int mt = 0; mt < MT; ++mt) {
+          MItem im = it;
+          im.k0 += 16 * mt;
+          const int64_t off = masked_y_off(p, im, V, n, g, 0);
+          if (off >= 0) {
+            const int nb = V == 1 ? 8 : 16;  // bytes per store
+            if ((off * 2) % nb) return ck.fail("Y run not aligned to its stores", off);
+            for (int r = 0; r < 4; ++r)
+              if (masked_y_off(p, im, V, n, g, r) != off + r * V) return ck.fail("Y run is not the lane's outputs", off);
+            ck.write_y(off, 4 * V);
+          }
         }
-      }
       for (int ch = 0; ch < t.nchunks; ++ch)
         for (int q = 0; q < LP; ++q) {
           const int l = ch * CH + LP * g + q;
@@ -257,31 +263,37 @@ bool verify_masked_v(Checker& ck, int V) {
           } else if (!runs && l < p.c && masked_col_valid(p, it, V, n)) {
             return ck.fail("needed X piece treated as padding", l);
           }
-          if (t.kvec && q == 0)
-            for (int e = 0; e < VK; ++e) {
-              const int64_t ko = masked_k_off(p, it, e, n, l);
-              if (ko >= 0) {
-                if ((ko * xs) % (LP * xs)) return ck.fail("K operand vector not aligned to its size", ko);
-                ck.read_k(ko, LP);
+          for (int mt = 0; mt < MT; ++mt) {
+            const int m = 16 * mt + n;  // K row k0 + m
+            if (t.kvec && q == 0)
+              for (int e = 0; e < VK; ++e) {
+                const int64_t ko = masked_k_off(p, it, e, m, l);
+                if (ko >= 0) {
+                  if ((ko * xs) % (LP * xs)) return ck.fail("K operand vector not aligned to its size", ko);
+                  ck.read_k(ko, LP);
+                }
               }
-            }
-          for (int e = 0; e < VK; ++e) {
-            const int64_t ko = masked_k_off(p, it, e, n, l);
-            if (ko >= 0) {
-              ck.read_k(ko, 1);
-              if (ko != (((int64_t)it.i * p.d + it.j0 + e) * p.b + it.k0 + n) * p.c + l)
-                return ck.fail("masked K element is not the block value needed", ko);
-            } else if (it.k0 + n < p.b && l < p.c) {
-              return ck.fail("needed K value treated as padding", l);
+            for (int e = 0; e < VK; ++e) {
+              const int64_t ko = masked_k_off(p, it, e, m, l);
+              if (ko >= 0) {
+                ck.read_k(ko, 1);
+                if (ko != (((int64_t)it.i * p.d + it.j0 + e) * p.b + it.k0 + m) * p.c + l)
+                  return ck.fail("masked K element is not the block value needed", ko);
+              } else if (it.k0 + m < p.b && l < p.c) {
+                return ck.fail("needed K value treated as padding", l);
+              }
             }
           }
         }
-      for (int r = 0; r < 4 && !rows8 && !yruns; ++r) {
-        const int64_t off = masked_y_off(p, it, V, n, g, r);
-        if (off < 0) continue;
-        if (yvec && (off * ys) % yvec) return ck.fail("Y vector not aligned to its size", off);
-        ck.write_y(off, V);
-      }
+      for (int mt = 0; mt < MT && !rows8 && !yruns; ++mt)
+        for (int r = 0; r < 4; ++r) {
+          MItem im = it;
+          im.k0 += 16 * mt;
+          const int64_t off = masked_y_off(p, im, V, n, g, r);
+          if (off < 0) continue;
+          if (yvec && (off * ys) % yvec) return ck.fail("Y vector not aligned to its size", off);
+          ck.write_y(off, V);
+        }
     }
   }
   return ck.err.empty();
@@ -290,11 +302,12 @@ bool verify_masked_v(Checker& ck, int V) {
 // The planned access width, then every narrower one the planner would pick
 // for less aligned buffers (each with its own coverage check).
 bool verify_masked(Checker& ck, const Plan& pl) {
-  if (!verify_masked_v(ck, pl.vec)) return false;
+  // the planned width and M-tiles, then the narrower widths with one M-tile
+  if (!verify_masked_v(ck, pl.vec, pl.variant == V_FP8 ? pl.waves_m : 1)) return false;
   for (int V = pl.vec / 2; V >= 1; V /= 2) {
     if (!ck.coverage()) return false;
     std::fill(ck.cover.begin(), ck.cover.end(), 0);
-    if (!verify_masked_v(ck, V)) return false;
+    if (!verify_masked_v(ck, V, 1)) return false;
   }
   return ck.err.empty();
 }

@@ -31,6 +31,8 @@ def kernel_of(pattern, batch, dtype, layout):
 
 def xy_bytes(pattern, batch, dtype):
     a, b, c, d = pattern
+    if dtype == "fp8":  # E4M3 X, bf16 Y
+        return batch * a * d * (2 * b + c)
     return batch * a * d * (b + c) * (4 if dtype == "f32" else 2)
 
 

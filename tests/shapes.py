@@ -36,11 +36,16 @@ MLP = [(6, 64, 16, 8), (6, 16, 64, 8)]
 def bench_points():
     """Every (pattern, batch, dtype, layout) single-factor call the benchmark
     makes: the 5600 sweep points, then the tiny, butterfly, Monarch and
-    Transformer-MLP workloads (the chains run the same factors)."""
+    Transformer-MLP workloads (the chains run the same factors), then the FP8
+    calls."""
     pts = [(p, batch, dtype, layout) for dtype in ("f32", "bf16") for batch in (4096, 25088)
            for layout in ("bsf", "bsl") for p in sweep_patterns()]
     pts += [((2, 4, 4, 2), 32, "f32", layout) for layout in ("bsf", "bsl")]
     pts += [(p, 4096, "f32", layout) for p in BUTTERFLY for layout in ("bsf", "bsl")]
     pts += [(p, 16384, dtype, layout) for p in MONARCH for dtype in ("f32", "bf16") for layout in ("bsf", "bsl")]
     pts += [(p, 25088, dtype, layout) for p in MLP for dtype in ("f32", "bf16") for layout in ("bsf", "bsl")]
+    # FP8 (E4M3 inputs, bf16 outputs): the MLP layers and every 7th sweep pattern
+    pts += [(p, 25088, "fp8", layout) for p in MLP for layout in ("bsf", "bsl")]
+    pts += [(p, batch, "fp8", layout) for batch in (4096, 25088) for layout in ("bsf", "bsl")
+            for p in sweep_patterns()[::7]]
     return pts
