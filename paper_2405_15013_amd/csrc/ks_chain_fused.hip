@@ -186,7 +186,18 @@ __device__ __forceinline__ void fused_radix_pass(const FusedChain& fc, int q, fl
 #pragma unroll
       for (int r = 0; r < P; ++r) {
         if ((r / st) % PR != 0) continue;  // digit t of r must be zero
+        // the block's PR x PR values: 16-byte LDS reads (blocks start at
+        // multiples of PR * PR >= 4 floats of the 16-byte aligned copy)
         const float* kb = kt + fused_radix_block<P, PR>(i, j0, d0, t, r) * (PR * PR);
+        float kq[PR * PR];
+#pragma unroll
+        for (int w = 0; w < PR * PR / 4; ++w) {
+          const f32x4 q4 = *reinterpret_cast<const f32x4*>(kb + 4 * w);
+          kq[4 * w] = q4[0];
+          kq[4 * w + 1] = q4[1];
+          kq[4 * w + 2] = q4[2];
+          kq[4 * w + 3] = q4[3];
+        }
         f32x4 in[PR];
 #pragma unroll
         for (int l = 0; l < PR; ++l) in[l] = v[r + l * st];
@@ -195,7 +206,7 @@ __device__ __forceinline__ void fused_radix_pass(const FusedChain& fc, int q, fl
           f32x4 acc = {0.f, 0.f, 0.f, 0.f};
 #pragma unroll
           for (int l = 0; l < PR; ++l) {
-            const float kk = kb[k * PR + l];
+            const float kk = kq[k * PR + l];
             acc[0] = __builtin_fmaf(kk, in[l][0], acc[0]);
             acc[1] = __builtin_fmaf(kk, in[l][1], acc[1]);
             acc[2] = __builtin_fmaf(kk, in[l][2], acc[2]);
