@@ -121,8 +121,8 @@ ks_status_t ks_matmul_bias_act(int64_t a, int64_t b, int64_t c, int64_t d,
 
 /*
  * Bytes of device workspace ks_chain needs for these factors: 0 for a single
- * factor and for chains that run fused (see ks_chain), else one (two factors)
- * or two (more) intermediate buffers.  Returns 0 as well for invalid
+ * factor and for chains that run fused in both layouts (see ks_chain), else
+ * one (two factors) or two (more) intermediate buffers.  Returns 0 as well for invalid
  * arguments; ks_chain reports those.  The answer depends on this thread's
  * ks_force_variant / ks_force_chain_fusion settings, as ks_chain's plan does.
  */
@@ -135,12 +135,15 @@ size_t ks_chain_workspace_bytes(const ks_factor_t *factors, int nfactors,
  * then K_{L-1}, ..., K_1.  Neighbouring factors must satisfy
  *     a_f * c_f * d_f == a_{f+1} * b_{f+1} * d_{f+1}   (KS_ERR_DIM_MISMATCH).
  * X has batch*a_L*c_L*d_L elements and Y batch*a_1*b_1*d_1, both in `layout`.
- * Chains of two to 24 factors whose blocks are at most 8 x 8 and whose widest
- * vector (times 16 batch columns of fp32) fits in 128 KB of LDS -- e.g. the
- * butterfly factors of a transform of size up to 1024 -- run as one fused
- * kernel: each workgroup keeps 16 batch columns of the intermediate vectors
- * in LDS in fp32 from the first factor to the last, so X is read once, Y is
- * written once and no workspace is used.  Other chains run factor by factor
+ * Chains of two to 24 factors whose blocks are all at most 8 x 8 -- e.g. the
+ * butterfly factors of a transform of size up to 1024 -- or, in the
+ * batch-size-first layout, all square b x b with one b in {16, 32, 48, 64} --
+ * e.g. Monarch factors -- and whose widest vector (times 16 batch columns of
+ * fp32, plus the small-block form's factor-value buffer) fits in 160 KB of
+ * LDS, run as one fused kernel: each workgroup keeps 16 batch columns of the
+ * intermediate vectors in LDS in fp32 from the first factor to the last, so X
+ * is read once, Y is written once and no workspace is used.  Other chains run
+ * factor by factor
  * (one ks_matmul each); their intermediates are stored in `dtype` in the
  * caller's `workspace` (device, at least ks_chain_workspace_bytes(...) bytes,
  * not overlapping X or Y).  ks_chain_describe tells which applies.

@@ -6,7 +6,12 @@
 // One workgroup owns a tile of kFusedCols batch columns and keeps the whole
 // intermediate vector of each of its columns in LDS, in fp32, for the whole
 // chain: X is read from HBM once, the factors are applied LDS -> LDS, and Y
-// is written once.
+// is written once.  Two forms: chains of small blocks (b, c <= 8) on the
+// VALU, in radix passes (below, ks_chain_fused.hip), and chains whose blocks
+// are all square with one b in {16, 32, 48, 64} (Monarch factors) on the fp32
+// MFMAs (ks_chain_mfma.hip), one factor per pass, each block's outputs written
+// over its own inputs (the index sets of a square block are the same rows)
+// after the whole block is computed.
 //
 // The factors are applied in passes.  A radix pass applies m >= 1
 // consecutive square factors with p x p blocks (applied order t = 0 .. m-1,
@@ -50,6 +55,7 @@ constexpr int kFusedThreads = 512;                               // threads per 
 constexpr int kFusedKPerThread = 16;                             // factor values fetched per thread and pass
 constexpr int kFusedKValues = kFusedThreads * kFusedKPerThread;  // largest value count of a pass (8192)
 constexpr int kFusedMaxGroup = 8;                                // largest P = p^m of a radix pass
+constexpr int kFusedMfmaMaxB = 64;                               // largest square block of the MFMA form
 
 struct FusedChain {
   int nf;                   // factors, in product order (factor nf-1 is applied first)
@@ -60,6 +66,8 @@ struct FusedChain {
   int buf_rows;             // rows of one LDS buffer (the widest vector)
   int kvec;                 // factor values fetched 4 at a time: every factor's count is a multiple
                             // of 4 and its values are aligned to 4 elements (set at launch)
+  int mfma;                 // 1: square b x b blocks, one b in {16, 32, 48, 64}, on the fp32 MFMAs
+                            // (ks_chain_mfma.hip), one factor per pass, in place, no factor-value copy
   int a[kFusedMaxFactors], b[kFusedMaxFactors], c[kFusedMaxFactors], d[kFusedMaxFactors];
   uint32_t md[kFusedMaxFactors];  // multiply-shift constants of the division by d
   int sd[kFusedMaxFactors];
@@ -148,12 +156,30 @@ __host__ __device__ __forceinline__ void fused_vec_unit(int layout, int E, int u
   }
 }
 
+// Tile of workgroup `block` in a grid of `tiles`: workgroups are dispatched
+// to the 8 XCDs round-robin (block % 8), so each XCD gets a contiguous range
+// of tiles, taken in order; neighbouring tiles then share that XCD's L2.  In
+// the batch-size-last layout a tile's row segments are 16 columns (32 or 64
+// bytes), and the tiles sharing a 128-byte line run on one XCD instead of
+// each fetching the whole line.  A bijection of [0, tiles) for any count.
+__host__ __device__ __forceinline__ int fused_tile(int block, int tiles) {
+  const int q = tiles >> 3, r = tiles & 7, x = block & 7, k = block >> 3;
+  return x * q + (x < r ? x : r) + k;
+}
+
 // LDS layout: the vector buffer(s), then the current pass's factor values.
 __host__ __device__ __forceinline__ int fused_kbuf_offset(const FusedChain& fc) {
   return (fc.inplace ? 1 : 2) * fc.buf_rows * kFusedPitch;  // floats
 }
 __host__ __device__ __forceinline__ int fused_lds_bytes(const FusedChain& fc) {
-  return (fused_kbuf_offset(fc) + kFusedKValues) * 4;
+  return (fused_kbuf_offset(fc) + (fc.mfma ? 0 : kFusedKValues)) * 4;
 }
+
+// MFMA form: every factor has b = c = 16*BT for one BT in 1 .. 4.  Work
+// items of factor f are its a*d blocks, one wavefront each (all b output rows
+// of the block for the tile's 16 columns); block index ij = i*d + j,
+// wavefront w takes ij = w, w + W, ... (W = kFusedThreads / 64).
+__host__ __device__ __forceinline__ int fused_mfma_bt(const FusedChain& fc) { return fc.b[0] / 16; }
+__host__ __device__ __forceinline__ int fused_mfma_blocks(const FusedChain& fc, int f) { return fc.a[f] * fc.d[f]; }
 
 }  // namespace ks

@@ -2,103 +2,20 @@
 //
 // Latency: a workgroup is the only one on its CU for most chain shapes (one
 // tile of 16 columns per CU at batch 4096), so nothing else hides its memory
-// latency.  The tile loads are issued in batches of kFusedLoadBatch 16-byte
-// loads per thread before any of them is used (one batch for a 64 KB tile of
-// fp32 or a 32 KB tile of 16-bit values), and each pass's values are
-// fetched from global memory into registers one pass ahead and parked in the
-// LDS copy after the pass, so the pass loop itself touches only LDS.
+// latency.  The tile loads are batched (ks_chain_fused_io.h), and each pass's
+// values are fetched from global memory into registers one pass ahead and
+// parked in the LDS copy after the pass, so the pass loop itself touches only
+// LDS.  Chains of square 16 .. 64 blocks run in ks_chain_mfma.hip.
 #include <type_traits>
 
 #include "ks_chain_fused.h"
+#include "ks_chain_fused_io.h"
 #include "ks_common.h"
 #include "ks_internal.h"
 
 namespace ks {
 
 namespace {
-
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-constexpr int kFusedLoadBatch = 8;
-
-// Load the tile's input columns into LDS rows [0, width_in) (fp32).
-//  BSL: X is (N, batch); row n of the tile is the run X[n, col0 .. col0+16).
-//  BSF: X is (batch, N); batch row col0+t is the run X[col0+t, 0 .. N).
-// VEC: 16-byte accesses (the host checked alignment and that the batch (BSL)
-// or N (BSF) is a multiple of the vector).  Columns beyond the batch are
-// filled with zeros and never stored.
-template <typename T, int LAYOUT, bool VEC>
-__device__ __forceinline__ void fused_load(const FusedChain& fc, float* lds, int col0) {
-  const T* __restrict__ x = static_cast<const T*>(fc.x);
-  const int N = fc.width_in, B = fc.batch, tid = threadIdx.x;
-  constexpr int E = VEC ? 16 / (int)sizeof(T) : 1;  // elements per access
-  const int total = N * kFusedCols / E;
-  for (int base = 0; base < total; base += kFusedThreads * kFusedLoadBatch) {
-    typedef typename std::conditional<VEC, u32x4, T>::type W;
-    W w[kFusedLoadBatch];
-#pragma unroll
-    for (int r = 0; r < kFusedLoadBatch; ++r) {
-      const int u = base + r * kFusedThreads + tid;
-      int row, col;
-      if constexpr (VEC) fused_vec_unit(LAYOUT, E, u, &row, &col);
-      else if constexpr (LAYOUT == BSL) { row = u / kFusedCols; col = u % kFusedCols; }
-      else { col = u % kFusedCols; row = u / kFusedCols; }
-      const bool ok = u < total && col0 + col < B;
-      const int64_t off = LAYOUT == BSL ? (int64_t)row * B + col0 + col : (int64_t)(col0 + col) * N + row;
-      if constexpr (VEC) w[r] = ok ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(x + off)) : u32x4{0, 0, 0, 0};
-      else w[r] = ok ? x[off] : T(0);
-    }
-#pragma unroll
-    for (int r = 0; r < kFusedLoadBatch; ++r) {
-      const int u = base + r * kFusedThreads + tid;
-      if (u >= total) break;
-      int row, col;
-      if constexpr (VEC) fused_vec_unit(LAYOUT, E, u, &row, &col);
-      else if constexpr (LAYOUT == BSL) { row = u / kFusedCols; col = u % kFusedCols; }
-      else { col = u % kFusedCols; row = u / kFusedCols; }
-      if constexpr (VEC) {
-        const T* e = reinterpret_cast<const T*>(&w[r]);
-        if constexpr (LAYOUT == BSL) {
-#pragma unroll
-          for (int q = 0; q < E; q += 4)
-            *reinterpret_cast<f32x4*>(lds + row * kFusedPitch + col + q) =
-                f32x4{to_f32(e[q]), to_f32(e[q + 1]), to_f32(e[q + 2]), to_f32(e[q + 3])};
-        } else {
-#pragma unroll
-          for (int q = 0; q < E; ++q) lds[(row + q) * kFusedPitch + col] = to_f32(e[q]);
-        }
-      } else {
-        lds[row * kFusedPitch + col] = to_f32(w[r]);
-      }
-    }
-  }
-}
-
-// Store LDS rows [0, width_out) of the tile's valid columns into Y, rounded to
-// the storage type (same layouts and vector rules as fused_load).
-template <typename T, int LAYOUT, bool VEC>
-__device__ __forceinline__ void fused_store(const FusedChain& fc, const float* lds, int col0) {
-  T* __restrict__ y = static_cast<T*>(fc.y);
-  const int M = fc.width_out, B = fc.batch, tid = threadIdx.x;
-  constexpr int E = VEC ? 16 / (int)sizeof(T) : 1;
-  const int total = M * kFusedCols / E;
-  for (int u = tid; u < total; u += kFusedThreads) {
-    int row, col;
-    if constexpr (VEC) fused_vec_unit(LAYOUT, E, u, &row, &col);
-    else if constexpr (LAYOUT == BSL) { row = u / kFusedCols; col = u % kFusedCols; }
-    else { col = u % kFusedCols; row = u / kFusedCols; }
-    if (col0 + col >= B) continue;
-    const int64_t off = LAYOUT == BSL ? (int64_t)row * B + col0 + col : (int64_t)(col0 + col) * M + row;
-    if constexpr (VEC) {
-      union { u32x4 w; T e[E]; } o;
-#pragma unroll
-      for (int q = 0; q < E; ++q)
-        o.e[q] = from_f32<T>(LAYOUT == BSL ? lds[row * kFusedPitch + col + q] : lds[(row + q) * kFusedPitch + col]);
-      __builtin_nontemporal_store(o.w, reinterpret_cast<u32x4*>(y + off));
-    } else {
-      y[off] = from_f32<T>(lds[row * kFusedPitch + col]);
-    }
-  }
-}
 
 // Values of pass q (its factors' packed blocks, one after the other): this
 // thread's share fetched into registers in the storage type (so that no
@@ -304,7 +221,7 @@ __device__ __forceinline__ void fused_radix_apply(const FusedChain& fc, int q, f
 template <typename T, int LAYOUT, bool VEC>
 __global__ __launch_bounds__(kFusedThreads) void ks_chain_fused_kernel(FusedChain fc) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
-  const int col0 = blockIdx.x * kFusedCols;
+  const int col0 = fused_tile((int)blockIdx.x, (int)gridDim.x) * kFusedCols;
   // src holds the current vector; single-factor passes with b != c write dst
   float* src = lds;
   float* dst = fc.inplace ? lds : lds + fc.buf_rows * kFusedPitch;
@@ -360,7 +277,10 @@ hipError_t launch_fused_t(const FusedChain& fc, bool vec, hipStream_t s) {
 
 }  // namespace
 
+hipError_t launch_chain_mfma(const FusedChain& fc, int dtype, bool vec, hipStream_t s);
+
 hipError_t launch_chain_fused(const FusedChain& fc, int dtype, bool vec, hipStream_t s) {
+  if (fc.mfma) return launch_chain_mfma(fc, dtype, vec, s);
   switch (dtype) {
     case F32: return launch_fused_t<float>(fc, vec, s);
     case BF16: return launch_fused_t<bf16_t>(fc, vec, s);

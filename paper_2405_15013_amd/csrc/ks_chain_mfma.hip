@@ -1,0 +1,189 @@
+// Fused chain kernel, MFMA form (ks_chain_fused.h): chains whose factors all
+// have square b x b blocks with one b = 16*BT, BT in 1 .. 4 (Monarch-type
+// chains; paper Section 1 and Appendix B.1).  The workgroup's tile of
+// kFusedCols batch columns stays in LDS in fp32 for the whole chain; each
+// factor is applied in place, one wavefront per block.
+//
+// Block product: v_mfma_f32_16x16x4_f32 in the register-direct operand
+// layout.  Lane (n, g) = (lane % 16, lane / 16) works on column n of the
+// tile; for row tile kt, l-chunk ct and t < 4 it supplies A = K[ij][16kt + n]
+// [16ct + 4g + t] (element t of one 4-value run of the packed block) and B =
+// the tile's value at input row l = 16ct + 4g + t, column n; accumulator r
+// of row tile kt is output k = 16kt + 4g + r.  A block's input and output
+// rows are the same set (b == c), so the wavefront writes its outputs over
+// its inputs once all BT row tiles are accumulated; blocks of one factor use
+// disjoint rows, and a barrier separates the factors.
+//
+// Factor values: each wavefront holds the runs of two blocks in registers
+// (ping-pong) and fetches the next block's while it multiplies the current
+// one; the last block of a factor fetches the first block of the next factor,
+// so its latency overlaps the barrier.
+#include "ks_chain_fused.h"
+#include "ks_chain_fused_io.h"
+#include "ks_common.h"
+#include "ks_internal.h"
+
+namespace ks {
+
+namespace {
+
+// A run of four consecutive factor values in the storage type.
+template <typename T> struct KRun { typedef u32x4 type; };
+template <> struct KRun<bf16_t> { typedef u32x2 type; };
+template <> struct KRun<_Float16> { typedef u32x2 type; };
+
+// Element t (0..3) of a run, as fp32.
+__device__ __forceinline__ float kelem(const u32x4& w, int t, float) { return __uint_as_float(w[t]); }
+__device__ __forceinline__ float kelem(const u32x2& w, int t, bf16_t) {
+  return __uint_as_float(((w[t >> 1] >> (16 * (t & 1))) & 0xffffu) << 16);
+}
+__device__ __forceinline__ float kelem(const u32x2& w, int t, _Float16) {
+  return (float)__builtin_bit_cast(_Float16, (uint16_t)((w[t >> 1] >> (16 * (t & 1))) & 0xffffu));
+}
+
+// This lane's runs of one block (kb = the block's packed b x b values):
+// kr[kt][ct] = K[16kt + n][16ct + 4g .. 16ct + 4g + 3].  KVEC: one 16- or
+// 8-byte load per run (the host checked that the values are aligned to 4
+// elements); else element loads.
+template <typename T, int BT, bool KVEC>
+__device__ __forceinline__ void mfma_kload(typename KRun<T>::type (&kr)[BT][BT], const T* __restrict__ kb, int n,
+                                           int g) {
+  typedef typename KRun<T>::type KW;
+  constexpr int B = 16 * BT;
+#pragma unroll
+  for (int kt = 0; kt < BT; ++kt)
+#pragma unroll
+    for (int ct = 0; ct < BT; ++ct) {
+      const T* src = kb + (16 * kt + n) * B + 16 * ct + 4 * g;
+      if constexpr (KVEC) {
+        kr[kt][ct] = *reinterpret_cast<const KW*>(src);
+      } else {
+        T e[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) e[t] = src[t];
+        __builtin_memcpy(&kr[kt][ct], e, sizeof(KW));
+      }
+    }
+}
+
+// One block, in place: addr is this lane's LDS float index of row
+// in_row(l = 4g) at column n, step the LDS distance of consecutive l (d rows).
+template <typename T, int BT>
+__device__ __forceinline__ void mfma_block(const typename KRun<T>::type (&kr)[BT][BT], float* lds, int addr,
+                                           int step) {
+  f32x4 acc[BT];
+#pragma unroll
+  for (int kt = 0; kt < BT; ++kt) acc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float xv[BT][4];
+#pragma unroll
+  for (int ct = 0; ct < BT; ++ct)
+#pragma unroll
+    for (int t = 0; t < 4; ++t) xv[ct][t] = lds[addr + (16 * ct + t) * step];
+#pragma unroll
+  for (int ct = 0; ct < BT; ++ct)
+#pragma unroll
+    for (int t = 0; t < 4; ++t)
+#pragma unroll
+      for (int kt = 0; kt < BT; ++kt)
+        acc[kt] = __builtin_amdgcn_mfma_f32_16x16x4f32(kelem(kr[kt][ct], t, T()), xv[ct][t], acc[kt], 0, 0, 0);
+  mfma_results_settle();
+#pragma unroll
+  for (int kt = 0; kt < BT; ++kt)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) lds[addr + (16 * kt + r) * step] = acc[kt][r];
+}
+
+template <typename T, int LAYOUT, bool VEC, int BT, bool KVEC>
+__global__ __launch_bounds__(kFusedThreads) void ks_chain_mfma_kernel(FusedChain fc) {
+  extern __shared__ __attribute__((aligned(16))) float lds[];
+  typedef typename KRun<T>::type KW;
+  constexpr int W = kFusedThreads / 64, B = 16 * BT;
+  const int col0 = fused_tile((int)blockIdx.x, (int)gridDim.x) * kFusedCols;
+  const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63, n = lane & 15, g = lane >> 4;
+  // Values of block ij of factor f; an index past the factor's last block is
+  // clamped to it (fetched, not used).  Every fetch is unconditional, so the
+  // count of loads in flight is the same on every path and each wait covers
+  // only the block about to be used.
+  auto kblock = [&](int f, int ij) {
+    const int nb = fused_mfma_blocks(fc, f);
+    return static_cast<const T*>(fc.kv[f]) + (int64_t)(ij < nb ? ij : nb - 1) * (B * B);
+  };
+  // LDS float index of row in_row(4g) of block ij = i*d + j, column n.
+  auto lane_addr = [&](int f, int ij) {
+    const int d = fc.d[f];
+    const int i = (int)div_fast((uint32_t)ij, fc.md[f], fc.sd[f]), j = ij - i * d;
+    return (i * B * d + j + 4 * g * d) * kFusedPitch + n;
+  };
+  KW ka[BT][BT], kb[BT][BT];
+  mfma_kload<T, BT, KVEC>(ka, kblock(fc.nf - 1, w), n, g);
+  fused_load<T, LAYOUT, VEC>(fc, lds, col0);
+  __syncthreads();
+  for (int f = fc.nf - 1; f >= 0; --f) {
+    const int nb = fused_mfma_blocks(fc, f), step = fc.d[f] * kFusedPitch;
+    for (int ij = w; ij < nb; ij += 2 * W) {
+      const int ij1 = ij + W;
+      mfma_kload<T, BT, KVEC>(kb, kblock(f, ij1), n, g);
+      mfma_block<T, BT>(ka, lds, lane_addr(f, ij), step);
+      // the wavefront's next block: ij + 2W of this factor, else its first
+      // block of the next factor
+      const bool here = ij + 2 * W < nb || f == 0;
+      mfma_kload<T, BT, KVEC>(ka, here ? kblock(f, ij + 2 * W) : kblock(f - 1, w), n, g);
+      if (ij1 < nb) mfma_block<T, BT>(kb, lds, lane_addr(f, ij1), step);
+    }
+    if (w >= nb && f > 0) mfma_kload<T, BT, KVEC>(ka, kblock(f - 1, w), n, g);
+    __syncthreads();
+  }
+  fused_store<T, LAYOUT, VEC>(fc, lds, col0);
+}
+
+template <typename T, int BT>
+hipError_t launch_mfma_bt(const FusedChain& fc, bool vec, hipStream_t s) {
+  const dim3 grid((fc.batch + kFusedCols - 1) / kFusedCols), block(kFusedThreads);
+  const int lds = fused_lds_bytes(fc);
+#define KS_MFMA_LAUNCH(L, V, KV)                                                                              \
+  {                                                                                                          \
+    if (lds > 64 * 1024) {                                                                                   \
+      static const hipError_t raised = hipFuncSetAttribute(                                                  \
+          reinterpret_cast<const void*>(&ks_chain_mfma_kernel<T, L, V, BT, KV>),                             \
+          hipFuncAttributeMaxDynamicSharedMemorySize, kFusedMaxLds);                                         \
+      if (raised != hipSuccess) return raised;                                                               \
+    }                                                                                                        \
+    hipLaunchKernelGGL((ks_chain_mfma_kernel<T, L, V, BT, KV>), grid, block, lds, s, fc);                    \
+    return hipGetLastError();                                                                                \
+  }
+#define KS_MFMA_LAUNCH_KV(L, V)                                                                               \
+  {                                                                                                          \
+    if (fc.kvec) KS_MFMA_LAUNCH(L, V, true) else KS_MFMA_LAUNCH(L, V, false)                                 \
+  }
+  if (fc.layout == BSL) {
+    if (vec) KS_MFMA_LAUNCH_KV(BSL, true) else KS_MFMA_LAUNCH_KV(BSL, false)
+  }
+  if (vec) KS_MFMA_LAUNCH_KV(BSF, true) else KS_MFMA_LAUNCH_KV(BSF, false)
+#undef KS_MFMA_LAUNCH_KV
+#undef KS_MFMA_LAUNCH
+}
+
+template <typename T>
+hipError_t launch_mfma_t(const FusedChain& fc, bool vec, hipStream_t s) {
+  switch (fused_mfma_bt(fc)) {
+    case 1: return launch_mfma_bt<T, 1>(fc, vec, s);
+    case 2: return launch_mfma_bt<T, 2>(fc, vec, s);
+    case 3: return launch_mfma_bt<T, 3>(fc, vec, s);
+    case 4: return launch_mfma_bt<T, 4>(fc, vec, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_chain_mfma(const FusedChain& fc, int dtype, bool vec, hipStream_t s) {
+  switch (dtype) {
+    case F32: return launch_mfma_t<float>(fc, vec, s);
+    case BF16: return launch_mfma_t<bf16_t>(fc, vec, s);
+    case F16: return launch_mfma_t<_Float16>(fc, vec, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+}  // namespace ks

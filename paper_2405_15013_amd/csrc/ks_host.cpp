@@ -347,22 +347,33 @@ namespace ks {
 void set_last_hip_error(int e) { g_last_hip_error = e; }
 
 // The fused chain kernel (ks_chain_fused.h) takes chains of two or more
-// factors whose blocks are at most 8 x 8 and whose widest vector, for 16
-// batch columns in fp32, fits the kernel's 160 KB of LDS next to one pass's
-// factor values (in place when every factor has b == c, else two buffers).  Not used while a kernel variant is forced or
-// fusion is switched off on this thread.  Fills the pattern part of `fc`.
+// factors whose blocks are all at most 8 x 8, or all square with one b = c
+// in {16, 32, 48, 64} (the MFMA form, batch-size-first), and whose widest
+// vector, for 16
+// batch columns in fp32, fits the kernel's 160 KB of LDS (next to one pass's
+// factor values for small blocks; in place when every factor has b == c,
+// else two buffers).  Not used while a kernel variant is forced or fusion is
+// switched off on this thread.  Fills the pattern part of `fc`.
 bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, int dtype, FusedChain* fc) {
   if (g_forced_variant >= 0 || g_chain_fusion == 0) return false;
   if (n < 2 || n > kFusedMaxFactors) return false;
   int64_t wmax = 0;
-  bool inplace = true;
+  bool inplace = true, small = true, square16 = true;
   for (int q = 0; q < n; ++q) {
-    if (f[q].b > kFusedMaxBC || f[q].c > kFusedMaxBC) return false;
+    small = small && f[q].b <= kFusedMaxBC && f[q].c <= kFusedMaxBC;
+    square16 = square16 && f[q].b == f[q].c && f[q].b == f[0].b && f[q].b % 16 == 0 && f[q].b <= kFusedMfmaMaxB;
     const int64_t N = f[q].a * f[q].c * f[q].d, M = f[q].a * f[q].b * f[q].d;
     wmax = std::max(wmax, std::max(N, M));
     inplace = inplace && f[q].b == f[q].c;
   }
-  if (((inplace ? 1 : 2) * wmax * kFusedPitch + kFusedKValues) * 4 > kFusedMaxLds) return false;
+  if (!small && !square16) return false;
+  // The MFMA form runs batch-size-first only: its tile of 16 batch columns
+  // is a contiguous run of X and Y there, but in the batch-size-last layout
+  // it is one 32- or 64-byte piece of every row, which the factor-by-factor
+  // kernels (long runs along the batch) read and write faster.
+  if (!small && layout != KS_LAYOUT_BSF) return false;
+  const int64_t kbuf = small ? kFusedKValues : 0;
+  if (((inplace ? 1 : 2) * wmax * kFusedPitch + kbuf) * 4 > kFusedMaxLds) return false;
   if ((batch + kFusedCols - 1) / kFusedCols > 0x7fffffff) return false;
   fc->nf = n;
   fc->batch = (int)batch;
@@ -372,10 +383,25 @@ bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, in
   fc->inplace = inplace ? 1 : 0;
   fc->buf_rows = (int)wmax;
   fc->kvec = 0;  // set at launch (chain_fused_kvec)
+  fc->mfma = small ? 0 : 1;
   for (int q = 0; q < n; ++q) {
     fc->a[q] = (int)f[q].a; fc->b[q] = (int)f[q].b; fc->c[q] = (int)f[q].c; fc->d[q] = (int)f[q].d;
     div_magic((uint32_t)f[q].d, &fc->md[q], &fc->sd[q]);
     fc->kv[q] = f[q].K_values;
+  }
+  if (fc->mfma) {
+    // One pass per factor; the values are read straight from global memory.
+    for (int q = 0; q < n; ++q) {
+      const int f0 = n - 1 - q;
+      fc->pf0[q] = f0;
+      fc->pm[q] = 1;
+      fc->pp[q] = 0;
+      fc->pP[q] = 1;
+      fc->pcnt[q] = fc->pk[q] = fc->a[f0] * fc->d[f0] * fc->b[f0] * fc->c[f0];
+      div_magic((uint32_t)fc->d[f0], &fc->mgd[q], &fc->sgd[q]);
+    }
+    fc->npass = n;
+    return fused_lds_bytes(*fc) <= kFusedMaxLds;
   }
   // Passes in application order (factor n-1 first): runs of square p x p
   // factors (p in {2, 4, 8}) whose strides nest (d of the next = p * d,
@@ -526,7 +552,10 @@ size_t ks_chain_workspace_bytes(const ks_factor_t* factors, int nfactors, int64_
   if (chain_check(factors, nfactors, batch, dtype, &per) != KS_OK) return 0;
   if (nfactors <= 1) return 0;
   FusedChain fc;
-  if (chain_fused_plan(factors, nfactors, batch, KS_LAYOUT_BSL, dtype, &fc)) return 0;  // layout-independent
+  // the workspace of the layout that needs one (the size does not depend on the layout)
+  if (chain_fused_plan(factors, nfactors, batch, KS_LAYOUT_BSL, dtype, &fc) &&
+      chain_fused_plan(factors, nfactors, batch, KS_LAYOUT_BSF, dtype, &fc))
+    return 0;
   return nfactors == 2 ? per : 2 * per;
 }
 
@@ -548,8 +577,8 @@ ks_status_t ks_chain_describe(const ks_factor_t* factors, int nfactors, int64_t 
       snprintf(pb, sizeof pb, "%s%d", q ? "," : "", fc.pp[q] ? fc.pP[q] : -fc.b[fc.pf0[q]]);
       passes += pb;
     }
-    snprintf(buf, len, "fused factors=%d passes=%d groups=%s inplace=%d lds=%d grid=%lld block=%d cols=%d",
-             fc.nf, fc.npass, passes.c_str(), fc.inplace, fused_lds_bytes(fc),
+    snprintf(buf, len, "fused%s factors=%d passes=%d groups=%s inplace=%d lds=%d grid=%lld block=%d cols=%d",
+             fc.mfma ? "-mfma" : "", fc.nf, fc.npass, passes.c_str(), fc.inplace, fused_lds_bytes(fc),
              (long long)((batch + kFusedCols - 1) / kFusedCols), kFusedThreads, kFusedCols);
   } else {
     snprintf(buf, len, "unfused factors=%d workspace=%zu", nfactors, nfactors <= 1 ? (size_t)0 : (nfactors == 2 ? per : 2 * per));

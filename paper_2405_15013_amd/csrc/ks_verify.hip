@@ -726,8 +726,86 @@ bool verify_fused_io(FusedChecker& ck, const FusedChain& fc, int width, int E, b
   return ck.err.empty();
 }
 
+// MFMA form (ks_chain_mfma.hip): the kernel applies factor nf-1 .. 0, one per
+// pass; wavefront w of W takes blocks w, w + W, ...; lane (n, g) reads the
+// 4-value runs K[ij][16kt + n][16ct + 4g ..] and the LDS rows
+// in_row(16ct + 4g + t), writes rows out_row(16kt + 4g + r), all at column n
+// (the kernel addresses them as in_row(4g) plus multiples of d).  Replays
+// every wavefront's blocks and every lane's accesses.
+bool verify_fused_mfma(FusedChecker& ck, const FusedChain& fc) {
+  constexpr int W = kFusedThreads / 64;
+  if (!fc.inplace) return ck.fail("MFMA form not in place", 0);
+  for (int f = fc.nf - 1; f >= 0; --f) {
+    const int a = fc.a[f], b = fc.b[f], d = fc.d[f];
+    if (b != fc.c[f] || b % 16 || b < 16 || b > kFusedMfmaMaxB) return ck.fail("MFMA form block not square 16..64", f);
+    if (b != 16 * fused_mfma_bt(fc)) return ck.fail("MFMA form blocks of different sizes", f);
+    const int BT = b / 16, nblk = fused_mfma_blocks(fc, f), width = a * b * d;
+    if (nblk != a * d) return ck.fail("MFMA block count", f);
+    const int64_t kcount = (int64_t)a * d * b * b;
+    std::vector<uint8_t> blk(nblk, 0), cover((size_t)width * kFusedCols, 0);
+    std::vector<uint8_t> kcov((size_t)kcount, 0);
+    for (int w = 0; w < W; ++w) {
+      for (int ij = w; ij < nblk; ij += W) {
+        blk[ij]++;
+        const int i = (int)div_fast((uint32_t)ij, fc.md[f], fc.sd[f]), j = ij - i * d;
+        if (i != ij / d || j < 0 || j >= d) return ck.fail("MFMA block decode", ij);
+        std::vector<int> rin, rout;
+        for (int lane = 0; lane < 64; ++lane) {
+          const int n = lane & 15, g = lane >> 4;
+          for (int kt = 0; kt < BT; ++kt)
+            for (int ct = 0; ct < BT; ++ct) {
+              const int64_t off = (int64_t)ij * b * b + (16 * kt + n) * b + 16 * ct + 4 * g;
+              if (off % 4) return ck.fail("MFMA K run not aligned to 4 values", off);
+              if (off < 0 || off + 4 > kcount) return ck.fail("MFMA K read out of range", off);
+              for (int t = 0; t < 4; ++t) kcov[(size_t)(off + t)]++;
+            }
+          // the kernel's addressing: row in_row(4g) plus (16ct + t) * d
+          const int lane_row = i * b * d + j + 4 * g * d;
+          for (int ct = 0; ct < BT; ++ct)
+            for (int t = 0; t < 4; ++t) {
+              const int r = fused_in_row(fc, f, i, j, 16 * ct + 4 * g + t);
+              if (r != lane_row + (16 * ct + t) * d) return ck.fail("MFMA lane row is not the input row", r);
+              if (r < 0 || r >= width || r >= fc.buf_rows) return ck.fail("MFMA input row out of range", r);
+              if (n == 0) rin.push_back(r);
+            }
+          for (int kt = 0; kt < BT; ++kt)
+            for (int r4 = 0; r4 < 4; ++r4) {
+              const int r = fused_out_row(fc, f, i, j, 16 * kt + 4 * g + r4);
+              if (r != lane_row + (16 * kt + r4) * d) return ck.fail("MFMA lane row is not the output row", r);
+              if (r < 0 || r >= width || r >= fc.buf_rows) return ck.fail("MFMA output row out of range", r);
+              cover[(size_t)r * kFusedCols + n]++;
+              if (n == 0) rout.push_back(r);
+            }
+        }
+        std::sort(rin.begin(), rin.end());
+        std::sort(rout.begin(), rout.end());
+        if (rin != rout || (int)rin.size() != b) return ck.fail("MFMA block writes rows it does not read", ij);
+      }
+    }
+    for (int q = 0; q < nblk; ++q)
+      if (blk[q] != 1) return ck.fail("MFMA block not taken exactly once", q);
+    for (size_t e = 0; e < cover.size(); ++e)
+      if (cover[e] != 1) return ck.fail("MFMA factor output not written exactly once", (int64_t)e);
+    // Each lane reads every K run of its row tiles once per block; over the
+    // 64 lanes and BT x BT tiles that is each value exactly once.
+    for (size_t e = 0; e < kcov.size(); ++e)
+      if (kcov[e] != 1) return ck.fail("MFMA factor value not read exactly once", (int64_t)e);
+  }
+  return ck.err.empty();
+}
+
 bool verify_fused(FusedChecker& ck, const FusedChain& fc, int dtype) {
   const int esize = dtype == F32 ? 4 : 2, E = 16 / esize;
+  // Workgroup -> tile order: a bijection of the grid.
+  {
+    const int tiles = (int)(((int64_t)fc.batch + kFusedCols - 1) / kFusedCols);
+    std::vector<uint8_t> seen(tiles, 0);
+    for (int b = 0; b < tiles; ++b) {
+      const int t = fused_tile(b, tiles);
+      if (t < 0 || t >= tiles) return ck.fail("workgroup tile out of range", b);
+      if (seen[t]++) return ck.fail("tile taken by two workgroups", t);
+    }
+  }
   // Widths along the chain: input of factor nf-1 ... output of factor 0.
   for (int f = 0; f + 1 < fc.nf; ++f)
     if (fc.a[f] * fc.c[f] * fc.d[f] != fc.a[f + 1] * fc.b[f + 1] * fc.d[f + 1]) return ck.fail("widths", f);
@@ -758,11 +836,13 @@ bool verify_fused(FusedChecker& ck, const FusedChain& fc, int dtype) {
         if (fc.a[f] * fc.b[f] * fc.c[f] * fc.d[f] != fc.pcnt[q]) return ck.fail("pass value count", q);
         kn += fc.pcnt[q];
       }
-      if (kn != fc.pk[q] || kn > kFusedKValues) return ck.fail("pass values exceed the LDS copy", q);
+      if (kn != fc.pk[q] || (!fc.mfma && kn > kFusedKValues)) return ck.fail("pass values exceed the LDS copy", q);
+      if (fc.mfma && fc.pm[q] != 1) return ck.fail("MFMA form pass with several factors", q);
       next -= fc.pm[q];
     }
     if (next != -1) return ck.fail("passes do not cover the chain", next);
   }
+  if (fc.mfma) return verify_fused_mfma(ck, fc);
   for (int q = 0; q < fc.npass; ++q) {
     if (fused_is_radix(fc, q)) {
       // Radix pass: every unit's P rows in range, the groups partition the

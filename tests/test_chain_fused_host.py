@@ -24,6 +24,12 @@ CHAINS = {
     "radix4": [(1, 4, 4, 16), (4, 4, 4, 4), (16, 4, 4, 1)],
     "mixed": [(4, 8, 8, 2), (8, 2, 2, 4), (2, 4, 3, 8), (6, 4, 4, 2)],
     "wide_inplace": [(1, 2, 2, 1024), (1024, 2, 2, 1)],            # width 2048: 160 KB of LDS, not fused
+    # square blocks of one size in {16, 32, 48, 64}: the MFMA form
+    "monarch1024": [(1, 32, 32, 32), (32, 32, 32, 1)],
+    "monarch256": [(1, 16, 16, 16), (16, 16, 16, 1)],
+    "square48": [(16, 48, 48, 1), (1, 48, 48, 16), (4, 48, 48, 4)],
+    "square64": [(2, 64, 64, 8), (16, 64, 64, 1)],
+    "square_wide": [(1, 16, 16, 128), (128, 16, 16, 1)],           # width 2048: 160 KB, one buffer
 }
 
 
@@ -38,8 +44,11 @@ def test_fused_chain_replay(name, layout, dtype, batch):
     assert st == 0, (desc, rep)
     if desc.startswith("fused"):
         assert rep == "ok"
+        assert desc.startswith("fused-mfma") == name.startswith(("monarch", "square"))
     else:
         assert rep == "not fused"
+    if name.startswith(("monarch", "square")):
+        assert desc.startswith("fused-mfma" if layout == "bsf" else "unfused"), desc
 
 
 def test_which_chains_fuse():
@@ -48,10 +57,24 @@ def test_which_chains_fuse():
         for dtype in ("f32", "bf16"):
             assert ks.ks_chain_describe(bf, 4096, layout, dtype).startswith("fused")
             assert ks.ks_chain_workspace_bytes(bf, 4096, dtype) == 0
-    # Monarch factors (32 x 32 blocks) run factor by factor
+    # Monarch factors (32 x 32 blocks) run fused on the MFMAs, in one LDS
+    # buffer, batch-size-first; batch-size-last factor by factor
     mon = factors([(1, 32, 32, 32), (32, 32, 32, 1)])
-    assert ks.ks_chain_describe(mon, 16384, "bsl", "f32").startswith("unfused")
-    assert ks.ks_chain_workspace_bytes(mon, 16384, "f32") == 1024 * 16384 * 4
+    for dtype in ("f32", "bf16", "f16"):
+        desc = ks.ks_chain_describe(mon, 16384, "bsf", dtype)
+        assert desc.startswith("fused-mfma ") and "inplace=1" in desc and "lds=81920 " in desc, desc
+        assert ks.ks_chain_describe(mon, 16384, "bsl", dtype).startswith("unfused")
+        # the workspace query has no layout: the batch-size-last run needs one
+        assert ks.ks_chain_workspace_bytes(mon, 16384, dtype) == 1024 * 16384 * (4 if dtype == "f32" else 2)
+    # blocks that are not all square of one size in {16, 32, 48, 64}, or that
+    # mix small and large blocks, run factor by factor
+    for pats in ([(1, 32, 16, 32), (32, 16, 32, 1)], [(1, 96, 96, 8), (8, 96, 96, 1)],
+                 [(1, 24, 24, 8), (8, 24, 24, 1)], [(1, 32, 32, 4), (16, 2, 2, 4)],
+                 [(2, 64, 64, 8), (16, 64, 64, 1), (4, 16, 16, 16)]):
+        assert ks.ks_chain_describe(factors(pats), 256, "bsf", "f32").startswith("unfused"), pats
+    # MFMA form of width 4096 needs 320 KB of LDS: not fused
+    assert ks.ks_chain_describe(factors([(1, 64, 64, 64), (64, 64, 64, 1)]), 64, "bsf", "f32").startswith("unfused")
+    assert ks.ks_chain_describe(factors(CHAINS["square_wide"]), 64, "bsf", "f32").startswith("fused-mfma")
     # width 2048 with 16 fp32 columns needs 160 KB of LDS: not fused
     assert ks.ks_chain_describe(factors(CHAINS["wide_inplace"]), 64, "bsl", "f32").startswith("unfused")
     # a single factor is not a chain to fuse

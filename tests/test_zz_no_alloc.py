@@ -61,5 +61,12 @@ def test_noalloc_rejects_chains_beyond_the_scratch_size():
     import torch
     kds = [torch.zeros(p[0] * p[1] * p[2] * p[3], device="cuda") for p in MONARCH]
     batch = 32768  # one intermediate of 128 MiB
-    st = ks.ks_chain_noalloc(list(zip(MONARCH, kds)), 1 << 40, 2 << 40, batch, "bsl", "f32", check=False)
+    # factor by factor (the fused Monarch chain needs no intermediates), so the
+    # call is rejected before any launch
+    ks.ks_force_chain_fusion(0)
+    try:
+        assert ks.ks_chain_workspace_bytes(list(zip(MONARCH, kds)), batch, "f32") == 128 << 20
+        st = ks.ks_chain_noalloc(list(zip(MONARCH, kds)), 1 << 40, 2 << 40, batch, "bsl", "f32", check=False)
+    finally:
+        ks.ks_force_chain_fusion(None)
     assert ks.STATUS_NAMES[st] == "KS_ERR_SCRATCH_LIMIT"
