@@ -103,7 +103,7 @@ KERNEL_FAMILY_SOURCES = {
     "ks_dma_kernel": "ks_dma_", "ks_direct_c_kernel": "ks_direct_", "ks_direct_kernel": "ks_direct_",
     "ks_staged_kernel": "ks_staged_", "ks_masked_kernel": "ks_masked_", "ks_fp8_kernel": "ks_fp8",
     "ks_valu_bsl_kernel": "ks_valu", "ks_valu_bsf_kernel": "ks_valu", "ks_generic_kernel": "ks_generic",
-    "ks_chain_fused_kernel": "ks_chain_fused", "ks_chain_mfma_kernel": "ks_chain_mfma",
+    "ks_chain_fused_kernel": "ks_chain_fused", "ks_chain_mfma_kernel": "ks_chain_mfma", "ks_chain_bfly_kernel": "ks_chain_bfly",
 }
 KERNEL_FAMILY_PLANNERS = {"ks_dma_": "ks_staged_plan.cpp", "ks_staged_": "ks_staged_plan.cpp",
                           "ks_direct_": "ks_direct_plan.cpp", "ks_masked_": "ks_direct_plan.cpp"}

@@ -186,8 +186,10 @@ ks_status_t ks_chain_noalloc(const ks_factor_t *factors, int nfactors,
 size_t ks_chain_noalloc_max_workspace(void);
 
 /*
- * How ks_chain would run these arguments: writes "fused ..." (one kernel;
- * LDS bytes, grid) or "unfused ... workspace=<bytes>" into `buf` (host, `len`
+ * How ks_chain would run these arguments: writes "fused ..." (one kernel:
+ * "fused" radix passes of small blocks, "fused-bfly" the dyadic butterfly in
+ * two register passes, "fused-mfma" square blocks on the MFMAs; LDS bytes,
+ * grid) or "unfused ... workspace=<bytes>" into `buf` (host, `len`
  * bytes, NUL-terminated).  Pure host call.  Returns KS_OK or the status
  * ks_chain would return for invalid factors, dtype or layout.
  */

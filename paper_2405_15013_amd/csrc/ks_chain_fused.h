@@ -68,6 +68,8 @@ struct FusedChain {
                             // of 4 and its values are aligned to 4 elements (set at launch)
   int mfma;                 // 1: square b x b blocks, one b in {16, 32, 48, 64}, on the fp32 MFMAs
                             // (ks_chain_mfma.hip), one factor per pass, in place, no factor-value copy
+  int bfly;                 // L >= 2: the chain is the dyadic butterfly of size N = 2^L <= 1024
+                            // (ks_chain_bfly.hip, two register passes); 0 otherwise
   int a[kFusedMaxFactors], b[kFusedMaxFactors], c[kFusedMaxFactors], d[kFusedMaxFactors];
   uint32_t md[kFusedMaxFactors];  // multiply-shift constants of the division by d
   int sd[kFusedMaxFactors];
@@ -167,11 +169,34 @@ __host__ __device__ __forceinline__ int fused_tile(int block, int tiles) {
   return x * q + (x < r ? x : r) + k;
 }
 
+// Butterfly form (ks_chain_bfly.hip): the chain is K_1 ... K_L with K_l of
+// pattern (2^(l-1), 2, 2, 2^(L-l)), N = 2^L (paper Section 1 and Figure 1:
+// the butterfly factors of a fast transform).  In application order factor
+// s = L - l has d = 2^s, and its 2 x 2 block (i, j) mixes rows
+// R = i*2d + j and R + d (Section 4.1 index sets with b = c = 2).  The L
+// factors are split in two register passes: pass A applies s < LA = ceil(L/2)
+// to groups of PA = 2^LA consecutive rows, pass B applies the rest to groups
+// of PB = 2^(L-LA) rows j + PA*r.  A unit is (group, one batch column), so a
+// pass has 16*N/P units; N <= 1024 keeps both at most 512 (one per thread).
+__host__ __device__ __forceinline__ int bfly_la(int L) { return (L + 1) / 2; }
+// Block of factor s (d = 2^s) that holds row R, and whether R is its second row.
+__host__ __device__ __forceinline__ int bfly_block(int R, int s) {
+  return (R >> (s + 1)) * (1 << s) + (R & ((1 << s) - 1));
+}
+// LDS row of vector row R (16 floats per row): rows of one pass-A group lie
+// PA apart and rows of one pass-B group are consecutive across a wavefront,
+// so XOR-ing the low two bits with (R >> LA) puts the four groups a wavefront
+// touches in four different bank windows in both passes.
+__host__ __device__ __forceinline__ int bfly_lds_row(int R, int la) { return R ^ ((R >> la) & 3); }
+// LDS floats: the vector, N rows of 16 (the factor values stay in registers).
+__host__ __device__ __forceinline__ int bfly_lds_floats(int N) { return N * 16; }
+
 // LDS layout: the vector buffer(s), then the current pass's factor values.
 __host__ __device__ __forceinline__ int fused_kbuf_offset(const FusedChain& fc) {
   return (fc.inplace ? 1 : 2) * fc.buf_rows * kFusedPitch;  // floats
 }
 __host__ __device__ __forceinline__ int fused_lds_bytes(const FusedChain& fc) {
+  if (fc.bfly) return bfly_lds_floats(fc.width_in) * 4;
   return (fused_kbuf_offset(fc) + (fc.mfma ? 0 : kFusedKValues)) * 4;
 }
 

@@ -278,9 +278,11 @@ hipError_t launch_fused_t(const FusedChain& fc, bool vec, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_chain_mfma(const FusedChain& fc, int dtype, bool vec, hipStream_t s);
+hipError_t launch_chain_bfly(const FusedChain& fc, int dtype, bool vec, hipStream_t s);
 
 hipError_t launch_chain_fused(const FusedChain& fc, int dtype, bool vec, hipStream_t s) {
   if (fc.mfma) return launch_chain_mfma(fc, dtype, vec, s);
+  if (fc.bfly) return launch_chain_bfly(fc, dtype, vec, s);
   switch (dtype) {
     case F32: return launch_fused_t<float>(fc, vec, s);
     case BF16: return launch_fused_t<bf16_t>(fc, vec, s);

@@ -16,14 +16,20 @@ namespace ks {
 
 constexpr int kFusedLoadBatch = 8;
 
+// LDS float index of (row, column) of the tile: rows at kFusedPitch floats.
+// The butterfly form passes its own map (16 floats per row, rows swizzled).
+struct FusedPitchAddr {
+  __device__ __forceinline__ int operator()(int row, int col) const { return row * kFusedPitch + col; }
+};
+
 // Load the tile's input columns into LDS rows [0, width_in) (fp32).
 //  BSL: X is (N, batch); row n of the tile is the run X[n, col0 .. col0+16).
 //  BSF: X is (batch, N); batch row col0+t is the run X[col0+t, 0 .. N).
 // VEC: 16-byte accesses (the host checked alignment and that the batch (BSL)
 // or N (BSF) is a multiple of the vector).  Columns beyond the batch are
 // filled with zeros and never stored.
-template <typename T, int LAYOUT, bool VEC>
-__device__ __forceinline__ void fused_load(const FusedChain& fc, float* lds, int col0) {
+template <typename T, int LAYOUT, bool VEC, typename A = FusedPitchAddr>
+__device__ __forceinline__ void fused_load(const FusedChain& fc, float* lds, int col0, A at = A()) {
   const T* __restrict__ x = static_cast<const T*>(fc.x);
   const int N = fc.width_in, B = fc.batch, tid = threadIdx.x;
   constexpr int E = VEC ? 16 / (int)sizeof(T) : 1;  // elements per access
@@ -56,14 +62,14 @@ __device__ __forceinline__ void fused_load(const FusedChain& fc, float* lds, int
         if constexpr (LAYOUT == BSL) {
 #pragma unroll
           for (int q = 0; q < E; q += 4)
-            *reinterpret_cast<f32x4*>(lds + row * kFusedPitch + col + q) =
+            *reinterpret_cast<f32x4*>(lds + at(row, col + q)) =
                 f32x4{to_f32(e[q]), to_f32(e[q + 1]), to_f32(e[q + 2]), to_f32(e[q + 3])};
         } else {
 #pragma unroll
-          for (int q = 0; q < E; ++q) lds[(row + q) * kFusedPitch + col] = to_f32(e[q]);
+          for (int q = 0; q < E; ++q) lds[at(row + q, col)] = to_f32(e[q]);
         }
       } else {
-        lds[row * kFusedPitch + col] = to_f32(w[r]);
+        lds[at(row, col)] = to_f32(w[r]);
       }
     }
   }
@@ -71,8 +77,8 @@ __device__ __forceinline__ void fused_load(const FusedChain& fc, float* lds, int
 
 // Store LDS rows [0, width_out) of the tile's valid columns into Y, rounded to
 // the storage type (same layouts and vector rules as fused_load).
-template <typename T, int LAYOUT, bool VEC>
-__device__ __forceinline__ void fused_store(const FusedChain& fc, const float* lds, int col0) {
+template <typename T, int LAYOUT, bool VEC, typename A = FusedPitchAddr>
+__device__ __forceinline__ void fused_store(const FusedChain& fc, const float* lds, int col0, A at = A()) {
   T* __restrict__ y = static_cast<T*>(fc.y);
   const int M = fc.width_out, B = fc.batch, tid = threadIdx.x;
   constexpr int E = VEC ? 16 / (int)sizeof(T) : 1;
@@ -88,10 +94,10 @@ __device__ __forceinline__ void fused_store(const FusedChain& fc, const float* l
       union { u32x4 w; T e[E]; } o;
 #pragma unroll
       for (int q = 0; q < E; ++q)
-        o.e[q] = from_f32<T>(LAYOUT == BSL ? lds[row * kFusedPitch + col + q] : lds[(row + q) * kFusedPitch + col]);
+        o.e[q] = from_f32<T>(LAYOUT == BSL ? lds[at(row, col + q)] : lds[at(row + q, col)]);
       __builtin_nontemporal_store(o.w, reinterpret_cast<u32x4*>(y + off));
     } else {
-      y[off] = from_f32<T>(lds[row * kFusedPitch + col]);
+      y[off] = from_f32<T>(lds[at(row, col)]);
     }
   }
 }

@@ -384,6 +384,15 @@ bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, in
   fc->buf_rows = (int)wmax;
   fc->kvec = 0;  // set at launch (chain_fused_kvec)
   fc->mfma = small ? 0 : 1;
+  // the dyadic butterfly of size 2^L, L = 4 .. 10: factor q of pattern
+  // (2^q, 2, 2, 2^(L-1-q)) in product order
+  fc->bfly = 0;
+  if (small && n >= 4 && n <= 10) {
+    bool bf = true;
+    for (int q = 0; q < n && bf; ++q)
+      bf = f[q].b == 2 && f[q].c == 2 && f[q].a == ((int64_t)1 << q) && f[q].d == ((int64_t)1 << (n - 1 - q));
+    if (bf) fc->bfly = n;
+  }
   for (int q = 0; q < n; ++q) {
     fc->a[q] = (int)f[q].a; fc->b[q] = (int)f[q].b; fc->c[q] = (int)f[q].c; fc->d[q] = (int)f[q].d;
     div_magic((uint32_t)f[q].d, &fc->md[q], &fc->sd[q]);
@@ -577,8 +586,10 @@ ks_status_t ks_chain_describe(const ks_factor_t* factors, int nfactors, int64_t 
       snprintf(pb, sizeof pb, "%s%d", q ? "," : "", fc.pp[q] ? fc.pP[q] : -fc.b[fc.pf0[q]]);
       passes += pb;
     }
+    if (fc.bfly) passes = std::to_string(1 << bfly_la(fc.bfly)) + "," + std::to_string(1 << (fc.bfly - bfly_la(fc.bfly)));
     snprintf(buf, len, "fused%s factors=%d passes=%d groups=%s inplace=%d lds=%d grid=%lld block=%d cols=%d",
-             fc.mfma ? "-mfma" : "", fc.nf, fc.npass, passes.c_str(), fc.inplace, fused_lds_bytes(fc),
+             fc.mfma ? "-mfma" : (fc.bfly ? "-bfly" : ""), fc.nf, fc.bfly ? 2 : fc.npass, passes.c_str(), fc.inplace,
+             fused_lds_bytes(fc),
              (long long)((batch + kFusedCols - 1) / kFusedCols), kFusedThreads, kFusedCols);
   } else {
     snprintf(buf, len, "unfused factors=%d workspace=%zu", nfactors, nfactors <= 1 ? (size_t)0 : (nfactors == 2 ? per : 2 * per));

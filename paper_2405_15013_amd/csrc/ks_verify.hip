@@ -794,6 +794,69 @@ bool verify_fused_mfma(FusedChecker& ck, const FusedChain& fc) {
   return ck.err.empty();
 }
 
+// Butterfly form (ks_chain_bfly.hip; its tile load and store are the shared
+// ones, replayed by verify_fused): the chain's patterns, which lane of a row
+// fetches each block, the kernel's block formulas against the index-set
+// definition (each block of each factor applied exactly once per column), and
+// the LDS row map.
+bool verify_fused_bfly(FusedChecker& ck, const FusedChain& fc, int dtype) {
+  const int L = fc.bfly, LA = bfly_la(L), LB = L - LA, PA = 1 << LA, PB = 1 << LB, N = PA * PB;
+  (void)dtype;
+  if (fc.nf != L || fc.width_in != N || fc.width_out != N) return ck.fail("butterfly widths", L);
+  for (int q = 0; q < L; ++q)
+    if (fc.b[q] != 2 || fc.c[q] != 2 || fc.a[q] != (1 << q) || fc.d[q] != (1 << (L - 1 - q)))
+      return ck.fail("factor is not the butterfly pattern", q);
+  if (16 * PA > kFusedThreads || 16 * PB > kFusedThreads) return ck.fail("butterfly too wide for one unit per thread", N);
+  if (bfly_lds_floats(N) * 4 != fused_lds_bytes(fc) || fused_lds_bytes(fc) > kFusedMaxLds)
+    return ck.fail("butterfly LDS", fused_lds_bytes(fc));
+  // factor blocks fetched by lane i of a unit's row: pass A block u*PA/2 + i,
+  // pass B block j + block(PA*r_i) with r_i the i-th r whose bit t is clear;
+  // the butterfly of r reads lane block(r) (A) or its rank among those r (B)
+  for (int s = 0; s < L; ++s) {
+    const int t = s - LA;
+    for (int r = 0; r < (s < LA ? PA : PB); ++r) {
+      if (s < LA ? (r & (1 << s)) : (r & (1 << t))) continue;
+      const int lanei = s < LA ? bfly_block(r, s) : (((r >> (t + 1)) << t) | (r & ((1 << t) - 1)));
+      if (lanei < 0 || lanei >= 16 || lanei >= (s < LA ? PA : PB) / 2) return ck.fail("block lane out of range", lanei);
+      if (s >= LA) {
+        const int ri = ((lanei >> t) << (t + 1)) | (lanei & ((1 << t) - 1));
+        if (ri != r) return ck.fail("pass B block lane does not hold the block of r", r);
+      }
+    }
+  }
+  // LDS row map: a bijection of [0, N)
+  {
+    std::vector<uint8_t> seen(N, 0);
+    for (int R = 0; R < N; ++R) {
+      const int p = bfly_lds_row(R, LA);
+      if (p < 0 || p >= N || seen[p]++) return ck.fail("LDS row map not a bijection", R);
+    }
+  }
+  // blocks of every factor: once per column (n is a column; every column
+  // runs the same units, so one column is replayed)
+  std::vector<std::vector<uint8_t>> used(L, std::vector<uint8_t>(N / 2, 0));
+  auto check_pair = [&](int R, int s, int blk) -> bool {
+    const int d = 1 << s, i = R / (2 * d), j = R % (2 * d);
+    if (j >= d) return ck.fail("first row of a pair has bit s set", R);
+    if (blk != i * d + j || blk != bfly_block(R, s)) return ck.fail("block formula differs from the index sets", R);
+    if (blk < 0 || blk >= N / 2) return ck.fail("block out of range", blk);
+    used[s][blk]++;
+    return true;
+  };
+  for (int g = 0; g < PB; ++g)
+    for (int s = 0; s < LA; ++s)
+      for (int r = 0; r < PA; ++r)
+        if (!(r & (1 << s)) && !check_pair(g * PA + r, s, g * (PA / 2) + bfly_block(r, s))) return false;
+  for (int j = 0; j < PA; ++j)
+    for (int s = LA; s < L; ++s)
+      for (int r = 0; r < PB; ++r)
+        if (!(r & (1 << (s - LA))) && !check_pair(j + PA * r, s, j + bfly_block(PA * r, s))) return false;
+  for (int s = 0; s < L; ++s)
+    for (int b = 0; b < N / 2; ++b)
+      if (used[s][b] != 1) return ck.fail("block not applied exactly once", s * N + b);
+  return ck.err.empty();
+}
+
 bool verify_fused(FusedChecker& ck, const FusedChain& fc, int dtype) {
   const int esize = dtype == F32 ? 4 : 2, E = 16 / esize;
   // Workgroup -> tile order: a bijection of the grid.
@@ -825,6 +888,7 @@ bool verify_fused(FusedChecker& ck, const FusedChain& fc, int dtype) {
       if (cover[q] != 1) return ck.fail(cover[q] ? "Y element stored more than once" : "Y element never stored",
                                         (int64_t)q);
   }
+  if (fc.bfly) return verify_fused_bfly(ck, fc, dtype);  // tile I/O as above; its own passes
   // Passes cover the factors in application order, each exactly once.
   {
     int next = fc.nf - 1;

@@ -18,6 +18,9 @@ def factors(pats):
 
 CHAINS = {
     "butterfly1024": butterfly(10),
+    "butterfly512": butterfly(9),
+    "butterfly32": butterfly(5),
+    "butterfly16": butterfly(4),
     "butterfly8": butterfly(3),
     "butterfly2": butterfly(1) * 2,
     "deformable": [(2, 3, 4, 1), (1, 8, 6, 1), (3, 2, 2, 1)],      # b != c: two LDS buffers
@@ -55,8 +58,15 @@ def test_which_chains_fuse():
     bf = factors(butterfly(10))
     for layout in ("bsl", "bsf"):
         for dtype in ("f32", "bf16"):
-            assert ks.ks_chain_describe(bf, 4096, layout, dtype).startswith("fused")
+            desc = ks.ks_chain_describe(bf, 4096, layout, dtype)
+            # the dyadic butterfly of size 16 .. 1024: two register passes of 32 rows
+            assert desc.startswith("fused-bfly ") and "passes=2 groups=32,32 " in desc, desc
             assert ks.ks_chain_workspace_bytes(bf, 4096, dtype) == 0
+    assert ks.ks_chain_describe(factors(butterfly(9)), 64, "bsl", "f32").startswith("fused-bfly ")
+    assert ks.ks_chain_describe(factors(butterfly(4)), 64, "bsl", "f32").startswith("fused-bfly ")
+    # shorter butterflies and other small-block chains: radix passes
+    assert ks.ks_chain_describe(factors(butterfly(3)), 64, "bsl", "f32").startswith("fused factors=3")
+    assert ks.ks_chain_describe(factors(CHAINS["radix4"]), 64, "bsl", "f32").startswith("fused factors=3")
     # Monarch factors (32 x 32 blocks) run fused on the MFMAs, in one LDS
     # buffer, batch-size-first; batch-size-last factor by factor
     mon = factors([(1, 32, 32, 32), (32, 32, 32, 1)])

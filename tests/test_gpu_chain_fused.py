@@ -21,6 +21,9 @@ def butterfly(L):
 
 CHAINS = {
     "butterfly1024": butterfly(10),
+    "butterfly512": butterfly(9),
+    "butterfly64": butterfly(6),
+    "butterfly16": butterfly(4),
     "butterfly8": butterfly(3),
     "deformable": [(2, 3, 4, 1), (1, 8, 6, 1), (3, 2, 2, 1)],
     "radix4": [(1, 4, 4, 16), (4, 4, 4, 4), (16, 4, 4, 1)],
