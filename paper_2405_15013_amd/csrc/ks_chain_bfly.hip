@@ -3,20 +3,26 @@
 // (2^(l-1), 2, 2, 2^(L-l)), N = 2^L (paper Section 1, Figure 1; Appendix B.1,
 // Table 5).
 //
-// One workgroup of 512 threads owns 16 batch columns, loaded into LDS as
-// fp32 (16 floats per row, rows swizzled so that the four units of a
-// wavefront hit four bank windows).  Pass A: unit (column n, group g) takes
-// the PA = 2^LA rows g*PA .. g*PA + PA-1 of its column into registers and
-// applies the factors with d = 1 .. PA/2 there (all their 2 x 2 blocks lie
-// inside the group), then writes them back.  Pass B: unit (column n, j)
-// takes rows j + PA*r (r < PB) and applies the remaining factors.  Ten
-// factors cost two LDS round trips and three barriers.
+// One workgroup of 512 threads owns 16 batch columns, kept in LDS as fp32
+// between the passes (16 floats per row, rows swizzled so that the four units
+// of a wavefront hit four bank windows).  Pass A: unit (column n, group g)
+// takes the PA = 2^LA rows g*PA .. g*PA + PA-1 of its column into registers
+// and applies the factors with d = 1 .. PA/2 there (all their 2 x 2 blocks lie
+// inside the group).  Pass B: unit (column n, j) takes rows j + PA*r (r < PB)
+// and applies the remaining factors.  A wavefront loads the X rows of its own
+// pass-A units and, batch-size-last, stores the Y rows of its own pass-B
+// units, so the only barrier is the one between the passes (batch-size-first
+// a wavefront's output rows are 16-byte runs interleaved with the others' in
+// each batch row, and the tile is stored by the shared store after a second
+// barrier).
 //
 // Factor values: the 16 lanes of a wavefront row work on the 16 columns of
 // one unit and need the same blocks, so lane i fetches the unit's i-th block
 // of each factor (one 16- or 8-byte load per factor, issued before X) into
 // registers and each butterfly takes its block's values from the owning lane
 // by DPP row broadcast; the factor values never go through LDS.
+#include <type_traits>
+
 #include "ks_chain_fused.h"
 #include "ks_chain_fused_io.h"
 #include "ks_common.h"
@@ -67,7 +73,7 @@ __device__ __forceinline__ void bfly_apply(const f32x4& k, int src, float& a, fl
   b = k10 * a0 + k11 * b0;
 }
 
-// LDS map of the butterfly form for the tile load and store.
+// LDS map of the butterfly form for the shared tile store.
 struct BflyAddr {
   int la;
   __device__ __forceinline__ int operator()(int row, int col) const { return bfly_lds_row(row, la) * 16 + col; }
@@ -115,16 +121,79 @@ __global__ __launch_bounds__(kFusedThreads) void ks_chain_bfly_kernel(FusedChain
       kb[s - LA] = fetch(L - 1 - s, jb + bfly_block(PA * ri, s));
     }
   }
-  fused_load<T, LAYOUT, VEC>(fc, lds, col0, BflyAddr{LA});
-  __syncthreads();
+  // Tile pieces: EP consecutive elements (16 bytes when VEC, else one); in
+  // the batch-size-last layout PR pieces make one row of the tile.
+  constexpr int EP = VEC ? 16 / (int)sizeof(T) : 1, PR = kFusedCols / EP;
+  typedef typename std::conditional<VEC, u32x4, T>::type PW;
+  const T* __restrict__ xp = static_cast<const T*>(fc.x);
+  T* __restrict__ yp = static_cast<T*>(fc.y);
+  const int B = fc.batch;
+  auto lds_at = [&](int row, int col) { return lds + bfly_lds_row(row, LA) * 16 + col; };
 
-  // Pass A, in place: rows u*PA + r of column n; application steps
-  // s = 0 .. LA-1 (factor L-1-s, d = 2^s): block (R >> (s+1), R mod d) mixes
-  // rows R and R + d of the group.
+  // Pass A, rows u*PA + r of column n.  Each wavefront loads exactly the rows
+  // of its own four units, as pieces regrouped by column through its own LDS
+  // rows, so it starts as soon as its own loads arrive.  Steps s = 0 .. LA-1 (factor
+  // L-1-s, d = 2^s): block (R >> (s+1), R mod d) mixes rows R and R + d.
   if (4 * w < PB) {
     float x[PA];
+    if (LAYOUT == BSL) {
+      constexpr int TOT = 4 * PA * PR, NP = (TOT + 63) / 64;  // pieces of the wavefront, per lane
+      PW pw[NP];
 #pragma unroll
-    for (int r = 0; r < PA; ++r) x[r] = lds[bfly_lds_row(u * PA + r, LA) * 16 + n];
+      for (int i = 0; i < NP; ++i) {
+        const int p = i * 64 + lane, row = 4 * w * PA + p / PR, col = (p % PR) * EP;
+        const bool ok = p < TOT && col0 + col < B;
+        const T* src = xp + (int64_t)row * B + col0 + col;
+        if constexpr (VEC) pw[i] = ok ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src)) : u32x4{0, 0, 0, 0};
+        else pw[i] = ok ? *src : T(0);
+      }
+#pragma unroll
+      for (int i = 0; i < NP; ++i) {
+        const int p = i * 64 + lane, row = 4 * w * PA + p / PR, col = (p % PR) * EP;
+        if (TOT % 64 && p >= TOT) continue;
+        if constexpr (VEC) {
+          T e[EP];
+          __builtin_memcpy(e, &pw[i], 16);
+#pragma unroll
+          for (int q = 0; q < EP; q += 4)
+            *reinterpret_cast<f32x4*>(lds_at(row, col + q)) = f32x4{to_f32(e[q]), to_f32(e[q + 1]), to_f32(e[q + 2]), to_f32(e[q + 3])};
+        } else {
+          *lds_at(row, col) = to_f32(pw[i]);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < PA; ++r) x[r] = *lds_at(u * PA + r, n);
+    } else {
+      // the wavefront's span of vector rows 4w*PA .. +4PA of every batch row
+      // t of the tile, as pieces of EP consecutive rows: lane (t, k) takes
+      // piece k (16 batch rows x 4 consecutive pieces per load)
+      constexpr int KP = 4 * PA / EP, NI = (KP + 3) / 4;
+      const int t = lane & 15;
+      PW pw[NI];
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int k = 4 * i + (lane >> 4);
+        const bool ok = (KP % 4 == 0 || k < KP) && col0 + t < B;
+        const T* src = xp + (int64_t)(col0 + t) * (PA * PB) + 4 * w * PA + k * EP;
+        if constexpr (VEC) pw[i] = ok ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(src)) : u32x4{0, 0, 0, 0};
+        else pw[i] = ok ? *src : T(0);
+      }
+#pragma unroll
+      for (int i = 0; i < NI; ++i) {
+        const int k = 4 * i + (lane >> 4);
+        if (KP % 4 && k >= KP) continue;
+        if constexpr (VEC) {
+          T e[EP];
+          __builtin_memcpy(e, &pw[i], 16);
+#pragma unroll
+          for (int q = 0; q < EP; ++q) *lds_at(4 * w * PA + k * EP + q, t) = to_f32(e[q]);
+        } else {
+          *lds_at(4 * w * PA + k, t) = to_f32(pw[i]);
+        }
+      }
+#pragma unroll
+      for (int r = 0; r < PA; ++r) x[r] = *lds_at(u * PA + r, n);
+    }
 #pragma unroll
     for (int s = 0; s < LA; ++s) {
       const int d = 1 << s;
@@ -133,17 +202,18 @@ __global__ __launch_bounds__(kFusedThreads) void ks_chain_bfly_kernel(FusedChain
         if (!(r & d)) bfly_apply(ka[s], bfly_block(r, s), x[r], x[r + d]);
     }
 #pragma unroll
-    for (int r = 0; r < PA; ++r) lds[bfly_lds_row(u * PA + r, LA) * 16 + n] = x[r];
+    for (int r = 0; r < PA; ++r) *lds_at(u * PA + r, n) = x[r];
   }
   __syncthreads();
 
-  // Pass B, in place: rows j + PA*r of column n (j = u); steps s = LA .. L-1
-  // (d = 2^s = PA * 2^(s-LA): local partner r + 2^(s-LA)).
+  // Pass B, rows j + PA*r of column n (j = u); steps s = LA .. L-1 (d = 2^s =
+  // PA * 2^(s-LA): local partner r + 2^(s-LA)).  The results go back to the
+  // wavefront's own rows; batch-size-last it stores them itself as row pieces.
   if (4 * w < PA) {
     const int j = u;
     float y[PB];
 #pragma unroll
-    for (int r = 0; r < PB; ++r) y[r] = lds[bfly_lds_row(j + PA * r, LA) * 16 + n];
+    for (int r = 0; r < PB; ++r) y[r] = *lds_at(j + PA * r, n);
 #pragma unroll
     for (int s = LA; s < L; ++s) {
       const int t = s - LA, ds = 1 << t;
@@ -152,10 +222,32 @@ __global__ __launch_bounds__(kFusedThreads) void ks_chain_bfly_kernel(FusedChain
         if (!(r & ds)) bfly_apply(kb[s - LA], ((r >> (t + 1)) << t) | (r & (ds - 1)), y[r], y[r + ds]);
     }
 #pragma unroll
-    for (int r = 0; r < PB; ++r) lds[bfly_lds_row(j + PA * r, LA) * 16 + n] = y[r];
+    for (int r = 0; r < PB; ++r) *lds_at(j + PA * r, n) = y[r];
+    if constexpr (LAYOUT == BSL) {
+      constexpr int TOT = 4 * PB * PR, NP = (TOT + 63) / 64;  // pieces: rows 4w + a + PA*r
+#pragma unroll
+      for (int i = 0; i < NP; ++i) {
+        const int p = i * 64 + lane, rho = p / PR, col = (p % PR) * EP;
+        const int row = 4 * w + (rho & 3) + PA * (rho >> 2);
+        if ((TOT % 64 && p >= TOT) || col0 + col >= B) continue;
+        T* dst = yp + (int64_t)row * B + col0 + col;
+        if constexpr (VEC) {
+          union { u32x4 w4; T e[EP]; } o;
+#pragma unroll
+          for (int q = 0; q < EP; ++q) o.e[q] = from_f32<T>(*lds_at(row, col + q));
+          __builtin_nontemporal_store(o.w4, reinterpret_cast<u32x4*>(dst));
+        } else {
+          *dst = from_f32<T>(*lds_at(row, col));
+        }
+      }
+    }
   }
-  __syncthreads();
-  fused_store<T, LAYOUT, VEC>(fc, lds, col0, BflyAddr{LA});
+  if (LAYOUT == BSF) {
+    // a wavefront's output rows interleave with the others' along each batch
+    // row: store the whole tile in contiguous runs after a barrier
+    __syncthreads();
+    fused_store<T, LAYOUT, VEC>(fc, lds, col0, BflyAddr{LA});
+  }
 }
 
 template <typename T, int LA, int LB>

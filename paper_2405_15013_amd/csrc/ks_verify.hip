@@ -794,14 +794,12 @@ bool verify_fused_mfma(FusedChecker& ck, const FusedChain& fc) {
   return ck.err.empty();
 }
 
-// Butterfly form (ks_chain_bfly.hip; its tile load and store are the shared
-// ones, replayed by verify_fused): the chain's patterns, which lane of a row
-// fetches each block, the kernel's block formulas against the index-set
-// definition (each block of each factor applied exactly once per column), and
-// the LDS row map.
+// Butterfly form (ks_chain_bfly.hip): the chain's patterns, which lane of a
+// row fetches each block, the kernel's block formulas against the index-set
+// definition (each block of each factor applied exactly once per column), the
+// LDS row map and the per-wavefront tile loads and stores.
 bool verify_fused_bfly(FusedChecker& ck, const FusedChain& fc, int dtype) {
   const int L = fc.bfly, LA = bfly_la(L), LB = L - LA, PA = 1 << LA, PB = 1 << LB, N = PA * PB;
-  (void)dtype;
   if (fc.nf != L || fc.width_in != N || fc.width_out != N) return ck.fail("butterfly widths", L);
   for (int q = 0; q < L; ++q)
     if (fc.b[q] != 2 || fc.c[q] != 2 || fc.a[q] != (1 << q) || fc.d[q] != (1 << (L - 1 - q)))
@@ -854,6 +852,79 @@ bool verify_fused_bfly(FusedChecker& ck, const FusedChain& fc, int dtype) {
   for (int s = 0; s < L; ++s)
     for (int b = 0; b < N / 2; ++b)
       if (used[s][b] != 1) return ck.fail("block not applied exactly once", s * N + b);
+  // Tile I/O, wavefront by wavefront as the kernel does it, in both access
+  // forms the host may pick (pieces of EP elements when VEC): every X element
+  // of the batch read once, every Y element written once, pass-A rows loaded
+  // by the wavefront whose units use them, pass-B rows stored by the one that
+  // wrote them.
+  constexpr int W = kFusedThreads / 64;
+  const int esize = dtype == F32 ? 4 : 2;
+  const int64_t B = fc.batch;
+  const int tiles = (int)((B + kFusedCols - 1) / kFusedCols);
+  const bool bsl = fc.layout == BSL;
+  const bool vec_ok = bsl ? B % (16 / esize) == 0 : N % (16 / esize) == 0;
+  std::vector<uint8_t> xin((size_t)B * N), yout((size_t)B * N);
+  for (int form = 0; form < (vec_ok ? 2 : 1); ++form) {
+    const bool vec = form == 1;
+    const int EP = vec ? 16 / esize : 1, PR = kFusedCols / EP;
+    std::fill(xin.begin(), xin.end(), 0);
+    std::fill(yout.begin(), yout.end(), 0);
+    for (int tile = 0; tile < tiles; ++tile) {
+      const int64_t col0 = (int64_t)tile * kFusedCols;
+      for (int w = 0; w < W; ++w) {
+        if (4 * w < PB) {
+          if (bsl) {
+            const int TOT = 4 * PA * PR, NP = (TOT + 63) / 64;
+            for (int i = 0; i < NP; ++i)
+              for (int lane = 0; lane < 64; ++lane) {
+                const int p = i * 64 + lane, row = 4 * w * PA + p / PR, col = (p % PR) * EP;
+                if (p >= TOT || col0 + col >= B) continue;
+                if (row < 4 * w * PA || row >= (4 * w + 4) * PA || row >= N) return ck.fail("pass A piece row", row);
+                if (vec && col0 + col + EP > B) return ck.fail("X piece straddles the batch end", col0 + col);
+                const int64_t off = (int64_t)row * B + col0 + col;
+                if (vec && off % EP) return ck.fail("X piece not aligned to its size", off);
+                for (int e = 0; e < EP; ++e) xin[(size_t)(off + e)]++;
+              }
+          } else {
+            const int KP = 4 * PA / EP, NI = (KP + 3) / 4;
+            for (int i = 0; i < NI; ++i)
+              for (int lane = 0; lane < 64; ++lane) {
+                const int k = 4 * i + (lane >> 4), t = lane & 15;
+                if (k >= KP || col0 + t >= B) continue;
+                const int row = 4 * w * PA + k * EP;
+                if (row + EP > (4 * w + 4) * PA || row + EP > N) return ck.fail("pass A piece rows", row);
+                const int64_t off = (col0 + t) * N + row;
+                if (vec && off % EP) return ck.fail("X piece not aligned to its size", off);
+                for (int e = 0; e < EP; ++e) xin[(size_t)(off + e)]++;
+              }
+          }
+        }
+        if (4 * w < PA) {
+          if (bsl) {
+            const int TOT = 4 * PB * PR, NP = (TOT + 63) / 64;
+            for (int i = 0; i < NP; ++i)
+              for (int lane = 0; lane < 64; ++lane) {
+                const int p = i * 64 + lane, rho = p / PR, col = (p % PR) * EP;
+                const int row = 4 * w + (rho & 3) + PA * (rho >> 2);
+                if (p >= TOT || col0 + col >= B) continue;
+                // a row of this wavefront's pass-B units j = 4w .. 4w+3
+                if ((row % PA) / 4 != w || row >= N) return ck.fail("pass B piece row", row);
+                if (vec && col0 + col + EP > B) return ck.fail("Y piece straddles the batch end", col0 + col);
+                const int64_t off = (int64_t)row * B + col0 + col;
+                if (vec && off % EP) return ck.fail("Y piece not aligned to its size", off);
+                for (int e = 0; e < EP; ++e) yout[(size_t)(off + e)]++;
+              }
+          }
+        }
+      }
+    }
+    // batch-size-first: the shared tile store after the second barrier
+    if (!bsl && !verify_fused_io(ck, fc, N, EP, true, &yout)) return false;
+    for (size_t e = 0; e < xin.size(); ++e)
+      if (xin[e] != 1) return ck.fail("X element not read exactly once", (int64_t)e);
+    for (size_t e = 0; e < yout.size(); ++e)
+      if (yout[e] != 1) return ck.fail("Y element not written exactly once", (int64_t)e);
+  }
   return ck.err.empty();
 }
 
@@ -873,6 +944,7 @@ bool verify_fused(FusedChecker& ck, const FusedChain& fc, int dtype) {
   for (int f = 0; f + 1 < fc.nf; ++f)
     if (fc.a[f] * fc.c[f] * fc.d[f] != fc.a[f + 1] * fc.b[f + 1] * fc.d[f + 1]) return ck.fail("widths", f);
   if (fused_lds_bytes(fc) > kFusedMaxLds) return ck.fail("LDS", fused_lds_bytes(fc));
+  if (fc.bfly) return verify_fused_bfly(ck, fc, dtype);  // its own tile I/O and passes
   // Vector rows end where the factor-value copies begin.
   if (fused_kbuf_offset(fc) < (fc.inplace ? 1 : 2) * fc.buf_rows * kFusedPitch) return ck.fail("LDS overlap", 0);
   // Tile I/O, both forms the host may choose (vector form only when the
@@ -888,7 +960,6 @@ bool verify_fused(FusedChecker& ck, const FusedChain& fc, int dtype) {
       if (cover[q] != 1) return ck.fail(cover[q] ? "Y element stored more than once" : "Y element never stored",
                                         (int64_t)q);
   }
-  if (fc.bfly) return verify_fused_bfly(ck, fc, dtype);  // tile I/O as above; its own passes
   // Passes cover the factors in application order, each exactly once.
   {
     int next = fc.nf - 1;
