@@ -91,36 +91,25 @@ __global__ __launch_bounds__(kFusedThreads) void ks_chain_bfly_kernel(FusedChain
   const int col0 = fused_tile((int)blockIdx.x, (int)gridDim.x) * kFusedCols;
   const int n = lane & 15, u = 4 * w + (lane >> 4);  // column, unit
 
-  // Factor blocks, fetched first, straight into registers: at step s of pass
-  // A the unit's PA/2 blocks are u*PA/2 + block(r) (PA is a multiple of 2d,
-  // and block(r) runs over 0 .. PA/2-1), and lane n of the row holds block
-  // u*PA/2 + n; at step s of pass B the block of row j + PA*r is j + block(PA*r)
-  // (j < PA <= d leaves the bits above s alone), the butterflies are the r
-  // with bit t = s - LA clear, and lane i holds the i-th of them.
-  f32x4 ka[LA], kb[LB];
-  {
-    auto fetch = [&](int q, int blk) {
-      const T* kv = static_cast<const T*>(fc.kv[q]) + 4 * blk;
-      T e[4];
-      if (fc.kvec) {
-        const KW w4 = *reinterpret_cast<const KW*>(kv);
-        __builtin_memcpy(e, &w4, sizeof(KW));
-      } else {
+  // Factor blocks go straight into registers: at step s of pass A the unit's
+  // PA/2 blocks are u*PA/2 + block(r) (PA is a multiple of 2d, and block(r)
+  // runs over 0 .. PA/2-1), and lane n of the row holds block u*PA/2 + n; at
+  // step s of pass B the block of row j + PA*r is j + block(PA*r) (j < PA <= d
+  // leaves the bits above s alone), the butterflies are the r with bit
+  // t = s - LA clear, and lane i holds the i-th of them.  Pass A's blocks are
+  // fetched right after the wavefront's X loads, pass B's before the barrier.
+  auto fetch = [&](int q, int blk) {
+    const T* kv = static_cast<const T*>(fc.kv[q]) + 4 * blk;
+    T e[4];
+    if (fc.kvec) {
+      const KW w4 = *reinterpret_cast<const KW*>(kv);
+      __builtin_memcpy(e, &w4, sizeof(KW));
+    } else {
 #pragma unroll
-        for (int t = 0; t < 4; ++t) e[t] = kv[t];
-      }
-      return f32x4{to_f32(e[0]), to_f32(e[1]), to_f32(e[2]), to_f32(e[3])};
-    };
-    const int ua = 4 * w < PB ? u : 0, ia = n < PA / 2 ? n : 0;
-#pragma unroll
-    for (int s = 0; s < LA; ++s) ka[s] = fetch(L - 1 - s, ua * (PA / 2) + ia);
-    const int jb = 4 * w < PA ? u : 0, ib = n < PB / 2 ? n : 0;
-#pragma unroll
-    for (int s = LA; s < L; ++s) {
-      const int t = s - LA, ri = ((ib >> t) << (t + 1)) | (ib & ((1 << t) - 1));
-      kb[s - LA] = fetch(L - 1 - s, jb + bfly_block(PA * ri, s));
+      for (int t = 0; t < 4; ++t) e[t] = kv[t];
     }
-  }
+    return f32x4{to_f32(e[0]), to_f32(e[1]), to_f32(e[2]), to_f32(e[3])};
+  };
   // Tile pieces: EP consecutive elements (16 bytes when VEC, else one); in
   // the batch-size-last layout PR pieces make one row of the tile.
   constexpr int EP = VEC ? 16 / (int)sizeof(T) : 1, PR = kFusedCols / EP;
@@ -194,6 +183,9 @@ __global__ __launch_bounds__(kFusedThreads) void ks_chain_bfly_kernel(FusedChain
 #pragma unroll
       for (int r = 0; r < PA; ++r) x[r] = *lds_at(u * PA + r, n);
     }
+    f32x4 ka[LA];
+#pragma unroll
+    for (int s = 0; s < LA; ++s) ka[s] = fetch(L - 1 - s, u * (PA / 2) + (n < PA / 2 ? n : 0));
 #pragma unroll
     for (int s = 0; s < LA; ++s) {
       const int d = 1 << s;
@@ -203,6 +195,15 @@ __global__ __launch_bounds__(kFusedThreads) void ks_chain_bfly_kernel(FusedChain
     }
 #pragma unroll
     for (int r = 0; r < PA; ++r) *lds_at(u * PA + r, n) = x[r];
+  }
+  f32x4 kb[LB];
+  {
+    const int jb = 4 * w < PA ? u : 0, ib = n < PB / 2 ? n : 0;
+#pragma unroll
+    for (int s = LA; s < L; ++s) {
+      const int t = s - LA, ri = ((ib >> t) << (t + 1)) | (ib & ((1 << t) - 1));
+      kb[s - LA] = fetch(L - 1 - s, jb + bfly_block(PA * ri, s));
+    }
   }
   __syncthreads();
 
@@ -221,12 +222,20 @@ __global__ __launch_bounds__(kFusedThreads) void ks_chain_bfly_kernel(FusedChain
       for (int r = 0; r < PB; ++r)
         if (!(r & ds)) bfly_apply(kb[s - LA], ((r >> (t + 1)) << t) | (r & (ds - 1)), y[r], y[r + ds]);
     }
+    if constexpr (LAYOUT != BSL) {
 #pragma unroll
-    for (int r = 0; r < PB; ++r) *lds_at(j + PA * r, n) = y[r];
-    if constexpr (LAYOUT == BSL) {
-      constexpr int TOT = 4 * PB * PR, NP = (TOT + 63) / 64;  // pieces: rows 4w + a + PA*r
+      for (int r = 0; r < PB; ++r) *lds_at(j + PA * r, n) = y[r];
+    } else {
+      // pieces of rows 4w + a + PA*r; load i of the lane takes the rows of
+      // RPI consecutive r, written just before it
+      constexpr int TOT = 4 * PB * PR, NP = (TOT + 63) / 64;
+      constexpr int RPI = TOT % 64 ? PB : 16 / PR;
 #pragma unroll
       for (int i = 0; i < NP; ++i) {
+        if (TOT % 64 == 0 || i == 0) {
+#pragma unroll
+          for (int r = RPI * i; r < RPI * i + RPI; ++r) *lds_at(j + PA * r, n) = y[r];
+        }
         const int p = i * 64 + lane, rho = p / PR, col = (p % PR) * EP;
         const int row = 4 * w + (rho & 3) + PA * (rho >> 2);
         if ((TOT % 64 && p >= TOT) || col0 + col >= B) continue;
