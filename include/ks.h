@@ -136,13 +136,14 @@ size_t ks_chain_workspace_bytes(const ks_factor_t *factors, int nfactors,
  *     a_f * c_f * d_f == a_{f+1} * b_{f+1} * d_{f+1}   (KS_ERR_DIM_MISMATCH).
  * X has batch*a_L*c_L*d_L elements and Y batch*a_1*b_1*d_1, both in `layout`.
  * Chains of two to 24 factors whose blocks are all at most 8 x 8 -- e.g. the
- * butterfly factors of a transform of size up to 1024 -- or, in the
- * batch-size-first layout, all square b x b with one b in {16, 32, 48, 64} --
- * e.g. Monarch factors -- and whose widest vector (times 16 batch columns of
- * fp32, plus the small-block form's factor-value buffer) fits in 160 KB of
- * LDS, run as one fused kernel: each workgroup keeps 16 batch columns of the
- * intermediate vectors in LDS in fp32 from the first factor to the last, so X
- * is read once, Y is written once and no workspace is used.  Other chains run
+ * butterfly factors of a transform of size up to 1024 -- or all square b x b
+ * with one b in {16, 32, 48, 64} -- e.g. Monarch factors; batch-size-first,
+ * and batch-size-last in fp32 with b <= 32 and width <= 1024 -- and whose
+ * widest vector (times 16 or 32 batch columns of fp32, plus the small-block
+ * form's factor-value buffer) fits in 160 KB of LDS, run as one fused kernel:
+ * each workgroup keeps 16 or 32 batch columns of the intermediate vectors in
+ * LDS in fp32 from the first factor to the last, so X is read once, Y is
+ * written once and no workspace is used.  Other chains run
  * factor by factor
  * (one ks_matmul each); their intermediates are stored in `dtype` in the
  * caller's `workspace` (device, at least ks_chain_workspace_bytes(...) bytes,

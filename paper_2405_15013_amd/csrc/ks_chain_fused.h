@@ -37,7 +37,9 @@
 //
 // LDS layout: row r of the vector holds the tile's 16 columns at
 // r * kFusedPitch floats (16 columns + 4 pad floats, so 16-byte accesses of
-// consecutive rows spread over all banks); then the factor-value copy.
+// consecutive rows spread over all banks); then the factor-value copy.  The
+// MFMA form may take tiles of 32 columns (pitch 36) when they fit: every
+// factor value it fetches then serves twice the columns.
 #pragma once
 #include <hip/hip_runtime.h>
 #include <cstdint>
@@ -70,6 +72,9 @@ struct FusedChain {
                             // (ks_chain_mfma.hip), one factor per pass, in place, no factor-value copy
   int bfly;                 // L >= 2: the chain is the dyadic butterfly of size N = 2^L <= 1024
                             // (ks_chain_bfly.hip, two register passes); 0 otherwise
+  int cols;                 // batch columns per workgroup tile: kFusedCols, or 2*kFusedCols for the
+                            // MFMA form when the wider tile fits
+  int pitch;                // floats per LDS row of the vector buffers (cols + 4)
   int a[kFusedMaxFactors], b[kFusedMaxFactors], c[kFusedMaxFactors], d[kFusedMaxFactors];
   uint32_t md[kFusedMaxFactors];  // multiply-shift constants of the division by d
   int sd[kFusedMaxFactors];
@@ -141,20 +146,21 @@ __host__ __device__ __forceinline__ int fused_out_row(const FusedChain& fc, int 
   return i * fc.b[f] * fc.d[f] + k * fc.d[f] + j;
 }
 
-// Tile loads and stores, 16-byte form: unit u of a pass over the tile covers
-// E = 16 / sizeof(T) consecutive elements.
+// Tile loads and stores, 16-byte form: unit u of a pass over the tile (of
+// `cols` batch columns) covers E = 16 / sizeof(T) consecutive elements.
 //  BSL: u -> (row n, column t0 = E * v), global element n*batch + col0 + t0,
 //       LDS float n*kFusedPitch + t0 (+1 per element).
 //  BSF: u -> (batch row t = u % 16, first element n0 = E * (u / 16)), global
 //       element (col0 + t)*width + n0, LDS floats (n0 + e)*kFusedPitch + t.
-__host__ __device__ __forceinline__ void fused_vec_unit(int layout, int E, int u, int* row, int* col) {
+__host__ __device__ __forceinline__ void fused_vec_unit(int layout, int E, int u, int* row, int* col,
+                                                        int cols = kFusedCols) {
   if (layout == 1) {  // BSL
-    const int pr = kFusedCols / E;
+    const int pr = cols / E;
     *row = u / pr;
     *col = (u - *row * pr) * E;
   } else {
-    *col = u % kFusedCols;
-    *row = (u / kFusedCols) * E;
+    *col = u % cols;
+    *row = (u / cols) * E;
   }
 }
 
@@ -193,7 +199,7 @@ __host__ __device__ __forceinline__ int bfly_lds_floats(int N) { return N * 16; 
 
 // LDS layout: the vector buffer(s), then the current pass's factor values.
 __host__ __device__ __forceinline__ int fused_kbuf_offset(const FusedChain& fc) {
-  return (fc.inplace ? 1 : 2) * fc.buf_rows * kFusedPitch;  // floats
+  return (fc.inplace ? 1 : 2) * fc.buf_rows * fc.pitch;  // floats
 }
 __host__ __device__ __forceinline__ int fused_lds_bytes(const FusedChain& fc) {
   if (fc.bfly) return bfly_lds_floats(fc.width_in) * 4;

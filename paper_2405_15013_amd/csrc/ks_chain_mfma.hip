@@ -1,8 +1,8 @@
 // Fused chain kernel, MFMA form (ks_chain_fused.h): chains whose factors all
 // have square b x b blocks with one b = 16*BT, BT in 1 .. 4 (Monarch-type
-// chains; paper Section 1 and Appendix B.1).  The workgroup's tile of
-// kFusedCols batch columns stays in LDS in fp32 for the whole chain; each
-// factor is applied in place, one wavefront per block.
+// chains; paper Section 1 and Appendix B.1).  The workgroup's tile of 16 or
+// 32 batch columns stays in LDS in fp32 for the whole chain; each factor is
+// applied in place, one wavefront per block.
 //
 // Block product: v_mfma_f32_16x16x4_f32 in the register-direct operand
 // layout.  Lane (n, g) = (lane % 16, lane / 16) works on column n of the
@@ -67,38 +67,49 @@ __device__ __forceinline__ void mfma_kload(typename KRun<T>::type (&kr)[BT][BT],
 }
 
 // One block, in place: addr is this lane's LDS float index of row
-// in_row(l = 4g) at column n, step the LDS distance of consecutive l (d rows).
-template <typename T, int BT>
+// in_row(l = 4g) at column n, step the LDS distance of consecutive l (d rows);
+// H column halves of 16 (columns n and 16 + n) share every factor value.
+template <typename T, int BT, int H>
 __device__ __forceinline__ void mfma_block(const typename KRun<T>::type (&kr)[BT][BT], float* lds, int addr,
                                            int step) {
-  f32x4 acc[BT];
+  f32x4 acc[H][BT];
 #pragma unroll
-  for (int kt = 0; kt < BT; ++kt) acc[kt] = f32x4{0.f, 0.f, 0.f, 0.f};
-  float xv[BT][4];
+  for (int h = 0; h < H; ++h)
 #pragma unroll
-  for (int ct = 0; ct < BT; ++ct)
+    for (int kt = 0; kt < BT; ++kt) acc[h][kt] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float xv[H][BT][4];
 #pragma unroll
-    for (int t = 0; t < 4; ++t) xv[ct][t] = lds[addr + (16 * ct + t) * step];
+  for (int h = 0; h < H; ++h)
+#pragma unroll
+    for (int ct = 0; ct < BT; ++ct)
+#pragma unroll
+      for (int t = 0; t < 4; ++t) xv[h][ct][t] = lds[addr + 16 * h + (16 * ct + t) * step];
 #pragma unroll
   for (int ct = 0; ct < BT; ++ct)
 #pragma unroll
     for (int t = 0; t < 4; ++t)
 #pragma unroll
-      for (int kt = 0; kt < BT; ++kt)
-        acc[kt] = __builtin_amdgcn_mfma_f32_16x16x4f32(kelem(kr[kt][ct], t, T()), xv[ct][t], acc[kt], 0, 0, 0);
+      for (int kt = 0; kt < BT; ++kt) {
+        const float a = kelem(kr[kt][ct], t, T());
+#pragma unroll
+        for (int h = 0; h < H; ++h)
+          acc[h][kt] = __builtin_amdgcn_mfma_f32_16x16x4f32(a, xv[h][ct][t], acc[h][kt], 0, 0, 0);
+      }
   mfma_results_settle();
 #pragma unroll
-  for (int kt = 0; kt < BT; ++kt)
+  for (int h = 0; h < H; ++h)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) lds[addr + (16 * kt + r) * step] = acc[kt][r];
+    for (int kt = 0; kt < BT; ++kt)
+#pragma unroll
+      for (int r = 0; r < 4; ++r) lds[addr + 16 * h + (16 * kt + r) * step] = acc[h][kt][r];
 }
 
-template <typename T, int LAYOUT, bool VEC, int BT, bool KVEC>
+template <typename T, int LAYOUT, bool VEC, int BT, bool KVEC, int NC>
 __global__ __launch_bounds__(kFusedThreads) void ks_chain_mfma_kernel(FusedChain fc) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
   typedef typename KRun<T>::type KW;
-  constexpr int W = kFusedThreads / 64, B = 16 * BT;
-  const int col0 = fused_tile((int)blockIdx.x, (int)gridDim.x) * kFusedCols;
+  constexpr int W = kFusedThreads / 64, B = 16 * BT, H = NC / 16, P = NC + 4;
+  const int col0 = fused_tile((int)blockIdx.x, (int)gridDim.x) * NC;
   const int w = __builtin_amdgcn_readfirstlane((int)threadIdx.x >> 6);
   const int lane = threadIdx.x & 63, n = lane & 15, g = lane >> 4;
   // Values of block ij of factor f; an index past the factor's last block is
@@ -113,43 +124,43 @@ __global__ __launch_bounds__(kFusedThreads) void ks_chain_mfma_kernel(FusedChain
   auto lane_addr = [&](int f, int ij) {
     const int d = fc.d[f];
     const int i = (int)div_fast((uint32_t)ij, fc.md[f], fc.sd[f]), j = ij - i * d;
-    return (i * B * d + j + 4 * g * d) * kFusedPitch + n;
+    return (i * B * d + j + 4 * g * d) * P + n;
   };
   KW ka[BT][BT], kb[BT][BT];
   mfma_kload<T, BT, KVEC>(ka, kblock(fc.nf - 1, w), n, g);
-  fused_load<T, LAYOUT, VEC>(fc, lds, col0);
+  fused_load<T, LAYOUT, VEC, FusedPitchAddr, NC>(fc, lds, col0, FusedPitchAddr{P});
   __syncthreads();
   for (int f = fc.nf - 1; f >= 0; --f) {
-    const int nb = fused_mfma_blocks(fc, f), step = fc.d[f] * kFusedPitch;
+    const int nb = fused_mfma_blocks(fc, f), step = fc.d[f] * P;
     for (int ij = w; ij < nb; ij += 2 * W) {
       const int ij1 = ij + W;
       mfma_kload<T, BT, KVEC>(kb, kblock(f, ij1), n, g);
-      mfma_block<T, BT>(ka, lds, lane_addr(f, ij), step);
+      mfma_block<T, BT, H>(ka, lds, lane_addr(f, ij), step);
       // the wavefront's next block: ij + 2W of this factor, else its first
       // block of the next factor
       const bool here = ij + 2 * W < nb || f == 0;
       mfma_kload<T, BT, KVEC>(ka, here ? kblock(f, ij + 2 * W) : kblock(f - 1, w), n, g);
-      if (ij1 < nb) mfma_block<T, BT>(kb, lds, lane_addr(f, ij1), step);
+      if (ij1 < nb) mfma_block<T, BT, H>(kb, lds, lane_addr(f, ij1), step);
     }
     if (w >= nb && f > 0) mfma_kload<T, BT, KVEC>(ka, kblock(f - 1, w), n, g);
     __syncthreads();
   }
-  fused_store<T, LAYOUT, VEC>(fc, lds, col0);
+  fused_store<T, LAYOUT, VEC, FusedPitchAddr, NC>(fc, lds, col0, FusedPitchAddr{P});
 }
 
-template <typename T, int BT>
-hipError_t launch_mfma_bt(const FusedChain& fc, bool vec, hipStream_t s) {
-  const dim3 grid((fc.batch + kFusedCols - 1) / kFusedCols), block(kFusedThreads);
+template <typename T, int BT, int NC>
+hipError_t launch_mfma_nc(const FusedChain& fc, bool vec, hipStream_t s) {
+  const dim3 grid((fc.batch + NC - 1) / NC), block(kFusedThreads);
   const int lds = fused_lds_bytes(fc);
 #define KS_MFMA_LAUNCH(L, V, KV)                                                                              \
   {                                                                                                          \
     if (lds > 64 * 1024) {                                                                                   \
       static const hipError_t raised = hipFuncSetAttribute(                                                  \
-          reinterpret_cast<const void*>(&ks_chain_mfma_kernel<T, L, V, BT, KV>),                             \
+          reinterpret_cast<const void*>(&ks_chain_mfma_kernel<T, L, V, BT, KV, NC>),                         \
           hipFuncAttributeMaxDynamicSharedMemorySize, kFusedMaxLds);                                         \
       if (raised != hipSuccess) return raised;                                                               \
     }                                                                                                        \
-    hipLaunchKernelGGL((ks_chain_mfma_kernel<T, L, V, BT, KV>), grid, block, lds, s, fc);                    \
+    hipLaunchKernelGGL((ks_chain_mfma_kernel<T, L, V, BT, KV, NC>), grid, block, lds, s, fc);                \
     return hipGetLastError();                                                                                \
   }
 #define KS_MFMA_LAUNCH_KV(L, V)                                                                               \
@@ -162,6 +173,15 @@ hipError_t launch_mfma_bt(const FusedChain& fc, bool vec, hipStream_t s) {
   if (vec) KS_MFMA_LAUNCH_KV(BSF, true) else KS_MFMA_LAUNCH_KV(BSF, false)
 #undef KS_MFMA_LAUNCH_KV
 #undef KS_MFMA_LAUNCH
+}
+
+// Tiles of 32 columns for blocks of 16 and 32 (ks_host.cpp picks them only there).
+template <typename T, int BT>
+hipError_t launch_mfma_bt(const FusedChain& fc, bool vec, hipStream_t s) {
+  if constexpr (BT <= 2)
+    if (fc.cols == 2 * kFusedCols) return launch_mfma_nc<T, BT, 2 * kFusedCols>(fc, vec, s);
+  if (fc.cols != kFusedCols) return hipErrorInvalidValue;
+  return launch_mfma_nc<T, BT, kFusedCols>(fc, vec, s);
 }
 
 template <typename T>

@@ -367,11 +367,13 @@ bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, in
     inplace = inplace && f[q].b == f[q].c;
   }
   if (!small && !square16) return false;
-  // The MFMA form runs batch-size-first only: its tile of 16 batch columns
-  // is a contiguous run of X and Y there, but in the batch-size-last layout
-  // it is one 32- or 64-byte piece of every row, which the factor-by-factor
-  // kernels (long runs along the batch) read and write faster.
-  if (!small && layout != KS_LAYOUT_BSF) return false;
+  // The MFMA form: batch-size-first, tiles of 16 batch columns (a contiguous
+  // run of X and Y); batch-size-last only in fp32, with tiles of 32 columns,
+  // whose row pieces are whole 128-byte lines.  Narrower pieces (16-bit
+  // types, or 16 fp32 columns) are read and written faster by the
+  // factor-by-factor kernels, which run along the batch.
+  const bool wide_fits = wmax * (2 * kFusedCols + 4) * 4 <= kFusedMaxLds && f[0].b <= 32;
+  if (!small && layout != KS_LAYOUT_BSF && !(dtype == KS_F32 && wide_fits)) return false;
   const int64_t kbuf = small ? kFusedKValues : 0;
   if (((inplace ? 1 : 2) * wmax * kFusedPitch + kbuf) * 4 > kFusedMaxLds) return false;
   if ((batch + kFusedCols - 1) / kFusedCols > 0x7fffffff) return false;
@@ -384,6 +386,13 @@ bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, in
   fc->buf_rows = (int)wmax;
   fc->kvec = 0;  // set at launch (chain_fused_kvec)
   fc->mfma = small ? 0 : 1;
+  fc->cols = kFusedCols;
+  fc->pitch = kFusedPitch;
+  // MFMA form, batch-size-last: tiles of 32 columns
+  if (!small && layout != KS_LAYOUT_BSF) {
+    fc->cols = 2 * kFusedCols;
+    fc->pitch = 2 * kFusedCols + 4;
+  }
   // the dyadic butterfly of size 2^L, L = 4 .. 10: factor q of pattern
   // (2^q, 2, 2, 2^(L-1-q)) in product order
   fc->bfly = 0;
@@ -589,8 +598,7 @@ ks_status_t ks_chain_describe(const ks_factor_t* factors, int nfactors, int64_t 
     if (fc.bfly) passes = std::to_string(1 << bfly_la(fc.bfly)) + "," + std::to_string(1 << (fc.bfly - bfly_la(fc.bfly)));
     snprintf(buf, len, "fused%s factors=%d passes=%d groups=%s inplace=%d lds=%d grid=%lld block=%d cols=%d",
              fc.mfma ? "-mfma" : (fc.bfly ? "-bfly" : ""), fc.nf, fc.bfly ? 2 : fc.npass, passes.c_str(), fc.inplace,
-             fused_lds_bytes(fc),
-             (long long)((batch + kFusedCols - 1) / kFusedCols), kFusedThreads, kFusedCols);
+             fused_lds_bytes(fc), (long long)((batch + fc.cols - 1) / fc.cols), kFusedThreads, fc.cols);
   } else {
     snprintf(buf, len, "unfused factors=%d workspace=%zu", nfactors, nfactors <= 1 ? (size_t)0 : (nfactors == 2 ? per : 2 * per));
   }

@@ -690,28 +690,31 @@ struct FusedChecker {
 bool verify_fused_io(FusedChecker& ck, const FusedChain& fc, int width, int E, bool store,
                      std::vector<uint8_t>* cover) {
   const int64_t B = fc.batch, total = (int64_t)B * width;
-  const int tiles = (int)((B + kFusedCols - 1) / kFusedCols);
-  const int units = width * kFusedCols / E;
+  const int NC = fc.cols;
+  const int tiles = (int)((B + NC - 1) / NC);
+  const int units = width * NC / E;
   const int rows_lds = fc.buf_rows;
+  if (NC != kFusedCols && !(fc.mfma && NC == 2 * kFusedCols)) return ck.fail("tile width", NC);
+  if (fc.pitch != NC + 4) return ck.fail("LDS pitch", fc.pitch);
   for (int tile = 0; tile < tiles; ++tile) {
-    const int col0 = tile * kFusedCols;
+    const int col0 = tile * NC;
     for (int u = 0; u < units; ++u) {
       int row, col;
       if (E > 1) {
-        fused_vec_unit(fc.layout, E, u, &row, &col);
+        fused_vec_unit(fc.layout, E, u, &row, &col, NC);
       } else if (fc.layout == BSL) {
-        row = u / kFusedCols;
-        col = u % kFusedCols;
+        row = u / NC;
+        col = u % NC;
       } else {
-        col = u % kFusedCols;
-        row = u / kFusedCols;
+        col = u % NC;
+        row = u / NC;
       }
       // The element(s) this unit moves: BSL a run of E columns of one row,
       // BSF a run of E rows (vector elements) of one batch row.
       const int r_hi = fc.layout == BSL ? row : row + E - 1;
       const int c_hi = fc.layout == BSL ? col + E - 1 : col;
       if (row < 0 || r_hi >= width || r_hi >= rows_lds) return ck.fail("tile row out of range", row);
-      if (col < 0 || c_hi >= kFusedCols) return ck.fail("tile column out of range", col);
+      if (col < 0 || c_hi >= NC) return ck.fail("tile column out of range", col);
       const int bcol = col0 + (fc.layout == BSL ? col : col);
       const bool valid = fc.layout == BSL ? bcol < B : bcol < B;
       if (!valid) continue;  // beyond the batch: loads fill zeros, stores skip
@@ -742,7 +745,10 @@ bool verify_fused_mfma(FusedChecker& ck, const FusedChain& fc) {
     const int BT = b / 16, nblk = fused_mfma_blocks(fc, f), width = a * b * d;
     if (nblk != a * d) return ck.fail("MFMA block count", f);
     const int64_t kcount = (int64_t)a * d * b * b;
-    std::vector<uint8_t> blk(nblk, 0), cover((size_t)width * kFusedCols, 0);
+    const int NC = fc.cols, H = NC / 16;
+    if (NC != 16 && NC != 32) return ck.fail("MFMA form tile width", NC);
+    if (NC == 32 && BT > 2) return ck.fail("32-column tiles only for blocks up to 32", b);
+    std::vector<uint8_t> blk(nblk, 0), cover((size_t)width * NC, 0);
     std::vector<uint8_t> kcov((size_t)kcount, 0);
     for (int w = 0; w < W; ++w) {
       for (int ij = w; ij < nblk; ij += W) {
@@ -773,7 +779,7 @@ bool verify_fused_mfma(FusedChecker& ck, const FusedChain& fc) {
               const int r = fused_out_row(fc, f, i, j, 16 * kt + 4 * g + r4);
               if (r != lane_row + (16 * kt + r4) * d) return ck.fail("MFMA lane row is not the output row", r);
               if (r < 0 || r >= width || r >= fc.buf_rows) return ck.fail("MFMA output row out of range", r);
-              cover[(size_t)r * kFusedCols + n]++;
+              for (int h = 0; h < H; ++h) cover[(size_t)r * NC + 16 * h + n]++;
               if (n == 0) rout.push_back(r);
             }
         }
@@ -932,7 +938,7 @@ bool verify_fused(FusedChecker& ck, const FusedChain& fc, int dtype) {
   const int esize = dtype == F32 ? 4 : 2, E = 16 / esize;
   // Workgroup -> tile order: a bijection of the grid.
   {
-    const int tiles = (int)(((int64_t)fc.batch + kFusedCols - 1) / kFusedCols);
+    const int tiles = (int)(((int64_t)fc.batch + fc.cols - 1) / fc.cols);
     std::vector<uint8_t> seen(tiles, 0);
     for (int b = 0; b < tiles; ++b) {
       const int t = fused_tile(b, tiles);

@@ -51,7 +51,16 @@ def test_fused_chain_replay(name, layout, dtype, batch):
     else:
         assert rep == "not fused"
     if name.startswith(("monarch", "square")):
-        assert desc.startswith("fused-mfma" if layout == "bsf" else "unfused"), desc
+        # batch-size-first: tiles of 16 columns; batch-size-last only fp32 with
+        # tiles of 32 columns (blocks up to 32, width up to 1024)
+        pats = CHAINS[name]
+        wide = pats[0][1] <= 32 and pats[0][0] * pats[0][1] * pats[0][3] <= 1024
+        if layout == "bsf":
+            assert desc.startswith("fused-mfma") and desc.endswith("cols=16"), desc
+        elif dtype == "f32" and wide:
+            assert desc.startswith("fused-mfma") and desc.endswith("cols=32"), desc
+        else:
+            assert desc.startswith("unfused"), desc
 
 
 def test_which_chains_fuse():
@@ -72,10 +81,16 @@ def test_which_chains_fuse():
     mon = factors([(1, 32, 32, 32), (32, 32, 32, 1)])
     for dtype in ("f32", "bf16", "f16"):
         desc = ks.ks_chain_describe(mon, 16384, "bsf", dtype)
-        assert desc.startswith("fused-mfma ") and "inplace=1" in desc and "lds=81920 " in desc, desc
-        assert ks.ks_chain_describe(mon, 16384, "bsl", dtype).startswith("unfused")
-        # the workspace query has no layout: the batch-size-last run needs one
-        assert ks.ks_chain_workspace_bytes(mon, 16384, dtype) == 1024 * 16384 * (4 if dtype == "f32" else 2)
+        assert desc.startswith("fused-mfma ") and "inplace=1" in desc and "lds=81920 " in desc and "cols=16" in desc, desc
+        desc = ks.ks_chain_describe(mon, 16384, "bsl", dtype)
+        if dtype == "f32":
+            assert desc.startswith("fused-mfma ") and "lds=147456 " in desc and desc.endswith("grid=512 block=512 cols=32"), desc
+            assert ks.ks_chain_workspace_bytes(mon, 16384, dtype) == 0
+        else:
+            # batch-size-last 16-bit chains run factor by factor; the workspace
+            # query has no layout and answers for that run
+            assert desc.startswith("unfused"), desc
+            assert ks.ks_chain_workspace_bytes(mon, 16384, dtype) == 1024 * 16384 * 2
     # blocks that are not all square of one size in {16, 32, 48, 64}, or that
     # mix small and large blocks, run factor by factor
     for pats in ([(1, 32, 16, 32), (32, 16, 32, 1)], [(1, 96, 96, 8), (8, 96, 96, 1)],

@@ -47,8 +47,12 @@ def run_chain(pats, x, kvs, batch, dtype, layout, fused=True, x_offset=0, y_offs
     ks.ks_force_chain_fusion(None if fused else 0)
     try:
         desc = ks.ks_chain_describe(factors, batch, layout, dtype)
-        # the MFMA form (square blocks of 16 .. 64) fuses batch-size-first only
-        fuses = fused and (layout == "bsf" or max(max(p[1], p[2]) for p in pats) <= 8)
+        # the MFMA form (square blocks of 16 .. 64) fuses batch-size-first, and
+        # batch-size-last in fp32 with 32-column tiles (blocks up to 32, width
+        # up to 1024)
+        small = max(max(p[1], p[2]) for p in pats) <= 8
+        wide = pats[0][1] <= 32 and pats[0][0] * pats[0][1] * pats[0][3] <= 1024
+        fuses = fused and (small or layout == "bsf" or (dtype == "f32" and wide))
         assert desc.startswith("fused" if fuses else "unfused"), desc
         need = ks.ks_chain_workspace_bytes(factors, batch, dtype)
         ws = torch.empty(max(need, 1), dtype=torch.uint8, device="cuda")
