@@ -379,6 +379,57 @@ def mfma_summary(csv_paths, out_md, command_lines):
     print("\n".join(lines))
 
 
+BUTTERFLY10 = [(2 ** (l - 1), 2, 2, 2 ** (10 - l)) for l in range(1, 11)]
+MONARCH2 = [(1, 32, 32, 32), (32, 32, 32, 1)]
+
+
+def chain_workloads(run):
+    """The chain workloads, each as planned (fused where the planner fuses
+    it) and factor by factor: the butterfly 10-chain (N = 1024) at batch
+    4096 and the Monarch 2-chain (N = 1024) at batch 16384, fp32 and bf16,
+    both layouts."""
+    out = []
+    for dtype in ("f32", "bf16"):
+        run.fill(dtype)
+        for pats, batch in ((BUTTERFLY10, 4096), (MONARCH2, 16384)):
+            for layout in ("bsl", "bsf"):
+                for fused in (True, False):
+                    out.append(run.chain(pats, batch, dtype, layout, fused=fused))
+    return out
+
+
+def chain_summary(stats_csv, chains_jsonl, out_md, command_lines):
+    """Write the chain workloads' timings (per call through HIP graphs, and
+    the per-launch median) beside the device time rocprofv3 reports for each
+    chain kernel of the same run."""
+    import csv
+    recs = [json.loads(l) for l in open(chains_jsonl) if l.strip()]
+    rows = [r for r in csv.DictReader(open(stats_csv)) if "ks_chain_" in r["Name"]]
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    lines = ["# Chain workloads: fused kernels and factor by factor", "",
+             "Butterfly 10-chain (2^(l-1), 2, 2, 2^(10-l)), l = 1..10, at batch 4096 and Monarch 2-chain "
+             "(1,32,32,32)·(32,32,32,1) at batch 16384 (both N = 1024), fp32 and bf16, both layouts; each as "
+             "planned and factor by factor; %s." % (
+                 "per call: graph replay over a >= 768 MB buffer rotation; per launch: median of HIP events"), "",
+             "Command (from the repository root):", "", "```"] + command_lines + ["```", "",
+             "| chain | B | dtype | layout | path | us per call | us per launch (median) | fused bound us "
+             "(X + ΣK + Y at 8 TB/s) | fraction of fused bound |",
+             "|---|---:|---|---|---|---:|---:|---:|---:|"]
+    for r in recs:
+        lines.append("| %s | %d | %s | %s | %s | %.2f | %.2f | %.2f | %.3f |" % (
+            "butterfly 10" if len(r["chain"]) == 10 else "Monarch 2", r["batch"], r["dtype"], r["layout"].upper(),
+            r["path"], r["us"], r.get("launch_us_median", float("nan")), r["fused_lower_bound_us"],
+            r["frac_fused_bound"]))
+    lines += ["", "Device time of the chain kernels (rocprofv3, all dispatches of the run, warmup included):", "",
+              "| kernel | calls | avg us | min us | max us |", "|---|---:|---:|---:|---:|"]
+    for r in rows:
+        name = r["Name"].replace("(anonymous namespace)::", "")
+        lines.append("| `%s` | %s | %.2f | %.2f | %.2f |" % (
+            name, r["Calls"], float(r["AverageNs"]) / 1e3, float(r["MinNs"]) / 1e3, float(r["MaxNs"]) / 1e3))
+    with open(out_md, "w") as fh:
+        fh.write("\n".join(lines) + "\n")
+
+
 def trace_summary(stats_csv, bench_json, out_md, command_lines, top=25):
     """Write the kernel-trace summary (rocprofv3 --kernel-trace --stats) of a
     bench run, with the dominant kernel's profiler average beside the
@@ -756,6 +807,11 @@ def main():
                     help="summarise MFMA counter passes (counter_collection.csv files, then OUT_MD; no GPU)")
     ap.add_argument("--copy-floor-in", default=None, metavar="FLOOR_JSON",
                     help="a --copy-floor result for --points-summary")
+    ap.add_argument("--chains", default=None, metavar="OUT_JSONL",
+                    help="time only the chain workloads (butterfly 10-chain at batch 4096, Monarch 2-chain at "
+                         "batch 16384; fp32 and bf16, both layouts, as planned and factor by factor) into OUT_JSONL")
+    ap.add_argument("--chain-summary", nargs=3, metavar=("STATS_CSV", "CHAINS_JSONL", "OUT_MD"),
+                    help="summarise a --chains run under rocprofv3 --kernel-trace --stats (no GPU)")
     ap.add_argument("--pmc-command", action="append", default=[],
                     help="command line recorded in the --pmc-summary / --trace-summary output (repeatable)")
     args = ap.parse_args()
@@ -770,6 +826,9 @@ def main():
         return
     if args.points_summary:
         points_summary(args.points_summary[0], args.points_summary[1], args.pmc_command, args.copy_floor_in)
+        return
+    if args.chain_summary:
+        chain_summary(*args.chain_summary, args.pmc_command)
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU only: the KS matmul path shards over the batch with no "
@@ -786,6 +845,15 @@ def main():
         with open(args.copy_floor, "w") as fh:
             json.dump({"copy_floor": rows}, fh)
         print(json.dumps({"copy_floor": rows}), flush=True)
+        return
+    if args.chains:
+        run = Runner(args.steps, args.warmup)
+        with open(args.chains, "w") as fout:
+            for r in chain_workloads(run):
+                fout.write(json.dumps(r) + "\n")
+                print("[bench] chain %s B=%d %s %s %s: %.2f us" % (
+                    "butterfly10" if len(r["chain"]) == 10 else "monarch2", r["batch"], r["dtype"], r["layout"],
+                    r["path"], r["us"]), file=sys.stderr, flush=True)
         return
     t_start = time.time()
     run = Runner(args.steps, args.warmup, eager=args.eager)

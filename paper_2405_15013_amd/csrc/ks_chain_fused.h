@@ -159,8 +159,12 @@ __host__ __device__ __forceinline__ void fused_vec_unit(int layout, int E, int u
     *row = u / pr;
     *col = (u - *row * pr) * E;
   } else {
-    *col = u % cols;
-    *row = (u / cols) * E;
+    // 16 batch rows x 4 consecutive pieces per 64 units (64-byte runs of each
+    // batch row for 16-byte pieces), then the next 16 columns, then the next
+    // 4 pieces; with 32 columns the width must be a multiple of 4 pieces
+    const int h = (u >> 6) % (cols >> 4), kk = (u >> 6) / (cols >> 4);
+    *col = (u & 15) + 16 * h;
+    *row = (4 * kk + ((u >> 4) & 3)) * E;
   }
 }
 
@@ -211,6 +215,24 @@ __host__ __device__ __forceinline__ int fused_lds_bytes(const FusedChain& fc) {
 // of the block for the tile's 16 columns); block index ij = i*d + j,
 // wavefront w takes ij = w, w + W, ... (W = kFusedThreads / 64).
 __host__ __device__ __forceinline__ int fused_mfma_bt(const FusedChain& fc) { return fc.b[0] / 16; }
+// When the first factor applied has d = 1 its blocks are runs of B rows, and
+// wavefront w loads the rows of its own blocks itself (no barrier first).
+// Piece p (EP elements) of one block's B rows x NC columns of the tile, as
+// (row offset r, column c).  BSL: EP consecutive columns of one row.  BSF: EP
+// consecutive rows of one batch row; consecutive p run over 16 batch rows,
+// then over the pieces of a row, so 64 lanes read 16 batch rows x 4 pieces.
+__host__ __device__ __forceinline__ void fused_block_piece(int layout, int B, int NC, int EP, int p, int* r,
+                                                           int* c) {
+  if (layout == 1) {
+    const int pr = NC / EP;
+    *r = p / pr;
+    *c = (p % pr) * EP;
+  } else {
+    const int kp = B / EP, m = p >> 4;
+    *c = (p & 15) + 16 * ((m / kp) % (NC / 16));
+    *r = (m % kp) * EP;
+  }
+}
 __host__ __device__ __forceinline__ int fused_mfma_blocks(const FusedChain& fc, int f) { return fc.a[f] * fc.d[f]; }
 
 }  // namespace ks

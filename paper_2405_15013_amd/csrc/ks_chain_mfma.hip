@@ -18,6 +18,8 @@
 // (ping-pong) and fetches the next block's while it multiplies the current
 // one; the last block of a factor fetches the first block of the next factor,
 // so its latency overlaps the barrier.
+#include <type_traits>
+
 #include "ks_chain_fused.h"
 #include "ks_chain_fused_io.h"
 #include "ks_common.h"
@@ -104,6 +106,70 @@ __device__ __forceinline__ void mfma_block(const typename KRun<T>::type (&kr)[BT
       for (int r = 0; r < 4; ++r) lds[addr + 16 * h + (16 * kt + r) * step] = acc[h][kt][r];
 }
 
+// Rows [ij*B, ij*B + B) of the tile for the blocks ij = w, w + W, ... < nb
+// of a first factor with d = 1, loaded by wavefront w into LDS (pitch NC + 4)
+// as pieces of EP elements (16 bytes when VEC), four blocks' loads in flight
+// before any is written.  BSF: a piece is EP consecutive rows of one batch row
+// (lanes: 16 batch rows x 4 pieces per load); BSL: EP consecutive columns of
+// one row.  Columns beyond the batch are zero.
+template <typename T, int LAYOUT, bool VEC, int B, int NC>
+__device__ __forceinline__ void wave_load_blocks(const FusedChain& fc, float* lds, int col0, int w, int nb) {
+  constexpr int W = kFusedThreads / 64, P = NC + 4, QMAX = 4;
+  constexpr int EP = VEC ? 16 / (int)sizeof(T) : 1;
+  constexpr int PPB = B * NC / EP;                 // pieces per block
+  constexpr int PPL = (PPB + 63) / 64;             // per lane and block
+  typedef typename std::conditional<VEC, u32x4, T>::type PW;
+  const T* __restrict__ xp = static_cast<const T*>(fc.x);
+  const int Bt = fc.batch, N = fc.width_in, lane = threadIdx.x & 63;
+  // piece p of a block: (row offset, column) in the tile (fused_block_piece)
+  auto piece = [&](int p, int* r, int* c) { fused_block_piece(LAYOUT, B, NC, EP, p, r, c); };
+  for (int q0 = w; q0 < nb; q0 += QMAX * W) {
+    PW pw[QMAX][PPL];
+#pragma unroll
+    for (int q = 0; q < QMAX; ++q) {
+      const int ij = q0 + q * W;
+#pragma unroll
+      for (int i = 0; i < PPL; ++i) {
+        const int p = i * 64 + lane;
+        int r, c;
+        piece(p, &r, &c);
+        const bool ok = ij < nb && (PPB % 64 == 0 || p < PPB) && col0 + c < Bt;
+        const int64_t off = LAYOUT == BSL ? (int64_t)(ij * B + r) * Bt + col0 + c
+                                          : (int64_t)(col0 + c) * N + ij * B + r;
+        if constexpr (VEC) pw[q][i] = ok ? __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(xp + off)) : u32x4{0, 0, 0, 0};
+        else pw[q][i] = ok ? xp[off] : T(0);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < QMAX; ++q) {
+      const int ij = q0 + q * W;
+      if (ij >= nb) break;
+#pragma unroll
+      for (int i = 0; i < PPL; ++i) {
+        const int p = i * 64 + lane;
+        if (PPB % 64 && p >= PPB) continue;
+        int r, c;
+        piece(p, &r, &c);
+        const int row = ij * B + r;
+        if constexpr (VEC) {
+          T e[EP];
+          __builtin_memcpy(e, &pw[q][i], 16);
+          if (LAYOUT == BSL) {
+#pragma unroll
+            for (int x = 0; x < EP; x += 4)
+              *reinterpret_cast<f32x4*>(lds + row * P + c + x) = f32x4{to_f32(e[x]), to_f32(e[x + 1]), to_f32(e[x + 2]), to_f32(e[x + 3])};
+          } else {
+#pragma unroll
+            for (int x = 0; x < EP; ++x) lds[(row + x) * P + c] = to_f32(e[x]);
+          }
+        } else {
+          lds[row * P + c] = to_f32(pw[q][i]);
+        }
+      }
+    }
+  }
+}
+
 template <typename T, int LAYOUT, bool VEC, int BT, bool KVEC, int NC>
 __global__ __launch_bounds__(kFusedThreads) void ks_chain_mfma_kernel(FusedChain fc) {
   extern __shared__ __attribute__((aligned(16))) float lds[];
@@ -128,8 +194,15 @@ __global__ __launch_bounds__(kFusedThreads) void ks_chain_mfma_kernel(FusedChain
   };
   KW ka[BT][BT], kb[BT][BT];
   mfma_kload<T, BT, KVEC>(ka, kblock(fc.nf - 1, w), n, g);
-  fused_load<T, LAYOUT, VEC, FusedPitchAddr, NC>(fc, lds, col0, FusedPitchAddr{P});
-  __syncthreads();
+  if (fc.d[fc.nf - 1] == 1) {
+    // The first factor's blocks are runs of B consecutive rows (d = 1): each
+    // wavefront loads exactly the rows of its own blocks (w, w + W, ...) and
+    // starts on them without waiting for the others.
+    wave_load_blocks<T, LAYOUT, VEC, B, NC>(fc, lds, col0, w, fused_mfma_blocks(fc, fc.nf - 1));
+  } else {
+    fused_load<T, LAYOUT, VEC, FusedPitchAddr, NC>(fc, lds, col0, FusedPitchAddr{P});
+    __syncthreads();
+  }
   for (int f = fc.nf - 1; f >= 0; --f) {
     const int nb = fused_mfma_blocks(fc, f), step = fc.d[f] * P;
     for (int ij = w; ij < nb; ij += 2 * W) {

@@ -367,11 +367,10 @@ bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, in
     inplace = inplace && f[q].b == f[q].c;
   }
   if (!small && !square16) return false;
-  // The MFMA form: batch-size-first, tiles of 16 batch columns (a contiguous
-  // run of X and Y); batch-size-last only in fp32, with tiles of 32 columns,
-  // whose row pieces are whole 128-byte lines.  Narrower pieces (16-bit
-  // types, or 16 fp32 columns) are read and written faster by the
-  // factor-by-factor kernels, which run along the batch.
+  // The MFMA form: batch-size-first in every type; batch-size-last only in
+  // fp32, with tiles of 32 columns, whose row pieces are whole 128-byte lines.
+  // Narrower pieces (16-bit types, or 16 fp32 columns) are read and written
+  // faster by the factor-by-factor kernels, which run along the batch.
   const bool wide_fits = wmax * (2 * kFusedCols + 4) * 4 <= kFusedMaxLds && f[0].b <= 32;
   if (!small && layout != KS_LAYOUT_BSF && !(dtype == KS_F32 && wide_fits)) return false;
   const int64_t kbuf = small ? kFusedKValues : 0;
@@ -388,8 +387,11 @@ bool chain_fused_plan(const ks_factor_t* f, int n, int64_t batch, int layout, in
   fc->mfma = small ? 0 : 1;
   fc->cols = kFusedCols;
   fc->pitch = kFusedPitch;
-  // MFMA form, batch-size-last: tiles of 32 columns
-  if (!small && layout != KS_LAYOUT_BSF) {
+  // MFMA form in fp32: tiles of 32 columns when they fit (batch-size-last
+  // always; batch-size-first when the tile's 16-byte pieces per batch row
+  // come in groups of 4, which its coalesced load and store order needs)
+  if (!small && dtype == KS_F32 && wide_fits &&
+      (layout != KS_LAYOUT_BSF || (fc->width_in % 16 == 0 && fc->width_out % 16 == 0))) {
     fc->cols = 2 * kFusedCols;
     fc->pitch = 2 * kFusedCols + 4;
   }

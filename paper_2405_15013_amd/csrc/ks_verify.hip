@@ -735,9 +735,42 @@ bool verify_fused_io(FusedChecker& ck, const FusedChain& fc, int width, int E, b
 // in_row(16ct + 4g + t), writes rows out_row(16kt + 4g + r), all at column n
 // (the kernel addresses them as in_row(4g) plus multiples of d).  Replays
 // every wavefront's blocks and every lane's accesses.
-bool verify_fused_mfma(FusedChecker& ck, const FusedChain& fc) {
+bool verify_fused_mfma(FusedChecker& ck, const FusedChain& fc, int dtype) {
   constexpr int W = kFusedThreads / 64;
   if (!fc.inplace) return ck.fail("MFMA form not in place", 0);
+  // Per-wavefront load of the first factor's blocks (d = 1): each X element
+  // of the batch read once, by the wavefront whose blocks hold its row, in
+  // both access forms.
+  if (fc.d[fc.nf - 1] == 1) {
+    const int f = fc.nf - 1, B = fc.b[f], NC = fc.cols, nb = fused_mfma_blocks(fc, f), N = fc.width_in;
+    const int esize = dtype == F32 ? 4 : 2;
+    const int64_t Bt = fc.batch;
+    const bool bsl = fc.layout == BSL;
+    const bool vec_ok = bsl ? Bt % (16 / esize) == 0 : N % (16 / esize) == 0;
+    std::vector<uint8_t> xin((size_t)Bt * N);
+    for (int form = 0; form < (vec_ok ? 2 : 1); ++form) {
+      const int EP = form ? 16 / esize : 1, PPB = B * NC / EP, PPL = (PPB + 63) / 64;
+      std::fill(xin.begin(), xin.end(), 0);
+      for (int64_t col0 = 0; col0 < Bt; col0 += NC)
+        for (int w = 0; w < W; ++w)
+          for (int ij = w; ij < nb; ij += W)
+            for (int i = 0; i < PPL; ++i)
+              for (int lane = 0; lane < 64; ++lane) {
+                const int p = i * 64 + lane;
+                if (p >= PPB) continue;
+                int r, c;
+                fused_block_piece(fc.layout, B, NC, EP, p, &r, &c);
+                if (r < 0 || r + (bsl ? 0 : EP - 1) >= B || c < 0 || c + (bsl ? EP - 1 : 0) >= NC)
+                  return ck.fail("block piece outside the block", p);
+                if (col0 + c >= Bt) continue;
+                const int64_t off = bsl ? (int64_t)(ij * B + r) * Bt + col0 + c : (col0 + c) * N + ij * B + r;
+                if (EP > 1 && off % EP) return ck.fail("block piece not aligned to its size", off);
+                for (int e = 0; e < EP; ++e) xin[(size_t)(off + (bsl ? e : e))]++;
+              }
+      for (size_t e = 0; e < xin.size(); ++e)
+        if (xin[e] != 1) return ck.fail("X element not loaded exactly once by the block loads", (int64_t)e);
+    }
+  }
   for (int f = fc.nf - 1; f >= 0; --f) {
     const int a = fc.a[f], b = fc.b[f], d = fc.d[f];
     if (b != fc.c[f] || b % 16 || b < 16 || b > kFusedMfmaMaxB) return ck.fail("MFMA form block not square 16..64", f);
@@ -983,7 +1016,7 @@ bool verify_fused(FusedChecker& ck, const FusedChain& fc, int dtype) {
     }
     if (next != -1) return ck.fail("passes do not cover the chain", next);
   }
-  if (fc.mfma) return verify_fused_mfma(ck, fc);
+  if (fc.mfma) return verify_fused_mfma(ck, fc, dtype);
   for (int q = 0; q < fc.npass; ++q) {
     if (fused_is_radix(fc, q)) {
       // Radix pass: every unit's P rows in range, the groups partition the

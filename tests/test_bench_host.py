@@ -161,3 +161,22 @@ def test_kernel_family_hash_covers_its_sources_only():
     files = [os.path.basename(p) for p in bench._include_closure(
         [os.path.join(bench.ROOT, "paper_2405_15013_amd", "csrc", "ks_dma_f32_v1.hip")])]
     assert "ks_dma.h" in files and "ks_direct.h" in files and "ks_fp8.hip" not in files
+
+
+def test_chain_summary_tables(tmp_path):
+    stats = tmp_path / "stats.csv"
+    stats.write_text('"Name","Calls","TotalDurationNs","AverageNs","Percentage","MinNs","MaxNs","StdDev"\n'
+                     '"void ks::(anonymous namespace)::ks_chain_bfly_kernel<float, 1, true, 5, 5>(ks::FusedChain)",'
+                     '20,200000,10000.0,50.0,9000,11000,100.0\n'
+                     '"void ks::(anonymous namespace)::ks_dma_kernel<float, 4, true, 1, 4, 4, 2>(ks::Problem)",'
+                     '5,100,20.0,1.0,10,30,1.0\n')
+    recs = tmp_path / "chains.jsonl"
+    recs.write_text(json.dumps({"chain": [[1, 2, 2, 1]] * 10, "batch": 4096, "dtype": "f32", "layout": "bsl",
+                                "path": "fused-bfly", "us": 11.9, "launch_us_median": 14.0,
+                                "fused_lower_bound_us": 4.2, "frac_fused_bound": 0.353}) + "\n")
+    out = tmp_path / "out.md"
+    bench.chain_summary(str(stats), str(recs), str(out), ["python3 bench.py --chains chains.jsonl"])
+    text = out.read_text()
+    assert "| butterfly 10 | 4096 | f32 | BSL | fused-bfly | 11.90 | 14.00 | 4.20 | 0.353 |" in text
+    assert "`void ks::ks_chain_bfly_kernel<float, 1, true, 5, 5>(ks::FusedChain)` | 20 | 10.00 | 9.00 | 11.00 |" in text
+    assert "ks_dma_kernel" not in text

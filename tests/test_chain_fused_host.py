@@ -55,10 +55,10 @@ def test_fused_chain_replay(name, layout, dtype, batch):
         # tiles of 32 columns (blocks up to 32, width up to 1024)
         pats = CHAINS[name]
         wide = pats[0][1] <= 32 and pats[0][0] * pats[0][1] * pats[0][3] <= 1024
-        if layout == "bsf":
-            assert desc.startswith("fused-mfma") and desc.endswith("cols=16"), desc
-        elif dtype == "f32" and wide:
+        if dtype == "f32" and wide:
             assert desc.startswith("fused-mfma") and desc.endswith("cols=32"), desc
+        elif layout == "bsf":
+            assert desc.startswith("fused-mfma") and desc.endswith("cols=16"), desc
         else:
             assert desc.startswith("unfused"), desc
 
@@ -81,7 +81,10 @@ def test_which_chains_fuse():
     mon = factors([(1, 32, 32, 32), (32, 32, 32, 1)])
     for dtype in ("f32", "bf16", "f16"):
         desc = ks.ks_chain_describe(mon, 16384, "bsf", dtype)
-        assert desc.startswith("fused-mfma ") and "inplace=1" in desc and "lds=81920 " in desc and "cols=16" in desc, desc
+        if dtype == "f32":  # fp32: tiles of 32 columns (144 KB of LDS)
+            assert desc.startswith("fused-mfma ") and "inplace=1" in desc and "lds=147456 " in desc and "cols=32" in desc, desc
+        else:
+            assert desc.startswith("fused-mfma ") and "inplace=1" in desc and "lds=81920 " in desc and "cols=16" in desc, desc
         desc = ks.ks_chain_describe(mon, 16384, "bsl", dtype)
         if dtype == "f32":
             assert desc.startswith("fused-mfma ") and "lds=147456 " in desc and desc.endswith("grid=512 block=512 cols=32"), desc
