@@ -9,14 +9,16 @@ where erfcx(z) = exp(z^2) erfc(z).  R is smooth on the whole interval (it tends
 to -log2(2 sqrt(pi)) as u -> 0), so a low-degree polynomial fits it to near
 single precision.  This script fits R by Chebyshev interpolation over
 |x| <= 16 (beyond which x Phi(-|x|) underflows in fp32) and prints the
-monomial coefficients R(u) = sum_k C[k] u^k as float literals.
+monomial coefficients R(u) = sum_k C[k] u^k as float literals: degree 9 for
+fp32 outputs, degree 5 for 16-bit outputs.
 
 Run: python gelu_fit.py   (numpy + scipy; writes nothing)
 """
 import numpy as np
 from scipy.special import erfcx
 
-DEGREE = 9
+DEGREE = 9          # fp32 outputs (kGeluR*)
+DEGREE_16BIT = 5    # 16-bit outputs (kGeluS*)
 XMAX = 16.0
 NODES = 800
 
@@ -40,7 +42,8 @@ def fit(degree=DEGREE):
 
 
 if __name__ == "__main__":
-    c, err = fit()
-    print("// max |R_fit - R| over |x| <= %g: %.2e (log2 units)" % (XMAX, err))
-    for k, v in enumerate(c):
-        print("constexpr float kGeluR%d = %.9gf;" % (k, v))
+    for degree, name in ((DEGREE, "kGeluR"), (DEGREE_16BIT, "kGeluS")):
+        c, err = fit(degree)
+        print("// degree %d: max |R_fit - R| over |x| <= %g: %.2e (log2 units)" % (degree, XMAX, err))
+        for k, v in enumerate(c):
+            print("constexpr float %s%d = %.9gf;" % (name, k, v))

@@ -201,7 +201,7 @@ __device__ __forceinline__ void direct_store(const Problem& p, const DItem& it, 
         }
         if (gelu) {
 #pragma unroll
-          for (int u = 0; u < YPE; ++u) y[u] = gelu_f32(y[u]);
+          for (int u = 0; u < YPE; ++u) y[u] = gelu_f32<T>(y[u]);
         }
       }
       uint32_t w[YPB / 4];

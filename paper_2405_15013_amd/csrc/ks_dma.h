@@ -272,7 +272,7 @@ void ks_dma_kernel(Problem p, StagedTile t) {
 #pragma unroll
         for (int e = 0; e < V; ++e)
 #pragma unroll
-          for (int r4 = 0; r4 < 4; ++r4) acc[u][mt][e][r4] = gelu_f32(acc[u][mt][e][r4]);
+          for (int r4 = 0; r4 < 4; ++r4) acc[u][mt][e][r4] = gelu_f32<T>(acc[u][mt][e][r4]);
   }
   __syncthreads();  // every wavefront is done with the stage buffers
   char* ycell0 = smem + dma_y_lds_lane(p, t, si, MT, S, n, g);

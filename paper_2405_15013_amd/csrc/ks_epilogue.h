@@ -38,6 +38,16 @@ constexpr float kGeluR7 = 235.065887f;
 constexpr float kGeluR8 = -269.774841f;
 constexpr float kGeluR9 = 113.810883f;
 
+// Degree 5 (gelu_fit.py, same fit): |R_fit - R| <= 1.2e-5 in log2 units, a
+// relative error of 8e-6 in the tail, far below the precision of 16-bit
+// outputs (bf16 2^-8, fp16 2^-11); used when the result is stored in 16 bits.
+constexpr float kGeluS0 = -1.82723665f;
+constexpr float kGeluS1 = 2.93737769f;
+constexpr float kGeluS2 = 1.46866286f;
+constexpr float kGeluS3 = 5.47383213f;
+constexpr float kGeluS4 = -16.3639202f;
+constexpr float kGeluS5 = 10.5570784f;
+
 // Exact GELU without branches.  With z = |x| / sqrt 2 and u = 1 / (2 + z),
 // the normal tail is Phi(-|x|) = erfc(z) / 2 = u * 2^(-log2(e) x^2 / 2 + R(u))
 // where R(u) = log2(exp(z^2) erfc(z) / (2u)) is smooth on (0, 1/2] (fitted
@@ -45,21 +55,33 @@ constexpr float kGeluR9 = 113.810883f;
 // GELU(x) = max(x, 0) - |x| Phi(-|x|).  The tail keeps its relative accuracy
 // (no 1 + erf cancellation); x is clamped to [-16, 16] for the tail only,
 // where Phi(-16) already underflows, so GELU(+inf) = +inf and GELU(-inf) = -0.
-// Cost: 16 VALU operations, one v_rcp_f32 and one v_exp_f32.
+// Cost: 16 VALU operations, one v_rcp_f32 and one v_exp_f32 (12 VALU with
+// the degree-5 R for 16-bit outputs, OUT the type the result is stored in).
+template <typename OUT = float>
 __device__ __forceinline__ float gelu_f32(float x) {
   const float xc = __builtin_amdgcn_fmed3f(x, -16.0f, 16.0f);
   const float ax = __builtin_fabsf(xc);
   const float u = __builtin_amdgcn_rcpf(__builtin_fmaf(ax, 0.70710678118654752f, 2.0f));
-  float r = kGeluR9;
-  r = __builtin_fmaf(r, u, kGeluR8);
-  r = __builtin_fmaf(r, u, kGeluR7);
-  r = __builtin_fmaf(r, u, kGeluR6);
-  r = __builtin_fmaf(r, u, kGeluR5);
-  r = __builtin_fmaf(r, u, kGeluR4);
-  r = __builtin_fmaf(r, u, kGeluR3);
-  r = __builtin_fmaf(r, u, kGeluR2);
-  r = __builtin_fmaf(r, u, kGeluR1);
-  r = __builtin_fmaf(r, u, kGeluR0);
+  float r;
+  if constexpr (sizeof(OUT) == 4) {
+    r = kGeluR9;
+    r = __builtin_fmaf(r, u, kGeluR8);
+    r = __builtin_fmaf(r, u, kGeluR7);
+    r = __builtin_fmaf(r, u, kGeluR6);
+    r = __builtin_fmaf(r, u, kGeluR5);
+    r = __builtin_fmaf(r, u, kGeluR4);
+    r = __builtin_fmaf(r, u, kGeluR3);
+    r = __builtin_fmaf(r, u, kGeluR2);
+    r = __builtin_fmaf(r, u, kGeluR1);
+    r = __builtin_fmaf(r, u, kGeluR0);
+  } else {
+    r = kGeluS5;
+    r = __builtin_fmaf(r, u, kGeluS4);
+    r = __builtin_fmaf(r, u, kGeluS3);
+    r = __builtin_fmaf(r, u, kGeluS2);
+    r = __builtin_fmaf(r, u, kGeluS1);
+    r = __builtin_fmaf(r, u, kGeluS0);
+  }
   // -log2(e)/2 * x^2 + R(u)
   const float t = __builtin_fmaf(xc * -0.72134752044448170f, xc, r);
   const float tail = u * __builtin_amdgcn_exp2f(t);
@@ -70,7 +92,7 @@ __device__ __forceinline__ float gelu_f32(float x) {
 template <typename T>
 __device__ __forceinline__ float epilogue_apply(const Problem& p, float v, int64_t m) {
   if (p.bias != nullptr) v += bias_value<T>(p, m);
-  if (epilogue_gelu(p)) v = gelu_f32(v);
+  if (epilogue_gelu(p)) v = gelu_f32<T>(v);
   return v;
 }
 

@@ -231,7 +231,7 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
 #pragma unroll
       for (int r = 0; r < 4; ++r)
 #pragma unroll
-        for (int e = 0; e < V; ++e) acc[mt][e][r] = gelu_f32(acc[mt][e][r]);
+        for (int e = 0; e < V; ++e) acc[mt][e][r] = gelu_f32<bf16_t>(acc[mt][e][r]);
   }
 
 #pragma unroll

@@ -149,7 +149,7 @@ __global__ __launch_bounds__(256) void ks_masked_kernel(Problem p, MaskedTile t)
 #pragma unroll
       for (int r = 0; r < 4; ++r)
 #pragma unroll
-        for (int e = 0; e < V; ++e) acc[0][e][r] = gelu_f32(acc[0][e][r]);
+        for (int e = 0; e < V; ++e) acc[0][e][r] = gelu_f32<T>(acc[0][e][r]);
     }
   } else {
     mfma_results_settle();

@@ -221,7 +221,7 @@ __global__ __launch_bounds__(512) void ks_staged_kernel(Problem p, StagedTile t)
 #pragma unroll
         for (int e = 0; e < V; ++e)
 #pragma unroll
-          for (int r4 = 0; r4 < 4; ++r4) acc[mt][e][r4] = gelu_f32(acc[mt][e][r4]);
+          for (int r4 = 0; r4 < 4; ++r4) acc[mt][e][r4] = gelu_f32<T>(acc[mt][e][r4]);
     }
     const int r = 16 * si.rs + n;
 #pragma unroll

@@ -97,7 +97,7 @@ __global__ __launch_bounds__(256) void ks_valu_bsl_kernel(Problem p) {
       }
       if (epilogue_gelu(p)) {
 #pragma unroll
-        for (int e = 0; e < VEC; ++e) acc[e] = gelu_f32(acc[e]);
+        for (int e = 0; e < VEC; ++e) acc[e] = gelu_f32<T>(acc[e]);
       }
       store_vec<T, VEC>(y + yrow0 * batch + k * ystep + (size_t)v * VEC, acc);
     }
@@ -153,7 +153,7 @@ __global__ __launch_bounds__(256) void ks_valu_bsf_kernel(Problem p) {
     }
     if (epilogue_gelu(p)) {
 #pragma unroll
-      for (int e = 0; e < V; ++e) acc[e] = gelu_f32(acc[e]);
+      for (int e = 0; e < V; ++e) acc[e] = gelu_f32<T>(acc[e]);
     }
     store_vec<T, V>(ys + (size_t)k * d, acc);
   }

@@ -22,16 +22,17 @@ ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 CSRC = os.path.join(ROOT, "paper_2405_15013_amd", "csrc")
 
 
-def header_coefficients():
+def header_coefficients(prefix="kGeluR"):
     text = open(os.path.join(CSRC, "ks_epilogue.h")).read()
-    found = dict(re.findall(r"constexpr float kGeluR(\d+) = ([-0-9.e+]+)f;", text))
+    found = dict(re.findall(r"constexpr float %s(\d+) = ([-0-9.e+]+)f;" % prefix, text))
     return np.array([np.float32(found[str(k)]) for k in range(len(found))], dtype=np.float32)
 
 
-def gelu_f32_emulated(x):
+def gelu_f32_emulated(x, prefix="kGeluR"):
+    """prefix kGeluR: fp32 outputs (degree 9); kGeluS: 16-bit outputs (degree 5)."""
     f = np.float32
     x = np.asarray(x, dtype=np.float32)
-    c = header_coefficients()
+    c = header_coefficients(prefix)
 
     def fma(a, b, d):
         return (a.astype(np.float64) * b.astype(np.float64) + np.float64(d) if np.ndim(d) == 0
@@ -56,6 +57,30 @@ def test_coefficients_match_fit_script():
     fitted, err = mod.fit()
     assert err < 2e-7
     np.testing.assert_array_equal(fitted, header_coefficients())
+    fitted, err = mod.fit(mod.DEGREE_16BIT)
+    assert err < 2e-5 and len(fitted) == 6
+    np.testing.assert_array_equal(fitted, header_coefficients("kGeluS"))
+
+
+def test_gelu_16bit_form_accuracy():
+    # the degree-5 tail for 16-bit outputs: errors far below the output's own
+    # rounding (bf16: 2^-9 relative, fp16: 2^-12) and below 1e-5 of max(1, |x|)
+    x = np.linspace(-17.0, 17.0, 1_000_001).astype(np.float32)
+    y = gelu_f32_emulated(x, "kGeluS").astype(np.float64)
+    x64 = x.astype(np.float64)
+    ref = 0.5 * x64 * erfc(-x64 / np.sqrt(2.0))
+    err = np.abs(y - ref)
+    assert np.max(err / np.maximum(1.0, np.abs(x64))) < 2e-6
+    mask = np.abs(ref) > 1e-30
+    assert np.max(err[mask] / np.abs(ref[mask])) < 4e-5
+    # rounded to fp16, every result is the correctly rounded value or its
+    # neighbour (one ulp), and 999 in 1000 or more are the correctly rounded one
+    y16 = y.astype(np.float16) + np.float16(0)  # -0 -> +0
+    r16 = ref.astype(np.float16) + np.float16(0)
+    ulps = np.abs(y16.view(np.int16).astype(np.int64) - r16.view(np.int16).astype(np.int64))
+    same_sign = np.sign(y16) == np.sign(r16)
+    assert np.all(ulps[same_sign] <= 1)
+    assert np.mean(ulps != 0) < 2e-3
 
 
 def test_gelu_accuracy_dense_grid():
