@@ -18,9 +18,10 @@
 //
 // Factor values: the 16 lanes of a wavefront row work on the 16 columns of
 // one unit and need the same blocks, so lane i fetches the unit's i-th block
-// of each factor (one 16- or 8-byte load per factor, issued before X) into
-// registers and each butterfly takes its block's values from the owning lane
-// by DPP row broadcast; the factor values never go through LDS.
+// of each factor (one 16- or 8-byte load per factor: pass A's after the
+// wavefront's X loads, pass B's before the barrier) into registers and each
+// butterfly takes its block's values from the owning lane by DPP row
+// broadcast; the factor values never go through LDS.
 #include <type_traits>
 
 #include "ks_chain_fused.h"
@@ -121,8 +122,9 @@ __global__ __launch_bounds__(kFusedThreads) void ks_chain_bfly_kernel(FusedChain
 
   // Pass A, rows u*PA + r of column n.  Each wavefront loads exactly the rows
   // of its own four units, as pieces regrouped by column through its own LDS
-  // rows, so it starts as soon as its own loads arrive.  Steps s = 0 .. LA-1 (factor
-  // L-1-s, d = 2^s): block (R >> (s+1), R mod d) mixes rows R and R + d.
+  // rows, so it starts as soon as its own loads arrive.  Steps s = 0 .. LA-1
+  // (factor L-1-s, d = 2^s): block (R >> (s+1), R mod d) mixes rows R and
+  // R + d.
   if (4 * w < PB) {
     float x[PA];
     if (LAYOUT == BSL) {
