@@ -33,6 +33,7 @@ CHAINS = {
     "monarch256": [(1, 16, 16, 16), (16, 16, 16, 1)],
     "square48": [(16, 48, 48, 1), (1, 48, 48, 16), (4, 48, 48, 4)],
     "square64": [(2, 64, 64, 8), (16, 64, 64, 1)],
+    "square_wide": [(1, 16, 16, 128), (128, 16, 16, 1)],  # width 2048: 160 KB of LDS, one workgroup per CU
 }
 
 
