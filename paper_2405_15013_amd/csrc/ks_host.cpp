@@ -145,6 +145,14 @@ bool plan_auto(const Problem& p, bool al16, Plan* pl) {
   const int64_t xy_bytes = (int64_t)p.batch * (p.N + p.M) * (p.dtype == F32 ? 4 : 2);
   if (p.layout == BSF && (p.d >= 4 || xy_bytes >= (8 << 20)) && plan_dma(p, al16, pl)) return true;
   if (p.layout == BSF && p.d >= 4 && plan_staged(p, al16, pl)) return true;
+  // Batch-size-last: the DMA kernel for fp32, and for 16-bit types with b a
+  // power of two from 32 and c of 32 or 64 (measured on the sampled sweep
+  // points: fp32 sweep median 0.437 -> 0.549 at batch 25088 and 0.367 ->
+  // 0.412 at 4096; for 16-bit types elsewhere, where the k-groups of b = 48
+  // or 96 re-read X or the stages of 32 values of l leave too few tiles, the
+  // register-direct kernel is faster).
+  const bool bsl_dma = p.dtype == F32 || ((p.b & (p.b - 1)) == 0 && p.b >= 32 && p.c <= 64);
+  if (p.layout == BSL && bsl_dma && plan_dma(p, al16, pl)) return true;
   if (plan_direct(p, al16, pl)) return true;
   if (p.layout == BSL && plan_valu_bsl(p, al16, pl)) return true;
   if (p.layout == BSF && plan_valu_bsf(p, al16, pl)) return true;
@@ -282,6 +290,10 @@ std::string kernel_name(const Problem& p, const Plan& pl) {
                pl.unroll ? "true" : "false", pl.waves_m, pl.cps);
       break;
     case V_DMA:
+      if (p.layout == BSL) {
+        snprintf(buf, sizeof buf, "ks_dma_bsl_kernel<%s,%d,%d,%s>", t, pl.waves_m, pl.rs, epi);
+        break;
+      }
       // DMA instructions per wavefront per stage: 16*rs rows of lch*d*esize
       // bytes over four wavefronts of 64 16-byte lanes.
       snprintf(buf, sizeof buf, "ks_dma_kernel<%s,%d,%s,%d,%d,%d,%d>", t, pl.vec, pl.unroll ? "true" : "false",

@@ -55,8 +55,8 @@ struct StagedTile {
   // DMA kernel: log2 of the power-of-two sizes, and multiply-shift constants
   // for the divisions of the tile decode (div_fast, ks_divide.h).
   int lUR, lRS, lJG, lUY;
-  uint32_t mkgt, mnbt;
-  int skgt, snbt;
+  uint32_t mkgt, mnbt, md;
+  int skgt, snbt, sd;
 };
 
 
@@ -187,7 +187,7 @@ KS_HD int64_t staged_y_unit(const Problem& p, const StagedTile& t, const STile& 
 }
 
 // ---- LDS-DMA stages (ks_dma.h) ---------------------------------------------
-// Batch-size-first only.  A stage buffer holds 16*RS*NT rows of UR 16-byte
+// Batch-size-first (the batch-size-last form follows further down).  A stage buffer holds 16*RS*NT rows of UR 16-byte
 // units with no padding; logical unit v of row r sits at physical unit
 // v ^ swizzle(r) of that row, which puts the same logical unit of 16
 // consecutive rows (what an operand read touches) at 16 distinct 16-byte
@@ -266,5 +266,57 @@ KS_HD int64_t dma_y_tile_base(const Problem& p, const StagedTile& t, const STile
   return (int64_t)s.bt * 16 * t.RS * t.NT * p.M + (int64_t)s.i * p.b * p.d + (int64_t)s.kt * t.KGW * 16 * MT * p.d;
 }
 KS_HD int dma_y_row(const Problem& p, int row, int v, int esize) { return row * p.M + v * (16 / esize); }
+
+// ---- LDS-DMA stages, batch-size-last (ks_dma_bsl.h) --------------------------
+// A tile is 16*V*RS consecutive batch entries (V = 16 / esize: one 16-byte
+// unit per lane column) of one (i, j), and KGW k-groups of 16*MT rows; the
+// four wavefronts take rs = w % RS, kgw = w / RS.  A stage buffer holds the
+// input rows of CH consecutive values of l, each the tile's UR = 16*RS units
+// of one row of X (unpadded: the sixteen lanes of an operand read take one
+// row's 256 contiguous bytes).  DMA instruction m of wavefront w writes the
+// 64 physical units (m*W + w)*64 + lane: stage row P / UR, unit P % UR.
+KS_HD void dma_bsl_unit_of(const StagedTile& t, int P, int* r, int* v) {
+  *r = (int)((uint32_t)P >> t.lUR);
+  *v = (int)((uint32_t)P & (uint32_t)(t.UR - 1));
+}
+// X element offset of unit v of stage row r, relative to the stage's first
+// row: the unit holds batch entries bt*16*V*RS + V*v .. + V of row
+// i*c*d + (ls + r)*d + j (the stage and i parts, (i*c*d + ls*d) * batch, are
+// added by the kernel as pointer steps).  Units beyond the batch read the
+// last unit of the row instead (the batch is a multiple of V).
+KS_HD int dma_bsl_src(const Problem& p, const StagedTile& t, const STile& s, int V, int r, int v) {
+  int beta = s.bt * 16 * V * t.RS + V * v;
+  if (beta >= p.batch) beta = p.batch - V;
+  return (r * p.d + s.j) * p.batch + beta;
+}
+// LDS byte offset (within a stage buffer) of operand piece q of lane (n, g):
+// stage row LP*g + q (value l of the MFMA chunk), the lane's unit 16*rs + n.
+KS_HD int dma_bsl_op_byte(const StagedTile& t, const SItem& it, int LP, int n, int g, int q) {
+  return ((LP * g + q) * t.UR + 16 * it.rs + n) * 16;
+}
+// Tile and work item with multiply-shift divisions (staged_tile and
+// staged_item for batch-size-last; the verifier compares them).
+KS_HD STile dma_bsl_tile(const Problem& p, const StagedTile& t, int block) {
+  const uint32_t tile = t.remap ? (uint32_t)staged_remap(block, t.tiles) : (uint32_t)block;
+  STile s;
+  const uint32_t q1 = div_fast(tile, t.mkgt, t.skgt);
+  s.kt = (int)(tile - q1 * (uint32_t)t.kgt);
+  const uint32_t q2 = div_fast(q1, t.mnbt, t.snbt);
+  s.bt = (int)(q1 - q2 * (uint32_t)t.nbt);
+  const uint32_t q3 = div_fast(q2, t.md, t.sd);
+  s.j = (int)(q2 - q3 * (uint32_t)p.d);
+  s.i = (int)q3;
+  return s;
+}
+KS_HD SItem dma_bsl_item(const StagedTile& t, const STile& s, int V, int MT, int w) {
+  SItem it;
+  it.rs = w & (t.RS - 1);
+  it.jg = 0;
+  it.kgw = w >> t.lRS;
+  it.k0 = (s.kt * t.KGW + it.kgw) * 16 * MT;
+  it.j0 = s.j;
+  it.beta0 = s.bt * 16 * V * t.RS + it.rs * 16 * V;
+  return it;
+}
 
 }  // namespace ks

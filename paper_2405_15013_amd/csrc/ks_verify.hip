@@ -494,8 +494,114 @@ bool verify_staged(Checker& ck, const Plan& pl) {
 // in-bounds, 16-byte aligned X address; every operand piece a lane reads from
 // the swizzled stage holds the X values its products need; K, the output
 // tile and the Y stores as in the staged kernel.
+// Batch-size-last DMA kernel (ks_dma_bsl.h): every stage's DMA units land on
+// distinct LDS cells inside the buffer, each operand piece a lane reads holds
+// the X values its products need, K operands inside the block, the stage
+// buffers inside the allocation, and every Y element written once by the
+// register-direct store.
+bool verify_dma_bsl(Checker& ck, const Plan& pl) {
+  const Problem& p = ck.p;
+  const StagedTile t = staged_tile_of(p, pl);
+  const int S = p.dtype == F32 ? 4 : 2, V = 16 / S, LP = S == 4 ? 4 : 8, CH = 4 * LP, MT = pl.waves_m;
+  if (pl.vec != V || pl.unroll != 0 || pl.cps != LP) return ck.fail("bad vector or lane depth", pl.vec);
+  if (p.batch % V) return ck.fail("batch not a multiple of the vector width", p.batch);
+  if (MT < 1 || MT > (S == 4 ? 4 : 2)) return ck.fail("no instance for this MT", MT);
+  if (t.W != 4 || t.RS * t.KGW != t.W || t.JG != 1 || (t.RS != 1 && t.RS != 2 && t.RS != 4))
+    return ck.fail("waves do not split the tile", t.W);
+  if (t.kgt * t.KGW * 16 * MT != p.b) return ck.fail("k-groups do not cover b", p.b);
+  if (t.LCH != CH || p.c % CH) return ck.fail("stages do not cover c", t.LCH);
+  if (t.UR != 16 * t.RS || (1 << t.lUR) != t.UR || (1 << t.lRS) != t.RS)
+    return ck.fail("stage row is not the tile's units", t.UR);
+  if (t.stage != CH * t.UR * 16 || t.UD * 64 * t.W * 16 != t.stage) return ck.fail("stage is not whole DMA instructions", t.stage);
+  if ((int)pl.grid != t.tiles || (int)pl.block != 64 * t.W) return ck.fail("grid does not match the tiles", pl.grid);
+  const int nst = p.c / CH;
+  {
+    int top = 0;
+    for (int s = 0; s < nst; ++s) top = std::max(top, s % 3);
+    if (pl.lds_bytes != t.lds || t.lds < (int64_t)(top + 1) * t.stage || dma_stage_buffers(nst) != top + 1)
+      return ck.fail("LDS allocation does not hold the stage buffers the kernel touches", t.lds);
+  }
+  if (t.remap && t.tiles % 8) return ck.fail("XCD remap needs a multiple of 8 tiles", t.tiles);
+  std::vector<uint8_t> seen(t.tiles, 0);
+  std::vector<int64_t> shadow((size_t)t.stage / S);
+  for (int blk = 0; blk < t.tiles && ck.err.empty(); ++blk) {
+    const STile st = staged_tile(p, t, blk);
+    const int logical = t.remap ? staged_remap(blk, t.tiles) : blk;
+    if (logical < 0 || logical >= t.tiles || seen[logical]++) return ck.fail("tile visited twice", logical);
+    const STile sf = dma_bsl_tile(p, t, blk);
+    if (sf.i != st.i || sf.bt != st.bt || sf.kt != st.kt || sf.j != st.j) return ck.fail("fast tile decode differs", blk);
+    for (int w = 0; w < t.W; ++w) {
+      const SItem a1 = staged_item(p, t, st, V, MT, w), a2 = dma_bsl_item(t, st, V, MT, w);
+      if (a1.rs != a2.rs || a1.kgw != a2.kgw || a1.j0 != a2.j0 || a1.k0 != a2.k0 || a1.beta0 != a2.beta0)
+        return ck.fail("fast work-item decode differs", w);
+    }
+    for (int s = 0; s < nst; ++s) {
+      std::fill(shadow.begin(), shadow.end(), (int64_t)-1);
+      for (int w = 0; w < t.W; ++w)
+        for (int m = 0; m < t.UD; ++m)
+          for (int lane = 0; lane < 64; ++lane) {
+            const int P = dma_phys_unit(t, m, w, lane);
+            if (P < 0 || (P + 1) * 16 > t.stage) return ck.fail("DMA writes outside the stage buffer", P);
+            int r, v;
+            dma_bsl_unit_of(t, P, &r, &v);
+            if (r < 0 || r >= CH || v < 0 || v >= t.UR) return ck.fail("DMA unit outside the stage rows", P);
+            // the kernel's form: X + i*c*d*batch (tile) + s*CH*d*batch (stage) + dma_bsl_src
+            const int64_t src = dma_bsl_src(p, t, st, V, r, v);
+            const int64_t off = (int64_t)st.i * p.c * p.d * p.batch + (int64_t)s * CH * p.d * p.batch + src;
+            if ((off * S) % 16) return ck.fail("DMA source not 16-byte aligned", off);
+            ck.read_x(off, V);
+            for (int e = 0; e < V; ++e) {
+              int64_t& cell = shadow[(size_t)(P * 16 / S + e)];
+              if (cell != -1) return ck.fail("LDS cell written twice in a stage", P);
+              cell = off + e;
+            }
+          }
+      for (int w = 0; w < t.W; ++w) {
+        const SItem si = staged_item(p, t, st, V, MT, w);
+        DItem it;
+        it.i = st.i; it.j0 = si.j0; it.k0 = si.k0; it.beta0 = si.beta0;
+        for (int lane = 0; lane < 64; ++lane) {
+          const int n = lane & 15, g = lane >> 4;
+          const bool valid = direct_lane_valid(p, it, V, n);
+          for (int q = 0; q < LP; ++q) {
+            const int o = dma_bsl_op_byte(t, si, LP, n, g, q);
+            if (o < 0 || o + 16 > t.stage || o % 16) return ck.fail("operand read outside the stage or unaligned", o);
+            for (int e = 0; e < V; ++e) {
+              const int64_t have = shadow[(size_t)(o / S + e)];
+              if (have < 0) return ck.fail("operand read of an LDS cell not written in this stage", o);
+              if (valid && have != expected_x(p, it, V, LP, s * CH, n, g, q * V + e))
+                return ck.fail("operand element is not the X value the product needs", have);
+            }
+          }
+          for (int mt = 0; mt < MT; ++mt) {
+            const int64_t off = direct_k_off(p, it, LP, s * CH, n, g, mt, 0);
+            if ((off * S) % (LP * S)) return ck.fail("K operand not aligned to its size", off);
+            ck.read_k(off, LP);
+          }
+        }
+      }
+    }
+    // Y: the register-direct store of each wavefront's item.
+    for (int w = 0; w < t.W; ++w) {
+      const SItem si = staged_item(p, t, st, V, MT, w);
+      DItem it;
+      it.i = st.i; it.j0 = si.j0; it.k0 = si.k0; it.beta0 = si.beta0;
+      for (int mt = 0; mt < MT; ++mt)
+        for (int lane = 0; lane < 64; ++lane)
+          for (int q = 0; q < 4; ++q) {
+            const int64_t off = direct_y_off(p, it, false, V, S, mt, lane & 15, lane >> 4, q);
+            if (off < 0) continue;
+            if ((off * S) % 16) return ck.fail("Y piece not aligned to 16 bytes", off);
+            ck.write_y(off, V);
+          }
+    }
+  }
+  return ck.err.empty();
+}
+
 bool verify_dma(Checker& ck, const Plan& pl) {
   const Problem& p = ck.p;
+  if (p.layout == BSL) return verify_dma_bsl(ck, pl);
   const StagedTile t = staged_tile_of(p, pl);
   const int V = pl.vec, MT = pl.waves_m, S = p.dtype == F32 ? 4 : 2, LP = pl.cps, CH = 4 * LP, UE = 16 / S;
   const bool strided = pl.unroll != 0;

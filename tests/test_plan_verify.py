@@ -99,15 +99,20 @@ def test_all_sweep_plans_dma(dtype, batch, every):
 
 def test_sweep_plans_use_mfma_kernels():
     """The whole sweep runs on the MFMA kernels (aligned buffers): LDS-DMA for
-    batch-size-first with d >= 4 or at least 8 MB of X and Y, register-direct
-    otherwise."""
+    batch-size-first with d >= 4 or at least 8 MB of X and Y, and for
+    batch-size-last in fp32, or in 16-bit types with b a power of two from 32
+    and c of 32 or 64; register-direct otherwise."""
     for pattern in sweep_patterns()[::7]:
         for layout in ("bsf", "bsl"):
             for dtype in ("f32", "bf16", "f16"):
                 desc = ks.ks_plan_describe(*pattern, 4096, layout, dtype)
                 a, b, c, d = pattern
                 big = 4096 * (a * c * d + a * b * d) * (4 if dtype == "f32" else 2) >= 8 << 20
-                want = "name=dma" if (layout == "bsf" and (d >= 4 or big)) else "name=direct"
+                if layout == "bsf":
+                    dma = d >= 4 or big
+                else:
+                    dma = dtype == "f32" or (b in (32, 64, 128) and c in (32, 64))
+                want = "name=dma" if dma else "name=direct"
                 assert want in desc, (pattern, layout, dtype, desc)
 
 
