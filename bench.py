@@ -100,7 +100,7 @@ def plan_field(desc, key):
 # the .hip files; the .cpp files that plan its launches, which decide the
 # tiles and which calls run it, count too, as does ks_host.cpp).
 KERNEL_FAMILY_SOURCES = {
-    "ks_dma_kernel": "ks_dma_", "ks_direct_c_kernel": "ks_direct_", "ks_direct_kernel": "ks_direct_",
+    "ks_dma_kernel": "ks_dma_", "ks_dma_bsl_kernel": "ks_dma_", "ks_direct_c_kernel": "ks_direct_", "ks_direct_kernel": "ks_direct_",
     "ks_staged_kernel": "ks_staged_", "ks_masked_kernel": "ks_masked_", "ks_fp8_kernel": "ks_fp8",
     "ks_valu_bsl_kernel": "ks_valu", "ks_valu_bsf_kernel": "ks_valu", "ks_generic_kernel": "ks_generic",
     "ks_chain_fused_kernel": "ks_chain_fused", "ks_chain_mfma_kernel": "ks_chain_mfma", "ks_chain_bfly_kernel": "ks_chain_bfly",
