@@ -277,16 +277,44 @@ def test_dma_full_batch(pattern, dtype):
     check(pattern, 25088, dtype, "bsf", cfg=15, variant=VARIANTS["dma"], kdist="normal")
 
 
+# Batch-size-last DMA kernel: b covers MT = 1..4 (fp32) and the RS/KGW splits,
+# c gives 1, 2, 3 and 8 stages of 16 (fp32) or 1, 2, 4 of 32 (16-bit).
+DMA_BSL_SHAPES = [(1, 16, 16, 1), (2, 32, 32, 4), (1, 48, 48, 2), (3, 64, 64, 1), (1, 96, 128, 2),
+                  (1, 128, 96, 1), (2, 64, 32, 8)]
+
+
+@pytest.mark.parametrize("pattern", DMA_BSL_SHAPES)
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("batch", [64, 200, 1000])
+def test_dma_bsl_forced(pattern, dtype, batch):
+    """The batch-size-last LDS-DMA kernel forced: every M-tile count and
+    batch-group split the planner can pick, one to eight stages of l, batches
+    that end inside a tile (columns beyond the batch read clamped units and
+    are not stored)."""
+    a, b, c, d = pattern
+    if dtype != "f32" and c % 32:
+        pytest.skip("16-bit stages hold 32 values of l")
+    check(pattern, batch, dtype, "bsl", cfg=17, variant=VARIANTS["dma"], kdist="normal")
+
+
+@pytest.mark.parametrize("pattern", [(8, 96, 64, 8), (1, 128, 128, 16), (4, 16, 64, 8)])
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_dma_bsl_full_batch(pattern, dtype):
+    """The batch-size-last LDS-DMA kernel at the full batch of 25088 entries
+    (thousands of tiles, XCD remap)."""
+    check(pattern, 25088, dtype, "bsl", cfg=18, variant=VARIANTS["dma"], kdist="normal")
+
+
 @pytest.mark.parametrize("pattern", [(1, 32, 32, 32), (6, 64, 16, 8), (4, 96, 48, 2)])
 @pytest.mark.parametrize("layout", ["bsf", "bsl"])
 def test_every_kernel_family_against_oracle(pattern, layout):
-    """The generic, register-direct, LDS-staged and (batch-size-first,
-    d <= 16) LDS-DMA kernels, each forced on the same inputs and each compared
-    with the fp64 oracle."""
+    """The generic, register-direct, LDS-staged and LDS-DMA (batch-size-first
+    with d <= 16, and batch-size-last) kernels, each forced on the same inputs
+    and each compared with the fp64 oracle."""
     names = ["generic", "direct"]
     if layout == "bsl" or pattern[3] <= 16:  # BSF staging takes d <= 16 (at most 4 j-groups per tile)
         names.append("staged")
-    if layout == "bsf" and pattern[3] in (1, 2, 4, 8, 16):
+    if layout == "bsl" or pattern[3] in (1, 2, 4, 8, 16):
         names.append("dma")
     for name in names:
         check(pattern, 512, "f32", layout, cfg=10, variant=VARIANTS[name], kdist="normal")
@@ -357,6 +385,7 @@ EPI_CASES = [("generic", (2, 4, 4, 2), "bsl", 40), ("valu_bsl", (2, 4, 4, 2), "b
              ("valu_bsf", (4, 2, 2, 8), "bsf", 50), ("direct", (6, 64, 16, 8), "bsl", 256),
              ("direct", (2, 48, 80, 2), "bsf", 72), ("staged", (1, 32, 32, 32), "bsf", 100),
              ("dma", (6, 64, 16, 8), "bsf", 1000), ("dma", (4, 48, 96, 4), "bsf", 72),
+             ("dma", (2, 64, 64, 4), "bsl", 200), ("dma", (1, 128, 32, 2), "bsl", 1000),
              ("masked", (1, 24, 24, 8), "bsl", 100), ("masked", (1, 100, 36, 2), "bsf", 37),
              (None, (6, 64, 16, 8), "bsl", 25088), (None, (6, 16, 64, 8), "bsf", 25088)]
 VARIANTS["masked"] = 7

@@ -116,6 +116,31 @@ def test_sweep_plans_use_mfma_kernels():
                 assert want in desc, (pattern, layout, dtype, desc)
 
 
+@pytest.mark.parametrize("dtype", ["f32", "bf16", "f16"])
+@pytest.mark.parametrize("batch,every", [(72, 3), (1000, 7), (25088, 97)])
+def test_all_sweep_plans_dma_bsl(dtype, batch, every):
+    """The batch-size-last LDS-DMA kernel (forced) on the batch-size-last sweep
+    patterns it accepts (c a multiple of its stage: 16 for fp32, 32 for 16-bit
+    types; the batch a multiple of the vector): DMA units in bounds and each
+    written once per stage, every operand read the X value its products need,
+    every output written once.  It must accept every such pattern."""
+    bad = []
+    ks.ks_force_variant(6)
+    try:
+        for pattern in sweep_patterns()[::every]:
+            a, b, c, d = pattern
+            if c % (16 if dtype == "f32" else 32) or batch % (4 if dtype == "f32" else 8):
+                continue
+            st, rep = ks.ks_plan_verify(*pattern, batch, "bsl", dtype)
+            if st != 0:
+                bad.append((pattern, rep))
+            else:
+                assert "kernel=ks_dma_bsl_kernel" in ks.ks_plan_describe(*pattern, batch, "bsl", dtype)
+    finally:
+        ks.ks_force_variant(None)
+    assert not bad, bad[:5]
+
+
 @pytest.mark.parametrize("variant", [0, 1, 2, 3, 4, 5, 6])
 def test_forced_variants(variant):
     """Every variant that accepts a shape produces a valid launch for it."""
