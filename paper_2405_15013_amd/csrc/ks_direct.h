@@ -35,6 +35,15 @@ typedef _Float16 f16x8_t __attribute__((ext_vector_type(8)));
 typedef short i16x4_t __attribute__((ext_vector_type(4)));
 typedef _Float16 f16x4_t __attribute__((ext_vector_type(4)));
 
+// Puts the problem's sizes and pointers in scalar registers at kernel entry,
+// so that they arrive in the same round of kernel-argument loads as the rest;
+// otherwise the compiler fetches them only after the first branches of the
+// work-item decode, a second memory round trip before the first load of X.
+#define KS_PROBLEM_FIELDS(p)                                                                               \
+  "s"(p.a), "s"(p.b), "s"(p.c), "s"(p.d), "s"(p.batch), "s"(p.N), "s"(p.M), "s"(p.layout), "s"(p.align), \
+      "s"(p.x), "s"(p.y), "s"(p.kv)
+__device__ __forceinline__ void kernarg_fetch(const Problem& p) { asm volatile("" ::KS_PROBLEM_FIELDS(p)); }
+
 // One MFMA step: acc += A * B where each lane supplies LP values of l.
 template <typename T, int LP> struct DMma;
 template <> struct DMma<float, 4> {
@@ -259,8 +268,15 @@ __global__ __launch_bounds__(256) void ks_direct_kernel(Problem p, DirectTile t)
   constexpr int LP = S == 4 ? 4 : 8;
   constexpr int CH = 4 * LP;  // l values per chunk
   const int lane = threadIdx.x & 63;
-  const int item = blockIdx.x * t.waves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  if (item >= t.items) return;  // wave-uniform
+  // A wavefront past the last item (spare waves of the last workgroup) works
+  // on the last item with in-bounds loads and stores nothing.  No branch
+  // precedes the loads, so every kernel argument arrives in one round of
+  // scalar loads instead of one round for the item count and another after
+  // the exit test.
+  const int item0 = blockIdx.x * t.waves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool live = item0 < t.items;  // wave-uniform
+  const int item = live ? item0 : t.items - 1;
+  kernarg_fetch(p);
   const int n = lane & 15, g = lane >> 4;
   const DItem it = direct_item_fast(p, t, V, MT, item);
   const T* __restrict__ x = static_cast<const T*>(p.x);
@@ -303,6 +319,7 @@ __global__ __launch_bounds__(256) void ks_direct_kernel(Problem p, DirectTile t)
     }
   }
 
+  if (!live) return;
   direct_store<T, LAYOUT, V, STRIDED, MT, EPI>(p, it, n, g, acc);
 }
 
@@ -323,8 +340,15 @@ __global__ __launch_bounds__(256) void ks_direct_c_kernel(Problem p, DirectTile 
   constexpr int PD0 = 32 / R;
   constexpr int PD = NCH <= 1 ? 0 : (PD0 < 1 ? 1 : (PD0 > NCH - 1 ? NCH - 1 : PD0));
   const int lane = threadIdx.x & 63;
-  const int item = blockIdx.x * t.waves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  if (item >= t.items) return;  // wave-uniform
+  // A wavefront past the last item (spare waves of the last workgroup) works
+  // on the last item with in-bounds loads and stores nothing.  No branch
+  // precedes the loads, so every kernel argument arrives in one round of
+  // scalar loads instead of one round for the item count and another after
+  // the exit test.
+  const int item0 = blockIdx.x * t.waves + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool live = item0 < t.items;  // wave-uniform
+  const int item = live ? item0 : t.items - 1;
+  kernarg_fetch(p);
   const int n = lane & 15, g = lane >> 4;
   const DItem it = direct_item_fast(p, t, V, MT, item);
   const T* __restrict__ x = static_cast<const T*>(p.x);
@@ -364,6 +388,7 @@ __global__ __launch_bounds__(256) void ks_direct_c_kernel(Problem p, DirectTile 
   }
   if constexpr (TAIL) tl.mma(acc);
 
+  if (!live) return;
   direct_store<T, LAYOUT, V, STRIDED, MT, EPI>(p, it, n, g, acc);
 }
 

@@ -44,6 +44,15 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
+// The problem's and the tile description's fields in scalar registers at
+// kernel entry, in one statement so that they arrive in one round of
+// kernel-argument loads (as kernarg_fetch(Problem) in ks_direct.h).
+__device__ __forceinline__ void kernarg_fetch(const Problem& p, const StagedTile& t) {
+  asm volatile("" ::KS_PROBLEM_FIELDS(p), "s"(t.tiles), "s"(t.remap), "s"(t.kgt), "s"(t.nbt), "s"(t.mkgt),
+               "s"(t.skgt), "s"(t.mnbt), "s"(t.snbt), "s"(t.RS), "s"(t.lRS), "s"(t.JG), "s"(t.lJG), "s"(t.KGW),
+               "s"(t.UR), "s"(t.lUR), "s"(t.stage));
+}
+
 // Workgroup barrier without a memory fence (a fence would wait for every DMA
 // in flight); the empty asm statements keep the compiler from moving memory
 // accesses across it, the scheduling barriers keep the scheduler from doing so.
@@ -106,6 +115,7 @@ void ks_dma_kernel(Problem p, StagedTile t) {
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, g = lane >> 4;
+  kernarg_fetch(p, t);
   const STile st = dma_tile(t, blockIdx.x);
   const SItem si = dma_item(t, st, V, MT, w);
   DItem it;

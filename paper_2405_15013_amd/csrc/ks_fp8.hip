@@ -9,7 +9,7 @@
 // zeros, accesses of V consecutive elements (V bytes of X, 2V bytes of Y).
 #include "ks_direct.h"
 #include "ks_epilogue.h"
-#include "ks_masked_index.h"
+#include "ks_masked.h"
 
 namespace ks {
 
@@ -74,8 +74,12 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
   constexpr int VK = LAYOUT == BSL ? 1 : V;
   using Chunk = Fp8Chunk<V, MT, VK>;
   const int lane = threadIdx.x & 63;
-  const int item = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  if (item >= t.items) return;  // wave-uniform
+  // Spare waves of the last workgroup work on the last item and store
+  // nothing: no branch before the loads, one round of kernel-argument loads.
+  const int item0 = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool live = item0 < t.items;  // wave-uniform
+  const int item = live ? item0 : t.items - 1;
+  kernarg_fetch(p, t);
   const int n = lane & 15, g = lane >> 4;
   const MItem it = masked_item(p, t, V, item);
   // Batch-size-first with V = d, c a multiple of 8 and 16-byte aligned
@@ -200,6 +204,7 @@ __global__ __launch_bounds__(256) void ks_fp8_kernel(Problem p, MaskedTile t) {
     mma(cur);
   }
 
+  if (!live) return;
   // Epilogue: output feature of (mt, e, r) is row k = k0 + 16 mt + 4g + r of
   // block (i, j0 [+ e in BSF]); padding rows (k >= b) take no bias.
   constexpr int BV = LAYOUT == BSF ? V : 1;

@@ -7,6 +7,16 @@
 #include "ks_masked_index.h"
 
 namespace ks {
+// The problem's and the tile description's fields in scalar registers at
+// kernel entry, in one round of kernel-argument loads (as kernarg_fetch of
+// Problem in ks_direct.h).
+__device__ __forceinline__ void kernarg_fetch(const Problem& p, const MaskedTile& t) {
+  asm volatile("" ::KS_PROBLEM_FIELDS(p), "s"(t.mt), "s"(t.kgroups), "s"(t.jgroups), "s"(t.nbt), "s"(t.items),
+               "s"(t.nchunks), "s"(t.kvec));
+}
+}  // namespace ks
+
+namespace ks {
 
 // V consecutive elements of type T (V * sizeof(T) bytes, aligned to that).
 template <typename T, int V>
@@ -51,8 +61,12 @@ __global__ __launch_bounds__(256) void ks_masked_kernel(Problem p, MaskedTile t)
   constexpr int CH = 4 * LP;
   constexpr int VK = LAYOUT == BSL ? 1 : V;  // K blocks per lane (BSF: one per j of the piece)
   const int lane = threadIdx.x & 63;
-  const int item = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-  if (item >= t.items) return;  // wave-uniform
+  // Spare waves of the last workgroup work on the last item and store
+  // nothing: no branch before the loads, one round of kernel-argument loads.
+  const int item0 = blockIdx.x * 4 + __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const bool live = item0 < t.items;  // wave-uniform
+  const int item = live ? item0 : t.items - 1;
+  kernarg_fetch(p, t);
   const int n = lane & 15, g = lane >> 4;
   const MItem it = masked_item(p, t, V, item);
   const T* __restrict__ x = static_cast<const T*>(p.x);
@@ -122,6 +136,7 @@ __global__ __launch_bounds__(256) void ks_masked_kernel(Problem p, MaskedTile t)
     }
     direct_mma<T, LAYOUT, V, 1, LP>(xw, kw, acc);
   }
+  if (!live) return;
   // Epilogue (EPI instances only): output feature of (e, r) is row
   // k = k0 + 4g + r of block (i, j0 [+ e in BSF]); padding rows (k >= b) take
   // no bias.

@@ -37,6 +37,7 @@ struct MItem {
   int i, j0, k0, beta0;
 };
 
+
 // LP values of l per lane and chunk: 4 (fp32, 16x16x4 MFMA), 8 (16-bit and
 // FP8, 16x16x32 MFMAs).
 KS_MHD int masked_lp(int esize) { return esize == 4 ? 4 : 8; }

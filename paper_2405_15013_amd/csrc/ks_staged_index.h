@@ -197,7 +197,9 @@ KS_HD int64_t staged_y_unit(const Problem& p, const StagedTile& t, const STile& 
 // consecutive physical units (m*W + w)*64 + lane, so each lane loads the
 // logical unit that lands there.
 KS_HD int dma_swizzle(const StagedTile& t, int r) {
-  return t.UR >= 16 ? (r & 15) : (int)((((uint32_t)r * (uint32_t)t.UR) >> 4) & (uint32_t)(t.UR - 1));
+  const int wide = r & 15;
+  const int narrow = (int)((((uint32_t)r * (uint32_t)t.UR) >> 4) & (uint32_t)(t.UR - 1));
+  return t.UR >= 16 ? wide : narrow;  // both computed: a select, not a branch
 }
 // Physical unit P of a stage buffer -> row r and logical unit v.
 KS_HD void dma_unit_of(const StagedTile& t, int P, int* r, int* v) {
@@ -225,11 +227,21 @@ KS_HD int dma_op_byte(const Problem& p, const SItem& it, int LP, int V, bool str
 // not allocated (more workgroups fit in a CU's LDS).
 KS_HD int dma_stage_buffers(int nst) { return nst < 3 ? nst : 3; }
 
+// Logical tile of workgroup `block` in the DMA kernels: the XCD remap when
+// t.remap is set, else the identity, selected without a branch (both forms
+// computed), so that the tile count arrives with the other kernel arguments
+// instead of in a second round of scalar loads behind the test of t.remap.
+KS_HD uint32_t dma_tile_index(const StagedTile& t, int block) {
+  const uint32_t rm = (uint32_t)staged_remap(block, t.tiles);
+  const uint32_t mask = 0u - (uint32_t)(t.remap != 0);
+  return (rm & mask) | ((uint32_t)block & ~mask);
+}
+
 // Tile and work item of the DMA kernel: staged_tile and staged_item computed
 // with the multiply-shift divisions and the power-of-two shifts above (the
 // plan verifier checks both against the plain forms for every tile).
 KS_HD STile dma_tile(const StagedTile& t, int block) {
-  const uint32_t tile = t.remap ? (uint32_t)staged_remap(block, t.tiles) : (uint32_t)block;
+  const uint32_t tile = dma_tile_index(t, block);
   STile s;
   const uint32_t q1 = div_fast(tile, t.mkgt, t.skgt);
   s.kt = (int)(tile - q1 * (uint32_t)t.kgt);
@@ -297,7 +309,7 @@ KS_HD int dma_bsl_op_byte(const StagedTile& t, const SItem& it, int LP, int n, i
 // Tile and work item with multiply-shift divisions (staged_tile and
 // staged_item for batch-size-last; the verifier compares them).
 KS_HD STile dma_bsl_tile(const Problem& p, const StagedTile& t, int block) {
-  const uint32_t tile = t.remap ? (uint32_t)staged_remap(block, t.tiles) : (uint32_t)block;
+  const uint32_t tile = dma_tile_index(t, block);
   STile s;
   const uint32_t q1 = div_fast(tile, t.mkgt, t.skgt);
   s.kt = (int)(tile - q1 * (uint32_t)t.kgt);
