@@ -75,3 +75,48 @@ def test_scanner_flags_a_read_at_the_minimum_distance():
     lines = ["v_mfma_f32_16x16x16_bf16 v[0:3], v[4:5], v[6:7], 0", "s_cbranch_scc1 .LBB0_2", "s_nop 7",
              "s_nop 7", ".LBB0_2:", "v_cvt_pk_bf16_f32 v8, v2, v3", "s_endpgm"]
     assert isa_scan.mfma_result_reads(lines)[0][0] == 1  # the branch skips the nops
+
+
+# Kernels whose arguments must arrive in one round of scalar loads (mangled
+# name fragments: length-prefixed identifiers).
+ONE_ROUND_FAMILIES = ("18ks_direct_c_kernel", "16ks_direct_kernel", "17ks_dma_bsl_kernel")
+BSF_DMA = "13ks_dma_kernel"
+
+
+def _argument_rounds(lines):
+    """Waits on the scalar-load counter before the first global load."""
+    waits = 0
+    for line in lines:
+        if line.startswith(("global_load", "buffer_load")):
+            break
+        if line.startswith("s_waitcnt") and "lgkmcnt" in line:
+            waits += 1
+    return waits
+
+
+def test_kernel_arguments_arrive_in_one_round(kernel_asm):
+    """The register-direct and batch-size-last DMA kernels wait for scalar
+    (kernel argument) loads once before their first global load; the
+    batch-size-first DMA kernel at most twice, and once for nine instances in
+    ten (in the others the compiler fetches a few tile fields again after the
+    entry statement that names them, having reused their registers).  The
+    compiler loads a structure field at its first use, so an exit test or a
+    branch on an argument before the loads splits the fetch into dependent
+    rounds, each a memory round trip added to every call; the kernels exit
+    after their loads and name their arguments at entry to avoid that."""
+    checked, bad, dma, dma_one = 0, [], 0, 0
+    for f, fns in kernel_asm.items():
+        for fn, lines in fns.items():
+            if any(k in fn for k in ONE_ROUND_FAMILIES):
+                checked += 1
+                if _argument_rounds(lines) > 1:
+                    bad.append((f, fn))
+            elif BSF_DMA in fn:
+                dma += 1
+                r = _argument_rounds(lines)
+                dma_one += r == 1
+                if r > 2:
+                    bad.append((f, fn))
+    assert checked > 250 and dma > 250
+    assert not bad, bad[:10]
+    assert dma_one >= 0.9 * dma, (dma_one, dma)
