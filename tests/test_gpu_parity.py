@@ -10,7 +10,7 @@ import pytest
 import oracle
 import paper_2405_15013_amd as ks
 from paper_2405_15013_amd import inputs
-from parity_util import TOL, case, from_device, nan_tensor, oracle_y, rel_err, to_device
+from parity_util import TOL, case, from_device, nan_tensor, oracle_y, rel_err, to_device, torch_dtype
 from shapes import DMA_ROW_GROUP_SHAPES, DMA_SHAPES, MFMA_SHAPES
 
 pytestmark = pytest.mark.gpu
@@ -429,3 +429,38 @@ def test_bias_act_rejects_bad_arguments():
     y = torch.empty(16, 8, device="cuda")
     assert ks.ks_matmul_bias_act(2, 4, 4, 2, kd, None, 2, x, y, 8, "bsl", "f32", check=False) == 5  # unknown act
     assert ks.ks_matmul_bias_act(2, 4, 4, 2, kd, y, 0, x, y, 8, "bsl", "f32", check=False) == 4     # bias aliases Y
+
+
+# Calls whose last workgroup has wavefronts past the last work item (the item
+# count is not a multiple of the wavefronts per workgroup): those wavefronts
+# run the last item's loads and MFMAs and must store nothing.
+SPARE_WAVE_CASES = [((1, 16, 16, 1), 72, "f32", "bsf", "direct"), ((1, 16, 16, 1), 200, "bf16", "bsl", "direct"),
+                    ((3, 48, 32, 1), 40, "bf16", "bsf", "direct"), ((1, 32, 16, 2), 40, "f32", "bsf", "direct"),
+                    ((1, 40, 24, 1), 100, "f32", "bsl", "masked"), ((1, 100, 36, 2), 37, "bf16", "bsf", "masked")]
+
+
+@pytest.mark.parametrize("case_", SPARE_WAVE_CASES, ids=["%s-%d-%s-%s" % c[:4] for c in SPARE_WAVE_CASES])
+def test_spare_waves_store_nothing(case_):
+    """Y between two guard regions of a sentinel value: the guards are intact
+    after the call (nothing is written before or after Y) and Y matches the
+    oracle, for plans whose last workgroup has spare wavefronts."""
+    import torch
+    pattern, batch, dtype, layout, name = case_
+    a, b, c, d = pattern
+    M = a * b * d
+    desc = ks.ks_plan_describe(*pattern, batch, layout, dtype)
+    assert "name=%s" % name in desc, desc
+    x, kv, _, _ = case(19, pattern, batch, dtype, "normal", "normal")
+    xd = to_device(inputs.to_layout(x, layout).reshape(-1), dtype)
+    kd = to_device(kv, dtype)
+    guard, sentinel = 4096, -7.5  # exact in every storage type
+    buf = torch.full((guard + batch * M + guard,), sentinel, dtype=torch_dtype(dtype), device="cuda")
+    y_view = buf[guard:guard + batch * M]
+    y_view.fill_(float("nan"))
+    ks.ks_matmul(a, b, c, d, kd, xd, y_view, batch, layout, dtype)
+    torch.cuda.synchronize()
+    host = buf.float().cpu().numpy()
+    assert np.all(host[:guard] == sentinel) and np.all(host[guard + batch * M:] == sentinel), "write outside Y"
+    y = from_device(y_view, dtype).reshape((batch, M) if layout == "bsf" else (M, batch))
+    err = rel_err(inputs.from_layout(y, layout), oracle_y(19, pattern, batch, dtype, "normal", "normal"))
+    assert err <= TOL[dtype], err
