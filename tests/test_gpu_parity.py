@@ -433,17 +433,22 @@ def test_bias_act_rejects_bad_arguments():
 
 # Calls whose last workgroup has wavefronts past the last work item (the item
 # count is not a multiple of the wavefronts per workgroup): those wavefronts
-# run the last item's loads and MFMAs and must store nothing.
+# run the last item's loads and MFMAs and must store nothing; and DMA tiles
+# that end past the batch (their rows or columns beyond it are loaded from
+# clamped addresses and not stored).
 SPARE_WAVE_CASES = [((1, 16, 16, 1), 72, "f32", "bsf", "direct"), ((1, 16, 16, 1), 200, "bf16", "bsl", "direct"),
                     ((3, 48, 32, 1), 40, "bf16", "bsf", "direct"), ((1, 32, 16, 2), 40, "f32", "bsf", "direct"),
-                    ((1, 40, 24, 1), 100, "f32", "bsl", "masked"), ((1, 100, 36, 2), 37, "bf16", "bsf", "masked")]
+                    ((1, 40, 24, 1), 100, "f32", "bsl", "masked"), ((1, 100, 36, 2), 37, "bf16", "bsf", "masked"),
+                    ((6, 64, 16, 8), 1000, "f32", "bsf", "dma"), ((2, 64, 64, 4), 200, "f32", "bsl", "dma"),
+                    ((1, 64, 64, 4), 1000, "bf16", "bsl", "dma")]
 
 
 @pytest.mark.parametrize("case_", SPARE_WAVE_CASES, ids=["%s-%d-%s-%s" % c[:4] for c in SPARE_WAVE_CASES])
 def test_spare_waves_store_nothing(case_):
     """Y between two guard regions of a sentinel value: the guards are intact
     after the call (nothing is written before or after Y) and Y matches the
-    oracle, for plans whose last workgroup has spare wavefronts."""
+    oracle, for plans whose last workgroup has spare wavefronts or whose last
+    DMA tile ends past the batch."""
     import torch
     pattern, batch, dtype, layout, name = case_
     a, b, c, d = pattern
