@@ -79,12 +79,17 @@ void ks_dma_bsl_kernel(Problem p, StagedTile t) {
     soff[m] = dma_bsl_src(p, t, st, V, r, v);
   }
   const int64_t xstage = (int64_t)CH * p.d * p.batch;  // X elements between the first rows of two stages
+  // The DMAs stream X with the nontemporal hint (cache policy bit 1): the
+  // tile reads its X once for all its k-groups, and keeping X out of the
+  // caches' retention leaves them to K (measured: fp32 batch-size-last 1-3 %
+  // faster; the batch-size-first kernel, whose k-group tiles re-read X from
+  // L2, got 1-2 % slower with it and keeps the default).
   auto dma = [&](const T* xs, int buf) {
     char* dst = smem + buf * STAGE + w * 1024;
 #pragma unroll
     for (int m = 0; m < UD; ++m)
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(xs + soff[m]),
-                                       (lds_void_t*)(dst + m * W * 1024), 16, 0, 0);
+                                       (lds_void_t*)(dst + m * W * 1024), 16, 0, 2);
   };
 
   // Operand pieces: one 16-byte unit (V batch entries) of stage row LP*g + q.
